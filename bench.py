@@ -1,0 +1,246 @@
+"""Benchmark: STaR-Quant W4A4 SGAT linear layer set per denoising step on one MI355X.
+
+Workload (default): the LLaDA-8B-shaped layer set, one sequence of 1024 tokens
+(512 unmasked prompt tokens, 512 generation tokens with 8 of 16 32-token blocks
+masked): QKV 4096->12288, O 4096->4096 with TAC (g = 16) ahead of it,
+gate+up 4096->24576, down 12288->4096, all W4A4 SGAT, fp16 in and out.
+
+One step = the whole per-step hot path for every linear of the set:
+    [TAC] -> x P G_s (dense fp32 transform, Eq. 11) -> per-token int4 -> W4A4 GEMM
+with the weights prepared offline (Eq. 12, outside the timed region) and every
+input resident in HBM.  A second measurement runs the deployment form in which P
+is folded into the weights and the upstream activations, so the step is
+[TAC] -> gate -> int4 -> GEMM; it is reported next to the main figure.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+
+Prints one JSON line.  Synthetic, seeded inputs (no datasets, no trained weights).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+# MI355X published peaks
+PEAK_HBM_GBS = 8000.0
+PEAK_INT8_TOPS = 5000.0           # dense int8 MFMA, TOP/s
+# fp32 FMA on the VALU without packed-fp32 instructions (the library is built
+# without them): 256 CU x 4 SIMD x 16 lanes x 2 flop x 2.4 GHz
+PEAK_FP32_VALU_TFLOPS = 78.6
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample", type=int, default=384, help="tokens in the oracle timing sample")
+    ap.add_argument("--only", choices=["dense", "folded", "both"], default="both")
+    return ap.parse_args()
+
+
+class Timer:
+    """HIP event pairs on the launching stream, summed per label."""
+
+    def __init__(self, torch):
+        self.torch = torch
+        self.pairs = {}
+
+    def wrap(self, label, fn):
+        s = self.torch.cuda.Event(enable_timing=True)
+        e = self.torch.cuda.Event(enable_timing=True)
+        s.record()
+        fn()
+        e.record()
+        self.pairs.setdefault(label, []).append((s, e))
+
+    def ms(self, label):
+        ps = self.pairs.get(label, [])
+        return sum(s.elapsed_time(e) for s, e in ps), len(ps)
+
+    def reset(self):
+        self.pairs = {}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this benchmark runs on exactly one GPU; --gpus must be 1"}), flush=True)
+        sys.exit(2)
+    import torch
+    import paper_2606_04945_amd as sq
+    import synth
+
+    sq.lib()                                    # raises if the HIP library is missing
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    cfg = synth.CONFIGS[1]
+    M = cfg.M
+    state_np = synth.config_state(1)
+    state = torch.from_numpy(state_np).to(dev)
+    t0 = time.time()
+    sites = []
+    for si, site in enumerate(cfg.sites):
+        t = synth.site_tensors(1, si, state_np)
+        d = dict(site=site, K=site.K, N=site.N, dm=t.dm, du=t.du,
+                 X=torch.from_numpy(t.X).to(dev), P=torch.from_numpy(t.P).to(dev),
+                 W=torch.from_numpy(t.W).to(dev))
+        if site.tac:
+            d.update(tac_M=torch.from_numpy(t.tac_M).to(dev), tac_d=torch.from_numpy(t.tac_d).to(dev), g=t.g)
+        sites.append(d)
+    print(f"# inputs generated in {time.time() - t0:.1f}s", file=sys.stderr, flush=True)
+
+    # offline weight preparation (Eq. 12), outside the timed region
+    for d in sites:
+        d["Wq"], d["s_w"] = sq.sgat_prepare_weights(d["W"], d["P"])
+        K, N = d["K"], d["N"]
+        d["z"] = torch.empty((M, K), dtype=torch.float16, device=dev) if "tac_M" in d else None
+        d["xp"] = torch.empty((M, K), dtype=torch.float32, device=dev)
+        d["Aq"] = torch.empty((M, K // 2), dtype=torch.uint8, device=dev)
+        d["s_a"] = torch.empty((M,), dtype=torch.float32, device=dev)
+        d["Y"] = torch.empty((M, N), dtype=torch.float16, device=dev)
+        nb = sq.gemm_workspace_bytes(M, N, K)
+        d["gws"] = torch.empty(max(nb, 1), dtype=torch.uint8, device=dev)
+        nq = sq.quant_act_workspace_bytes(M, K, False, "tac_M" in d)
+        d["qws"] = torch.empty(max(nq, 1), dtype=torch.uint8, device=dev)
+    # three rotating copies of the prepared weights for the folded-basis run, so
+    # that the 256 MB MALL cannot hold a whole layer set's weights between steps
+    wcopies = [[(d["Wq"].clone(), d["s_w"].clone()) for d in sites] for _ in range(3)]
+    torch.cuda.synchronize()
+    timer = Timer(torch)
+
+    def step_dense(tm):
+        for d in sites:
+            src = d["X"]
+            if d["z"] is not None:
+                tm.wrap("tac", lambda: sq.tac_apply(d["X"], d["tac_M"], d["tac_d"], d["g"], out=d["z"]))
+                src = d["z"]
+            tm.wrap("transform/" + d["site"].name,
+                    lambda: sq.sgat_transform(src, state, d["P"], d["dm"], d["du"], out=d["xp"]))
+            tm.wrap("quant", lambda: sq.sgat_quantize(d["xp"], Aq=d["Aq"], s=d["s_a"]))
+            tm.wrap("gemm/" + d["site"].name,
+                    lambda: sq.w4a4_gemm(d["Aq"], d["s_a"], d["Wq"], d["s_w"], Y=d["Y"], ws=d["gws"]))
+
+    def step_folded(tm, it):
+        ws = wcopies[it % len(wcopies)]
+        for d, (Wq, s_w) in zip(sites, ws):
+            tm.wrap("quant_act/" + d["site"].name,
+                    lambda: sq.sgat_quant_act(d["X"], state, None, d["dm"], d["du"], d.get("tac_M"),
+                                              d.get("tac_d"), d.get("g", 0), Aq=d["Aq"], s_a=d["s_a"],
+                                              ws=d["qws"]))
+            tm.wrap("gemm/" + d["site"].name,
+                    lambda: sq.w4a4_gemm(d["Aq"], d["s_a"], Wq, s_w, Y=d["Y"], ws=d["gws"]))
+
+    def run(step, steps, warmup):
+        for i in range(warmup):
+            step(Timer(torch), i)
+        torch.cuda.synchronize()
+        timer.reset()
+        start = torch.cuda.Event(enable_timing=True)
+        end = torch.cuda.Event(enable_timing=True)
+        start.record()
+        for i in range(steps):
+            step(timer, i)
+        end.record()
+        torch.cuda.synchronize()
+        return start.elapsed_time(end) / steps
+
+    out = {}
+    flops_tr = {d["site"].name: 2.0 * M * d["K"] * (d["K"] - d["K"] // 32) for d in sites}
+    ops_gemm = {d["site"].name: 2.0 * M * d["N"] * d["K"] for d in sites}
+
+    if args.only in ("dense", "both"):
+        ms_dense = run(lambda tm, i: step_dense(tm), args.steps, args.warmup)
+        tr_ms = sum(timer.ms("transform/" + n)[0] for n in flops_tr)
+        tr_flop = sum(flops_tr.values()) * args.steps
+        gm_ms = sum(timer.ms("gemm/" + n)[0] for n in ops_gemm)
+        gm_ops = sum(ops_gemm.values()) * args.steps
+        out["dense"] = dict(ms=ms_dense, transform_ms=tr_ms / args.steps, transform_tflops=tr_flop / tr_ms / 1e9,
+                            gemm_ms=gm_ms / args.steps, gemm_tops=gm_ops / gm_ms / 1e9,
+                            tac_ms=timer.ms("tac")[0] / args.steps, quant_ms=timer.ms("quant")[0] / args.steps,
+                            per_site_transform_ms={n: timer.ms("transform/" + n)[0] / args.steps for n in flops_tr})
+    if args.only in ("folded", "both"):
+        ms_fold = run(step_folded, args.steps, args.warmup)
+        gm_ms = sum(timer.ms("gemm/" + n)[0] for n in ops_gemm)
+        gm_ops = sum(ops_gemm.values()) * args.steps
+        qa_ms = sum(timer.ms("quant_act/" + d["site"].name)[0] for d in sites)
+        out["folded"] = dict(ms=ms_fold, gemm_ms=gm_ms / args.steps, gemm_tops=gm_ops / gm_ms / 1e9,
+                             quant_act_ms=qa_ms / args.steps,
+                             per_site_gemm_ms={n: timer.ms("gemm/" + n)[0] / args.steps for n in ops_gemm})
+
+    # ---------------------------------------------------------------- CPU baseline
+    cpu = None
+    if not args.no_cpu_baseline:
+        from oracle import oracle as O
+        threads = min(16, os.cpu_count() or 1)
+        n = args.cpu_sample
+        rows = np.linspace(0, M - 1, n).astype(int)
+        rng = np.random.default_rng(0)
+        hosts = []
+        for d in sites:
+            h = dict(X=d["X"][rows].cpu().numpy(), P=d["P"].cpu().numpy(), st=state_np[rows],
+                     Wq=rng.integers(0, 256, (d["N"], d["K"] // 2), dtype=np.uint8),
+                     s_w=np.ones(d["N"], np.float32))
+            if "tac_M" in d:
+                h.update(tM=d["tac_M"].cpu().numpy(), td=d["tac_d"].cpu().numpy(), g=d["g"])
+            hosts.append((d, h))
+        t1 = time.time()
+        for d, h in hosts:
+            Aq, s_a = O.quant_act(h["X"], h["st"], h["P"], d["dm"], d["du"], h.get("tM"), h.get("td"),
+                                  h.get("g", 0), threads=threads)
+            O.gemm(Aq, s_a, h["Wq"], h["s_w"], threads=threads)
+        el = time.time() - t1
+        cpu = {"value": n / el, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+               "sample": f"{n} of the {M} tokens through the whole dense-P layer set (TAC, transform, "
+                         f"quantise, GEMM against all N); weight preparation excluded; {el:.1f} s"}
+
+    dense = out.get("dense")
+    fold = out.get("folded")
+    main_ms = dense["ms"] if dense else fold["ms"]
+    res = {
+        "metric": "W4A4 SGAT-linear TOPS & % int8-MFMA peak; layer-set tokens/s per denoise step",
+        "value": M / (main_ms / 1e3),
+        "unit": "tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": main_ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "int4xint4->int32 GEMM, fp32 transform, fp16 I/O",
+        "data": "synthetic (seeded; random-init weights and orthogonal bases)",
+        "config": {"workload": "LLaDA-8B-shaped SGAT layer set (QKV, O+TAC g=16, gate+up, down), "
+                               "1024 tokens, dense online P" if dense else
+                               "LLaDA-8B-shaped SGAT layer set, 1024 tokens, folded P",
+                   "tokens": M, "hidden": 4096, "ffn": 12288, "tac_block": 16},
+    }
+    if dense:
+        ach = dense["transform_tflops"]
+        res["roofline"] = {"bound": "alu", "achieved": ach, "peak": PEAK_FP32_VALU_TFLOPS, "unit": "TFLOP/s",
+                           "frac": ach / PEAK_FP32_VALU_TFLOPS, "traffic": None,
+                           "kernel": "transform (dense fp32 x P, fixed order)"}
+        res["breakdown_ms"] = {k: dense[k] for k in ("transform_ms", "gemm_ms", "tac_ms", "quant_ms")}
+        res["gemm"] = {"tops": dense["gemm_tops"], "frac_int8_peak": dense["gemm_tops"] / PEAK_INT8_TOPS}
+        res["sgat_linear_tops"] = sum(ops_gemm.values()) / (dense["ms"] / 1e3) / 1e12
+    if fold:
+        res["folded_P"] = {
+            "value": M / (fold["ms"] / 1e3), "unit": "tokens/s", "ms_per_step": fold["ms"],
+            "sgat_linear_tops": sum(ops_gemm.values()) / (fold["ms"] / 1e3) / 1e12,
+            "roofline": {"bound": "mfma", "achieved": fold["gemm_tops"], "peak": PEAK_INT8_TOPS, "unit": "TOP/s",
+                         "frac": fold["gemm_tops"] / PEAK_INT8_TOPS, "kernel": "w4a4 gemm"},
+            "quant_act_ms": fold["quant_act_ms"], "per_site_gemm_ms": fold["per_site_gemm_ms"]}
+        if not dense:
+            res["roofline"] = dict(res["folded_P"]["roofline"], traffic=None)
+    if cpu:
+        res["cpu_baseline"] = cpu
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

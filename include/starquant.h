@@ -1,0 +1,166 @@
+/*
+ * starquant.h -- C ABI of the STaR-Quant W4A4 hot path for AMD MI355X (gfx950).
+ *
+ * STaR-Quant (arXiv 2606.04945) quantises the linear layers of a diffusion LLM
+ * to 4-bit weights and 4-bit activations.  At every denoising step a quantised
+ * linear layer runs:
+ *   (1) the State-Guided Activation Transformation (SGAT): each token's row x is
+ *       mapped to x P G_s, where P = [U_sh, U_m, U_u] is an orthogonal basis and
+ *       the binary gate G_s keeps the shared columns plus the band of the token's
+ *       own mask state s in {masked, unmasked} (Sec. 3.2, Eq. 8-11);
+ *   (2) per-token symmetric int4 quantisation of the transformed row (Sec. 3.1,
+ *       Eq. 2 and 5);
+ *   (3) an int4 x int4 product with the shared, offline-quantised weight
+ *       W~ = Q_w(P^T W^T) (Eq. 12-13), dequantised to fp16;
+ *   (4) ahead of the attention output projection only, Temporal Attention
+ *       Compensation (TAC): a block-diagonal affine map z_b -> M_b z_b + d_b on
+ *       the attention output (Sec. 3.3, Eq. 17; App. C).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Every tensor pointer is a DEVICE pointer owned by the caller; the library
+ *    never allocates, frees or retains device memory, and keeps no state between
+ *    calls other than the thread-local error message.
+ *  - Row-major, dense.  fp16 tensors are passed as uint16_t* holding IEEE
+ *    binary16 bits.  Packed int4 tensors are uint8_t* with two codes per byte:
+ *    byte t of a row holds code 2t in bits 0-3 and code 2t+1 in bits 4-7, each a
+ *    two's-complement nibble.
+ *  - `stream` is a hipStream_t (NULL = the null stream).  Work is enqueued on it
+ *    and the call returns without synchronising.  Calls are reentrant.
+ *  - Every argument is checked before anything is enqueued; on a non-zero
+ *    return nothing was enqueued and no output was touched.  M == 0 (or N == 0)
+ *    is a successful no-op.  sq_last_error() describes the last failure on the
+ *    calling thread.
+ *  - Shape rules: K % 64 == 0 and 64 <= K <= 131072; N % 8 == 0; all pointers
+ *    16-byte aligned.  TAC block size g is a power of two, 1 <= g <= 128, g | C.
+ *  - Arithmetic is fixed so that results are a unique function of the inputs:
+ *    fp32 IEEE throughout (correctly rounded divide, round-to-nearest-even, no
+ *    flush of subnormals); the transform accumulates k in chunks of 256 with a
+ *    fused multiply-add in ascending k from +0 and adds the chunk sums in
+ *    ascending order; the quantiser is s = absmax / 7, q = clamp(rint(x / s),
+ *    -8, 7), a zero scale giving zero codes.
+ */
+#ifndef STARQUANT_H
+#define STARQUANT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Return codes. */
+#define SQ_OK 0
+#define SQ_ERR_NULL 1        /* a required pointer is NULL                     */
+#define SQ_ERR_SHAPE 2       /* a size or band/block parameter breaks a rule   */
+#define SQ_ERR_ALIGN 3       /* a pointer is not 16-byte aligned               */
+#define SQ_ERR_WORKSPACE 4   /* workspace missing or smaller than required     */
+#define SQ_ERR_HIP 5         /* the HIP runtime reported an error at launch    */
+
+/* Message for the last non-zero return on the calling thread ("" if none). */
+const char* sq_last_error(void);
+
+/* Library version string. */
+const char* sq_version(void);
+
+/* TAC default block size (App. C): 16, or the largest g <= 16 dividing C;
+ * 0 if C <= 0. */
+int32_t sq_tac_default_block(int32_t C);
+
+/* Device workspace, in bytes, that sgat_quant_act needs for these arguments
+ * (has_P, has_tac: 0 or 1).  0 means ws may be NULL. */
+size_t sq_quant_act_workspace_bytes(int32_t M, int32_t K, int32_t has_P, int32_t has_tac);
+
+/* Device workspace, in bytes, that sgat_prepare_weights needs. */
+size_t sq_prepare_weights_workspace_bytes(int32_t N, int32_t K, int32_t has_P);
+
+/* Device workspace, in bytes, that w4a4_gemm needs for this shape (split-K
+ * partial sums for short M); 0 means ws may be NULL. */
+size_t sq_gemm_workspace_bytes(int32_t M, int32_t N, int32_t K);
+
+/*
+ * sgat_prepare_weights -- offline weight side of SGAT (Eq. 12; App. A, App. B).
+ * W~ = Q_w(P^T W^T) is stored transposed, as the rows of W P: for output channel
+ * n, w'_n = W[n, :] P (no gate), then per-output-channel symmetric int4:
+ * s_w[n] = max_j |w'_nj| / 7, codes clamp(rint(w'_nj / s_w[n]), -8, 7).
+ *   W    [N][K] fp16, row n = output channel n's input weights.
+ *   P    [K][K] fp32, P[k][j]; NULL = identity (W is already in the P basis).
+ *   Wq   out [N][K/2] packed int4.     s_w  out [N] fp32.
+ *   ws   device workspace of at least sq_prepare_weights_workspace_bytes().
+ */
+int sgat_prepare_weights(const uint16_t* W, const float* P, int32_t N, int32_t K,
+                         uint8_t* Wq, float* s_w, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * sgat_transform -- the SGAT activation transform alone (Eq. 11): x'_i = x_i P G_{s_i}.
+ * Columns of P are ordered [shared | masked band (d_m) | unmasked band (d_u)]
+ * (Eq. 8); a masked token's unmasked band and an unmasked token's masked band
+ * are exactly +0 (Eq. 9-10).
+ *   X      [M][K] fp16 tokens.        state [M] uint8, 0 = unmasked, else masked;
+ *                                     NULL = no gate (every column kept).
+ *   P      [K][K] fp32, or NULL (X already in the P basis: x' = x, then gated).
+ *   d_m, d_u  band widths, d_m, d_u >= 0, d_m + d_u < K (default K/32 each).
+ *   Xp     out [M][K] fp32.
+ */
+int sgat_transform(const uint16_t* X, const uint8_t* state, const float* P,
+                   int32_t M, int32_t K, int32_t d_m, int32_t d_u, float* Xp, void* stream);
+
+/*
+ * sgat_quantize -- per-row symmetric int4 quantisation of fp32 rows (Sec. 3.1,
+ * Eq. 2 with zero point 0; per token for activations, Eq. 5):
+ * s[i] = max_j |X[i][j]| / 7 and codes clamp(rint(X[i][j] / s[i]), -8, 7), all
+ * codes 0 when s[i] == 0.  Used on the output of sgat_transform.
+ *   Xp  [M][K] fp32.   Aq out [M][K/2] packed int4.   s out [M] fp32.
+ */
+int sgat_quantize(const float* Xp, int32_t M, int32_t K, uint8_t* Aq, float* s, void* stream);
+
+/*
+ * sgat_quant_act -- activation side of one SGAT linear, per denoising step:
+ * [TAC] -> x P G_s (Eq. 11) -> per-token symmetric int4 (Eq. 2, 5).
+ *   X      [M][K] fp16 tokens (for the O-projection: the attention output Z).
+ *   state  [M] uint8, 0 = unmasked, else masked; NULL = no gate.
+ *   P      [K][K] fp32 or NULL (X already in the P basis).
+ *   d_m, d_u  band widths as in sgat_transform.
+ *   tac_M  [K/g][g][g] fp16, tac_M[b][r][c] = M_b[r][c]; NULL = no TAC.
+ *   tac_d  [K] fp16 bias d, required iff tac_M != NULL.  g: TAC block size.
+ *          TAC output z'_{b g + r} = fp16(sum_c M_b[r][c] z_{b g + c} + d_{b g + r}),
+ *          fp32 fused multiply-adds in ascending c from +0, bias added last.
+ *   Aq     out [M][K/2] packed int4.   s_a out [M] fp32 per-token scales.
+ *   ws     device workspace of at least sq_quant_act_workspace_bytes().
+ */
+int sgat_quant_act(const uint16_t* X, const uint8_t* state, const float* P,
+                   int32_t M, int32_t K, int32_t d_m, int32_t d_u,
+                   const uint16_t* tac_M, const uint16_t* tac_d, int32_t g,
+                   uint8_t* Aq, float* s_a, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * w4a4_gemm -- the state-guided quantised projection (Eq. 13; Eq. 5):
+ * acc[i][n] = sum_j qa[i][j] qw[n][j] (exact int32), and
+ * Y[i][n] = fp16((float(acc[i][n]) * s_a[i]) * s_w[n]).
+ *   Aq [M][K/2], s_a [M]: from sgat_quant_act.  Wq [N][K/2], s_w [N]: from
+ *   sgat_prepare_weights.  Both operands are K-contiguous (Y = A B^T).
+ *   Y    out [M][N] fp16 (may be NULL if acc is given).
+ *   acc  out [M][N] int32, or NULL.
+ *   ws   device workspace of at least sq_gemm_workspace_bytes(M, N, K).
+ */
+int w4a4_gemm(const uint8_t* Aq, const float* s_a, const uint8_t* Wq, const float* s_w,
+              int32_t M, int32_t N, int32_t K, uint16_t* Y, int32_t* acc,
+              void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * tac_apply -- Temporal Attention Compensation on its own (Eq. 17, App. C):
+ * for token i and block b of g channels, Z_out[i, b g + r] =
+ * fp16(sum_c M_b[r][c] Z[i, b g + c] + d[b g + r]) with the arithmetic stated
+ * at sgat_quant_act.  Not state-dependent; parameters fixed across steps.
+ *   Z [M][C] fp16; tac_M [C/g][g][g] fp16; tac_d [C] fp16.
+ *   Z_out out [M][C] fp16; must not overlap Z.
+ */
+int tac_apply(const uint16_t* Z, const uint16_t* tac_M, const uint16_t* tac_d,
+              int32_t M, int32_t C, int32_t g, uint16_t* Z_out, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* STARQUANT_H */

@@ -1,0 +1,186 @@
+"""STaR-Quant W4A4 hot path on MI355X (gfx950): thin torch binding of libstarquant.
+
+Every function here only checks and marshals arguments (device pointers, sizes,
+the current HIP stream) and calls the C ABI declared in include/starquant.h;
+all arithmetic runs in the library's HIP kernels.  torch provides device memory
+and streams.  Outputs and workspaces are allocated with torch when not given.
+
+    Aq, s_a = sgat_quant_act(X, state, P)            # Eq. 11 + per-token int4
+    Wq, s_w = sgat_prepare_weights(W, P)             # Eq. 12, offline
+    Y = w4a4_gemm(Aq, s_a, Wq, s_w)                  # Eq. 13
+    Zc = tac_apply(Z, tac_M, tac_d, g)               # Eq. 17
+"""
+from __future__ import annotations
+
+from typing import Optional, Tuple
+
+import torch
+
+from ._lib import SQ_OK, StarQuantError, check, lib  # noqa: F401
+
+__all__ = ["sgat_prepare_weights", "sgat_transform", "sgat_quantize", "sgat_quant_act", "w4a4_gemm", "tac_apply",
+           "tac_default_block", "default_band", "quant_act_workspace_bytes", "gemm_workspace_bytes",
+           "prepare_weights_workspace_bytes", "StarQuantError", "lib"]
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _need(t: Optional[torch.Tensor], name: str, dtype, shape=None, optional=False):
+    if t is None:
+        if optional:
+            return
+        raise ValueError(f"{name} is required")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+
+
+def _ws(nbytes: int, ws: Optional[torch.Tensor], device) -> Tuple[Optional[torch.Tensor], int]:
+    if nbytes == 0:
+        return ws, (ws.numel() if ws is not None else 0)
+    if ws is None:
+        ws = torch.empty(nbytes, dtype=torch.uint8, device=device)
+    return ws, ws.numel() * ws.element_size()
+
+
+def tac_default_block(C: int) -> int:
+    return int(lib().sq_tac_default_block(int(C)))
+
+
+def default_band(K: int) -> Tuple[int, int]:
+    """d_m = d_u = K/32 (App. B default subspace allocation)."""
+    return K // 32, K // 32
+
+
+def quant_act_workspace_bytes(M: int, K: int, has_P: bool, has_tac: bool) -> int:
+    return int(lib().sq_quant_act_workspace_bytes(M, K, int(has_P), int(has_tac)))
+
+
+def prepare_weights_workspace_bytes(N: int, K: int, has_P: bool) -> int:
+    return int(lib().sq_prepare_weights_workspace_bytes(N, K, int(has_P)))
+
+
+def gemm_workspace_bytes(M: int, N: int, K: int) -> int:
+    return int(lib().sq_gemm_workspace_bytes(M, N, K))
+
+
+def sgat_prepare_weights(W: torch.Tensor, P: Optional[torch.Tensor] = None, *, Wq=None, s_w=None, ws=None,
+                         stream=None):
+    """W~ = Q_w(P^T W^T) as rows of W P: returns (Wq [N][K/2] uint8, s_w [N] fp32)."""
+    N, K = W.shape
+    _need(W, "W", torch.float16)
+    _need(P, "P", torch.float32, (K, K), optional=True)
+    if Wq is None:
+        Wq = torch.empty((N, K // 2), dtype=torch.uint8, device=W.device)
+    if s_w is None:
+        s_w = torch.empty((N,), dtype=torch.float32, device=W.device)
+    _need(Wq, "Wq", torch.uint8, (N, K // 2))
+    _need(s_w, "s_w", torch.float32, (N,))
+    ws, wsb = _ws(prepare_weights_workspace_bytes(N, K, P is not None), ws, W.device)
+    check(lib().sgat_prepare_weights(_ptr(W), _ptr(P), N, K, _ptr(Wq), _ptr(s_w), _ptr(ws), wsb, _stream(stream)))
+    return Wq, s_w
+
+
+def sgat_transform(X: torch.Tensor, state: Optional[torch.Tensor], P: Optional[torch.Tensor],
+                   d_m: Optional[int] = None, d_u: Optional[int] = None, *, out=None, stream=None):
+    """x'_i = x_i P G_{s_i} (Eq. 11), fp32 [M][K]."""
+    M, K = X.shape
+    dm0, du0 = default_band(K)
+    d_m = dm0 if d_m is None else d_m
+    d_u = du0 if d_u is None else d_u
+    _need(X, "X", torch.float16)
+    _need(state, "state", torch.uint8, (M,), optional=True)
+    _need(P, "P", torch.float32, (K, K), optional=True)
+    if out is None:
+        out = torch.empty((M, K), dtype=torch.float32, device=X.device)
+    _need(out, "out", torch.float32, (M, K))
+    check(lib().sgat_transform(_ptr(X), _ptr(state), _ptr(P), M, K, d_m, d_u, _ptr(out), _stream(stream)))
+    return out
+
+
+def sgat_quantize(Xp: torch.Tensor, *, Aq=None, s=None, stream=None):
+    """Per-row symmetric int4 of fp32 rows (Eq. 2, z = 0): returns (Aq [M][K/2] uint8, s [M] fp32)."""
+    M, K = Xp.shape
+    _need(Xp, "Xp", torch.float32)
+    if Aq is None:
+        Aq = torch.empty((M, K // 2), dtype=torch.uint8, device=Xp.device)
+    if s is None:
+        s = torch.empty((M,), dtype=torch.float32, device=Xp.device)
+    _need(Aq, "Aq", torch.uint8, (M, K // 2))
+    _need(s, "s", torch.float32, (M,))
+    check(lib().sgat_quantize(_ptr(Xp), M, K, _ptr(Aq), _ptr(s), _stream(stream)))
+    return Aq, s
+
+
+def sgat_quant_act(X: torch.Tensor, state: Optional[torch.Tensor], P: Optional[torch.Tensor] = None,
+                   d_m: Optional[int] = None, d_u: Optional[int] = None, tac_M: Optional[torch.Tensor] = None,
+                   tac_d: Optional[torch.Tensor] = None, g: int = 0, *, Aq=None, s_a=None, ws=None, stream=None):
+    """[TAC] -> x P G_s -> per-token int4: returns (Aq [M][K/2] uint8, s_a [M] fp32)."""
+    M, K = X.shape
+    dm0, du0 = default_band(K)
+    d_m = dm0 if d_m is None else d_m
+    d_u = du0 if d_u is None else d_u
+    _need(X, "X", torch.float16)
+    _need(state, "state", torch.uint8, (M,), optional=True)
+    _need(P, "P", torch.float32, (K, K), optional=True)
+    if tac_M is not None:
+        _need(tac_M, "tac_M", torch.float16, (K // g, g, g))
+        _need(tac_d, "tac_d", torch.float16, (K,))
+    if Aq is None:
+        Aq = torch.empty((M, K // 2), dtype=torch.uint8, device=X.device)
+    if s_a is None:
+        s_a = torch.empty((M,), dtype=torch.float32, device=X.device)
+    _need(Aq, "Aq", torch.uint8, (M, K // 2))
+    _need(s_a, "s_a", torch.float32, (M,))
+    ws, wsb = _ws(quant_act_workspace_bytes(M, K, P is not None, tac_M is not None), ws, X.device)
+    check(lib().sgat_quant_act(_ptr(X), _ptr(state), _ptr(P), M, K, d_m, d_u, _ptr(tac_M), _ptr(tac_d), g,
+                               _ptr(Aq), _ptr(s_a), _ptr(ws), wsb, _stream(stream)))
+    return Aq, s_a
+
+
+def w4a4_gemm(Aq: torch.Tensor, s_a: torch.Tensor, Wq: torch.Tensor, s_w: torch.Tensor, *, Y=None, acc=None,
+              want_Y: bool = True, want_acc: bool = False, ws=None, stream=None):
+    """Y = fp16((acc * s_a) * s_w) with acc = Aq . Wq^T exact (Eq. 13).  Returns Y, or (Y, acc)."""
+    M, Kh = Aq.shape
+    N = Wq.shape[0]
+    K = 2 * Kh
+    _need(Aq, "Aq", torch.uint8)
+    _need(Wq, "Wq", torch.uint8, (N, Kh))
+    _need(s_a, "s_a", torch.float32, (M,))
+    _need(s_w, "s_w", torch.float32, (N,))
+    if Y is None and want_Y:
+        Y = torch.empty((M, N), dtype=torch.float16, device=Aq.device)
+    if acc is None and want_acc:
+        acc = torch.empty((M, N), dtype=torch.int32, device=Aq.device)
+    _need(Y, "Y", torch.float16, (M, N), optional=True)
+    _need(acc, "acc", torch.int32, (M, N), optional=True)
+    ws, wsb = _ws(gemm_workspace_bytes(M, N, K), ws, Aq.device)
+    check(lib().w4a4_gemm(_ptr(Aq), _ptr(s_a), _ptr(Wq), _ptr(s_w), M, N, K, _ptr(Y), _ptr(acc), _ptr(ws), wsb,
+                          _stream(stream)))
+    return (Y, acc) if want_acc else Y
+
+
+def tac_apply(Z: torch.Tensor, tac_M: torch.Tensor, tac_d: torch.Tensor, g: int, *, out=None, stream=None):
+    """Z_b M_b^T + 1 d_b^T per block of g channels (Eq. 17), fp16 out."""
+    M, C = Z.shape
+    _need(Z, "Z", torch.float16)
+    _need(tac_M, "tac_M", torch.float16, (C // g, g, g))
+    _need(tac_d, "tac_d", torch.float16, (C,))
+    if out is None:
+        out = torch.empty_like(Z)
+    _need(out, "out", torch.float16, (M, C))
+    check(lib().tac_apply(_ptr(Z), _ptr(tac_M), _ptr(tac_d), M, C, g, _ptr(out), _stream(stream)))
+    return out

@@ -1,0 +1,201 @@
+// C ABI of libstarquant: argument checks, workspace layout and kernel dispatch.
+// Every argument is checked before the first launch; on failure nothing is
+// enqueued and the reason is kept in a thread-local message.
+#include <stdarg.h>
+#include <stdio.h>
+
+#include "../../include/starquant.h"
+#include "sq_internal.hpp"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+int fail(int code, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof(g_err), fmt, ap);
+    va_end(ap);
+    return code;
+}
+
+int hip_status(hipError_t e, const char* what) {
+    if (e == hipSuccess) return SQ_OK;
+    return fail(SQ_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+constexpr size_t kAlign = 256;
+size_t round_up(size_t n) { return (n + kAlign - 1) / kAlign * kAlign; }
+
+int check_K(int32_t K) {
+    if (K < 64 || K > 131072 || K % 64)
+        return fail(SQ_ERR_SHAPE, "K=%d: need 64 <= K <= 131072 and K %% 64 == 0", K);
+    return SQ_OK;
+}
+
+int check_band(int32_t K, int32_t dm, int32_t du) {
+    if (dm < 0 || du < 0 || (int64_t)dm + du >= K)
+        return fail(SQ_ERR_SHAPE, "bands d_m=%d d_u=%d: need d_m, d_u >= 0 and d_m + d_u < K=%d", dm, du, K);
+    return SQ_OK;
+}
+
+int check_tac(int32_t C, int32_t g) {
+    if (g < 1 || g > 128 || (g & (g - 1)) || C % g)
+        return fail(SQ_ERR_SHAPE, "TAC block g=%d: need a power of two in [1, 128] dividing C=%d", g, C);
+    return SQ_OK;
+}
+
+#define SQ_REQUIRE(cond, code, ...) \
+    do {                            \
+        if (!(cond)) return fail(code, __VA_ARGS__); \
+    } while (0)
+
+#define SQ_TRY(expr)                 \
+    do {                             \
+        int _rc = (expr);            \
+        if (_rc != SQ_OK) return _rc; \
+    } while (0)
+
+}  // namespace
+
+extern "C" {
+
+const char* sq_last_error(void) { return g_err; }
+
+const char* sq_version(void) { return "starquant 0.1 gfx950"; }
+
+int32_t sq_tac_default_block(int32_t C) {
+    if (C <= 0) return 0;
+    for (int g = 16; g > 1; --g)
+        if (C % g == 0) return g;
+    return 1;
+}
+
+size_t sq_quant_act_workspace_bytes(int32_t M, int32_t K, int32_t has_P, int32_t has_tac) {
+    if (M <= 0 || K <= 0) return 0;
+    size_t n = 0;
+    if (has_tac) n += round_up((size_t)M * K * sizeof(uint16_t));
+    if (has_P) n += round_up((size_t)M * K * sizeof(float));
+    return n;
+}
+
+size_t sq_prepare_weights_workspace_bytes(int32_t N, int32_t K, int32_t has_P) {
+    if (N <= 0 || K <= 0 || !has_P) return 0;
+    return round_up((size_t)N * K * sizeof(float));
+}
+
+size_t sq_gemm_workspace_bytes(int32_t M, int32_t N, int32_t K) {
+    if (M <= 0 || N <= 0 || K <= 0) return 0;
+    return round_up(sq::gemm_workspace_bytes(M, N, K));
+}
+
+int sgat_prepare_weights(const uint16_t* W, const float* P, int32_t N, int32_t K, uint8_t* Wq, float* s_w,
+                         void* ws, size_t ws_bytes, void* stream) {
+    SQ_TRY(check_K(K));
+    SQ_REQUIRE(N >= 0, SQ_ERR_SHAPE, "N=%d < 0", N);
+    if (N == 0) return SQ_OK;
+    SQ_REQUIRE(W && Wq && s_w, SQ_ERR_NULL, "sgat_prepare_weights: W, Wq and s_w are required");
+    SQ_REQUIRE(aligned16(W) && aligned16(Wq) && aligned16(s_w) && aligned16(P) && aligned16(ws), SQ_ERR_ALIGN,
+               "sgat_prepare_weights: pointers must be 16-byte aligned");
+    const size_t need = sq_prepare_weights_workspace_bytes(N, K, P != nullptr);
+    SQ_REQUIRE(ws_bytes >= need && (need == 0 || ws), SQ_ERR_WORKSPACE,
+               "sgat_prepare_weights: workspace %zu B < %zu B", ws_bytes, need);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    if (!P) return hip_status(sq::launch_quant_f16(W, nullptr, N, K, 0, 0, Wq, s_w, st), "quant_f16");
+    float* wp = static_cast<float*>(ws);
+    SQ_TRY(hip_status(sq::launch_transform(W, nullptr, P, N, K, 0, 0, wp, st), "transform"));
+    return hip_status(sq::launch_quant_f32(wp, N, K, Wq, s_w, st), "quant_f32");
+}
+
+int sgat_transform(const uint16_t* X, const uint8_t* state, const float* P, int32_t M, int32_t K, int32_t d_m,
+                   int32_t d_u, float* Xp, void* stream) {
+    SQ_TRY(check_K(K));
+    SQ_TRY(check_band(K, d_m, d_u));
+    SQ_REQUIRE(M >= 0, SQ_ERR_SHAPE, "M=%d < 0", M);
+    if (M == 0) return SQ_OK;
+    SQ_REQUIRE(X && Xp, SQ_ERR_NULL, "sgat_transform: X and Xp are required");
+    SQ_REQUIRE(aligned16(X) && aligned16(Xp) && aligned16(P), SQ_ERR_ALIGN,
+               "sgat_transform: X, P and Xp must be 16-byte aligned");
+    return hip_status(sq::launch_transform(X, state, P, M, K, d_m, d_u, Xp, static_cast<hipStream_t>(stream)),
+                      "transform");
+}
+
+int sgat_quantize(const float* Xp, int32_t M, int32_t K, uint8_t* Aq, float* s, void* stream) {
+    SQ_TRY(check_K(K));
+    SQ_REQUIRE(M >= 0, SQ_ERR_SHAPE, "M=%d < 0", M);
+    if (M == 0) return SQ_OK;
+    SQ_REQUIRE(Xp && Aq && s, SQ_ERR_NULL, "sgat_quantize: Xp, Aq and s are required");
+    SQ_REQUIRE(aligned16(Xp) && aligned16(Aq) && aligned16(s), SQ_ERR_ALIGN,
+               "sgat_quantize: pointers must be 16-byte aligned");
+    return hip_status(sq::launch_quant_f32(Xp, M, K, Aq, s, static_cast<hipStream_t>(stream)), "quant_f32");
+}
+
+int sgat_quant_act(const uint16_t* X, const uint8_t* state, const float* P, int32_t M, int32_t K, int32_t d_m,
+                   int32_t d_u, const uint16_t* tac_M, const uint16_t* tac_d, int32_t g, uint8_t* Aq, float* s_a,
+                   void* ws, size_t ws_bytes, void* stream) {
+    SQ_TRY(check_K(K));
+    SQ_TRY(check_band(K, d_m, d_u));
+    SQ_REQUIRE(M >= 0, SQ_ERR_SHAPE, "M=%d < 0", M);
+    if (tac_M) {
+        SQ_REQUIRE(tac_d, SQ_ERR_NULL, "sgat_quant_act: tac_d is required with tac_M");
+        SQ_TRY(check_tac(K, g));
+    }
+    if (M == 0) return SQ_OK;
+    SQ_REQUIRE(X && Aq && s_a, SQ_ERR_NULL, "sgat_quant_act: X, Aq and s_a are required");
+    SQ_REQUIRE(aligned16(X) && aligned16(Aq) && aligned16(s_a) && aligned16(P) && aligned16(ws) &&
+                   aligned16(tac_M) && aligned16(tac_d),
+               SQ_ERR_ALIGN, "sgat_quant_act: pointers must be 16-byte aligned");
+    const size_t need = sq_quant_act_workspace_bytes(M, K, P != nullptr, tac_M != nullptr);
+    SQ_REQUIRE(ws_bytes >= need && (need == 0 || ws), SQ_ERR_WORKSPACE,
+               "sgat_quant_act: workspace %zu B < %zu B", ws_bytes, need);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    uint8_t* wsb = static_cast<uint8_t*>(ws);
+    const uint16_t* src = X;
+    if (tac_M) {
+        uint16_t* z = reinterpret_cast<uint16_t*>(wsb);
+        SQ_TRY(hip_status(sq::launch_tac(X, tac_M, tac_d, M, K, g, z, st), "tac"));
+        src = z;
+        wsb += round_up((size_t)M * K * sizeof(uint16_t));
+    }
+    if (!P) return hip_status(sq::launch_quant_f16(src, state, M, K, d_m, d_u, Aq, s_a, st), "quant_f16");
+    float* xp = reinterpret_cast<float*>(wsb);
+    SQ_TRY(hip_status(sq::launch_transform(src, state, P, M, K, d_m, d_u, xp, st), "transform"));
+    return hip_status(sq::launch_quant_f32(xp, M, K, Aq, s_a, st), "quant_f32");
+}
+
+int w4a4_gemm(const uint8_t* Aq, const float* s_a, const uint8_t* Wq, const float* s_w, int32_t M, int32_t N,
+              int32_t K, uint16_t* Y, int32_t* acc, void* ws, size_t ws_bytes, void* stream) {
+    SQ_TRY(check_K(K));
+    SQ_REQUIRE(M >= 0 && N >= 0, SQ_ERR_SHAPE, "M=%d N=%d: need >= 0", M, N);
+    SQ_REQUIRE(N % 8 == 0, SQ_ERR_SHAPE, "N=%d: need N %% 8 == 0", N);
+    if (M == 0 || N == 0) return SQ_OK;
+    SQ_REQUIRE(Aq && s_a && Wq && s_w && (Y || acc), SQ_ERR_NULL,
+               "w4a4_gemm: Aq, s_a, Wq, s_w and one of Y / acc are required");
+    SQ_REQUIRE(aligned16(Aq) && aligned16(s_a) && aligned16(Wq) && aligned16(s_w) && aligned16(Y) &&
+                   aligned16(acc) && aligned16(ws),
+               SQ_ERR_ALIGN, "w4a4_gemm: pointers must be 16-byte aligned");
+    const size_t need = sq_gemm_workspace_bytes(M, N, K);
+    SQ_REQUIRE(ws_bytes >= need && (need == 0 || ws), SQ_ERR_WORKSPACE, "w4a4_gemm: workspace %zu B < %zu B",
+               ws_bytes, need);
+    return hip_status(sq::launch_gemm(Aq, s_a, Wq, s_w, M, N, K, Y, acc, ws, static_cast<hipStream_t>(stream)),
+                      "gemm");
+}
+
+int tac_apply(const uint16_t* Z, const uint16_t* tac_M, const uint16_t* tac_d, int32_t M, int32_t C, int32_t g,
+              uint16_t* Z_out, void* stream) {
+    SQ_TRY(check_K(C));
+    SQ_TRY(check_tac(C, g));
+    SQ_REQUIRE(M >= 0, SQ_ERR_SHAPE, "M=%d < 0", M);
+    if (M == 0) return SQ_OK;
+    SQ_REQUIRE(Z && tac_M && tac_d && Z_out, SQ_ERR_NULL, "tac_apply: Z, tac_M, tac_d and Z_out are required");
+    SQ_REQUIRE(aligned16(Z) && aligned16(tac_M) && aligned16(tac_d) && aligned16(Z_out), SQ_ERR_ALIGN,
+               "tac_apply: pointers must be 16-byte aligned");
+    const uintptr_t a0 = (uintptr_t)Z, a1 = a0 + (size_t)M * C * 2;
+    const uintptr_t b0 = (uintptr_t)Z_out, b1 = b0 + (size_t)M * C * 2;
+    SQ_REQUIRE(a1 <= b0 || b1 <= a0, SQ_ERR_SHAPE, "tac_apply: Z_out overlaps Z");
+    return hip_status(sq::launch_tac(Z, tac_M, tac_d, M, C, g, Z_out, static_cast<hipStream_t>(stream)), "tac");
+}
+
+}  // extern "C"

@@ -1,0 +1,184 @@
+// Per-token symmetric int4 quantisation (Sec. 3.1, Eq. 2 with zero point 0 and
+// Eq. 5: per-token activations, per-output-channel weights):
+//   a = max_j |x_j|,  s = a / 7 (fp32, correctly rounded),
+//   q_j = clamp(rint(x_j / s), -8, 7)  (0 when s == 0),
+//   byte t = (q_{2t} & 15) | (q_{2t+1} & 15) << 4.
+//
+// One 256-thread workgroup per row: coalesced 16-byte loads held in registers,
+// a wavefront max reduction plus one LDS exchange across the four waves, then
+// quantise-and-pack straight from the registers.  Two input forms:
+//   quant_f16: fp16 rows already in the P basis, with the SGAT gate applied on
+//              the fly (state select, Eq. 9-11) -- the folded-basis hot path;
+//   quant_f32: fp32 rows from the dense transform (already gated).
+// Rows longer than NV*256 vectors are read twice instead of held.
+#include "sq_internal.hpp"
+
+namespace sq {
+namespace {
+
+constexpr int kThreads = 256;
+
+__device__ __forceinline__ float block_max(float v, float* red) {
+    v = wave_max(v);
+    const int w = threadIdx.x / kWave, l = threadIdx.x % kWave;
+    if (l == 0) red[w] = v;
+    __syncthreads();
+    float r = red[0];
+#pragma unroll
+    for (int i = 1; i < kThreads / kWave; ++i) r = fmaxf(r, red[i]);
+    return r;
+}
+
+__device__ __forceinline__ uint32_t pack8(const float* x, float s) {
+    uint32_t out = 0;
+    if (s != 0.0f) {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) out |= (uint32_t)(quant4(x[q], s) & 15) << (4 * q);
+    }
+    return out;
+}
+
+__device__ __forceinline__ void load_f16x8(const uint16_t* p, const uint8_t* state, int row, int c0, int K,
+                                           int dm, int du, float* x) {
+    const uint4 raw = *reinterpret_cast<const uint4*>(p);
+    const uint16_t* h = reinterpret_cast<const uint16_t*>(&raw);
+    const bool masked = state ? state[row] != 0 : false;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) x[q] = (!state || kept(c0 + q, K, dm, du, masked)) ? h2f(h[q]) : 0.0f;
+}
+
+// fp16 input; NV vectors of 8 per thread held in registers (NV == 0: reload).
+template <int NV>
+__global__ __launch_bounds__(kThreads) void quant_f16_kernel(const uint16_t* __restrict__ X,
+                                                             const uint8_t* __restrict__ state, int K, int dm,
+                                                             int du, uint8_t* __restrict__ Aq,
+                                                             float* __restrict__ s_out) {
+    __shared__ float red[kThreads / kWave];
+    const int row = blockIdx.x;
+    const int nvec = K / 8;
+    const uint16_t* xr = X + (size_t)row * K;
+    uint32_t* qr = reinterpret_cast<uint32_t*>(Aq + (size_t)row * (K / 2));
+    float amax = 0.0f;
+    if constexpr (NV > 0) {
+        float x[NV][8];
+#pragma unroll
+        for (int i = 0; i < NV; ++i) {
+            const int v = threadIdx.x + i * kThreads;
+            if (v < nvec) {
+                load_f16x8(xr + v * 8, state, row, v * 8, K, dm, du, x[i]);
+#pragma unroll
+                for (int q = 0; q < 8; ++q) amax = fmaxf(amax, fabsf(x[i][q]));
+            }
+        }
+        const float s = block_max(amax, red) / 7.0f;
+        if (threadIdx.x == 0) s_out[row] = s;
+#pragma unroll
+        for (int i = 0; i < NV; ++i) {
+            const int v = threadIdx.x + i * kThreads;
+            if (v < nvec) qr[v] = pack8(x[i], s);
+        }
+    } else {
+        float x[8];
+        for (int v = threadIdx.x; v < nvec; v += kThreads) {
+            load_f16x8(xr + v * 8, state, row, v * 8, K, dm, du, x);
+#pragma unroll
+            for (int q = 0; q < 8; ++q) amax = fmaxf(amax, fabsf(x[q]));
+        }
+        const float s = block_max(amax, red) / 7.0f;
+        if (threadIdx.x == 0) s_out[row] = s;
+        for (int v = threadIdx.x; v < nvec; v += kThreads) {
+            load_f16x8(xr + v * 8, state, row, v * 8, K, dm, du, x);
+            qr[v] = pack8(x, s);
+        }
+    }
+}
+
+// fp32 input (already gated); NV vectors of 8 floats per thread (NV == 0: reload).
+template <int NV>
+__global__ __launch_bounds__(kThreads) void quant_f32_kernel(const float* __restrict__ X, int K,
+                                                             uint8_t* __restrict__ Aq, float* __restrict__ s_out) {
+    __shared__ float red[kThreads / kWave];
+    const int row = blockIdx.x;
+    const int nvec = K / 8;
+    const float* xr = X + (size_t)row * K;
+    uint32_t* qr = reinterpret_cast<uint32_t*>(Aq + (size_t)row * (K / 2));
+    float amax = 0.0f;
+    auto ld = [&](int v, float* x) {
+        const float4 a = *reinterpret_cast<const float4*>(xr + v * 8);
+        const float4 b = *reinterpret_cast<const float4*>(xr + v * 8 + 4);
+        x[0] = a.x, x[1] = a.y, x[2] = a.z, x[3] = a.w, x[4] = b.x, x[5] = b.y, x[6] = b.z, x[7] = b.w;
+    };
+    if constexpr (NV > 0) {
+        float x[NV][8];
+#pragma unroll
+        for (int i = 0; i < NV; ++i) {
+            const int v = threadIdx.x + i * kThreads;
+            if (v < nvec) {
+                ld(v, x[i]);
+#pragma unroll
+                for (int q = 0; q < 8; ++q) amax = fmaxf(amax, fabsf(x[i][q]));
+            }
+        }
+        const float s = block_max(amax, red) / 7.0f;
+        if (threadIdx.x == 0) s_out[row] = s;
+#pragma unroll
+        for (int i = 0; i < NV; ++i) {
+            const int v = threadIdx.x + i * kThreads;
+            if (v < nvec) qr[v] = pack8(x[i], s);
+        }
+    } else {
+        float x[8];
+        for (int v = threadIdx.x; v < nvec; v += kThreads) {
+            ld(v, x);
+#pragma unroll
+            for (int q = 0; q < 8; ++q) amax = fmaxf(amax, fabsf(x[q]));
+        }
+        const float s = block_max(amax, red) / 7.0f;
+        if (threadIdx.x == 0) s_out[row] = s;
+        for (int v = threadIdx.x; v < nvec; v += kThreads) {
+            ld(v, x);
+            qr[v] = pack8(x, s);
+        }
+    }
+}
+
+template <template <int> class Launch, typename... A>
+hipError_t by_nv(int K, A... args) {
+    const int per = (K / 8 + kThreads - 1) / kThreads;   // vectors per thread
+    if (per <= 1) return Launch<1>::run(args...);
+    if (per <= 2) return Launch<2>::run(args...);
+    if (per <= 4) return Launch<4>::run(args...);
+    if (per <= 8) return Launch<8>::run(args...);
+    if (per <= 12) return Launch<12>::run(args...);
+    return Launch<0>::run(args...);
+}
+
+template <int NV>
+struct LaunchF16 {
+    static hipError_t run(const uint16_t* x, const uint8_t* state, int M, int K, int dm, int du, uint8_t* q,
+                          float* s, hipStream_t st) {
+        hipLaunchKernelGGL(quant_f16_kernel<NV>, dim3(M), dim3(kThreads), 0, st, x, state, K, dm, du, q, s);
+        return hipGetLastError();
+    }
+};
+
+template <int NV>
+struct LaunchF32 {
+    static hipError_t run(const float* x, int M, int K, uint8_t* q, float* s, hipStream_t st) {
+        hipLaunchKernelGGL(quant_f32_kernel<NV>, dim3(M), dim3(kThreads), 0, st, x, K, q, s);
+        return hipGetLastError();
+    }
+};
+
+}  // namespace
+
+hipError_t launch_quant_f16(const uint16_t* x, const uint8_t* state, int M, int K, int dm, int du, uint8_t* q,
+                            float* s, hipStream_t st) {
+    return by_nv<LaunchF16>(K, x, state, M, K, dm, du, q, s, st);
+}
+
+hipError_t launch_quant_f32(const float* x, int M, int K, uint8_t* q, float* s, hipStream_t st) {
+    return by_nv<LaunchF32>(K, x, M, K, q, s, st);
+}
+
+}  // namespace sq

@@ -1,0 +1,64 @@
+// Internal declarations shared by the HIP translation units of libstarquant.
+// gfx950 (CDNA4) only: wave64, int8 MFMA, 160 KB LDS per CU.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace sq {
+
+constexpr int kWave = 64;
+constexpr int kChunk = 256;          // transform k-chunk (fixed evaluation order)
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float h2f(uint16_t h) {
+    return (float)__builtin_bit_cast(_Float16, h);
+}
+// fp32 -> fp16, round to nearest even, from a materialised fp32 value.  The
+// empty asm keeps the compiler from folding the multiply or add that produced f
+// into a mixed-precision v_fma_mix*_f16, which would round the exact result once
+// to fp16 instead of rounding to fp32 first (and ignores -ffp-contract=off).
+__device__ __forceinline__ uint16_t f2h(float f) {
+    asm volatile("" : "+v"(f));
+    return __builtin_bit_cast(uint16_t, (_Float16)f);
+}
+
+// Column j of a transformed row is kept for this state (gate G_s, Eq. 9).
+__device__ __forceinline__ bool kept(int j, int K, int dm, int du, bool masked) {
+    const int m_lo = K - dm - du, u_lo = K - du;
+    return j < m_lo || (j < u_lo ? masked : !masked);
+}
+
+// Symmetric int4 code of x for scale s (s > 0): clamp(rint(x / s), -8, 7).
+// `/` is the correctly rounded fp32 divide (built without fast-math).
+__device__ __forceinline__ int quant4(float x, float s) {
+    float r = __builtin_rintf(x / s);
+    r = r < -8.0f ? -8.0f : (r > 7.0f ? 7.0f : r);
+    return (int)r;
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
+    return v;
+}
+
+// ---- launchers (each returns hipError_t of the launch) ----
+hipError_t launch_tac(const uint16_t* Z, const uint16_t* Mb, const uint16_t* d,
+                      int M, int C, int g, uint16_t* out, hipStream_t st);
+
+hipError_t launch_transform(const uint16_t* X, const uint8_t* state, const float* P,
+                            int M, int K, int dm, int du, float* Xp, hipStream_t st);
+
+hipError_t launch_quant_f32(const float* x, int M, int K, uint8_t* q, float* s, hipStream_t st);
+
+hipError_t launch_quant_f16(const uint16_t* x, const uint8_t* state, int M, int K, int dm, int du,
+                            uint8_t* q, float* s, hipStream_t st);
+
+size_t gemm_workspace_bytes(int M, int N, int K);
+hipError_t launch_gemm(const uint8_t* Aq, const float* s_a, const uint8_t* Wq, const float* s_w,
+                       int M, int N, int K, uint16_t* Y, int32_t* acc, void* ws, hipStream_t st);
+
+}  // namespace sq

@@ -1,0 +1,133 @@
+// Temporal Attention Compensation (Sec. 3.3, Eq. 17; App. C): per token and per
+// block b of g channels, z'_{bg+r} = fp16( sum_c M_b[r][c] z_{bg+c} + d_{bg+r} ),
+// each sum an fp32 fused multiply-add chain in ascending c from +0, bias last.
+//
+// The map is a batch of small [tokens x g] x [g x g] products, one per block.
+// It runs on the VALU because the fixed FMA order is part of the result; the
+// kernel is a register-tiled batched SGEMM: a workgroup owns TT tokens x CW
+// channels (CW = max(g, 64) so a span holds whole blocks), stages the span's
+// block matrices and the token tile through LDS as fp32, and each thread keeps
+// 8 tokens x 4 channels of accumulators.
+#include "sq_internal.hpp"
+
+namespace sq {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kTPT = 8;   // tokens per thread
+constexpr int kCPT = 4;   // channels per thread
+constexpr int kCC = 32;   // block-matrix columns staged per pass
+
+template <int CW>
+__global__ __launch_bounds__(kThreads) void tac_kernel(const uint16_t* __restrict__ Z,
+                                                       const uint16_t* __restrict__ Mb,
+                                                       const uint16_t* __restrict__ d, int M, int C,
+                                                       int g, uint16_t* __restrict__ out) {
+    constexpr int CG = CW / kCPT;            // channel groups per span
+    constexpr int TG = kThreads / CG;        // token groups
+    constexpr int TT = TG * kTPT;            // tokens per tile
+    constexpr int ZP = TT + 4;               // padded row of the transposed token tile
+    constexpr int MP = CW + 4;               // padded row of the transposed block tile
+    extern __shared__ float smem[];
+    float* zsT = smem;                       // [CW][ZP]   zsT[ch][tok]
+    float* msT = smem + CW * ZP;             // [kCC][MP]  msT[c-c0][ch] = M_{blk(ch)}[ch%g][c]
+
+    const int tid = threadIdx.x;
+    const int span0 = blockIdx.x * CW;       // first channel of this span
+    const int tok0 = blockIdx.y * TT;
+
+    // stage the token tile, 8 channels (16 B) per load
+    for (int e = tid; e < TT * (CW / 8); e += kThreads) {
+        const int t = e / (CW / 8), v = e % (CW / 8);
+        const int tok = tok0 + t;
+        uint4 raw = make_uint4(0, 0, 0, 0);
+        if (tok < M) raw = *reinterpret_cast<const uint4*>(Z + (size_t)tok * C + span0 + v * 8);
+        const uint16_t* h = reinterpret_cast<const uint16_t*>(&raw);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) zsT[(v * 8 + q) * ZP + t] = h2f(h[q]);
+    }
+    __syncthreads();
+
+    const int cg = tid % CG, tg = tid / CG;
+    const int ch0 = cg * kCPT;               // first of this thread's 4 channels (span-local)
+    float acc[kTPT][kCPT];
+#pragma unroll
+    for (int t = 0; t < kTPT; ++t)
+#pragma unroll
+        for (int q = 0; q < kCPT; ++q) acc[t][q] = 0.0f;
+
+    // the block matrices are staged kCC columns c at a time; every accumulator
+    // still sees c in ascending order
+    const int cc = g < kCC ? g : kCC;
+    for (int c0 = 0; c0 < g; c0 += cc) {
+        __syncthreads();
+        for (int e = tid; e < CW * cc; e += kThreads) {
+            const int ch = e / cc, c = e % cc;
+            // tac_M is [C/g][g][g] == [C][g]: row (span0 + ch), column c0 + c
+            msT[c * MP + ch] = h2f(Mb[(size_t)(span0 + ch) * g + c0 + c]);
+        }
+        __syncthreads();
+        if (g >= kCPT) {
+            const int base = (ch0 / g) * g;  // block start, shared by the 4 channels
+            for (int c = 0; c < cc; ++c) {
+                const float4 mv = *reinterpret_cast<const float4*>(msT + c * MP + ch0);
+                const float* zr = zsT + (base + c0 + c) * ZP + tg * kTPT;
+                const float4 z0 = *reinterpret_cast<const float4*>(zr);
+                const float4 z1 = *reinterpret_cast<const float4*>(zr + 4);
+                const float zv[8] = {z0.x, z0.y, z0.z, z0.w, z1.x, z1.y, z1.z, z1.w};
+                const float m[4] = {mv.x, mv.y, mv.z, mv.w};
+#pragma unroll
+                for (int t = 0; t < kTPT; ++t)
+#pragma unroll
+                    for (int q = 0; q < kCPT; ++q) acc[t][q] = __builtin_fmaf(m[q], zv[t], acc[t][q]);
+            }
+        } else {
+            // g in {1, 2}: the thread's channels lie in different blocks
+#pragma unroll
+            for (int q = 0; q < kCPT; ++q) {
+                const int ch = ch0 + q, base = (ch / g) * g;
+                for (int c = 0; c < cc; ++c) {
+                    const float m = msT[c * MP + ch];
+#pragma unroll
+                    for (int t = 0; t < kTPT; ++t)
+                        acc[t][q] = __builtin_fmaf(m, zsT[(base + c0 + c) * ZP + tg * kTPT + t], acc[t][q]);
+                }
+            }
+        }
+    }
+
+    float dv[kCPT];
+#pragma unroll
+    for (int q = 0; q < kCPT; ++q) dv[q] = h2f(d[span0 + ch0 + q]);
+#pragma unroll
+    for (int t = 0; t < kTPT; ++t) {
+        const int tok = tok0 + tg * kTPT + t;
+        if (tok >= M) break;
+        ushort4 o;
+        o.x = f2h(acc[t][0] + dv[0]);
+        o.y = f2h(acc[t][1] + dv[1]);
+        o.z = f2h(acc[t][2] + dv[2]);
+        o.w = f2h(acc[t][3] + dv[3]);
+        *reinterpret_cast<ushort4*>(out + (size_t)tok * C + span0 + ch0) = o;
+    }
+}
+
+template <int CW>
+hipError_t launch_cw(const uint16_t* Z, const uint16_t* Mb, const uint16_t* d, int M, int C, int g,
+                     uint16_t* out, hipStream_t st) {
+    constexpr int CG = CW / kCPT, TT = (kThreads / CG) * kTPT;
+    const size_t lds = sizeof(float) * ((size_t)CW * (TT + 4) + (size_t)kCC * (CW + 4));
+    dim3 grid(C / CW, (M + TT - 1) / TT);
+    hipLaunchKernelGGL(tac_kernel<CW>, grid, dim3(kThreads), lds, st, Z, Mb, d, M, C, g, out);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_tac(const uint16_t* Z, const uint16_t* Mb, const uint16_t* d, int M, int C, int g,
+                      uint16_t* out, hipStream_t st) {
+    if (g <= 64) return launch_cw<64>(Z, Mb, d, M, C, g, out, st);
+    return launch_cw<128>(Z, Mb, d, M, C, g, out, st);
+}
+
+}  // namespace sq

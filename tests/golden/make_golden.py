@@ -52,5 +52,5 @@ def tiny_case(name, seed, M, K, N, g, with_P=True):
 
 if __name__ == "__main__":
     tiny_case("tiny_sgat_tac", 31, 8, 64, 8, 16, with_P=True)
-    tiny_case("tiny_rtn", 32, 6, 64, 4, 0, with_P=False)
+    tiny_case("tiny_rtn", 32, 6, 64, 8, 0, with_P=False)
     print("ok")

@@ -1,0 +1,276 @@
+"""GPU parity: every entry point of libstarquant against the CPU oracle on the same
+seeded inputs.  Codes, scales, transformed rows and int32 accumulators must be
+bit-identical; fp16 outputs within 1e-3 rel / 1e-2 abs and in fact bit-identical."""
+import glob
+import json
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2606_04945_amd as sq
+import synth
+from oracle import oracle as O
+from gpu_util import assert_bits, assert_y, dev, host, pack_codes, say
+
+pytestmark = pytest.mark.gpu
+THREADS = min(16, os.cpu_count() or 1)
+
+
+def _x(M, K, seed, state=None, n_out=2):
+    st = state if state is not None else (np.random.default_rng(seed).random(M) < 0.5).astype(np.uint8)
+    rng = synth.rng_for(500 + seed, 0)
+    m_idx, u_idx = synth.outlier_channels(K, n_out, rng)
+    return synth.activations(M, K, st, m_idx, u_idx, rng), st
+
+
+# ------------------------------------------------------------------ quantiser
+
+@pytest.mark.parametrize("amax", [1.0, 7.0, 0.3, 1234.5, 3.0e-3, 65504.0])
+def test_quantiser_exhaustive_fp16(amax):
+    """Every finite fp16 value |v| <= amax in rows with absmax amax: GPU division,
+    rint and packing agree with the oracle bit for bit."""
+    h = np.arange(65536, dtype=np.uint16)
+    v = h.view(np.float16)
+    v = v[np.isfinite(v) & (np.abs(v.astype(np.float32)) <= amax)]
+    K = 4096
+    n = (len(v) + K - 2) // (K - 1)
+    rows = np.zeros((n, K), np.float16)
+    rows[:, 0] = np.float16(amax)
+    flat = np.zeros(n * (K - 1), np.float16)
+    flat[:len(v)] = v
+    rows[:, 1:] = flat.reshape(n, K - 1)
+    say(f"quantiser exhaustive amax={amax} rows={n}")
+    Aq, s = sq.sgat_quant_act(dev(rows), None, None, 0, 0)
+    ref_q, ref_s = O.quant_act(rows, None, None, 0, 0)
+    assert_bits(host(s), ref_s, "s_a")
+    assert_bits(host(Aq), ref_q, "Aq")
+    # the same rows through the fp32 entry point
+    Aq2, s2 = sq.sgat_quantize(dev(rows.astype(np.float32)))
+    assert_bits(host(s2), ref_s, "s (fp32 path)")
+    assert_bits(host(Aq2), ref_q, "Aq (fp32 path)")
+
+
+def test_zero_rows_and_tiny_scales():
+    K = 256
+    x = np.zeros((4, K), np.float32)
+    x[1, 3] = 1e-45                 # scale underflows to 0 -> all codes 0
+    x[2, :] = 1e-40                 # subnormal rows
+    x[3, 7] = -3e-39
+    Aq, s = sq.sgat_quantize(dev(x))
+    rq, rs, _ = O.quant_rows(x)
+    assert_bits(host(s), rs, "s")
+    assert_bits(host(Aq), rq, "Aq")
+
+
+# ------------------------------------------------------------------ folded basis (P = NULL)
+
+@pytest.mark.parametrize("M,K", [(1, 64), (3, 512), (77, 4096), (130, 3584), (64, 18944)])
+@pytest.mark.parametrize("layout", ["random", "all_masked", "none_masked", "alternating"])
+def test_quant_act_folded(M, K, layout):
+    st = None if layout == "random" else synth.state_edge(M, layout)
+    X, st = _x(M, K, 1, st)
+    dm, du = synth.default_band(K)
+    say(f"quant_act folded M={M} K={K} {layout}")
+    Aq, s = sq.sgat_quant_act(dev(X), dev(st), None, dm, du)
+    ref_q, ref_s = O.quant_act(X, st, None, dm, du)
+    assert_bits(host(s), ref_s, "s_a")
+    assert_bits(host(Aq), ref_q, "Aq")
+
+
+def test_quant_act_folded_no_gate_and_custom_bands():
+    X, st = _x(50, 512, 2)
+    for dm, du in [(0, 0), (16, 0), (0, 48), (100, 200)]:
+        Aq, s = sq.sgat_quant_act(dev(X), dev(st), None, dm, du)
+        ref_q, ref_s = O.quant_act(X, st, None, dm, du)
+        assert_bits(host(s), ref_s, f"s_a bands {dm},{du}")
+        assert_bits(host(Aq), ref_q, f"Aq bands {dm},{du}")
+
+
+# ------------------------------------------------------------------ dense transform
+
+@pytest.mark.parametrize("M,K", [(1, 64), (5, 192), (130, 512), (257, 1024), (33, 4096)])
+def test_transform_bit_exact(M, K):
+    X, st = _x(M, K, 3)
+    P = synth.orthogonal(K, synth.rng_for(600, K))
+    dm, du = synth.default_band(K)
+    say(f"transform M={M} K={K}")
+    xp = sq.sgat_transform(dev(X), dev(st), dev(P), dm, du)
+    ref = O.transform(X, st, P, dm, du, threads=THREADS)
+    assert_bits(host(xp), ref, "x'")
+    xp0 = sq.sgat_transform(dev(X), None, dev(P))
+    assert_bits(host(xp0), O.transform(X, None, P, 0, 0, threads=THREADS), "x' ungated")
+
+
+def test_transform_identity_basis_equals_folded():
+    X, st = _x(40, 512, 4)
+    dm, du = synth.default_band(512)
+    a = sq.sgat_transform(dev(X), dev(st), dev(np.eye(512, dtype=np.float32)), dm, du)
+    b = sq.sgat_transform(dev(X), dev(st), None, dm, du)
+    assert_bits(host(a), host(b), "P = I vs P = NULL")
+    assert_bits(host(b), O.transform(X, st, None, dm, du), "P = NULL")
+
+
+@pytest.mark.parametrize("M,K", [(7, 256), (200, 1024), (129, 4096)])
+def test_quant_act_dense(M, K):
+    X, st = _x(M, K, 5)
+    P = synth.orthogonal(K, synth.rng_for(601, K))
+    dm, du = synth.default_band(K)
+    say(f"quant_act dense M={M} K={K}")
+    Aq, s = sq.sgat_quant_act(dev(X), dev(st), dev(P), dm, du)
+    ref_q, ref_s = O.quant_act(X, st, P, dm, du, threads=THREADS)
+    assert_bits(host(s), ref_s, "s_a")
+    assert_bits(host(Aq), ref_q, "Aq")
+
+
+@pytest.mark.parametrize("N,K,withP", [(24, 512, True), (200, 1024, True), (64, 4096, False), (8, 64, True)])
+def test_prepare_weights(N, K, withP):
+    W = synth.weights(N, K, synth.rng_for(602, N, K))
+    P = synth.orthogonal(K, synth.rng_for(603, K)) if withP else None
+    say(f"prepare_weights N={N} K={K} P={withP}")
+    Wq, s_w = sq.sgat_prepare_weights(dev(W), dev(P) if withP else None)
+    if withP:
+        rq, rs = O.prepare_weights(W, P, threads=THREADS)
+    else:
+        rq, rs = O.quant_act(W, None, None, 0, 0)
+    assert_bits(host(s_w), rs, "s_w")
+    assert_bits(host(Wq), rq, "Wq")
+
+
+# ------------------------------------------------------------------ GEMM
+
+def _codes(M, K, seed, lo=-7, hi=7):
+    q = np.random.default_rng(seed).integers(lo, hi + 1, (M, K))
+    return pack_codes(q)
+
+
+@pytest.mark.parametrize("M,N,K", [(1, 8, 64), (16, 4096, 4096), (77, 200, 192), (128, 256, 512),
+                                   (300, 136, 4096), (1024, 1024, 1024), (513, 4104, 3584), (64, 512, 18944)])
+def test_gemm_bit_exact(M, N, K):
+    Aq = _codes(M, K, 1)
+    Wq = _codes(N, K, 2)
+    rng = np.random.default_rng(3)
+    s_a = rng.uniform(0.05, 3, M).astype(np.float32)
+    s_w = rng.uniform(1e-4, 5e-3, N).astype(np.float32)
+    say(f"gemm M={M} N={N} K={K} ws={sq.gemm_workspace_bytes(M, N, K)}")
+    Y, acc = sq.w4a4_gemm(dev(Aq), dev(s_a), dev(Wq), dev(s_w), want_acc=True)
+    Y, acc = host(Y), host(acc)
+    rows = np.arange(M) if M * N * K <= 3e9 else np.unique(np.r_[0, M - 1, np.random.default_rng(4).choice(M, 24)])
+    rY, racc = O.gemm(Aq[rows], s_a[rows], Wq, s_w, threads=THREADS)
+    assert_bits(acc[rows], racc, "acc")
+    assert_y(Y[rows], rY)
+
+
+def test_gemm_extreme_codes():
+    """All codes -8 or +7 at the largest config K: the scaled int8 sums stay exact."""
+    K, M, N = 18944, 8, 16
+    q = np.random.default_rng(5).choice([-8, 7], (M, K))
+    w = np.random.default_rng(6).choice([-8, 7], (N, K))
+    Aq, Wq = pack_codes(q), pack_codes(w)
+    s_a = np.ones(M, np.float32)
+    s_w = np.full(N, 1e-3, np.float32)
+    Y, acc = sq.w4a4_gemm(dev(Aq), dev(s_a), dev(Wq), dev(s_w), want_acc=True)
+    assert_bits(host(acc), (q @ w.T).astype(np.int32), "acc")
+    rY, _ = O.gemm(Aq, s_a, Wq, s_w)
+    assert_y(host(Y), rY)
+
+
+def test_gemm_split_and_unsplit_agree():
+    """Rows computed through the split-K path (short M) equal the same rows inside a
+    tall M that takes the single-pass path."""
+    K, N = 4096, 4096
+    Aq = _codes(2048, K, 7)
+    Wq = _codes(N, K, 8)
+    s_a = np.random.default_rng(9).uniform(0.1, 2, 2048).astype(np.float32)
+    s_w = np.random.default_rng(10).uniform(1e-3, 2e-3, N).astype(np.float32)
+    assert sq.gemm_workspace_bytes(16, N, K) > 0 and sq.gemm_workspace_bytes(2048, N, K) == 0
+    big = host(sq.w4a4_gemm(dev(Aq), dev(s_a), dev(Wq), dev(s_w)))
+    small = host(sq.w4a4_gemm(dev(Aq[:16]), dev(s_a[:16]), dev(Wq), dev(s_w)))
+    assert_bits(small, big[:16], "split vs unsplit")
+
+
+# ------------------------------------------------------------------ TAC
+
+@pytest.mark.parametrize("g", [1, 2, 4, 8, 16, 32, 64, 128])
+@pytest.mark.parametrize("M,C", [(1, 128), (100, 512), (257, 4096)])
+def test_tac_bit_exact(g, M, C):
+    Z = (np.random.default_rng(g + M).standard_normal((M, C)) * 2).astype(np.float16)
+    Mb, d = synth.tac_params(C, g, synth.rng_for(700, g, C))
+    say(f"tac g={g} M={M} C={C}")
+    out = host(sq.tac_apply(dev(Z), dev(Mb), dev(d), g))
+    assert_bits(out, O.tac(Z, Mb, d, g, threads=THREADS), "tac")
+
+
+@pytest.mark.parametrize("g", [16, 128])
+def test_tac_identity_is_a_no_op(g):
+    Z = (np.random.default_rng(1).standard_normal((64, 4096)) * 4).astype(np.float16)
+    Mb, d = synth.tac_params(4096, g, None, identity=True)
+    out = host(sq.tac_apply(dev(Z), dev(Mb), dev(d), g))
+    same = (out.view(np.uint16) == Z.view(np.uint16)) | ((out == 0) & (Z == 0))
+    assert same.all()
+
+
+@pytest.mark.parametrize("withP", [False, True])
+@pytest.mark.parametrize("g", [16, 128])
+def test_quant_act_with_tac(withP, g):
+    M, K = 150, 1024
+    X, st = _x(M, K, 6)
+    Mb, d = synth.tac_params(K, g, synth.rng_for(701, g))
+    P = synth.orthogonal(K, synth.rng_for(702, K)) if withP else None
+    dm, du = synth.default_band(K)
+    say(f"quant_act + tac g={g} P={withP}")
+    Aq, s = sq.sgat_quant_act(dev(X), dev(st), dev(P) if withP else None, dm, du, dev(Mb), dev(d), g)
+    rq, rs = O.quant_act(X, st, P, dm, du, Mb, d, g, threads=THREADS)
+    assert_bits(host(s), rs, "s_a")
+    assert_bits(host(Aq), rq, "Aq")
+
+
+# ------------------------------------------------------------------ end to end
+
+def test_config0_end_to_end():
+    """The small configuration in full: 128 tokens, K = N = 512, dense P."""
+    st = synth.config_state(0)
+    t = synth.site_tensors(0, 0, st)
+    say("config 0 end to end")
+    Xd, Pd = dev(t.X), dev(t.P)
+    Wq, s_w = sq.sgat_prepare_weights(dev(t.W), Pd)
+    Aq, s_a = sq.sgat_quant_act(Xd, dev(st), Pd, t.dm, t.du)
+    Y, acc = sq.w4a4_gemm(Aq, s_a, Wq, s_w, want_acc=True)
+    ref = O.sgat_linear(t.X, st, t.P, t.W, t.dm, t.du, threads=THREADS)
+    for k, v in dict(Aq=Aq, s_a=s_a, Wq=Wq, s_w=s_w, acc=acc).items():
+        assert_bits(host(v), ref[k], k)
+    assert_y(host(Y), ref["Y"])
+    # determinism: a second run is bitwise identical
+    Y2 = sq.w4a4_gemm(*sq.sgat_quant_act(Xd, dev(st), Pd, t.dm, t.du), Wq, s_w)
+    assert_bits(host(Y2), host(Y), "repeat")
+
+
+GOLD = sorted(glob.glob(os.path.join(os.path.dirname(__file__), "golden", "*.json")))
+
+
+@pytest.mark.parametrize("path", GOLD, ids=[os.path.basename(p) for p in GOLD])
+def test_golden_fixtures(path):
+    from test_oracle_golden import load
+    d, ins, outs = load(path)
+    g = d["g"]
+    say(f"golden {os.path.basename(path)}")
+    P = dev(ins["P"]) if d["has_P"] else None
+    Aq, s_a = sq.sgat_quant_act(dev(ins["X"]), dev(ins["state"]), P, d["dm"], d["du"],
+                                dev(ins["tac_M"]) if g else None, dev(ins["tac_d"]) if g else None, g)
+    Wq, s_w = sq.sgat_prepare_weights(dev(ins["W"]), P)
+    Y, acc = sq.w4a4_gemm(Aq, s_a, Wq, s_w, want_acc=True)
+    for k, v in dict(Aq=Aq, s_a=s_a, Wq=Wq, s_w=s_w, acc=acc, Y=Y).items():
+        assert_bits(host(v), outs[k], k)
+
+
+def test_empty_inputs_leave_outputs_untouched():
+    Aq = torch.full((0, 32), 7, dtype=torch.uint8, device="cuda")
+    s = torch.empty((0,), dtype=torch.float32, device="cuda")
+    sq.sgat_quant_act(torch.empty((0, 64), dtype=torch.float16, device="cuda"), None, None, 2, 2, Aq=Aq, s_a=s)
+    Y = torch.full((4, 16), 3.0, dtype=torch.float16, device="cuda")
+    sq.w4a4_gemm(torch.empty((4, 32), dtype=torch.uint8, device="cuda")[:0], s,
+                 torch.zeros((16, 32), dtype=torch.uint8, device="cuda"),
+                 torch.ones(16, dtype=torch.float32, device="cuda"), Y=Y[:0])
+    torch.cuda.synchronize()
+    assert (host(Y) == 3.0).all()
