@@ -37,6 +37,23 @@ PEAK_INT8_TOPS = 5000.0           # dense int8 MFMA, TOP/s
 PEAK_FP32_VALU_TFLOPS = 78.6
 
 
+def recorded_traffic(kernel: str):
+    """HBM bytes per launch of `kernel` from the committed counter record, or None
+    when the kernel's sources have changed since the counters were taken."""
+    import hashlib
+    try:
+        with open(os.path.join(ROOT, "profiles", "counters.json")) as f:
+            rec = json.load(f)[kernel]
+    except (OSError, KeyError, ValueError):
+        return None
+    for name, h in rec["sources_sha256_16"].items():
+        path = os.path.join(ROOT, "paper_2606_04945_amd", "csrc", name)
+        with open(path, "rb") as f:
+            if hashlib.sha256(f.read()).hexdigest()[:16] != h:
+                return None
+    return rec["traffic_bytes_per_launch_step_avg"]
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -45,6 +62,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=int, default=384, help="tokens in the oracle timing sample")
     ap.add_argument("--only", choices=["dense", "folded", "both"], default="both")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="also run a plain 1 GiB device copy (reference for HBM byte counters)")
     return ap.parse_args()
 
 
@@ -177,6 +196,16 @@ def main():
                              quant_act_ms=qa_ms / args.steps,
                              per_site_gemm_ms={n: timer.ms("gemm/" + n)[0] / args.steps for n in ops_gemm})
 
+    if args.calibrate_copy:
+        # a plain device-to-device copy of known size: its FETCH_SIZE / WRITE_SIZE
+        # readings scale the counters of the kernels above to bytes
+        src = torch.empty(1 << 29, dtype=torch.float16, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
     # ---------------------------------------------------------------- CPU baseline
     cpu = None
     if not args.no_cpu_baseline:
@@ -223,7 +252,7 @@ def main():
     if dense:
         ach = dense["transform_tflops"]
         res["roofline"] = {"bound": "alu", "achieved": ach, "peak": PEAK_FP32_VALU_TFLOPS, "unit": "TFLOP/s",
-                           "frac": ach / PEAK_FP32_VALU_TFLOPS, "traffic": None,
+                           "frac": ach / PEAK_FP32_VALU_TFLOPS, "traffic": recorded_traffic("transform"),
                            "kernel": "transform (dense fp32 x P, fixed order)"}
         res["breakdown_ms"] = {k: dense[k] for k in ("transform_ms", "gemm_ms", "tac_ms", "quant_ms")}
         res["gemm"] = {"tops": dense["gemm_tops"], "frac_int8_peak": dense["gemm_tops"] / PEAK_INT8_TOPS}
