@@ -1,0 +1,148 @@
+"""GPU parity at the full workload sizes, in the launch configurations the benchmark
+uses: every linear of the LLaDA- and Dream-shaped layer sets, the TAC + O-projection
+workload (g = 128, 16384 tokens), and the denoising-step sweep over token counts.
+
+The GPU runs each whole layer; the oracle recomputes sampled token rows and sampled
+output channels one by one (rows are independent), and those must match bit for
+bit.  Properties that hold at any size are checked on every row."""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2606_04945_amd as sq
+import synth
+from oracle import oracle as O
+from gpu_util import assert_bits, assert_y, dev, host, say
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+THREADS = min(16, os.cpu_count() or 1)
+
+
+def sample_rows(state, n, seed):
+    """First, last, first masked, first unmasked, and random rows."""
+    M = len(state)
+    rng = np.random.default_rng(seed)
+    pick = [0, M - 1]
+    for s in (0, 1):
+        idx = np.nonzero(state == s)[0]
+        if len(idx):
+            pick += [int(idx[0]), int(idx[-1])]
+    pick += list(rng.choice(M, size=min(n, M), replace=False))
+    return np.unique(np.array(pick))
+
+
+def check_codes_all_rows(Aq, s_a):
+    """Every row with a non-zero scale has codes in [-7, 7] and max |code| = 7."""
+    a = host(Aq)
+    lo = (a & 15).astype(np.int8)
+    hi = (a >> 4).astype(np.int8)
+    lo = np.where(lo >= 8, lo - 16, lo)
+    hi = np.where(hi >= 8, hi - 16, hi)
+    mx = np.maximum(np.abs(lo).max(axis=1), np.abs(hi).max(axis=1))
+    mn = np.minimum(lo.min(axis=1), hi.min(axis=1))
+    s = host(s_a)
+    assert (mn >= -7).all()
+    assert (mx[s > 0] == 7).all() and (mx[s == 0] == 0).all()
+
+
+def run_site(cid, si, state, *, g=None, folded=False, n_rows=6, n_cols=8, tac_identity=False):
+    t = synth.site_tensors(cid, si, state, tac_identity=tac_identity, g=g, with_P=not folded)
+    K, N, M = t.site.K, t.site.N, len(state)
+    say(f"config {cid} site {t.site.name} M={M} K={K} N={N} tac={t.g} folded={folded}")
+    Xd, Wd = dev(t.X), dev(t.W)
+    Pd = None if folded else dev(t.P)
+    tM = dev(t.tac_M) if t.tac_M is not None else None
+    td = dev(t.tac_d) if t.tac_d is not None else None
+    Wq, s_w = sq.sgat_prepare_weights(Wd, Pd)
+    Aq, s_a = sq.sgat_quant_act(Xd, dev(state), Pd, t.dm, t.du, tM, td, t.g)
+    Y, acc = sq.w4a4_gemm(Aq, s_a, Wq, s_w, want_acc=True)
+    torch.cuda.synchronize()
+    rows = sample_rows(state, n_rows, 1000 + si)
+    cols = np.unique(np.r_[0, N - 1, np.random.default_rng(2000 + si).choice(N, n_cols, replace=False)])
+    P = None if folded else t.P
+    rq, rs = O.quant_act(t.X[rows], state[rows], P, t.dm, t.du, t.tac_M, t.tac_d, t.g, threads=THREADS)
+    if folded:
+        wq, ws = O.quant_act(t.W[cols], None, None, 0, 0)
+    else:
+        wq, ws = O.prepare_weights(t.W[cols], P, threads=THREADS)
+    ry, racc = O.gemm(rq, rs, wq, ws)
+    assert_bits(host(s_a)[rows], rs, "s_a rows")
+    assert_bits(host(Aq)[rows], rq, "Aq rows")
+    assert_bits(host(s_w)[cols], ws, "s_w rows")
+    assert_bits(host(Wq)[cols], wq, "Wq rows")
+    ri = torch.from_numpy(rows).cuda()
+    ci = torch.from_numpy(cols).cuda()
+    assert_bits(host(acc.index_select(0, ri).index_select(1, ci)), racc, "acc samples")
+    assert_y(host(Y.index_select(0, ri).index_select(1, ci)), ry)
+    check_codes_all_rows(Aq, s_a)
+    check_codes_all_rows(Wq, s_w)
+    del Wq, s_w, Y, acc, Xd, Wd, Pd
+    return dict(Aq=Aq, s_a=s_a)
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("si", range(4), ids=[s.name for s in synth.CONFIGS[1].sites])
+@pytest.mark.parametrize("folded", [False, True], ids=["denseP", "foldedP"])
+def test_llada_layer_set(si, folded):
+    run_site(1, si, synth.config_state(1), folded=folded)
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("si", range(4), ids=[s.name for s in synth.CONFIGS[2].sites])
+def test_dream_layer_set(si):
+    run_site(2, si, synth.config_state(2), n_rows=4, n_cols=6)
+
+
+@pytest.mark.timeout(600)
+def test_dream_layer_set_folded_gate_up():
+    run_site(2, 2, synth.config_state(2), folded=True)
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("folded", [True, False], ids=["foldedP", "denseP"])
+def test_tac_oproj_g128(folded):
+    """TAC (32 blocks of 128) on 8 x 2048 tokens, then SGAT quantise, then the
+    4096 -> 4096 GEMM."""
+    run_site(3, 0, synth.config_state(3), folded=folded)
+
+
+@pytest.mark.timeout(600)
+def test_tac_oproj_identity_blocks_is_plain_sgat():
+    """With identity blocks and zero bias the TAC + O-projection equals the same layer
+    without TAC, bit for bit."""
+    st = synth.config_state(3)
+    t = synth.site_tensors(3, 0, st, tac_identity=True, with_W=False, with_P=False)
+    Xd = dev(t.X)
+    a = sq.sgat_quant_act(Xd, dev(st), None, t.dm, t.du, dev(t.tac_M), dev(t.tac_d), t.g)
+    b = sq.sgat_quant_act(Xd, dev(st), None, t.dm, t.du)
+    assert_bits(host(a[0]), host(b[0]), "Aq")
+    assert_bits(host(a[1]), host(b[1]), "s_a")
+
+
+SWEEP = [16, 32, 64, 256, 1024, 4096, 16384]
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("M", SWEEP)
+def test_denoise_sweep_token_counts(M):
+    """Denoising-step sweep: each token count through every linear of the LLaDA set
+    (folded P, the per-step GEMM path), at step t = 32, sampled rows vs the oracle."""
+    st = synth.config_state(4, M=M, t=32)
+    for si in range(4):
+        run_site(4, si, st, folded=True, n_rows=4, n_cols=4)
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("layout", ["t0", "t64", "all_masked", "none_masked", "alternating"])
+def test_denoise_sweep_layouts(layout):
+    """Step layouts (t = 0, all generation tokens masked; t = 64, none) and the edge
+    layouts at 1024 tokens through the dense-P QKV and down linears."""
+    M = 1024
+    if layout in ("t0", "t64"):
+        st = synth.config_state(4, M=M, t=int(layout[1:]))
+    else:
+        st = synth.state_edge(M, layout)
+    for si in (0, 3):
+        run_site(4, si, st, n_rows=4, n_cols=4)
