@@ -12,21 +12,21 @@
 // permutation is applied to A and W, and an integer sum does not depend on its
 // order, so the result is the plain dot product.
 //
-// Tiling: a 256-thread workgroup owns a 128 x 128 output tile; its four waves
-// each own 64 x 64 (4 x 4 MFMA tiles).  Packed int4 tiles (128 rows x 64 bytes
-// per 128-k step) are staged through double-buffered LDS with the next tile
-// prefetched into registers during compute, and unpacked to int8 operands as
-// they leave LDS.  Short M splits K across workgroups; the int32 partial sums
-// are then added exactly by a small epilogue kernel.
+// Tiling (template): WM x WN waves, each owning TM x TN MFMA tiles of 16 x 16, so
+// a workgroup owns (16 WM TM) x (16 WN TN) outputs.  Per k step (128 codes) the
+// workgroup reads 64 packed bytes of every row of both operands with raw buffer
+// loads (out-of-range reads return 0, so no predicates in the loop), prefetching
+// the next step into registers during compute, and stages them through
+// double-buffered LDS.  UNPACK selects where nibbles become int8: when staged
+// (LDS holds int8 rows, each tile unpacked once per workgroup) or as fragments
+// leave LDS (LDS holds packed rows, each wave unpacks what it reads).  LDS rows
+// are XOR-swizzled by 16-byte chunk so the row-wise fragment reads and the
+// segment-wise stores are free of bank conflicts.  Short M splits K across
+// workgroups; the int32 partial sums are then added exactly by a small kernel.
 #include "sq_internal.hpp"
 
 namespace sq {
 namespace {
-
-constexpr int kThreads = 256;
-constexpr int kBM = 128, kBN = 128;
-constexpr int kBKB = 64;                  // packed bytes per row per k step (128 codes)
-constexpr int kRowB = kBKB + 16;          // padded LDS row
 
 __device__ __forceinline__ v4i unpack_op(uint32_t w0, uint32_t w1) {
     v4i r;
@@ -45,90 +45,164 @@ __device__ __forceinline__ void store_out(int row, int col, int v, const float* 
     if (Y) Y[o] = f2h(((float)v * s_a[row]) * s_w[col]);
 }
 
+constexpr int kKB = 64;                              // packed bytes per row per k step (128 codes)
+
+template <int WM, int WN, int TM, int TN, bool UNPACK>
+struct GemmCfg {
+    static constexpr int NT = 64 * WM * WN;          // threads
+    static constexpr int BM = 16 * WM * TM;          // rows of A per tile
+    static constexpr int BN = 16 * WN * TN;          // rows of W (output columns) per tile
+    static constexpr int SEG = kKB / 16;             // 16-byte packed segments per row per k step
+    static constexpr int AV = BM * SEG / NT;         // segments per thread
+    static constexpr int BV = BN * SEG / NT;
+    static constexpr int RB = UNPACK ? 2 * kKB : kKB;   // LDS row bytes per k step
+    static constexpr int CH = RB / 16;                  // 16-byte chunks per LDS row
+    // chunk c of LDS row r sits at chunk (c ^ swz(r)), swz(r) = index of the
+    // 128-byte line the row starts in, modulo the chunks per row: any eight
+    // consecutive rows then touch distinct 16-byte bank groups
+    static __device__ __forceinline__ int chunk(int r, int c) { return c ^ ((r / (128 / RB)) & (CH - 1)); }
+};
+
+// Raw buffer resource over [base, base + bytes): loads outside it return 0, which
+// is how rows past M (or N) and the unused half of a last k step read as zeros.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+
+constexpr uint32_t kOOB = 0x80000000u;   // an offset past any buffer this kernel builds
+
 // SPLIT == false: full K, fused epilogue.  SPLIT == true: K range of blockIdx.z,
 // raw int32 sums to part[z][M][N].
-template <bool SPLIT>
-__global__ __launch_bounds__(kThreads) void gemm_kernel(const uint8_t* __restrict__ Aq,
-                                                        const float* __restrict__ s_a,
-                                                        const uint8_t* __restrict__ Wq,
-                                                        const float* __restrict__ s_w, int M, int N, int K,
-                                                        int ktiles_per_split, uint16_t* __restrict__ Y,
-                                                        int32_t* __restrict__ acc_out,
-                                                        int32_t* __restrict__ part) {
-    __shared__ __attribute__((aligned(16))) uint8_t sA[2][kBM * kRowB];
-    __shared__ __attribute__((aligned(16))) uint8_t sB[2][kBN * kRowB];
+template <int WM, int WN, int TM, int TN, bool UNPACK, bool SPLIT>
+__global__ __launch_bounds__(64 * WM * WN) void gemm_kernel(const uint8_t* __restrict__ Aq,
+                                                           const float* __restrict__ s_a,
+                                                           const uint8_t* __restrict__ Wq,
+                                                           const float* __restrict__ s_w, int M, int N, int K,
+                                                           int ksteps_per_split, uint16_t* __restrict__ Y,
+                                                           int32_t* __restrict__ acc_out,
+                                                           int32_t* __restrict__ part) {
+    using C = GemmCfg<WM, WN, TM, TN, UNPACK>;
+    static_assert(C::BM * C::SEG % C::NT == 0 && C::BN * C::SEG % C::NT == 0, "tile loads must divide evenly");
+    __shared__ __attribute__((aligned(16))) uint8_t sA[2][C::BM * C::RB];
+    __shared__ __attribute__((aligned(16))) uint8_t sB[2][C::BN * C::RB];
 
     const int tid = threadIdx.x;
     const int lane = tid % kWave, wave = tid / kWave;
-    const int wm = wave / 2, wn = wave % 2;
-    const int row0 = blockIdx.y * kBM, col0 = blockIdx.x * kBN;
-    const size_t ldb = (size_t)K / 2;         // bytes per packed row
+    const int wm = wave / WN, wn = wave % WN;
+    const int row0 = blockIdx.y * C::BM, col0 = blockIdx.x * C::BN;
+    const uint32_t ldb = (uint32_t)K / 2;                // bytes per packed row
 
-    const int nk_total = (K + 2 * kBKB - 1) / (2 * kBKB);   // last step may be half full
-    const int kt0 = SPLIT ? blockIdx.z * ktiles_per_split : 0;
-    const int kt1 = SPLIT ? min(nk_total, kt0 + ktiles_per_split) : nk_total;
+    const int nk_total = (int)((ldb + kKB - 1) / kKB);   // the last step may be half empty
+    const int nk_full = (int)(ldb / kKB);                // steps with every byte in range
+    const int kt0 = SPLIT ? blockIdx.z * ksteps_per_split : 0;
+    const int kt1 = SPLIT ? min(nk_total, kt0 + ksteps_per_split) : nk_total;
 
-    // global -> register staging: each thread moves 2 x 16 B of A and of W per k step
-    uint4 ra[2], rb[2];
-    auto load = [&](int kt) {
+    const __amdgpu_buffer_rsrc_t rA = make_rsrc(Aq, (uint32_t)M * ldb);
+    const __amdgpu_buffer_rsrc_t rW = make_rsrc(Wq, (uint32_t)N * ldb);
+    // this thread's 16-byte segments: tile row e / SEG, segment e % SEG
+    uint32_t oa[C::AV], ow[C::BV];
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            const int e = tid + i * kThreads;
-            const int r = e / 4, seg = e % 4;
-            const size_t off = (size_t)kt * kBKB + seg * 16;
-            ra[i] = make_uint4(0, 0, 0, 0);
-            rb[i] = make_uint4(0, 0, 0, 0);
-            if (off < ldb) {                  // K % 64 == 0: a 16-byte segment is all in or all out
-                if (row0 + r < M) ra[i] = *reinterpret_cast<const uint4*>(Aq + (size_t)(row0 + r) * ldb + off);
-                if (col0 + r < N) rb[i] = *reinterpret_cast<const uint4*>(Wq + (size_t)(col0 + r) * ldb + off);
-            }
+    for (int i = 0; i < C::AV; ++i) {
+        const int e = tid + i * C::NT, r = e / C::SEG;
+        oa[i] = row0 + r < M ? (uint32_t)(row0 + r) * ldb + (e % C::SEG) * 16 : kOOB;
+    }
+#pragma unroll
+    for (int i = 0; i < C::BV; ++i) {
+        const int e = tid + i * C::NT, r = e / C::SEG;
+        ow[i] = col0 + r < N ? (uint32_t)(col0 + r) * ldb + (e % C::SEG) * 16 : kOOB;
+    }
+
+    v4i ra[C::AV], rb[C::BV];
+    auto load = [&](int kt, bool tail) {
+        const uint32_t ko = (uint32_t)kt * kKB;
+#pragma unroll
+        for (int i = 0; i < C::AV; ++i) {
+            const int seg = ((tid + i * C::NT) % C::SEG) * 16;
+            const uint32_t o = (tail && ko + seg >= ldb) ? kOOB : oa[i] + ko;
+            ra[i] = __builtin_amdgcn_raw_buffer_load_b128(rA, (int)o, 0, 0);
+        }
+#pragma unroll
+        for (int i = 0; i < C::BV; ++i) {
+            const int seg = ((tid + i * C::NT) % C::SEG) * 16;
+            const uint32_t o = (tail && ko + seg >= ldb) ? kOOB : ow[i] + ko;
+            rb[i] = __builtin_amdgcn_raw_buffer_load_b128(rW, (int)o, 0, 0);
+        }
+    };
+    auto load_step = [&](int kt) {
+        if (kt < nk_full)
+            load(kt, false);
+        else
+            load(kt, true);
+    };
+    // packed segment s of row r -> LDS; with UNPACK its two int8 halves (MFMA steps
+    // h = 0, 1 of k group s) go to chunks 2s and 2s + 1
+    auto put = [&](uint8_t* base, int e, const v4i& v) {
+        const int r = e / C::SEG, s = e % C::SEG;
+        uint8_t* row = base + r * C::RB;
+        if (UNPACK) {
+            *reinterpret_cast<v4i*>(row + C::chunk(r, 2 * s) * 16) = unpack_op(v[0], v[1]);
+            *reinterpret_cast<v4i*>(row + C::chunk(r, 2 * s + 1) * 16) = unpack_op(v[2], v[3]);
+        } else {
+            *reinterpret_cast<v4i*>(row + C::chunk(r, s) * 16) = v;
         }
     };
     auto stash = [&](int buf) {
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            const int e = tid + i * kThreads;
-            const int r = e / 4, seg = e % 4;
-            *reinterpret_cast<uint4*>(&sA[buf][r * kRowB + seg * 16]) = ra[i];
-            *reinterpret_cast<uint4*>(&sB[buf][r * kRowB + seg * 16]) = rb[i];
-        }
+        for (int i = 0; i < C::AV; ++i) put(sA[buf], tid + i * C::NT, ra[i]);
+#pragma unroll
+        for (int i = 0; i < C::BV; ++i) put(sB[buf], tid + i * C::NT, rb[i]);
     };
 
-    v4i acc[4][4];
+    v4i acc[TM][TN];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = v4i{0, 0, 0, 0};
+        for (int j = 0; j < TN; ++j) acc[i][j] = v4i{0, 0, 0, 0};
 
-    const int lr = lane % 16, lg = lane / 16;     // operand row within a 16-tile, k group
+    const int lr = lane % 16, lg = lane / 16;            // row within a 16-tile, k group
+    // a lane's fragment rows differ by multiples of 16, so swz(row) == swz(lr)
+    const int offA = ((wm * TM) * 16 + lr) * C::RB;
+    const int offB = ((wn * TN) * 16 + lr) * C::RB;
     if (kt0 < kt1) {
-        load(kt0);
+        load_step(kt0);
         stash(0);
         __syncthreads();
     }
     for (int kt = kt0; kt < kt1; ++kt) {
         const int buf = (kt - kt0) & 1;
-        if (kt + 1 < kt1) load(kt + 1);
-        // each lane reads 16 packed bytes (32 codes) per operand tile: its k group
-        // holds bytes [16*lg, 16*lg + 16) of the 64-byte row slice
-        uint4 fa[4], fb[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            fa[i] = *reinterpret_cast<const uint4*>(&sA[buf][(wm * 64 + i * 16 + lr) * kRowB + lg * 16]);
-            fb[i] = *reinterpret_cast<const uint4*>(&sB[buf][(wn * 64 + i * 16 + lr) * kRowB + lg * 16]);
-        }
+        if (kt + 1 < kt1) load_step(kt + 1);
+        // k group lg of a lane covers packed bytes [16 lg, 16 lg + 16) of the row
+        // slice; MFMA step h uses 8 of them (same bytes for A and W)
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
-            v4i a[4], b[4];
+            v4i a[TM], b[TN];
+            if (UNPACK) {
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                a[i] = h ? unpack_op(fa[i].z, fa[i].w) : unpack_op(fa[i].x, fa[i].y);
-                b[i] = h ? unpack_op(fb[i].z, fb[i].w) : unpack_op(fb[i].x, fb[i].y);
+                for (int i = 0; i < TM; ++i)
+                    a[i] = *reinterpret_cast<const v4i*>(&sA[buf][offA + i * 16 * C::RB +
+                                                                   C::chunk(lr, 2 * lg + h) * 16]);
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    b[j] = *reinterpret_cast<const v4i*>(&sB[buf][offB + j * 16 * C::RB +
+                                                                   C::chunk(lr, 2 * lg + h) * 16]);
+            } else {
+#pragma unroll
+                for (int i = 0; i < TM; ++i) {
+                    const uint2 u = *reinterpret_cast<const uint2*>(&sA[buf][offA + i * 16 * C::RB +
+                                                                             C::chunk(lr, lg) * 16 + 8 * h]);
+                    a[i] = unpack_op(u.x, u.y);
+                }
+#pragma unroll
+                for (int j = 0; j < TN; ++j) {
+                    const uint2 u = *reinterpret_cast<const uint2*>(&sB[buf][offB + j * 16 * C::RB +
+                                                                             C::chunk(lr, lg) * 16 + 8 * h]);
+                    b[j] = unpack_op(u.x, u.y);
+                }
             }
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
+            for (int i = 0; i < TM; ++i)
 #pragma unroll
-                for (int j = 0; j < 4; ++j)
+                for (int j = 0; j < TN; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[i], b[j], acc[i][j], 0, 0, 0);
         }
         if (kt + 1 < kt1) {
@@ -137,16 +211,16 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const uint8_t* __restric
         }
     }
 
-    // D layout of the 16x16 tile: lane holds column (lane % 16), rows 4*(lane / 16) + r
+    // D layout of a 16x16 tile: lane holds column (lane % 16), rows 4*(lane / 16) + r
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int col = col0 + wn * 64 + j * 16 + lr;
+        for (int j = 0; j < TN; ++j) {
+            const int col = col0 + (wn * TN + j) * 16 + lr;
             if (col >= N) continue;
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-                const int row = row0 + wm * 64 + i * 16 + lg * 4 + r;
+                const int row = row0 + (wm * TM + i) * 16 + lg * 4 + r;
                 if (row >= M) continue;
                 const int v = acc[i][j][r] >> 8;
                 if (SPLIT)
@@ -158,57 +232,88 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const uint8_t* __restric
 }
 
 // Adds the split-K partial sums (exact int32) and applies the epilogue.
-__global__ __launch_bounds__(kThreads) void splitk_epilogue(const int32_t* __restrict__ part, int splits,
-                                                            const float* __restrict__ s_a,
-                                                            const float* __restrict__ s_w, int M, int N,
-                                                            uint16_t* __restrict__ Y, int32_t* __restrict__ acc) {
+__global__ __launch_bounds__(256) void splitk_epilogue(const int32_t* __restrict__ part, int splits,
+                                                       const float* __restrict__ s_a,
+                                                       const float* __restrict__ s_w, int M, int N,
+                                                       uint16_t* __restrict__ Y, int32_t* __restrict__ acc) {
     const size_t total = (size_t)M * N;
-    for (size_t e = (size_t)blockIdx.x * kThreads + threadIdx.x; e < total; e += (size_t)gridDim.x * kThreads) {
+    for (size_t e = (size_t)blockIdx.x * 256 + threadIdx.x; e < total; e += (size_t)gridDim.x * 256) {
         int v = 0;
         for (int z = 0; z < splits; ++z) v += part[(size_t)z * total + e];
         store_out((int)(e / N), (int)(e % N), v, s_a, s_w, Y, acc, N);
     }
 }
 
-int choose_splits(int M, int N, int K) {
-    const int tiles = ((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN);
-    const int nk = (K + 2 * kBKB - 1) / (2 * kBKB);
-    if (tiles >= 256) return 1;
-    int s = (512 + tiles - 1) / tiles;
-    s = s < nk ? s : nk;
-    s = s < 32 ? s : 32;
-    return s < 1 ? 1 : s;
+// A launch plan: tile shape and K split.
+struct Plan {
+    int bm, bn;
+    int splits;    // K split count actually used (1 = fused epilogue)
+    int per;       // k steps per split
+};
+
+Plan make_plan(int M, int N, int K, int bm, int bn, int want_splits) {
+    (void)M;
+    (void)N;
+    Plan p;
+    p.bm = bm;
+    p.bn = bn;
+    const int nk = (K / 2 + kKB - 1) / kKB;
+    const int s = want_splits < 1 ? 1 : (want_splits > nk ? nk : want_splits);
+    p.per = (nk + s - 1) / s;
+    p.splits = (nk + p.per - 1) / p.per;
+    return p;
+}
+
+template <int WM, int WN, int TM, int TN, bool UNPACK>
+hipError_t launch_cfg(const Plan& p, const uint8_t* Aq, const float* s_a, const uint8_t* Wq, const float* s_w,
+                      int M, int N, int K, uint16_t* Y, int32_t* acc, int32_t* part, hipStream_t st) {
+    dim3 grid((N + p.bn - 1) / p.bn, (M + p.bm - 1) / p.bm, p.splits);
+    dim3 block(64 * WM * WN);
+    if (p.splits == 1) {
+        hipLaunchKernelGGL((gemm_kernel<WM, WN, TM, TN, UNPACK, false>), grid, block, 0, st, Aq, s_a, Wq, s_w, M,
+                           N, K, p.per, Y, acc, (int32_t*)nullptr);
+    } else {
+        hipLaunchKernelGGL((gemm_kernel<WM, WN, TM, TN, UNPACK, true>), grid, block, 0, st, Aq, s_a, Wq, s_w, M, N,
+                           K, p.per, (uint16_t*)nullptr, (int32_t*)nullptr, part);
+    }
+    return hipGetLastError();
+}
+
+hipError_t finish_split(const Plan& p, int32_t* part, const float* s_a, const float* s_w, int M, int N, uint16_t* Y,
+                        int32_t* acc, hipStream_t st) {
+    if (p.splits == 1) return hipSuccess;
+    const size_t total = (size_t)M * N;
+    const int blocks = (int)((total + 255) / 256 < 4096 ? (total + 255) / 256 : 4096);
+    hipLaunchKernelGGL(splitk_epilogue, dim3(blocks), dim3(256), 0, st, part, p.splits, s_a, s_w, M, N, Y, acc);
+    return hipGetLastError();
+}
+
+// The production plan: 128 x 128 tiles (four waves of 64 x 64, nibbles unpacked as
+// fragments leave LDS), K split until there are at least two workgroups per CU.
+Plan choose_plan(int M, int N, int K) {
+    const int tiles = ((M + 127) / 128) * ((N + 127) / 128);
+    int s = 1;
+    if (tiles < 256) {
+        s = (512 + tiles - 1) / tiles;
+        s = s < 32 ? s : 32;
+    }
+    return make_plan(M, N, K, 128, 128, s);
 }
 
 }  // namespace
 
 size_t gemm_workspace_bytes(int M, int N, int K) {
-    const int s = choose_splits(M, N, K);
-    return s > 1 ? (size_t)s * M * N * sizeof(int32_t) : 0;
+    const Plan p = choose_plan(M, N, K);
+    return p.splits > 1 ? (size_t)p.splits * M * N * sizeof(int32_t) : 0;
 }
 
 hipError_t launch_gemm(const uint8_t* Aq, const float* s_a, const uint8_t* Wq, const float* s_w, int M, int N,
                        int K, uint16_t* Y, int32_t* acc, void* ws, hipStream_t st) {
-    const int splits = choose_splits(M, N, K);
-    const int nk = (K + 2 * kBKB - 1) / (2 * kBKB);
-    dim3 grid((N + kBN - 1) / kBN, (M + kBM - 1) / kBM, 1);
-    if (splits == 1) {
-        hipLaunchKernelGGL(gemm_kernel<false>, grid, dim3(kThreads), 0, st, Aq, s_a, Wq, s_w, M, N, K, nk, Y, acc,
-                           (int32_t*)nullptr);
-        return hipGetLastError();
-    }
-    const int per = (nk + splits - 1) / splits;
-    const int used = (nk + per - 1) / per;      // splits that own at least one k step
-    grid.z = used;
+    const Plan p = choose_plan(M, N, K);
     int32_t* part = static_cast<int32_t*>(ws);
-    hipLaunchKernelGGL(gemm_kernel<true>, grid, dim3(kThreads), 0, st, Aq, s_a, Wq, s_w, M, N, K, per,
-                       (uint16_t*)nullptr, (int32_t*)nullptr, part);
-    hipError_t e = hipGetLastError();
+    hipError_t e = launch_cfg<2, 2, 4, 4, false>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st);
     if (e != hipSuccess) return e;
-    const size_t total = (size_t)M * N;
-    const int blocks = (int)((total + kThreads - 1) / kThreads < 4096 ? (total + kThreads - 1) / kThreads : 4096);
-    hipLaunchKernelGGL(splitk_epilogue, dim3(blocks), dim3(kThreads), 0, st, part, used, s_a, s_w, M, N, Y, acc);
-    return hipGetLastError();
+    return finish_split(p, part, s_a, s_w, M, N, Y, acc, st);
 }
 
 }  // namespace sq
