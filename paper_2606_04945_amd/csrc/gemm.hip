@@ -73,7 +73,7 @@ constexpr uint32_t kOOB = 0x80000000u;   // an offset past any buffer this kerne
 
 // SPLIT == false: full K, fused epilogue.  SPLIT == true: K range of blockIdx.z,
 // raw int32 sums to part[z][M][N].
-template <int WM, int WN, int TM, int TN, bool UNPACK, bool SPLIT>
+template <int WM, int WN, int TM, int TN, bool UNPACK, bool SPLIT, int SCHED = 0>
 __global__ __launch_bounds__(64 * WM * WN) void gemm_kernel(const uint8_t* __restrict__ Aq,
                                                            const float* __restrict__ s_a,
                                                            const uint8_t* __restrict__ Wq,
@@ -171,39 +171,82 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_kernel(const uint8_t* __res
     for (int kt = kt0; kt < kt1; ++kt) {
         const int buf = (kt - kt0) & 1;
         if (kt + 1 < kt1) load_step(kt + 1);
-        // k group lg of a lane covers packed bytes [16 lg, 16 lg + 16) of the row
-        // slice; MFMA step h uses 8 of them (same bytes for A and W)
+        if (SCHED && !UNPACK) {
+            // one 16-byte fragment per tile per k step; unpack both MFMA steps, and
+            // let the scheduler interleave the second step's unpacking with the
+            // first step's MFMAs
+            uint4 fa[TM], fb[TN];
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            v4i a[TM], b[TN];
-            if (UNPACK) {
+            for (int i = 0; i < TM; ++i)
+                fa[i] = *reinterpret_cast<const uint4*>(&sA[buf][offA + i * 16 * C::RB + C::chunk(lr, lg) * 16]);
 #pragma unroll
-                for (int i = 0; i < TM; ++i)
-                    a[i] = *reinterpret_cast<const v4i*>(&sA[buf][offA + i * 16 * C::RB +
-                                                                   C::chunk(lr, 2 * lg + h) * 16]);
+            for (int j = 0; j < TN; ++j)
+                fb[j] = *reinterpret_cast<const uint4*>(&sB[buf][offB + j * 16 * C::RB + C::chunk(lr, lg) * 16]);
+            v4i a0[TM], b0[TN], a1[TM], b1[TN];
 #pragma unroll
-                for (int j = 0; j < TN; ++j)
-                    b[j] = *reinterpret_cast<const v4i*>(&sB[buf][offB + j * 16 * C::RB +
-                                                                   C::chunk(lr, 2 * lg + h) * 16]);
-            } else {
+            for (int i = 0; i < TM; ++i) a0[i] = unpack_op(fa[i].x, fa[i].y);
 #pragma unroll
-                for (int i = 0; i < TM; ++i) {
-                    const uint2 u = *reinterpret_cast<const uint2*>(&sA[buf][offA + i * 16 * C::RB +
-                                                                             C::chunk(lr, lg) * 16 + 8 * h]);
-                    a[i] = unpack_op(u.x, u.y);
-                }
+            for (int j = 0; j < TN; ++j) b0[j] = unpack_op(fb[j].x, fb[j].y);
 #pragma unroll
-                for (int j = 0; j < TN; ++j) {
-                    const uint2 u = *reinterpret_cast<const uint2*>(&sB[buf][offB + j * 16 * C::RB +
-                                                                             C::chunk(lr, lg) * 16 + 8 * h]);
-                    b[j] = unpack_op(u.x, u.y);
-                }
-            }
+            for (int i = 0; i < TM; ++i) a1[i] = unpack_op(fa[i].z, fa[i].w);
+#pragma unroll
+            for (int j = 0; j < TN; ++j) b1[j] = unpack_op(fb[j].z, fb[j].w);
 #pragma unroll
             for (int i = 0; i < TM; ++i)
 #pragma unroll
                 for (int j = 0; j < TN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[i], b[j], acc[i][j], 0, 0, 0);
+                    acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a0[i], b0[j], acc[i][j], 0, 0, 0);
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a1[i], b1[j], acc[i][j], 0, 0, 0);
+            constexpr int nmma = TM * TN;
+            constexpr int nvalu = 6 * (TM + TN);           // one MFMA step's unpacking
+            constexpr int per = (nvalu + nmma - 1) / nmma;
+            __builtin_amdgcn_sched_group_barrier(0x100, TM + TN, 0);     // fragment reads
+            __builtin_amdgcn_sched_group_barrier(0x002, nvalu, 0);       // step-0 unpack
+#pragma unroll
+            for (int q = 0; q < nmma; ++q) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);       // step-0 MFMA
+                __builtin_amdgcn_sched_group_barrier(0x002, per, 0);     // step-1 unpack
+            }
+            __builtin_amdgcn_sched_group_barrier(0x008, nmma, 0);        // step-1 MFMA
+        } else {
+            // k group lg of a lane covers packed bytes [16 lg, 16 lg + 16) of the row
+            // slice; MFMA step h uses 8 of them (same bytes for A and W)
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                v4i a[TM], b[TN];
+                if (UNPACK) {
+#pragma unroll
+                    for (int i = 0; i < TM; ++i)
+                        a[i] = *reinterpret_cast<const v4i*>(&sA[buf][offA + i * 16 * C::RB +
+                                                                       C::chunk(lr, 2 * lg + h) * 16]);
+#pragma unroll
+                    for (int j = 0; j < TN; ++j)
+                        b[j] = *reinterpret_cast<const v4i*>(&sB[buf][offB + j * 16 * C::RB +
+                                                                       C::chunk(lr, 2 * lg + h) * 16]);
+                } else {
+#pragma unroll
+                    for (int i = 0; i < TM; ++i) {
+                        const uint2 u = *reinterpret_cast<const uint2*>(&sA[buf][offA + i * 16 * C::RB +
+                                                                                 C::chunk(lr, lg) * 16 + 8 * h]);
+                        a[i] = unpack_op(u.x, u.y);
+                    }
+#pragma unroll
+                    for (int j = 0; j < TN; ++j) {
+                        const uint2 u = *reinterpret_cast<const uint2*>(&sB[buf][offB + j * 16 * C::RB +
+                                                                                 C::chunk(lr, lg) * 16 + 8 * h]);
+                        b[j] = unpack_op(u.x, u.y);
+                    }
+                }
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < TN; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[i], b[j], acc[i][j], 0, 0, 0);
+            }
         }
         if (kt + 1 < kt1) {
             stash(buf ^ 1);
@@ -246,6 +289,7 @@ __global__ __launch_bounds__(256) void splitk_epilogue(const int32_t* __restrict
 
 // A launch plan: tile shape and K split.
 struct Plan {
+    int cfg;       // 0: 128 x 128, 1: 64 x 128, 2: 64 x 64 (see launch_gemm)
     int bm, bn;
     int splits;    // K split count actually used (1 = fused epilogue)
     int per;       // k steps per split
@@ -255,6 +299,7 @@ Plan make_plan(int M, int N, int K, int bm, int bn, int want_splits) {
     (void)M;
     (void)N;
     Plan p;
+    p.cfg = -1;
     p.bm = bm;
     p.bn = bn;
     const int nk = (K / 2 + kKB - 1) / kKB;
@@ -264,16 +309,16 @@ Plan make_plan(int M, int N, int K, int bm, int bn, int want_splits) {
     return p;
 }
 
-template <int WM, int WN, int TM, int TN, bool UNPACK>
+template <int WM, int WN, int TM, int TN, bool UNPACK, int SCHED = 0>
 hipError_t launch_cfg(const Plan& p, const uint8_t* Aq, const float* s_a, const uint8_t* Wq, const float* s_w,
                       int M, int N, int K, uint16_t* Y, int32_t* acc, int32_t* part, hipStream_t st) {
     dim3 grid((N + p.bn - 1) / p.bn, (M + p.bm - 1) / p.bm, p.splits);
     dim3 block(64 * WM * WN);
     if (p.splits == 1) {
-        hipLaunchKernelGGL((gemm_kernel<WM, WN, TM, TN, UNPACK, false>), grid, block, 0, st, Aq, s_a, Wq, s_w, M,
+        hipLaunchKernelGGL((gemm_kernel<WM, WN, TM, TN, UNPACK, false, SCHED>), grid, block, 0, st, Aq, s_a, Wq, s_w, M,
                            N, K, p.per, Y, acc, (int32_t*)nullptr);
     } else {
-        hipLaunchKernelGGL((gemm_kernel<WM, WN, TM, TN, UNPACK, true>), grid, block, 0, st, Aq, s_a, Wq, s_w, M, N,
+        hipLaunchKernelGGL((gemm_kernel<WM, WN, TM, TN, UNPACK, true, SCHED>), grid, block, 0, st, Aq, s_a, Wq, s_w, M, N,
                            K, p.per, (uint16_t*)nullptr, (int32_t*)nullptr, part);
     }
     return hipGetLastError();
@@ -288,16 +333,32 @@ hipError_t finish_split(const Plan& p, int32_t* part, const float* s_a, const fl
     return hipGetLastError();
 }
 
-// The production plan: 128 x 128 tiles (four waves of 64 x 64, nibbles unpacked as
-// fragments leave LDS), K split until there are at least two workgroups per CU.
+// The production plan (from measured sweeps on MI355X):
+//  - M <= 64: 64 x 64 tiles and a K split up to ~512 workgroups (weight streaming);
+//  - at least 512 tiles of 128 x 128: 128 x 128 (four waves of 64 x 64);
+//  - otherwise 64 x 128 (four waves of 64 x 32), split along K below 512 tiles.
 Plan choose_plan(int M, int N, int K) {
-    const int tiles = ((M + 127) / 128) * ((N + 127) / 128);
-    int s = 1;
-    if (tiles < 256) {
-        s = (512 + tiles - 1) / tiles;
-        s = s < 32 ? s : 32;
+    const int nk = (K / 2 + kKB - 1) / kKB;
+    auto splits_for = [&](int tiles) {
+        int s = tiles >= 512 ? 1 : (512 + tiles - 1) / tiles;
+        const int cap = nk / 4 > 1 ? nk / 4 : 1;       // keep at least 4 k steps per split
+        s = s < cap ? s : cap;
+        return s < 32 ? s : 32;
+    };
+    Plan p;
+    if (M <= 64) {
+        const int tiles = ((M + 63) / 64) * ((N + 63) / 64);
+        p = make_plan(M, N, K, 64, 64, splits_for(tiles));
+        p.cfg = 2;
+    } else if (((M + 127) / 128) * ((N + 127) / 128) >= 512) {
+        p = make_plan(M, N, K, 128, 128, 1);
+        p.cfg = 0;
+    } else {
+        const int tiles = ((M + 63) / 64) * ((N + 127) / 128);
+        p = make_plan(M, N, K, 64, 128, splits_for(tiles));
+        p.cfg = 1;
     }
-    return make_plan(M, N, K, 128, 128, s);
+    return p;
 }
 
 }  // namespace
@@ -311,7 +372,12 @@ hipError_t launch_gemm(const uint8_t* Aq, const float* s_a, const uint8_t* Wq, c
                        int K, uint16_t* Y, int32_t* acc, void* ws, hipStream_t st) {
     const Plan p = choose_plan(M, N, K);
     int32_t* part = static_cast<int32_t*>(ws);
-    hipError_t e = launch_cfg<2, 2, 4, 4, false>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st);
+    hipError_t e;
+    switch (p.cfg) {
+        case 2: e = launch_cfg<2, 2, 2, 2, false, 1>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
+        case 1: e = launch_cfg<1, 4, 4, 2, false, 1>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
+        default: e = launch_cfg<2, 2, 4, 4, false, 1>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
+    }
     if (e != hipSuccess) return e;
     return finish_split(p, part, s_a, s_w, M, N, Y, acc, st);
 }
