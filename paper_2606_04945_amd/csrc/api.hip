@@ -151,6 +151,8 @@ int sgat_quant_act(const uint16_t* X, const uint8_t* state, const float* P, int3
     SQ_REQUIRE(ws_bytes >= need && (need == 0 || ws), SQ_ERR_WORKSPACE,
                "sgat_quant_act: workspace %zu B < %zu B", ws_bytes, need);
     hipStream_t st = static_cast<hipStream_t>(stream);
+    if (tac_M && !P && sq::tac_quant_fusable(K, g))
+        return hip_status(sq::launch_tac_quant(X, tac_M, tac_d, state, M, K, g, d_m, d_u, Aq, s_a, st), "tac_quant");
     uint8_t* wsb = static_cast<uint8_t*>(ws);
     const uint16_t* src = X;
     if (tac_M) {

@@ -49,6 +49,11 @@ __device__ __forceinline__ float wave_max(float v) {
 hipError_t launch_tac(const uint16_t* Z, const uint16_t* Mb, const uint16_t* d,
                       int M, int C, int g, uint16_t* out, hipStream_t st);
 
+// TAC fused with gate + int4 quantisation (P = NULL); valid when tac_quant_fusable.
+bool tac_quant_fusable(int K, int g);
+hipError_t launch_tac_quant(const uint16_t* Z, const uint16_t* Mb, const uint16_t* d, const uint8_t* state, int M,
+                            int K, int g, int dm, int du, uint8_t* Aq, float* s, hipStream_t st);
+
 hipError_t launch_transform(const uint16_t* X, const uint8_t* state, const float* P,
                             int M, int K, int dm, int du, float* Xp, hipStream_t st);
 

@@ -131,3 +131,123 @@ hipError_t launch_tac(const uint16_t* Z, const uint16_t* Mb, const uint16_t* d, 
 }
 
 }  // namespace sq
+
+// ---------------------------------------------------------------------------
+// TAC fused with the gate and the per-token int4 quantiser, for g <= 16 and an
+// input already in the P basis (no dense transform): z -> fp16(M_b z_b + d_b)
+// -> G_s -> absmax -> codes, without materialising z'.  Thread t owns channels
+// [8t, 8t + 8) of every token row (K / 8 active threads), keeps those channels'
+// block-matrix rows (8 x g) and biases in registers, and walks the workgroup's
+// tokens one row at a time: 8 outputs of g fused multiply-adds each (same order
+// and rounding as tac_kernel), the gate, a block max, then the 8 codes packed
+// into 4 bytes.
+namespace sq {
+namespace {
+
+constexpr int kFusedThreads = 512;
+
+__device__ __forceinline__ float block_max_db(float v, float (*red)[kFusedThreads / kWave], int parity) {
+    v = wave_max(v);
+    const int w = threadIdx.x / kWave, l = threadIdx.x % kWave;
+    if (l == 0) red[parity][w] = v;
+    __syncthreads();
+    float r = 0.0f;
+    const int nw = (int)(blockDim.x + kWave - 1) / kWave;
+    for (int i = 0; i < nw; ++i) r = fmaxf(r, red[parity][i]);
+    return r;
+}
+
+template <int G>
+__global__ __launch_bounds__(kFusedThreads) void tac_quant_kernel(const uint16_t* __restrict__ Z,
+                                                                  const uint16_t* __restrict__ Mb,
+                                                                  const uint16_t* __restrict__ d,
+                                                                  const uint8_t* __restrict__ state, int M, int K,
+                                                                  int dm, int du, int rows_per_wg,
+                                                                  uint8_t* __restrict__ Aq,
+                                                                  float* __restrict__ s_out) {
+    constexpr int ZW = G > 8 ? G : 8;                   // input channels a thread reads (whole blocks)
+    __shared__ float red[2][kFusedThreads / kWave];
+    const int t = threadIdx.x;
+    const bool active = 8 * t < K;
+    const int c0 = 8 * t;                               // first output channel of this thread
+    const int z0 = (c0 / ZW) * ZW;                      // first input channel it reads
+    float m[8][G];                                      // tac_M viewed as [K][G]: rows c0 .. c0 + 7
+    float dv[8];
+    if (active) {
+#pragma unroll
+        for (int r = 0; r < 8; ++r) {
+#pragma unroll
+            for (int c = 0; c < G; ++c) m[r][c] = h2f(Mb[(size_t)(c0 + r) * G + c]);
+            dv[r] = h2f(d[c0 + r]);
+        }
+    }
+    const int row_begin = blockIdx.x * rows_per_wg;
+    const int row_end = min(M, row_begin + rows_per_wg);
+    for (int row = row_begin; row < row_end; ++row) {
+        float o[8];
+        float amax = 0.0f;
+        if (active) {
+            float z[ZW];
+            const uint4* src = reinterpret_cast<const uint4*>(Z + (size_t)row * K + z0);
+#pragma unroll
+            for (int v = 0; v < ZW / 8; ++v) {
+                const uint4 q = src[v];
+                const uint16_t* h = reinterpret_cast<const uint16_t*>(&q);
+#pragma unroll
+                for (int i = 0; i < 8; ++i) z[8 * v + i] = h2f(h[i]);
+            }
+            const bool masked = state ? state[row] != 0 : false;
+#pragma unroll
+            for (int r = 0; r < 8; ++r) {
+                const int base = ((c0 - z0 + r) / G) * G;   // block start within z[]
+                float acc = 0.0f;
+#pragma unroll
+                for (int c = 0; c < G; ++c) acc = __builtin_fmaf(m[r][c], z[base + c], acc);
+                const float v = h2f(f2h(acc + dv[r]));  // TAC output, materialised as fp16
+                o[r] = (!state || kept(c0 + r, K, dm, du, masked)) ? v : 0.0f;
+                amax = fmaxf(amax, fabsf(o[r]));
+            }
+        }
+        const float s = block_max_db(amax, red, row & 1) / 7.0f;
+        if (t == 0) s_out[row] = s;
+        if (active) {
+            uint32_t w = 0;
+            if (s != 0.0f) {
+#pragma unroll
+                for (int q = 0; q < 8; ++q) w |= (uint32_t)(quant4(o[q], s) & 15) << (4 * q);
+            }
+            *reinterpret_cast<uint32_t*>(Aq + (size_t)row * (K / 2) + 4 * t) = w;
+        }
+    }
+}
+
+}  // namespace
+
+bool tac_quant_fusable(int K, int g) { return g <= 16 && K % 16 == 0 && K / 8 <= kFusedThreads; }
+
+hipError_t launch_tac_quant(const uint16_t* Z, const uint16_t* Mb, const uint16_t* d, const uint8_t* state, int M,
+                            int K, int g, int dm, int du, uint8_t* Aq, float* s, hipStream_t st) {
+    const int threads = ((K / 8 + kWave - 1) / kWave) * kWave;
+    // enough workgroups to fill the chip, each reusing its parameters over several rows
+    int rows = M / 512;
+    rows = rows < 1 ? 1 : (rows > 16 ? 16 : rows);
+    const dim3 grid((M + rows - 1) / rows);
+    switch (g) {
+#define SQ_TQ(G)                                                                                                  \
+    case G:                                                                                                       \
+        hipLaunchKernelGGL(tac_quant_kernel<G>, grid, dim3(threads), 0, st, Z, Mb, d, state, M, K, dm, du, rows, \
+                           Aq, s);                                                                                \
+        break;
+        SQ_TQ(1)
+        SQ_TQ(2)
+        SQ_TQ(4)
+        SQ_TQ(8)
+        SQ_TQ(16)
+#undef SQ_TQ
+        default:
+            return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+}  // namespace sq

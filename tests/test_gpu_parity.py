@@ -226,6 +226,26 @@ def test_quant_act_with_tac(withP, g):
     assert_bits(host(Aq), rq, "Aq")
 
 
+@pytest.mark.parametrize("g", [1, 2, 4, 8, 16])
+@pytest.mark.parametrize("M,K", [(1, 64), (37, 512), (300, 3584), (129, 4096), (20, 8192)])
+def test_quant_act_tac_folded_fused(g, M, K):
+    """TAC fused with the gate and quantiser (folded basis, g <= 16, K <= 4096; wider
+    rows take the staged path): bit-exact with the oracle's TAC-then-quantise."""
+    X, st = _x(M, K, 8)
+    Mb, d = synth.tac_params(K, g, synth.rng_for(703, g, K))
+    dm, du = synth.default_band(K)
+    say(f"quant_act + fused tac g={g} M={M} K={K}")
+    Aq, s = sq.sgat_quant_act(dev(X), dev(st), None, dm, du, dev(Mb), dev(d), g)
+    rq, rs = O.quant_act(X, st, None, dm, du, Mb, d, g, threads=THREADS)
+    assert_bits(host(s), rs, "s_a")
+    assert_bits(host(Aq), rq, "Aq")
+    # no gate
+    Aq, s = sq.sgat_quant_act(dev(X), None, None, 0, 0, dev(Mb), dev(d), g)
+    rq, rs = O.quant_act(X, None, None, 0, 0, Mb, d, g, threads=THREADS)
+    assert_bits(host(s), rs, "s_a (no gate)")
+    assert_bits(host(Aq), rq, "Aq (no gate)")
+
+
 # ------------------------------------------------------------------ end to end
 
 def test_config0_end_to_end():
