@@ -274,6 +274,94 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_kernel(const uint8_t* __res
         }
 }
 
+// Short M (<= 64 tokens): the weights are streamed once and each is used by at
+// most 64 rows, so the kernel is bound by HBM bandwidth, not by the MFMA.  No
+// LDS and no barriers: each wave owns 16 output columns and walks its K range,
+// loading its W rows and the (L2-resident) activation rows straight into MFMA
+// operand registers with raw buffer loads, U k steps in flight per batch.  Lane
+// (c, g) reads bytes [16 g, 16 g + 16) of the 64-byte slice of row c (W) or of
+// the activation row, exactly as the tiled kernel's fragments.
+template <int TM, int U, bool SPLIT>
+__global__ __launch_bounds__(256) void gemm_skinny_kernel(const uint8_t* __restrict__ Aq,
+                                                          const float* __restrict__ s_a,
+                                                          const uint8_t* __restrict__ Wq,
+                                                          const float* __restrict__ s_w, int M, int N, int K,
+                                                          int ksteps_per_split, uint16_t* __restrict__ Y,
+                                                          int32_t* __restrict__ acc_out,
+                                                          int32_t* __restrict__ part) {
+    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    const int lr = lane % 16, lg = lane / 16;
+    const int col0 = (blockIdx.x * 4 + wave) * 16;
+    if (col0 >= N) return;                                   // whole wave past N: nothing to do
+    const uint32_t ldb = (uint32_t)K / 2;
+    const int nk_total = (int)((ldb + kKB - 1) / kKB);
+    const int kt0 = SPLIT ? blockIdx.z * ksteps_per_split : 0;
+    const int kt1 = SPLIT ? min(nk_total, kt0 + ksteps_per_split) : nk_total;
+    const __amdgpu_buffer_rsrc_t rA = make_rsrc(Aq, (uint32_t)M * ldb);
+    const __amdgpu_buffer_rsrc_t rW = make_rsrc(Wq, (uint32_t)N * ldb);
+    const uint32_t seg = 16 * lg;
+    const uint32_t ow = col0 + lr < N ? (uint32_t)(col0 + lr) * ldb + seg : kOOB;
+    uint32_t oa[TM];
+#pragma unroll
+    for (int i = 0; i < TM; ++i) oa[i] = 16 * i + lr < M ? (uint32_t)(16 * i + lr) * ldb + seg : kOOB;
+
+    v4i acc[TM];
+#pragma unroll
+    for (int i = 0; i < TM; ++i) acc[i] = v4i{0, 0, 0, 0};
+    // two register batches of U k steps: batch b + 1 is in flight while batch b is
+    // multiplied (steps past the split or the row read as zeros)
+    auto issue = [&](int kb, v4i (&w)[U], v4i (&a)[U][TM]) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const uint32_t ko = (uint32_t)(kb + u) * kKB;
+            const bool in = kb + u < kt1 && ko + seg < ldb;
+            w[u] = __builtin_amdgcn_raw_buffer_load_b128(rW, (int)(in ? ow + ko : kOOB), 0, 0);
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+                a[u][i] = __builtin_amdgcn_raw_buffer_load_b128(rA, (int)(in ? oa[i] + ko : kOOB), 0, 0);
+        }
+    };
+    auto compute = [&](const v4i (&w)[U], const v4i (&a)[U][TM]) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const v4i b = h ? unpack_op(w[u][2], w[u][3]) : unpack_op(w[u][0], w[u][1]);
+#pragma unroll
+                for (int i = 0; i < TM; ++i) {
+                    const v4i x = h ? unpack_op(a[u][i][2], a[u][i][3]) : unpack_op(a[u][i][0], a[u][i][1]);
+                    acc[i] = __builtin_amdgcn_mfma_i32_16x16x64_i8(x, b, acc[i], 0, 0, 0);
+                }
+            }
+        }
+    };
+    v4i w0[U], a0[U][TM], w1[U], a1[U][TM];
+    issue(kt0, w0, a0);
+    for (int kb = kt0; kb < kt1; kb += 2 * U) {
+        issue(kb + U, w1, a1);
+        __builtin_amdgcn_sched_barrier(0);
+        compute(w0, a0);
+        if (kb + U >= kt1) break;
+        issue(kb + 2 * U, w0, a0);
+        __builtin_amdgcn_sched_barrier(0);
+        compute(w1, a1);
+    }
+    const int col = col0 + lr;
+    if (col >= N) return;
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int row = 16 * i + 4 * lg + r;
+            if (row >= M) continue;
+            const int v = acc[i][r] >> 8;
+            if (SPLIT)
+                part[((size_t)blockIdx.z * M + row) * N + col] = v;
+            else
+                store_out(row, col, v, s_a, s_w, Y, acc_out, N);
+        }
+}
+
 // Adds the split-K partial sums (exact int32) and applies the epilogue.
 __global__ __launch_bounds__(256) void splitk_epilogue(const int32_t* __restrict__ part, int splits,
                                                        const float* __restrict__ s_a,
@@ -289,7 +377,7 @@ __global__ __launch_bounds__(256) void splitk_epilogue(const int32_t* __restrict
 
 // A launch plan: tile shape and K split.
 struct Plan {
-    int cfg;       // 0: 128 x 128, 1: 64 x 128, 2: 64 x 64 (see launch_gemm)
+    int cfg;       // 0: 128 x 128, 1: 64 x 128, 2: 64 x 64, 3: skinny (see launch_gemm)
     int bm, bn;
     int splits;    // K split count actually used (1 = fused epilogue)
     int per;       // k steps per split
@@ -307,6 +395,20 @@ Plan make_plan(int M, int N, int K, int bm, int bn, int want_splits) {
     p.per = (nk + s - 1) / s;
     p.splits = (nk + p.per - 1) / p.per;
     return p;
+}
+
+template <int TM, int U>
+hipError_t launch_skinny(const Plan& p, const uint8_t* Aq, const float* s_a, const uint8_t* Wq, const float* s_w,
+                         int M, int N, int K, uint16_t* Y, int32_t* acc, int32_t* part, hipStream_t st) {
+    dim3 grid((N + 63) / 64, 1, p.splits);
+    if (p.splits == 1) {
+        hipLaunchKernelGGL((gemm_skinny_kernel<TM, U, false>), grid, dim3(256), 0, st, Aq, s_a, Wq, s_w, M, N, K,
+                           p.per, Y, acc, (int32_t*)nullptr);
+    } else {
+        hipLaunchKernelGGL((gemm_skinny_kernel<TM, U, true>), grid, dim3(256), 0, st, Aq, s_a, Wq, s_w, M, N, K,
+                           p.per, (uint16_t*)nullptr, (int32_t*)nullptr, part);
+    }
+    return hipGetLastError();
 }
 
 template <int WM, int WN, int TM, int TN, bool UNPACK, int SCHED = 0>
@@ -334,7 +436,8 @@ hipError_t finish_split(const Plan& p, int32_t* part, const float* s_a, const fl
 }
 
 // The production plan (from measured sweeps on MI355X):
-//  - M <= 64: 64 x 64 tiles and a K split up to ~512 workgroups (weight streaming);
+//  - M <= 16: the skinny kernel (weight streaming, K split only for narrow N);
+//  - M <= 64: 64 x 64 tiles and a K split up to ~512 workgroups;
 //  - at least 512 tiles of 128 x 128: 128 x 128 (four waves of 64 x 64);
 //  - otherwise 64 x 128 (four waves of 64 x 32), split along K below 512 tiles.
 Plan choose_plan(int M, int N, int K) {
@@ -346,7 +449,15 @@ Plan choose_plan(int M, int N, int K) {
         return s < 32 ? s : 32;
     };
     Plan p;
-    if (M <= 64) {
+    if (M <= 16) {
+        // skinny kernel: one wave per 16 columns; split K only when there are few columns
+        const int wgs = (N + 63) / 64;
+        int s = wgs >= 128 ? 1 : (256 + wgs - 1) / wgs;
+        const int cap = nk / 16 > 1 ? nk / 16 : 1;     // keep two batches of 8 k steps per split
+        s = s < cap ? s : cap;
+        p = make_plan(M, N, K, 16, 64, s);
+        p.cfg = 3;
+    } else if (M <= 64) {
         const int tiles = ((M + 63) / 64) * ((N + 63) / 64);
         p = make_plan(M, N, K, 64, 64, splits_for(tiles));
         p.cfg = 2;
@@ -374,6 +485,7 @@ hipError_t launch_gemm(const uint8_t* Aq, const float* s_a, const uint8_t* Wq, c
     int32_t* part = static_cast<int32_t*>(ws);
     hipError_t e;
     switch (p.cfg) {
+        case 3: e = launch_skinny<1, 8>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
         case 2: e = launch_cfg<2, 2, 2, 2, false, 1>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
         case 1: e = launch_cfg<1, 4, 4, 2, false, 1>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
         default: e = launch_cfg<2, 2, 4, 4, false, 1>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;

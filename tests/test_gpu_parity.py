@@ -145,7 +145,8 @@ def _codes(M, K, seed, lo=-7, hi=7):
     return pack_codes(q)
 
 
-@pytest.mark.parametrize("M,N,K", [(1, 8, 64), (16, 4096, 4096), (77, 200, 192), (128, 256, 512),
+@pytest.mark.parametrize("M,N,K", [(1, 8, 64), (16, 4096, 4096), (5, 4104, 4096), (9, 136, 192), (16, 24, 18944),
+                                   (16, 12288, 4096), (33, 520, 1024), (77, 200, 192), (128, 256, 512),
                                    (300, 136, 4096), (1024, 1024, 1024), (513, 4104, 3584), (64, 512, 18944)])
 def test_gemm_bit_exact(M, N, K):
     Aq = _codes(M, K, 1)
