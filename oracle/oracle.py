@@ -51,6 +51,11 @@ def lib():
             L.sqo_prepare_weights.argtypes = [_p, _p, _i64, _i32, _p, _p]
             L.sqo_gemm.argtypes = [_p, _p, _p, _p, _i64, _i64, _i32, _p, _p]
             L.sqo_gemm.restype = _i32
+            L.sqo_quant_rows_q8.argtypes = [_p, _i64, _i32, _p, _p]
+            L.sqo_quant_act_q8.argtypes = [_p, _p, _p, _i64, _i32, _i32, _i32, _p, _p, _i32, _p, _p]
+            L.sqo_prepare_weights_q8.argtypes = [_p, _p, _i64, _i32, _p, _p]
+            L.sqo_gemm_q8.argtypes = [_p, _p, _p, _p, _i64, _i64, _i32, _p, _p]
+            L.sqo_gemm_q8.restype = _i32
             _lib = L
     return _lib
 
@@ -204,6 +209,69 @@ def sgat_linear(X, state, P, W, dm, du, tac_M=None, tac_d=None, g=0, threads: in
     Wq, s_w = prepare_weights(W, P, threads)
     Y, acc = gemm(Aq, s_a, Wq, s_w, threads)
     return dict(Aq=Aq, s_a=s_a, Wq=Wq, s_w=s_w, Y=Y, acc=acc)
+
+
+# ------------------------------------------------------------ W8A8 (App. D)
+
+def quant_rows_q8(x: np.ndarray):
+    """Per-row symmetric 8-bit quantisation: (codes int8 [M][K], scale [M] fp32)."""
+    x = _c(x, np.float32)
+    M, K = x.shape
+    codes = np.empty((M, K), np.int8)
+    scale = np.empty(M, np.float32)
+    lib().sqo_quant_rows_q8(_ptr(x), M, K, _ptr(codes), _ptr(scale))
+    return codes, scale
+
+
+def quant_act_q8(X, state, P, dm: int, du: int, tac_M=None, tac_d=None, g: int = 0, threads: int = 1):
+    """W8A8 activation side: [TAC] -> x P G_s -> 8-bit per token.  Returns (Aq int8, s_a)."""
+    X = _c(X.view(np.uint16), np.uint16)
+    M, K = X.shape
+    P = _c(P, np.float32)
+    state = _c(state, np.uint8)
+    tM = None if tac_M is None else _c(tac_M.view(np.uint16), np.uint16)
+    td = None if tac_d is None else _c(tac_d.view(np.uint16), np.uint16)
+    Aq = np.empty((M, K), np.int8)
+    s_a = np.empty(M, np.float32)
+
+    def run(r0, r1):
+        lib().sqo_quant_act_q8(_ptr(X[r0:]), None if state is None else _ptr(state[r0:]), _ptr(P),
+                               r1 - r0, K, dm, du, _ptr(tM), _ptr(td), g, _ptr(Aq[r0:]), _ptr(s_a[r0:]))
+    _rows_parallel(run, M, threads)
+    return Aq, s_a
+
+
+def prepare_weights_q8(W, P, threads: int = 1):
+    W = _c(W.view(np.uint16), np.uint16)
+    N, K = W.shape
+    P = _c(P, np.float32)
+    Wq = np.empty((N, K), np.int8)
+    s_w = np.empty(N, np.float32)
+
+    def run(r0, r1):
+        lib().sqo_prepare_weights_q8(_ptr(W[r0:]), _ptr(P), r1 - r0, K, _ptr(Wq[r0:]), _ptr(s_w[r0:]))
+    _rows_parallel(run, N, threads)
+    return Wq, s_w
+
+
+def gemm_q8(Aq, s_a, Wq, s_w, threads: int = 1):
+    Aq = _c(Aq, np.int8)
+    Wq = _c(Wq, np.int8)
+    s_a = _c(s_a, np.float32)
+    s_w = _c(s_w, np.float32)
+    M, K = Aq.shape
+    N = Wq.shape[0]
+    Y = np.empty((M, N), np.uint16)
+    acc = np.empty((M, N), np.int32)
+    bad = [0]
+
+    def run(r0, r1):
+        bad[0] |= lib().sqo_gemm_q8(_ptr(Aq[r0:]), _ptr(s_a[r0:]), _ptr(Wq), _ptr(s_w), r1 - r0, N, K,
+                                    _ptr(Y[r0:]), _ptr(acc[r0:]))
+    _rows_parallel(run, M, threads)
+    if bad[0]:
+        raise OverflowError("int32 accumulator overflow")
+    return Y.view(np.float16), acc
 
 
 # ============================================================ fp64 / paper-literal layer

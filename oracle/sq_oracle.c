@@ -30,6 +30,8 @@
  *      rounded to fp16 (round to nearest even);
  *   G1 GEMM: int32 sum of code products, y = fp16((float(acc) * s_a) * s_w);
  *   packing: byte t = (q[2t] & 15) | (q[2t+1] & 15) << 4.
+ *   W8A8 (App. D): the same method with 8-bit codes, s = absmax / 127, codes
+ *      clamp(rint(x / s), -128, 127), one signed byte per code.
  */
 #include <math.h>
 #include <stdint.h>
@@ -187,6 +189,28 @@ void sqo_quant_rows(const float* x, int64_t M, int K, uint8_t* packed, float* sc
     }
 }
 
+/* Symmetric 8-bit quantisation of each row (W8A8, App. D): s = absmax/127;
+ * q = clamp(rint(x/s), -128, 127), one signed byte per code. */
+void sqo_quant_rows_q8(const float* x, int64_t M, int K, int8_t* codes, float* scale)
+{
+    for (int64_t i = 0; i < M; ++i) {
+        const float* row = x + i * K;
+        float a = 0.0f;
+        for (int j = 0; j < K; ++j)
+            if (fabsf(row[j]) > a) a = fabsf(row[j]);
+        float s = a / 127.0f;
+        scale[i] = s;
+        for (int j = 0; j < K; ++j) {
+            int v = 0;
+            if (s != 0.0f) {
+                float r = rintf(row[j] / s);
+                v = r < -128.0f ? -128 : (r > 127.0f ? 127 : (int)r);
+            }
+            codes[i * K + j] = (int8_t)v;
+        }
+    }
+}
+
 /* Two's-complement nibble -> code. */
 static int sqo_nib(uint8_t byte, int hi)
 {
@@ -233,6 +257,55 @@ void sqo_prepare_weights(const uint16_t* W, const float* P, int64_t N, int K,
     sqo_transform(W, NULL, P, N, K, 0, 0, wp);
     sqo_quant_rows(wp, N, K, Wq, s_w, NULL);
     free(wp);
+}
+
+/* W8A8 activation side: [TAC] -> x P G_s -> 8-bit per-token codes. */
+void sqo_quant_act_q8(const uint16_t* X, const uint8_t* state, const float* P,
+                      int64_t M, int K, int dm, int du,
+                      const uint16_t* tacM, const uint16_t* tacd, int g,
+                      int8_t* Aq, float* s_a)
+{
+    const uint16_t* src = X;
+    uint16_t* z = NULL;
+    if (tacM) {
+        z = (uint16_t*)malloc(sizeof(uint16_t) * (size_t)(M * K));
+        sqo_tac(X, tacM, tacd, M, K, g, z);
+        src = z;
+    }
+    float* xp = (float*)malloc(sizeof(float) * (size_t)(M * K));
+    sqo_transform(src, state, P, M, K, dm, du, xp);
+    sqo_quant_rows_q8(xp, M, K, Aq, s_a);
+    free(xp);
+    free(z);
+}
+
+/* W8A8 weight side: rows of W P, per-output-channel 8-bit codes. */
+void sqo_prepare_weights_q8(const uint16_t* W, const float* P, int64_t N, int K, int8_t* Wq, float* s_w)
+{
+    float* wp = (float*)malloc(sizeof(float) * (size_t)(N * K));
+    sqo_transform(W, NULL, P, N, K, 0, 0, wp);
+    sqo_quant_rows_q8(wp, N, K, Wq, s_w);
+    free(wp);
+}
+
+/* W8A8 projection: acc = sum_j qa[i][j] qw[n][j] (int32), y as in sqo_gemm.
+ * Returns 1 if an accumulator left the int32 range. */
+int sqo_gemm_q8(const int8_t* Aq, const float* s_a, const int8_t* Wq, const float* s_w,
+                int64_t M, int64_t N, int K, uint16_t* Y, int32_t* acc_out)
+{
+    int bad = 0;
+    for (int64_t i = 0; i < M; ++i) {
+        const int8_t* a = Aq + i * K;
+        for (int64_t n = 0; n < N; ++n) {
+            const int8_t* w = Wq + n * K;
+            int64_t acc = 0;
+            for (int j = 0; j < K; ++j) acc += (int64_t)a[j] * w[j];
+            if (acc > INT32_MAX || acc < INT32_MIN) bad = 1;
+            if (acc_out) acc_out[i * N + n] = (int32_t)acc;
+            if (Y) Y[i * N + n] = sqo_f2h(((float)acc * s_a[i]) * s_w[n]);
+        }
+    }
+    return bad;
 }
 
 /* Quantised projection (Eq. 5 / Eq. 13): acc = sum_j qa[i][j] qw[n][j];
