@@ -62,6 +62,7 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=int, default=384, help="tokens in the oracle timing sample")
     ap.add_argument("--only", choices=["dense", "folded", "both"], default="both")
+    ap.add_argument("--no-w8", action="store_true", help="skip the W8A8 (App. D) folded-basis measurement")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain 1 GiB device copy (reference for HBM byte counters)")
     return ap.parse_args()
@@ -131,6 +132,12 @@ def main():
         d["gws"] = torch.empty(max(nb, 1), dtype=torch.uint8, device=dev)
         nq = sq.quant_act_workspace_bytes(M, K, False, "tac_M" in d)
         d["qws"] = torch.empty(max(nq, 1), dtype=torch.uint8, device=dev)
+    if not args.no_w8:
+        for d in sites:
+            d["Wq8"], d["s_w8"] = sq.sgat_prepare_weights_w8(d["W"], d["P"])
+            K, N = d["K"], d["N"]
+            d["Aq8"] = torch.empty((M, K), dtype=torch.int8, device=dev)
+            d["gws8"] = torch.empty(max(sq.gemm_workspace_bytes(M, N, K, 8), 1), dtype=torch.uint8, device=dev)
     # three rotating copies of the prepared weights for the folded-basis run, so
     # that the 256 MB MALL cannot hold a whole layer set's weights between steps
     wcopies = [[(d["Wq"].clone(), d["s_w"].clone()) for d in sites] for _ in range(3)]
@@ -158,6 +165,15 @@ def main():
                                               ws=d["qws"]))
             tm.wrap("gemm/" + d["site"].name,
                     lambda: sq.w4a4_gemm(d["Aq"], d["s_a"], Wq, s_w, Y=d["Y"], ws=d["gws"]))
+
+    def step_w8(tm, it):
+        for d in sites:
+            tm.wrap("quant_act8/" + d["site"].name,
+                    lambda: sq.sgat_quant_act_w8(d["X"], state, None, d["dm"], d["du"], d.get("tac_M"),
+                                                 d.get("tac_d"), d.get("g", 0), Aq=d["Aq8"], s_a=d["s_a"],
+                                                 ws=d["qws"]))
+            tm.wrap("gemm8/" + d["site"].name,
+                    lambda: sq.w8a8_gemm(d["Aq8"], d["s_a"], d["Wq8"], d["s_w8"], Y=d["Y"], ws=d["gws8"]))
 
     def run(step, steps, warmup):
         for i in range(warmup):
@@ -205,6 +221,13 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+
+    if not args.no_w8:
+        ms_w8 = run(step_w8, args.steps, args.warmup)
+        gm_ms = sum(timer.ms("gemm8/" + n)[0] for n in ops_gemm)
+        gm_ops = sum(ops_gemm.values()) * args.steps
+        out["w8"] = dict(ms=ms_w8, gemm_tops=gm_ops / gm_ms / 1e9,
+                         quant_act_ms=sum(timer.ms("quant_act8/" + n)[0] for n in ops_gemm) / args.steps)
 
     # ---------------------------------------------------------------- CPU baseline
     cpu = None
@@ -266,6 +289,11 @@ def main():
             "quant_act_ms": fold["quant_act_ms"], "per_site_gemm_ms": fold["per_site_gemm_ms"]}
         if not dense:
             res["roofline"] = dict(res["folded_P"]["roofline"], traffic=None)
+    if "w8" in out:
+        w8 = out["w8"]
+        res["w8a8_folded_P"] = {"value": M / (w8["ms"] / 1e3), "unit": "tokens/s", "ms_per_step": w8["ms"],
+                                "gemm_tops": w8["gemm_tops"], "gemm_frac_int8_peak": w8["gemm_tops"] / PEAK_INT8_TOPS,
+                                "quant_act_ms": w8["quant_act_ms"]}
     if cpu:
         res["cpu_baseline"] = cpu
     print(json.dumps(res), flush=True)

@@ -79,6 +79,9 @@ size_t sq_prepare_weights_workspace_bytes(int32_t N, int32_t K, int32_t has_P);
  * partial sums for short M); 0 means ws may be NULL. */
 size_t sq_gemm_workspace_bytes(int32_t M, int32_t N, int32_t K);
 
+/* The same for w8a8_gemm. */
+size_t sq_gemm_w8_workspace_bytes(int32_t M, int32_t N, int32_t K);
+
 /*
  * sgat_prepare_weights -- offline weight side of SGAT (Eq. 12; App. A, App. B).
  * W~ = Q_w(P^T W^T) is stored transposed, as the rows of W P: for output channel
@@ -143,6 +146,7 @@ int sgat_quant_act(const uint16_t* X, const uint8_t* state, const float* P,
  *   Y    out [M][N] fp16 (may be NULL if acc is given).
  *   acc  out [M][N] int32, or NULL.
  *   ws   device workspace of at least sq_gemm_workspace_bytes(M, N, K).
+ *   Each packed operand must be smaller than 2 GiB (M K / 2 and N K / 2 bytes).
  */
 int w4a4_gemm(const uint8_t* Aq, const float* s_a, const uint8_t* Wq, const float* s_w,
               int32_t M, int32_t N, int32_t K, uint16_t* Y, int32_t* acc,
@@ -158,6 +162,29 @@ int w4a4_gemm(const uint8_t* Aq, const float* s_a, const uint8_t* Wq, const floa
  */
 int tac_apply(const uint16_t* Z, const uint16_t* tac_M, const uint16_t* tac_d,
               int32_t M, int32_t C, int32_t g, uint16_t* Z_out, void* stream);
+
+/*
+ * W8A8 variant (App. D: the same method at 8 bits).  Identical arguments and
+ * arithmetic to the 4-bit calls above except for the quantiser, s = absmax / 127
+ * and codes clamp(rint(x / s), -128, 127), and the code layout: one signed byte
+ * per code, rows of K bytes.
+ *   sgat_prepare_weights_w8 -- Wq out [N][K] int8 (as sgat_prepare_weights).
+ *   sgat_quantize_w8        -- Aq out [M][K] int8 (as sgat_quantize).
+ *   sgat_quant_act_w8       -- Aq out [M][K] int8 (as sgat_quant_act).
+ *   w8a8_gemm               -- acc = sum_j qa qw (int32), Y = fp16((acc * s_a) * s_w);
+ *                              K <= 65536 so |acc| < 2^31; operands under 2 GiB;
+ *                              ws of at least sq_gemm_w8_workspace_bytes(M, N, K).
+ */
+int sgat_prepare_weights_w8(const uint16_t* W, const float* P, int32_t N, int32_t K,
+                            int8_t* Wq, float* s_w, void* ws, size_t ws_bytes, void* stream);
+int sgat_quantize_w8(const float* Xp, int32_t M, int32_t K, int8_t* Aq, float* s, void* stream);
+int sgat_quant_act_w8(const uint16_t* X, const uint8_t* state, const float* P,
+                      int32_t M, int32_t K, int32_t d_m, int32_t d_u,
+                      const uint16_t* tac_M, const uint16_t* tac_d, int32_t g,
+                      int8_t* Aq, float* s_a, void* ws, size_t ws_bytes, void* stream);
+int w8a8_gemm(const int8_t* Aq, const float* s_a, const int8_t* Wq, const float* s_w,
+              int32_t M, int32_t N, int32_t K, uint16_t* Y, int32_t* acc,
+              void* ws, size_t ws_bytes, void* stream);
 
 #ifdef __cplusplus
 }

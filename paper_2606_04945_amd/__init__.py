@@ -20,7 +20,8 @@ from ._lib import SQ_OK, StarQuantError, check, lib  # noqa: F401
 
 __all__ = ["sgat_prepare_weights", "sgat_transform", "sgat_quantize", "sgat_quant_act", "w4a4_gemm", "tac_apply",
            "tac_default_block", "default_band", "quant_act_workspace_bytes", "gemm_workspace_bytes",
-           "prepare_weights_workspace_bytes", "StarQuantError", "lib"]
+           "prepare_weights_workspace_bytes", "StarQuantError", "lib",
+           "sgat_prepare_weights_w8", "sgat_quantize_w8", "sgat_quant_act_w8", "w8a8_gemm"]
 
 
 def _ptr(t: Optional[torch.Tensor]):
@@ -73,25 +74,38 @@ def prepare_weights_workspace_bytes(N: int, K: int, has_P: bool) -> int:
     return int(lib().sq_prepare_weights_workspace_bytes(N, K, int(has_P)))
 
 
-def gemm_workspace_bytes(M: int, N: int, K: int) -> int:
-    return int(lib().sq_gemm_workspace_bytes(M, N, K))
+def gemm_workspace_bytes(M: int, N: int, K: int, bits: int = 4) -> int:
+    f = lib().sq_gemm_w8_workspace_bytes if bits == 8 else lib().sq_gemm_workspace_bytes
+    return int(f(M, N, K))
+
+
+def _codes_spec(bits: int, K: int):
+    """(dtype, row width) of a code tensor: packed int4 uint8 [K/2] or int8 [K]."""
+    return (torch.int8, K) if bits == 8 else (torch.uint8, K // 2)
 
 
 def sgat_prepare_weights(W: torch.Tensor, P: Optional[torch.Tensor] = None, *, Wq=None, s_w=None, ws=None,
-                         stream=None):
-    """W~ = Q_w(P^T W^T) as rows of W P: returns (Wq [N][K/2] uint8, s_w [N] fp32)."""
+                         stream=None, bits: int = 4):
+    """W~ = Q_w(P^T W^T) as rows of W P: returns (Wq, s_w [N] fp32); Wq is [N][K/2]
+    packed int4 (bits=4) or [N][K] int8 (bits=8, App. D)."""
     N, K = W.shape
+    dt, kw = _codes_spec(bits, K)
     _need(W, "W", torch.float16)
     _need(P, "P", torch.float32, (K, K), optional=True)
     if Wq is None:
-        Wq = torch.empty((N, K // 2), dtype=torch.uint8, device=W.device)
+        Wq = torch.empty((N, kw), dtype=dt, device=W.device)
     if s_w is None:
         s_w = torch.empty((N,), dtype=torch.float32, device=W.device)
-    _need(Wq, "Wq", torch.uint8, (N, K // 2))
+    _need(Wq, "Wq", dt, (N, kw))
     _need(s_w, "s_w", torch.float32, (N,))
     ws, wsb = _ws(prepare_weights_workspace_bytes(N, K, P is not None), ws, W.device)
-    check(lib().sgat_prepare_weights(_ptr(W), _ptr(P), N, K, _ptr(Wq), _ptr(s_w), _ptr(ws), wsb, _stream(stream)))
+    f = lib().sgat_prepare_weights_w8 if bits == 8 else lib().sgat_prepare_weights
+    check(f(_ptr(W), _ptr(P), N, K, _ptr(Wq), _ptr(s_w), _ptr(ws), wsb, _stream(stream)))
     return Wq, s_w
+
+
+def sgat_prepare_weights_w8(W, P=None, **kw):
+    return sgat_prepare_weights(W, P, bits=8, **kw)
 
 
 def sgat_transform(X: torch.Tensor, state: Optional[torch.Tensor], P: Optional[torch.Tensor],
@@ -111,25 +125,34 @@ def sgat_transform(X: torch.Tensor, state: Optional[torch.Tensor], P: Optional[t
     return out
 
 
-def sgat_quantize(Xp: torch.Tensor, *, Aq=None, s=None, stream=None):
-    """Per-row symmetric int4 of fp32 rows (Eq. 2, z = 0): returns (Aq [M][K/2] uint8, s [M] fp32)."""
+def sgat_quantize(Xp: torch.Tensor, *, Aq=None, s=None, stream=None, bits: int = 4):
+    """Per-row symmetric quantisation of fp32 rows (Eq. 2, z = 0): returns (Aq, s [M] fp32)."""
     M, K = Xp.shape
+    dt, kw = _codes_spec(bits, K)
     _need(Xp, "Xp", torch.float32)
     if Aq is None:
-        Aq = torch.empty((M, K // 2), dtype=torch.uint8, device=Xp.device)
+        Aq = torch.empty((M, kw), dtype=dt, device=Xp.device)
     if s is None:
         s = torch.empty((M,), dtype=torch.float32, device=Xp.device)
-    _need(Aq, "Aq", torch.uint8, (M, K // 2))
+    _need(Aq, "Aq", dt, (M, kw))
     _need(s, "s", torch.float32, (M,))
-    check(lib().sgat_quantize(_ptr(Xp), M, K, _ptr(Aq), _ptr(s), _stream(stream)))
+    f = lib().sgat_quantize_w8 if bits == 8 else lib().sgat_quantize
+    check(f(_ptr(Xp), M, K, _ptr(Aq), _ptr(s), _stream(stream)))
     return Aq, s
+
+
+def sgat_quantize_w8(Xp, **kw):
+    return sgat_quantize(Xp, bits=8, **kw)
 
 
 def sgat_quant_act(X: torch.Tensor, state: Optional[torch.Tensor], P: Optional[torch.Tensor] = None,
                    d_m: Optional[int] = None, d_u: Optional[int] = None, tac_M: Optional[torch.Tensor] = None,
-                   tac_d: Optional[torch.Tensor] = None, g: int = 0, *, Aq=None, s_a=None, ws=None, stream=None):
-    """[TAC] -> x P G_s -> per-token int4: returns (Aq [M][K/2] uint8, s_a [M] fp32)."""
+                   tac_d: Optional[torch.Tensor] = None, g: int = 0, *, Aq=None, s_a=None, ws=None, stream=None,
+                   bits: int = 4):
+    """[TAC] -> x P G_s -> per-token codes: returns (Aq, s_a [M] fp32), Aq packed int4
+    [M][K/2] uint8 (bits=4) or int8 [M][K] (bits=8)."""
     M, K = X.shape
+    dt, kw = _codes_spec(bits, K)
     dm0, du0 = default_band(K)
     d_m = dm0 if d_m is None else d_m
     d_u = du0 if d_u is None else d_u
@@ -140,25 +163,32 @@ def sgat_quant_act(X: torch.Tensor, state: Optional[torch.Tensor], P: Optional[t
         _need(tac_M, "tac_M", torch.float16, (K // g, g, g))
         _need(tac_d, "tac_d", torch.float16, (K,))
     if Aq is None:
-        Aq = torch.empty((M, K // 2), dtype=torch.uint8, device=X.device)
+        Aq = torch.empty((M, kw), dtype=dt, device=X.device)
     if s_a is None:
         s_a = torch.empty((M,), dtype=torch.float32, device=X.device)
-    _need(Aq, "Aq", torch.uint8, (M, K // 2))
+    _need(Aq, "Aq", dt, (M, kw))
     _need(s_a, "s_a", torch.float32, (M,))
     ws, wsb = _ws(quant_act_workspace_bytes(M, K, P is not None, tac_M is not None), ws, X.device)
-    check(lib().sgat_quant_act(_ptr(X), _ptr(state), _ptr(P), M, K, d_m, d_u, _ptr(tac_M), _ptr(tac_d), g,
-                               _ptr(Aq), _ptr(s_a), _ptr(ws), wsb, _stream(stream)))
+    f = lib().sgat_quant_act_w8 if bits == 8 else lib().sgat_quant_act
+    check(f(_ptr(X), _ptr(state), _ptr(P), M, K, d_m, d_u, _ptr(tac_M), _ptr(tac_d), g,
+            _ptr(Aq), _ptr(s_a), _ptr(ws), wsb, _stream(stream)))
     return Aq, s_a
 
 
+def sgat_quant_act_w8(X, state, P=None, d_m=None, d_u=None, tac_M=None, tac_d=None, g=0, **kw):
+    return sgat_quant_act(X, state, P, d_m, d_u, tac_M, tac_d, g, bits=8, **kw)
+
+
 def w4a4_gemm(Aq: torch.Tensor, s_a: torch.Tensor, Wq: torch.Tensor, s_w: torch.Tensor, *, Y=None, acc=None,
-              want_Y: bool = True, want_acc: bool = False, ws=None, stream=None):
-    """Y = fp16((acc * s_a) * s_w) with acc = Aq . Wq^T exact (Eq. 13).  Returns Y, or (Y, acc)."""
-    M, Kh = Aq.shape
+              want_Y: bool = True, want_acc: bool = False, ws=None, stream=None, bits: int = 4):
+    """Y = fp16((acc * s_a) * s_w) with acc = Aq . Wq^T exact (Eq. 13).  Returns Y, or (Y, acc).
+    bits=8 takes int8 codes (App. D)."""
+    M, Kc = Aq.shape
     N = Wq.shape[0]
-    K = 2 * Kh
-    _need(Aq, "Aq", torch.uint8)
-    _need(Wq, "Wq", torch.uint8, (N, Kh))
+    dt = torch.int8 if bits == 8 else torch.uint8
+    K = Kc if bits == 8 else 2 * Kc
+    _need(Aq, "Aq", dt)
+    _need(Wq, "Wq", dt, (N, Kc))
     _need(s_a, "s_a", torch.float32, (M,))
     _need(s_w, "s_w", torch.float32, (N,))
     if Y is None and want_Y:
@@ -167,10 +197,14 @@ def w4a4_gemm(Aq: torch.Tensor, s_a: torch.Tensor, Wq: torch.Tensor, s_w: torch.
         acc = torch.empty((M, N), dtype=torch.int32, device=Aq.device)
     _need(Y, "Y", torch.float16, (M, N), optional=True)
     _need(acc, "acc", torch.int32, (M, N), optional=True)
-    ws, wsb = _ws(gemm_workspace_bytes(M, N, K), ws, Aq.device)
-    check(lib().w4a4_gemm(_ptr(Aq), _ptr(s_a), _ptr(Wq), _ptr(s_w), M, N, K, _ptr(Y), _ptr(acc), _ptr(ws), wsb,
-                          _stream(stream)))
+    ws, wsb = _ws(gemm_workspace_bytes(M, N, K, bits), ws, Aq.device)
+    f = lib().w8a8_gemm if bits == 8 else lib().w4a4_gemm
+    check(f(_ptr(Aq), _ptr(s_a), _ptr(Wq), _ptr(s_w), M, N, K, _ptr(Y), _ptr(acc), _ptr(ws), wsb, _stream(stream)))
     return (Y, acc) if want_acc else Y
+
+
+def w8a8_gemm(Aq, s_a, Wq, s_w, **kw):
+    return w4a4_gemm(Aq, s_a, Wq, s_w, bits=8, **kw)
 
 
 def tac_apply(Z: torch.Tensor, tac_M: torch.Tensor, tac_d: torch.Tensor, g: int, *, out=None, stream=None):

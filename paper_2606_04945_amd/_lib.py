@@ -19,12 +19,17 @@ SIGNATURES = {
     "sq_quant_act_workspace_bytes": (_sz, [_i32, _i32, _i32, _i32]),
     "sq_prepare_weights_workspace_bytes": (_sz, [_i32, _i32, _i32]),
     "sq_gemm_workspace_bytes": (_sz, [_i32, _i32, _i32]),
+    "sq_gemm_w8_workspace_bytes": (_sz, [_i32, _i32, _i32]),
     "sgat_prepare_weights": (ctypes.c_int, [_p, _p, _i32, _i32, _p, _p, _p, _sz, _p]),
     "sgat_transform": (ctypes.c_int, [_p, _p, _p, _i32, _i32, _i32, _i32, _p, _p]),
     "sgat_quantize": (ctypes.c_int, [_p, _i32, _i32, _p, _p, _p]),
     "sgat_quant_act": (ctypes.c_int, [_p, _p, _p, _i32, _i32, _i32, _i32, _p, _p, _i32, _p, _p, _p, _sz, _p]),
     "w4a4_gemm": (ctypes.c_int, [_p, _p, _p, _p, _i32, _i32, _i32, _p, _p, _p, _sz, _p]),
     "tac_apply": (ctypes.c_int, [_p, _p, _p, _i32, _i32, _i32, _p, _p]),
+    "sgat_prepare_weights_w8": (ctypes.c_int, [_p, _p, _i32, _i32, _p, _p, _p, _sz, _p]),
+    "sgat_quantize_w8": (ctypes.c_int, [_p, _i32, _i32, _p, _p, _p]),
+    "sgat_quant_act_w8": (ctypes.c_int, [_p, _p, _p, _i32, _i32, _i32, _i32, _p, _p, _i32, _p, _p, _p, _sz, _p]),
+    "w8a8_gemm": (ctypes.c_int, [_p, _p, _p, _p, _i32, _i32, _i32, _p, _p, _p, _sz, _p]),
 }
 
 

@@ -88,25 +88,119 @@ size_t sq_prepare_weights_workspace_bytes(int32_t N, int32_t K, int32_t has_P) {
 
 size_t sq_gemm_workspace_bytes(int32_t M, int32_t N, int32_t K) {
     if (M <= 0 || N <= 0 || K <= 0) return 0;
-    return round_up(sq::gemm_workspace_bytes(M, N, K));
+    return round_up(sq::gemm_workspace_bytes(M, N, K, 4));
 }
 
-int sgat_prepare_weights(const uint16_t* W, const float* P, int32_t N, int32_t K, uint8_t* Wq, float* s_w,
-                         void* ws, size_t ws_bytes, void* stream) {
+size_t sq_gemm_w8_workspace_bytes(int32_t M, int32_t N, int32_t K) {
+    if (M <= 0 || N <= 0 || K <= 0) return 0;
+    return round_up(sq::gemm_workspace_bytes(M, N, K, 8));
+}
+
+}  // extern "C"
+
+namespace {
+
+int prepare_weights(const uint16_t* W, const float* P, int32_t N, int32_t K, uint8_t* Wq, float* s_w, void* ws,
+                    size_t ws_bytes, void* stream, int bits, const char* name) {
     SQ_TRY(check_K(K));
     SQ_REQUIRE(N >= 0, SQ_ERR_SHAPE, "N=%d < 0", N);
     if (N == 0) return SQ_OK;
-    SQ_REQUIRE(W && Wq && s_w, SQ_ERR_NULL, "sgat_prepare_weights: W, Wq and s_w are required");
+    SQ_REQUIRE(W && Wq && s_w, SQ_ERR_NULL, "%s: W, Wq and s_w are required", name);
     SQ_REQUIRE(aligned16(W) && aligned16(Wq) && aligned16(s_w) && aligned16(P) && aligned16(ws), SQ_ERR_ALIGN,
-               "sgat_prepare_weights: pointers must be 16-byte aligned");
+               "%s: pointers must be 16-byte aligned", name);
     const size_t need = sq_prepare_weights_workspace_bytes(N, K, P != nullptr);
-    SQ_REQUIRE(ws_bytes >= need && (need == 0 || ws), SQ_ERR_WORKSPACE,
-               "sgat_prepare_weights: workspace %zu B < %zu B", ws_bytes, need);
+    SQ_REQUIRE(ws_bytes >= need && (need == 0 || ws), SQ_ERR_WORKSPACE, "%s: workspace %zu B < %zu B", name,
+               ws_bytes, need);
     hipStream_t st = static_cast<hipStream_t>(stream);
-    if (!P) return hip_status(sq::launch_quant_f16(W, nullptr, N, K, 0, 0, Wq, s_w, st), "quant_f16");
+    if (!P) return hip_status(sq::launch_quant_f16(W, nullptr, N, K, 0, 0, Wq, s_w, st, bits), "quant_f16");
     float* wp = static_cast<float*>(ws);
     SQ_TRY(hip_status(sq::launch_transform(W, nullptr, P, N, K, 0, 0, wp, st), "transform"));
-    return hip_status(sq::launch_quant_f32(wp, N, K, Wq, s_w, st), "quant_f32");
+    return hip_status(sq::launch_quant_f32(wp, N, K, Wq, s_w, st, bits), "quant_f32");
+}
+
+int quantize(const float* Xp, int32_t M, int32_t K, uint8_t* Aq, float* s, void* stream, int bits,
+             const char* name) {
+    SQ_TRY(check_K(K));
+    SQ_REQUIRE(M >= 0, SQ_ERR_SHAPE, "M=%d < 0", M);
+    if (M == 0) return SQ_OK;
+    SQ_REQUIRE(Xp && Aq && s, SQ_ERR_NULL, "%s: Xp, Aq and s are required", name);
+    SQ_REQUIRE(aligned16(Xp) && aligned16(Aq) && aligned16(s), SQ_ERR_ALIGN, "%s: pointers must be 16-byte aligned",
+               name);
+    return hip_status(sq::launch_quant_f32(Xp, M, K, Aq, s, static_cast<hipStream_t>(stream), bits), "quant_f32");
+}
+
+int quant_act(const uint16_t* X, const uint8_t* state, const float* P, int32_t M, int32_t K, int32_t d_m,
+              int32_t d_u, const uint16_t* tac_M, const uint16_t* tac_d, int32_t g, uint8_t* Aq, float* s_a,
+              void* ws, size_t ws_bytes, void* stream, int bits, const char* name) {
+    SQ_TRY(check_K(K));
+    SQ_TRY(check_band(K, d_m, d_u));
+    SQ_REQUIRE(M >= 0, SQ_ERR_SHAPE, "M=%d < 0", M);
+    if (tac_M) {
+        SQ_REQUIRE(tac_d, SQ_ERR_NULL, "%s: tac_d is required with tac_M", name);
+        SQ_TRY(check_tac(K, g));
+    }
+    if (M == 0) return SQ_OK;
+    SQ_REQUIRE(X && Aq && s_a, SQ_ERR_NULL, "%s: X, Aq and s_a are required", name);
+    SQ_REQUIRE(aligned16(X) && aligned16(Aq) && aligned16(s_a) && aligned16(P) && aligned16(ws) &&
+                   aligned16(tac_M) && aligned16(tac_d),
+               SQ_ERR_ALIGN, "%s: pointers must be 16-byte aligned", name);
+    const size_t need = sq_quant_act_workspace_bytes(M, K, P != nullptr, tac_M != nullptr);
+    SQ_REQUIRE(ws_bytes >= need && (need == 0 || ws), SQ_ERR_WORKSPACE, "%s: workspace %zu B < %zu B", name,
+               ws_bytes, need);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    if (tac_M && !P && sq::tac_quant_fusable(K, g))
+        return hip_status(sq::launch_tac_quant(X, tac_M, tac_d, state, M, K, g, d_m, d_u, Aq, s_a, st, bits),
+                          "tac_quant");
+    uint8_t* wsb = static_cast<uint8_t*>(ws);
+    const uint16_t* src = X;
+    if (tac_M) {
+        uint16_t* z = reinterpret_cast<uint16_t*>(wsb);
+        SQ_TRY(hip_status(sq::launch_tac(X, tac_M, tac_d, M, K, g, z, st), "tac"));
+        src = z;
+        wsb += round_up((size_t)M * K * sizeof(uint16_t));
+    }
+    if (!P) return hip_status(sq::launch_quant_f16(src, state, M, K, d_m, d_u, Aq, s_a, st, bits), "quant_f16");
+    float* xp = reinterpret_cast<float*>(wsb);
+    SQ_TRY(hip_status(sq::launch_transform(src, state, P, M, K, d_m, d_u, xp, st), "transform"));
+    return hip_status(sq::launch_quant_f32(xp, M, K, Aq, s_a, st, bits), "quant_f32");
+}
+
+int gemm(const uint8_t* Aq, const float* s_a, const uint8_t* Wq, const float* s_w, int32_t M, int32_t N, int32_t K,
+         uint16_t* Y, int32_t* acc, void* ws, size_t ws_bytes, void* stream, int bits, const char* name) {
+    SQ_TRY(check_K(K));
+    SQ_REQUIRE(bits == 4 || K <= 65536, SQ_ERR_SHAPE, "%s: K=%d: 8-bit codes need K <= 65536", name, K);
+    SQ_REQUIRE(M >= 0 && N >= 0, SQ_ERR_SHAPE, "M=%d N=%d: need >= 0", M, N);
+    SQ_REQUIRE(N % 8 == 0, SQ_ERR_SHAPE, "N=%d: need N %% 8 == 0", N);
+    // operand rows are addressed with 32-bit buffer offsets
+    const size_t row_bytes = (size_t)K * bits / 8;
+    SQ_REQUIRE((size_t)M * row_bytes < (1u << 31) && (size_t)N * row_bytes < (1u << 31), SQ_ERR_SHAPE,
+               "%s: each operand must be under 2 GiB (M=%d N=%d K=%d)", name, M, N, K);
+    if (M == 0 || N == 0) return SQ_OK;
+    SQ_REQUIRE(Aq && s_a && Wq && s_w && (Y || acc), SQ_ERR_NULL,
+               "%s: Aq, s_a, Wq, s_w and one of Y / acc are required", name);
+    SQ_REQUIRE(aligned16(Aq) && aligned16(s_a) && aligned16(Wq) && aligned16(s_w) && aligned16(Y) &&
+                   aligned16(acc) && aligned16(ws),
+               SQ_ERR_ALIGN, "%s: pointers must be 16-byte aligned", name);
+    const size_t need = bits == 8 ? sq_gemm_w8_workspace_bytes(M, N, K) : sq_gemm_workspace_bytes(M, N, K);
+    SQ_REQUIRE(ws_bytes >= need && (need == 0 || ws), SQ_ERR_WORKSPACE, "%s: workspace %zu B < %zu B", name,
+               ws_bytes, need);
+    return hip_status(
+        sq::launch_gemm(Aq, s_a, Wq, s_w, M, N, K, Y, acc, ws, static_cast<hipStream_t>(stream), bits), "gemm");
+}
+
+}  // namespace
+
+extern "C" {
+
+int sgat_prepare_weights(const uint16_t* W, const float* P, int32_t N, int32_t K, uint8_t* Wq, float* s_w,
+                         void* ws, size_t ws_bytes, void* stream) {
+    return prepare_weights(W, P, N, K, Wq, s_w, ws, ws_bytes, stream, 4, "sgat_prepare_weights");
+}
+
+int sgat_prepare_weights_w8(const uint16_t* W, const float* P, int32_t N, int32_t K, int8_t* Wq, float* s_w,
+                            void* ws, size_t ws_bytes, void* stream) {
+    return prepare_weights(W, P, N, K, reinterpret_cast<uint8_t*>(Wq), s_w, ws, ws_bytes, stream, 8,
+                           "sgat_prepare_weights_w8");
 }
 
 int sgat_transform(const uint16_t* X, const uint8_t* state, const float* P, int32_t M, int32_t K, int32_t d_m,
@@ -123,66 +217,36 @@ int sgat_transform(const uint16_t* X, const uint8_t* state, const float* P, int3
 }
 
 int sgat_quantize(const float* Xp, int32_t M, int32_t K, uint8_t* Aq, float* s, void* stream) {
-    SQ_TRY(check_K(K));
-    SQ_REQUIRE(M >= 0, SQ_ERR_SHAPE, "M=%d < 0", M);
-    if (M == 0) return SQ_OK;
-    SQ_REQUIRE(Xp && Aq && s, SQ_ERR_NULL, "sgat_quantize: Xp, Aq and s are required");
-    SQ_REQUIRE(aligned16(Xp) && aligned16(Aq) && aligned16(s), SQ_ERR_ALIGN,
-               "sgat_quantize: pointers must be 16-byte aligned");
-    return hip_status(sq::launch_quant_f32(Xp, M, K, Aq, s, static_cast<hipStream_t>(stream)), "quant_f32");
+    return quantize(Xp, M, K, Aq, s, stream, 4, "sgat_quantize");
+}
+
+int sgat_quantize_w8(const float* Xp, int32_t M, int32_t K, int8_t* Aq, float* s, void* stream) {
+    return quantize(Xp, M, K, reinterpret_cast<uint8_t*>(Aq), s, stream, 8, "sgat_quantize_w8");
 }
 
 int sgat_quant_act(const uint16_t* X, const uint8_t* state, const float* P, int32_t M, int32_t K, int32_t d_m,
                    int32_t d_u, const uint16_t* tac_M, const uint16_t* tac_d, int32_t g, uint8_t* Aq, float* s_a,
                    void* ws, size_t ws_bytes, void* stream) {
-    SQ_TRY(check_K(K));
-    SQ_TRY(check_band(K, d_m, d_u));
-    SQ_REQUIRE(M >= 0, SQ_ERR_SHAPE, "M=%d < 0", M);
-    if (tac_M) {
-        SQ_REQUIRE(tac_d, SQ_ERR_NULL, "sgat_quant_act: tac_d is required with tac_M");
-        SQ_TRY(check_tac(K, g));
-    }
-    if (M == 0) return SQ_OK;
-    SQ_REQUIRE(X && Aq && s_a, SQ_ERR_NULL, "sgat_quant_act: X, Aq and s_a are required");
-    SQ_REQUIRE(aligned16(X) && aligned16(Aq) && aligned16(s_a) && aligned16(P) && aligned16(ws) &&
-                   aligned16(tac_M) && aligned16(tac_d),
-               SQ_ERR_ALIGN, "sgat_quant_act: pointers must be 16-byte aligned");
-    const size_t need = sq_quant_act_workspace_bytes(M, K, P != nullptr, tac_M != nullptr);
-    SQ_REQUIRE(ws_bytes >= need && (need == 0 || ws), SQ_ERR_WORKSPACE,
-               "sgat_quant_act: workspace %zu B < %zu B", ws_bytes, need);
-    hipStream_t st = static_cast<hipStream_t>(stream);
-    if (tac_M && !P && sq::tac_quant_fusable(K, g))
-        return hip_status(sq::launch_tac_quant(X, tac_M, tac_d, state, M, K, g, d_m, d_u, Aq, s_a, st), "tac_quant");
-    uint8_t* wsb = static_cast<uint8_t*>(ws);
-    const uint16_t* src = X;
-    if (tac_M) {
-        uint16_t* z = reinterpret_cast<uint16_t*>(wsb);
-        SQ_TRY(hip_status(sq::launch_tac(X, tac_M, tac_d, M, K, g, z, st), "tac"));
-        src = z;
-        wsb += round_up((size_t)M * K * sizeof(uint16_t));
-    }
-    if (!P) return hip_status(sq::launch_quant_f16(src, state, M, K, d_m, d_u, Aq, s_a, st), "quant_f16");
-    float* xp = reinterpret_cast<float*>(wsb);
-    SQ_TRY(hip_status(sq::launch_transform(src, state, P, M, K, d_m, d_u, xp, st), "transform"));
-    return hip_status(sq::launch_quant_f32(xp, M, K, Aq, s_a, st), "quant_f32");
+    return quant_act(X, state, P, M, K, d_m, d_u, tac_M, tac_d, g, Aq, s_a, ws, ws_bytes, stream, 4,
+                     "sgat_quant_act");
+}
+
+int sgat_quant_act_w8(const uint16_t* X, const uint8_t* state, const float* P, int32_t M, int32_t K, int32_t d_m,
+                      int32_t d_u, const uint16_t* tac_M, const uint16_t* tac_d, int32_t g, int8_t* Aq,
+                      float* s_a, void* ws, size_t ws_bytes, void* stream) {
+    return quant_act(X, state, P, M, K, d_m, d_u, tac_M, tac_d, g, reinterpret_cast<uint8_t*>(Aq), s_a, ws,
+                     ws_bytes, stream, 8, "sgat_quant_act_w8");
 }
 
 int w4a4_gemm(const uint8_t* Aq, const float* s_a, const uint8_t* Wq, const float* s_w, int32_t M, int32_t N,
               int32_t K, uint16_t* Y, int32_t* acc, void* ws, size_t ws_bytes, void* stream) {
-    SQ_TRY(check_K(K));
-    SQ_REQUIRE(M >= 0 && N >= 0, SQ_ERR_SHAPE, "M=%d N=%d: need >= 0", M, N);
-    SQ_REQUIRE(N % 8 == 0, SQ_ERR_SHAPE, "N=%d: need N %% 8 == 0", N);
-    if (M == 0 || N == 0) return SQ_OK;
-    SQ_REQUIRE(Aq && s_a && Wq && s_w && (Y || acc), SQ_ERR_NULL,
-               "w4a4_gemm: Aq, s_a, Wq, s_w and one of Y / acc are required");
-    SQ_REQUIRE(aligned16(Aq) && aligned16(s_a) && aligned16(Wq) && aligned16(s_w) && aligned16(Y) &&
-                   aligned16(acc) && aligned16(ws),
-               SQ_ERR_ALIGN, "w4a4_gemm: pointers must be 16-byte aligned");
-    const size_t need = sq_gemm_workspace_bytes(M, N, K);
-    SQ_REQUIRE(ws_bytes >= need && (need == 0 || ws), SQ_ERR_WORKSPACE, "w4a4_gemm: workspace %zu B < %zu B",
-               ws_bytes, need);
-    return hip_status(sq::launch_gemm(Aq, s_a, Wq, s_w, M, N, K, Y, acc, ws, static_cast<hipStream_t>(stream)),
-                      "gemm");
+    return gemm(Aq, s_a, Wq, s_w, M, N, K, Y, acc, ws, ws_bytes, stream, 4, "w4a4_gemm");
+}
+
+int w8a8_gemm(const int8_t* Aq, const float* s_a, const int8_t* Wq, const float* s_w, int32_t M, int32_t N,
+              int32_t K, uint16_t* Y, int32_t* acc, void* ws, size_t ws_bytes, void* stream) {
+    return gemm(reinterpret_cast<const uint8_t*>(Aq), s_a, reinterpret_cast<const uint8_t*>(Wq), s_w, M, N, K, Y,
+                acc, ws, ws_bytes, stream, 8, "w8a8_gemm");
 }
 
 int tac_apply(const uint16_t* Z, const uint16_t* tac_M, const uint16_t* tac_d, int32_t M, int32_t C, int32_t g,

@@ -23,6 +23,9 @@
 // are XOR-swizzled by 16-byte chunk so the row-wise fragment reads and the
 // segment-wise stores are free of bank conflicts.  Short M splits K across
 // workgroups; the int32 partial sums are then added exactly by a small kernel.
+//
+// BITS = 8 is the W8A8 variant (App. D): codes are int8 already, so the same
+// tiles feed the MFMA straight from LDS with no unpacking and no scaling.
 #include "sq_internal.hpp"
 
 namespace sq {
@@ -45,7 +48,19 @@ __device__ __forceinline__ void store_out(int row, int col, int v, const float* 
     if (Y) Y[o] = f2h(((float)v * s_a[row]) * s_w[col]);
 }
 
-constexpr int kKB = 64;                              // packed bytes per row per k step (128 codes)
+constexpr int kKB = 64;                              // bytes per row per k step (128 4-bit / 64 8-bit codes)
+
+// MFMA operand for step h of a lane's 16-byte fragment: two int4 halves unpacked
+// (4-bit) or the int8 codes themselves (8-bit, one step)
+template <int BITS>
+__device__ __forceinline__ v4i operand(const v4i& raw, int h) {
+    if (BITS == 8) return raw;
+    return h ? unpack_op(raw[2], raw[3]) : unpack_op(raw[0], raw[1]);
+}
+template <int BITS>
+__device__ __forceinline__ int acc_value(int raw) {   // 4-bit operands carry a factor 16 each
+    return BITS == 8 ? raw : raw >> 8;
+}
 
 template <int WM, int WN, int TM, int TN, bool UNPACK>
 struct GemmCfg {
@@ -73,7 +88,7 @@ constexpr uint32_t kOOB = 0x80000000u;   // an offset past any buffer this kerne
 
 // SPLIT == false: full K, fused epilogue.  SPLIT == true: K range of blockIdx.z,
 // raw int32 sums to part[z][M][N].
-template <int WM, int WN, int TM, int TN, bool UNPACK, bool SPLIT, int SCHED = 0>
+template <int WM, int WN, int TM, int TN, bool UNPACK, bool SPLIT, int SCHED = 0, int BITS = 4>
 __global__ __launch_bounds__(64 * WM * WN) void gemm_kernel(const uint8_t* __restrict__ Aq,
                                                            const float* __restrict__ s_a,
                                                            const uint8_t* __restrict__ Wq,
@@ -83,6 +98,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_kernel(const uint8_t* __res
                                                            int32_t* __restrict__ part) {
     using C = GemmCfg<WM, WN, TM, TN, UNPACK>;
     static_assert(C::BM * C::SEG % C::NT == 0 && C::BN * C::SEG % C::NT == 0, "tile loads must divide evenly");
+    static_assert(BITS == 4 || (BITS == 8 && !UNPACK && SCHED), "8-bit codes use the one-fragment loop");
     __shared__ __attribute__((aligned(16))) uint8_t sA[2][C::BM * C::RB];
     __shared__ __attribute__((aligned(16))) uint8_t sB[2][C::BN * C::RB];
 
@@ -90,7 +106,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_kernel(const uint8_t* __res
     const int lane = tid % kWave, wave = tid / kWave;
     const int wm = wave / WN, wn = wave % WN;
     const int row0 = blockIdx.y * C::BM, col0 = blockIdx.x * C::BN;
-    const uint32_t ldb = (uint32_t)K / 2;                // bytes per packed row
+    const uint32_t ldb = (uint32_t)K * BITS / 8;         // bytes per row of codes
 
     const int nk_total = (int)((ldb + kKB - 1) / kKB);   // the last step may be half empty
     const int nk_full = (int)(ldb / kKB);                // steps with every byte in range
@@ -172,46 +188,43 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_kernel(const uint8_t* __res
         const int buf = (kt - kt0) & 1;
         if (kt + 1 < kt1) load_step(kt + 1);
         if (SCHED && !UNPACK) {
-            // one 16-byte fragment per tile per k step; unpack both MFMA steps, and
-            // let the scheduler interleave the second step's unpacking with the
-            // first step's MFMAs
-            uint4 fa[TM], fb[TN];
+            // one 16-byte fragment per tile per k step; with 4-bit codes both MFMA
+            // steps are unpacked and the scheduler interleaves the second step's
+            // unpacking with the first step's MFMAs
+            constexpr int SUBS = BITS == 4 ? 2 : 1;
+            v4i fa[TM], fb[TN];
 #pragma unroll
             for (int i = 0; i < TM; ++i)
-                fa[i] = *reinterpret_cast<const uint4*>(&sA[buf][offA + i * 16 * C::RB + C::chunk(lr, lg) * 16]);
+                fa[i] = *reinterpret_cast<const v4i*>(&sA[buf][offA + i * 16 * C::RB + C::chunk(lr, lg) * 16]);
 #pragma unroll
             for (int j = 0; j < TN; ++j)
-                fb[j] = *reinterpret_cast<const uint4*>(&sB[buf][offB + j * 16 * C::RB + C::chunk(lr, lg) * 16]);
-            v4i a0[TM], b0[TN], a1[TM], b1[TN];
+                fb[j] = *reinterpret_cast<const v4i*>(&sB[buf][offB + j * 16 * C::RB + C::chunk(lr, lg) * 16]);
 #pragma unroll
-            for (int i = 0; i < TM; ++i) a0[i] = unpack_op(fa[i].x, fa[i].y);
+            for (int h = 0; h < SUBS; ++h) {
+                v4i a[TM], b[TN];
 #pragma unroll
-            for (int j = 0; j < TN; ++j) b0[j] = unpack_op(fb[j].x, fb[j].y);
+                for (int i = 0; i < TM; ++i) a[i] = operand<BITS>(fa[i], h);
 #pragma unroll
-            for (int i = 0; i < TM; ++i) a1[i] = unpack_op(fa[i].z, fa[i].w);
+                for (int j = 0; j < TN; ++j) b[j] = operand<BITS>(fb[j], h);
 #pragma unroll
-            for (int j = 0; j < TN; ++j) b1[j] = unpack_op(fb[j].z, fb[j].w);
+                for (int i = 0; i < TM; ++i)
 #pragma unroll
-            for (int i = 0; i < TM; ++i)
-#pragma unroll
-                for (int j = 0; j < TN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a0[i], b0[j], acc[i][j], 0, 0, 0);
-#pragma unroll
-            for (int i = 0; i < TM; ++i)
-#pragma unroll
-                for (int j = 0; j < TN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a1[i], b1[j], acc[i][j], 0, 0, 0);
-            constexpr int nmma = TM * TN;
-            constexpr int nvalu = 6 * (TM + TN);           // one MFMA step's unpacking
-            constexpr int per = (nvalu + nmma - 1) / nmma;
-            __builtin_amdgcn_sched_group_barrier(0x100, TM + TN, 0);     // fragment reads
-            __builtin_amdgcn_sched_group_barrier(0x002, nvalu, 0);       // step-0 unpack
-#pragma unroll
-            for (int q = 0; q < nmma; ++q) {
-                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);       // step-0 MFMA
-                __builtin_amdgcn_sched_group_barrier(0x002, per, 0);     // step-1 unpack
+                    for (int j = 0; j < TN; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[i], b[j], acc[i][j], 0, 0, 0);
             }
-            __builtin_amdgcn_sched_group_barrier(0x008, nmma, 0);        // step-1 MFMA
+            constexpr int nmma = TM * TN;
+            __builtin_amdgcn_sched_group_barrier(0x100, TM + TN, 0);         // fragment reads
+            if (BITS == 4) {
+                constexpr int nvalu = 6 * (TM + TN);                         // one MFMA step's unpacking
+                constexpr int per = (nvalu + nmma - 1) / nmma;
+                __builtin_amdgcn_sched_group_barrier(0x002, nvalu, 0);       // step-0 unpack
+#pragma unroll
+                for (int q = 0; q < nmma; ++q) {
+                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);       // step-0 MFMA
+                    __builtin_amdgcn_sched_group_barrier(0x002, per, 0);     // step-1 unpack
+                }
+            }
+            __builtin_amdgcn_sched_group_barrier(0x008, nmma, 0);            // remaining MFMAs
         } else {
             // k group lg of a lane covers packed bytes [16 lg, 16 lg + 16) of the row
             // slice; MFMA step h uses 8 of them (same bytes for A and W)
@@ -265,7 +278,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_kernel(const uint8_t* __res
             for (int r = 0; r < 4; ++r) {
                 const int row = row0 + (wm * TM + i) * 16 + lg * 4 + r;
                 if (row >= M) continue;
-                const int v = acc[i][j][r] >> 8;
+                const int v = acc_value<BITS>(acc[i][j][r]);
                 if (SPLIT)
                     part[((size_t)blockIdx.z * M + row) * N + col] = v;
                 else
@@ -281,7 +294,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_kernel(const uint8_t* __res
 // operand registers with raw buffer loads, U k steps in flight per batch.  Lane
 // (c, g) reads bytes [16 g, 16 g + 16) of the 64-byte slice of row c (W) or of
 // the activation row, exactly as the tiled kernel's fragments.
-template <int TM, int U, bool SPLIT>
+template <int TM, int U, bool SPLIT, int BITS = 4>
 __global__ __launch_bounds__(256) void gemm_skinny_kernel(const uint8_t* __restrict__ Aq,
                                                           const float* __restrict__ s_a,
                                                           const uint8_t* __restrict__ Wq,
@@ -293,7 +306,7 @@ __global__ __launch_bounds__(256) void gemm_skinny_kernel(const uint8_t* __restr
     const int lr = lane % 16, lg = lane / 16;
     const int col0 = (blockIdx.x * 4 + wave) * 16;
     if (col0 >= N) return;                                   // whole wave past N: nothing to do
-    const uint32_t ldb = (uint32_t)K / 2;
+    const uint32_t ldb = (uint32_t)K * BITS / 8;
     const int nk_total = (int)((ldb + kKB - 1) / kKB);
     const int kt0 = SPLIT ? blockIdx.z * ksteps_per_split : 0;
     const int kt1 = SPLIT ? min(nk_total, kt0 + ksteps_per_split) : nk_total;
@@ -325,13 +338,11 @@ __global__ __launch_bounds__(256) void gemm_skinny_kernel(const uint8_t* __restr
 #pragma unroll
         for (int u = 0; u < U; ++u) {
 #pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                const v4i b = h ? unpack_op(w[u][2], w[u][3]) : unpack_op(w[u][0], w[u][1]);
+            for (int h = 0; h < (BITS == 4 ? 2 : 1); ++h) {
+                const v4i b = operand<BITS>(w[u], h);
 #pragma unroll
-                for (int i = 0; i < TM; ++i) {
-                    const v4i x = h ? unpack_op(a[u][i][2], a[u][i][3]) : unpack_op(a[u][i][0], a[u][i][1]);
-                    acc[i] = __builtin_amdgcn_mfma_i32_16x16x64_i8(x, b, acc[i], 0, 0, 0);
-                }
+                for (int i = 0; i < TM; ++i)
+                    acc[i] = __builtin_amdgcn_mfma_i32_16x16x64_i8(operand<BITS>(a[u][i], h), b, acc[i], 0, 0, 0);
             }
         }
     };
@@ -354,7 +365,7 @@ __global__ __launch_bounds__(256) void gemm_skinny_kernel(const uint8_t* __restr
         for (int r = 0; r < 4; ++r) {
             const int row = 16 * i + 4 * lg + r;
             if (row >= M) continue;
-            const int v = acc[i][r] >> 8;
+            const int v = acc_value<BITS>(acc[i][r]);
             if (SPLIT)
                 part[((size_t)blockIdx.z * M + row) * N + col] = v;
             else
@@ -383,44 +394,44 @@ struct Plan {
     int per;       // k steps per split
 };
 
-Plan make_plan(int M, int N, int K, int bm, int bn, int want_splits) {
+Plan make_plan(int M, int N, int K, int bm, int bn, int want_splits, int bits = 4) {
     (void)M;
     (void)N;
     Plan p;
     p.cfg = -1;
     p.bm = bm;
     p.bn = bn;
-    const int nk = (K / 2 + kKB - 1) / kKB;
+    const int nk = (K * bits / 8 + kKB - 1) / kKB;
     const int s = want_splits < 1 ? 1 : (want_splits > nk ? nk : want_splits);
     p.per = (nk + s - 1) / s;
     p.splits = (nk + p.per - 1) / p.per;
     return p;
 }
 
-template <int TM, int U>
+template <int TM, int U, int BITS = 4>
 hipError_t launch_skinny(const Plan& p, const uint8_t* Aq, const float* s_a, const uint8_t* Wq, const float* s_w,
                          int M, int N, int K, uint16_t* Y, int32_t* acc, int32_t* part, hipStream_t st) {
     dim3 grid((N + 63) / 64, 1, p.splits);
     if (p.splits == 1) {
-        hipLaunchKernelGGL((gemm_skinny_kernel<TM, U, false>), grid, dim3(256), 0, st, Aq, s_a, Wq, s_w, M, N, K,
+        hipLaunchKernelGGL((gemm_skinny_kernel<TM, U, false, BITS>), grid, dim3(256), 0, st, Aq, s_a, Wq, s_w, M, N, K,
                            p.per, Y, acc, (int32_t*)nullptr);
     } else {
-        hipLaunchKernelGGL((gemm_skinny_kernel<TM, U, true>), grid, dim3(256), 0, st, Aq, s_a, Wq, s_w, M, N, K,
+        hipLaunchKernelGGL((gemm_skinny_kernel<TM, U, true, BITS>), grid, dim3(256), 0, st, Aq, s_a, Wq, s_w, M, N, K,
                            p.per, (uint16_t*)nullptr, (int32_t*)nullptr, part);
     }
     return hipGetLastError();
 }
 
-template <int WM, int WN, int TM, int TN, bool UNPACK, int SCHED = 0>
+template <int WM, int WN, int TM, int TN, bool UNPACK, int SCHED = 0, int BITS = 4>
 hipError_t launch_cfg(const Plan& p, const uint8_t* Aq, const float* s_a, const uint8_t* Wq, const float* s_w,
                       int M, int N, int K, uint16_t* Y, int32_t* acc, int32_t* part, hipStream_t st) {
     dim3 grid((N + p.bn - 1) / p.bn, (M + p.bm - 1) / p.bm, p.splits);
     dim3 block(64 * WM * WN);
     if (p.splits == 1) {
-        hipLaunchKernelGGL((gemm_kernel<WM, WN, TM, TN, UNPACK, false, SCHED>), grid, block, 0, st, Aq, s_a, Wq, s_w, M,
+        hipLaunchKernelGGL((gemm_kernel<WM, WN, TM, TN, UNPACK, false, SCHED, BITS>), grid, block, 0, st, Aq, s_a, Wq, s_w, M,
                            N, K, p.per, Y, acc, (int32_t*)nullptr);
     } else {
-        hipLaunchKernelGGL((gemm_kernel<WM, WN, TM, TN, UNPACK, true, SCHED>), grid, block, 0, st, Aq, s_a, Wq, s_w, M, N,
+        hipLaunchKernelGGL((gemm_kernel<WM, WN, TM, TN, UNPACK, true, SCHED, BITS>), grid, block, 0, st, Aq, s_a, Wq, s_w, M, N,
                            K, p.per, (uint16_t*)nullptr, (int32_t*)nullptr, part);
     }
     return hipGetLastError();
@@ -440,8 +451,8 @@ hipError_t finish_split(const Plan& p, int32_t* part, const float* s_a, const fl
 //  - M <= 64: 64 x 64 tiles and a K split up to ~512 workgroups;
 //  - at least 512 tiles of 128 x 128: 128 x 128 (four waves of 64 x 64);
 //  - otherwise 64 x 128 (four waves of 64 x 32), split along K below 512 tiles.
-Plan choose_plan(int M, int N, int K) {
-    const int nk = (K / 2 + kKB - 1) / kKB;
+Plan choose_plan(int M, int N, int K, int bits) {
+    const int nk = (K * bits / 8 + kKB - 1) / kKB;
     auto splits_for = [&](int tiles) {
         int s = tiles >= 512 ? 1 : (512 + tiles - 1) / tiles;
         const int cap = nk / 4 > 1 ? nk / 4 : 1;       // keep at least 4 k steps per split
@@ -455,18 +466,18 @@ Plan choose_plan(int M, int N, int K) {
         int s = wgs >= 128 ? 1 : (256 + wgs - 1) / wgs;
         const int cap = nk / 16 > 1 ? nk / 16 : 1;     // keep two batches of 8 k steps per split
         s = s < cap ? s : cap;
-        p = make_plan(M, N, K, 16, 64, s);
+        p = make_plan(M, N, K, 16, 64, s, bits);
         p.cfg = 3;
     } else if (M <= 64) {
         const int tiles = ((M + 63) / 64) * ((N + 63) / 64);
-        p = make_plan(M, N, K, 64, 64, splits_for(tiles));
+        p = make_plan(M, N, K, 64, 64, splits_for(tiles), bits);
         p.cfg = 2;
     } else if (((M + 127) / 128) * ((N + 127) / 128) >= 512) {
-        p = make_plan(M, N, K, 128, 128, 1);
+        p = make_plan(M, N, K, 128, 128, 1, bits);
         p.cfg = 0;
     } else {
         const int tiles = ((M + 63) / 64) * ((N + 127) / 128);
-        p = make_plan(M, N, K, 64, 128, splits_for(tiles));
+        p = make_plan(M, N, K, 64, 128, splits_for(tiles), bits);
         p.cfg = 1;
     }
     return p;
@@ -474,21 +485,26 @@ Plan choose_plan(int M, int N, int K) {
 
 }  // namespace
 
-size_t gemm_workspace_bytes(int M, int N, int K) {
-    const Plan p = choose_plan(M, N, K);
+size_t gemm_workspace_bytes(int M, int N, int K, int bits) {
+    const Plan p = choose_plan(M, N, K, bits);
     return p.splits > 1 ? (size_t)p.splits * M * N * sizeof(int32_t) : 0;
 }
 
 hipError_t launch_gemm(const uint8_t* Aq, const float* s_a, const uint8_t* Wq, const float* s_w, int M, int N,
-                       int K, uint16_t* Y, int32_t* acc, void* ws, hipStream_t st) {
-    const Plan p = choose_plan(M, N, K);
+                       int K, uint16_t* Y, int32_t* acc, void* ws, hipStream_t st, int bits) {
+    const Plan p = choose_plan(M, N, K, bits);
     int32_t* part = static_cast<int32_t*>(ws);
     hipError_t e;
-    switch (p.cfg) {
-        case 3: e = launch_skinny<1, 8>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
-        case 2: e = launch_cfg<2, 2, 2, 2, false, 1>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
-        case 1: e = launch_cfg<1, 4, 4, 2, false, 1>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
-        default: e = launch_cfg<2, 2, 4, 4, false, 1>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
+    const int sel = p.cfg + (bits == 8 ? 4 : 0);
+    switch (sel) {
+        case 3: e = launch_skinny<1, 8, 4>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
+        case 2: e = launch_cfg<2, 2, 2, 2, false, 1, 4>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
+        case 1: e = launch_cfg<1, 4, 4, 2, false, 1, 4>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
+        case 0: e = launch_cfg<2, 2, 4, 4, false, 1, 4>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
+        case 7: e = launch_skinny<1, 8, 8>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
+        case 6: e = launch_cfg<2, 2, 2, 2, false, 1, 8>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
+        case 5: e = launch_cfg<1, 4, 4, 2, false, 1, 8>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
+        default: e = launch_cfg<2, 2, 4, 4, false, 1, 8>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
     }
     if (e != hipSuccess) return e;
     return finish_split(p, part, s_a, s_w, M, N, Y, acc, st);

@@ -1,8 +1,10 @@
-// Per-token symmetric int4 quantisation (Sec. 3.1, Eq. 2 with zero point 0 and
-// Eq. 5: per-token activations, per-output-channel weights):
+// Per-token symmetric quantisation (Sec. 3.1, Eq. 2 with zero point 0 and
+// Eq. 5: per-token activations, per-output-channel weights), at BITS = 4:
 //   a = max_j |x_j|,  s = a / 7 (fp32, correctly rounded),
 //   q_j = clamp(rint(x_j / s), -8, 7)  (0 when s == 0),
-//   byte t = (q_{2t} & 15) | (q_{2t+1} & 15) << 4.
+//   byte t = (q_{2t} & 15) | (q_{2t+1} & 15) << 4;
+// and at BITS = 8 (the W8A8 variant of App. D): s = a / 127, q_j =
+// clamp(rint(x_j / s), -128, 127), one signed byte per code.
 //
 // One 256-thread workgroup per row: coalesced 16-byte loads held in registers,
 // a wavefront max reduction plus one LDS exchange across the four waves, then
@@ -29,14 +31,32 @@ __device__ __forceinline__ float block_max(float v, float* red) {
     return r;
 }
 
-__device__ __forceinline__ uint32_t pack8(const float* x, float s) {
-    uint32_t out = 0;
-    if (s != 0.0f) {
+// 8 values -> their codes, stored at code index 8v of the row: 4 bytes (4-bit)
+// or 8 bytes (8-bit)
+template <int BITS>
+__device__ __forceinline__ void store8(uint8_t* row, int v, const float* x, float s) {
+    if (BITS == 4) {
+        uint32_t out = 0;
+        if (s != 0.0f) {
 #pragma unroll
-        for (int q = 0; q < 8; ++q) out |= (uint32_t)(quant4(x[q], s) & 15) << (4 * q);
+            for (int q = 0; q < 8; ++q) out |= (uint32_t)(quant4(x[q], s) & 15) << (4 * q);
+        }
+        reinterpret_cast<uint32_t*>(row)[v] = out;
+    } else {
+        uint32_t lo = 0, hi = 0;
+        if (s != 0.0f) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                lo |= (uint32_t)(quant8(x[q], s) & 255) << (8 * q);
+                hi |= (uint32_t)(quant8(x[4 + q], s) & 255) << (8 * q);
+            }
+        }
+        reinterpret_cast<uint2*>(row)[v] = make_uint2(lo, hi);
     }
-    return out;
 }
+
+template <int BITS>
+__device__ __forceinline__ float qmaxf() { return BITS == 4 ? 7.0f : 127.0f; }
 
 __device__ __forceinline__ void load_f16x8(const uint16_t* p, const uint8_t* state, int row, int c0, int K,
                                            int dm, int du, float* x) {
@@ -48,7 +68,7 @@ __device__ __forceinline__ void load_f16x8(const uint16_t* p, const uint8_t* sta
 }
 
 // fp16 input; NV vectors of 8 per thread held in registers (NV == 0: reload).
-template <int NV>
+template <int NV, int BITS>
 __global__ __launch_bounds__(kThreads) void quant_f16_kernel(const uint16_t* __restrict__ X,
                                                              const uint8_t* __restrict__ state, int K, int dm,
                                                              int du, uint8_t* __restrict__ Aq,
@@ -57,7 +77,7 @@ __global__ __launch_bounds__(kThreads) void quant_f16_kernel(const uint16_t* __r
     const int row = blockIdx.x;
     const int nvec = K / 8;
     const uint16_t* xr = X + (size_t)row * K;
-    uint32_t* qr = reinterpret_cast<uint32_t*>(Aq + (size_t)row * (K / 2));
+    uint8_t* qr = Aq + (size_t)row * (K * BITS / 8);
     float amax = 0.0f;
     if constexpr (NV > 0) {
         float x[NV][8];
@@ -70,12 +90,12 @@ __global__ __launch_bounds__(kThreads) void quant_f16_kernel(const uint16_t* __r
                 for (int q = 0; q < 8; ++q) amax = fmaxf(amax, fabsf(x[i][q]));
             }
         }
-        const float s = block_max(amax, red) / 7.0f;
+        const float s = block_max(amax, red) / qmaxf<BITS>();
         if (threadIdx.x == 0) s_out[row] = s;
 #pragma unroll
         for (int i = 0; i < NV; ++i) {
             const int v = threadIdx.x + i * kThreads;
-            if (v < nvec) qr[v] = pack8(x[i], s);
+            if (v < nvec) store8<BITS>(qr, v, x[i], s);
         }
     } else {
         float x[8];
@@ -84,24 +104,24 @@ __global__ __launch_bounds__(kThreads) void quant_f16_kernel(const uint16_t* __r
 #pragma unroll
             for (int q = 0; q < 8; ++q) amax = fmaxf(amax, fabsf(x[q]));
         }
-        const float s = block_max(amax, red) / 7.0f;
+        const float s = block_max(amax, red) / qmaxf<BITS>();
         if (threadIdx.x == 0) s_out[row] = s;
         for (int v = threadIdx.x; v < nvec; v += kThreads) {
             load_f16x8(xr + v * 8, state, row, v * 8, K, dm, du, x);
-            qr[v] = pack8(x, s);
+            store8<BITS>(qr, v, x, s);
         }
     }
 }
 
 // fp32 input (already gated); NV vectors of 8 floats per thread (NV == 0: reload).
-template <int NV>
+template <int NV, int BITS>
 __global__ __launch_bounds__(kThreads) void quant_f32_kernel(const float* __restrict__ X, int K,
                                                              uint8_t* __restrict__ Aq, float* __restrict__ s_out) {
     __shared__ float red[kThreads / kWave];
     const int row = blockIdx.x;
     const int nvec = K / 8;
     const float* xr = X + (size_t)row * K;
-    uint32_t* qr = reinterpret_cast<uint32_t*>(Aq + (size_t)row * (K / 2));
+    uint8_t* qr = Aq + (size_t)row * (K * BITS / 8);
     float amax = 0.0f;
     auto ld = [&](int v, float* x) {
         const float4 a = *reinterpret_cast<const float4*>(xr + v * 8);
@@ -119,12 +139,12 @@ __global__ __launch_bounds__(kThreads) void quant_f32_kernel(const float* __rest
                 for (int q = 0; q < 8; ++q) amax = fmaxf(amax, fabsf(x[i][q]));
             }
         }
-        const float s = block_max(amax, red) / 7.0f;
+        const float s = block_max(amax, red) / qmaxf<BITS>();
         if (threadIdx.x == 0) s_out[row] = s;
 #pragma unroll
         for (int i = 0; i < NV; ++i) {
             const int v = threadIdx.x + i * kThreads;
-            if (v < nvec) qr[v] = pack8(x[i], s);
+            if (v < nvec) store8<BITS>(qr, v, x[i], s);
         }
     } else {
         float x[8];
@@ -133,39 +153,39 @@ __global__ __launch_bounds__(kThreads) void quant_f32_kernel(const float* __rest
 #pragma unroll
             for (int q = 0; q < 8; ++q) amax = fmaxf(amax, fabsf(x[q]));
         }
-        const float s = block_max(amax, red) / 7.0f;
+        const float s = block_max(amax, red) / qmaxf<BITS>();
         if (threadIdx.x == 0) s_out[row] = s;
         for (int v = threadIdx.x; v < nvec; v += kThreads) {
             ld(v, x);
-            qr[v] = pack8(x, s);
+            store8<BITS>(qr, v, x, s);
         }
     }
 }
 
-template <template <int> class Launch, typename... A>
+template <template <int, int> class Launch, int BITS, typename... A>
 hipError_t by_nv(int K, A... args) {
     const int per = (K / 8 + kThreads - 1) / kThreads;   // vectors per thread
-    if (per <= 1) return Launch<1>::run(args...);
-    if (per <= 2) return Launch<2>::run(args...);
-    if (per <= 4) return Launch<4>::run(args...);
-    if (per <= 8) return Launch<8>::run(args...);
-    if (per <= 12) return Launch<12>::run(args...);
-    return Launch<0>::run(args...);
+    if (per <= 1) return Launch<1, BITS>::run(args...);
+    if (per <= 2) return Launch<2, BITS>::run(args...);
+    if (per <= 4) return Launch<4, BITS>::run(args...);
+    if (per <= 8) return Launch<8, BITS>::run(args...);
+    if (per <= 12) return Launch<12, BITS>::run(args...);
+    return Launch<0, BITS>::run(args...);
 }
 
-template <int NV>
+template <int NV, int BITS>
 struct LaunchF16 {
     static hipError_t run(const uint16_t* x, const uint8_t* state, int M, int K, int dm, int du, uint8_t* q,
                           float* s, hipStream_t st) {
-        hipLaunchKernelGGL(quant_f16_kernel<NV>, dim3(M), dim3(kThreads), 0, st, x, state, K, dm, du, q, s);
+        hipLaunchKernelGGL((quant_f16_kernel<NV, BITS>), dim3(M), dim3(kThreads), 0, st, x, state, K, dm, du, q, s);
         return hipGetLastError();
     }
 };
 
-template <int NV>
+template <int NV, int BITS>
 struct LaunchF32 {
     static hipError_t run(const float* x, int M, int K, uint8_t* q, float* s, hipStream_t st) {
-        hipLaunchKernelGGL(quant_f32_kernel<NV>, dim3(M), dim3(kThreads), 0, st, x, K, q, s);
+        hipLaunchKernelGGL((quant_f32_kernel<NV, BITS>), dim3(M), dim3(kThreads), 0, st, x, K, q, s);
         return hipGetLastError();
     }
 };
@@ -173,12 +193,14 @@ struct LaunchF32 {
 }  // namespace
 
 hipError_t launch_quant_f16(const uint16_t* x, const uint8_t* state, int M, int K, int dm, int du, uint8_t* q,
-                            float* s, hipStream_t st) {
-    return by_nv<LaunchF16>(K, x, state, M, K, dm, du, q, s, st);
+                            float* s, hipStream_t st, int bits) {
+    if (bits == 8) return by_nv<LaunchF16, 8>(K, x, state, M, K, dm, du, q, s, st);
+    return by_nv<LaunchF16, 4>(K, x, state, M, K, dm, du, q, s, st);
 }
 
-hipError_t launch_quant_f32(const float* x, int M, int K, uint8_t* q, float* s, hipStream_t st) {
-    return by_nv<LaunchF32>(K, x, M, K, q, s, st);
+hipError_t launch_quant_f32(const float* x, int M, int K, uint8_t* q, float* s, hipStream_t st, int bits) {
+    if (bits == 8) return by_nv<LaunchF32, 8>(K, x, M, K, q, s, st);
+    return by_nv<LaunchF32, 4>(K, x, M, K, q, s, st);
 }
 
 }  // namespace sq

@@ -39,6 +39,13 @@ __device__ __forceinline__ int quant4(float x, float s) {
     return (int)r;
 }
 
+// Symmetric int8 code of x for scale s (s > 0): clamp(rint(x / s), -128, 127).
+__device__ __forceinline__ int quant8(float x, float s) {
+    float r = __builtin_rintf(x / s);
+    r = r < -128.0f ? -128.0f : (r > 127.0f ? 127.0f : r);
+    return (int)r;
+}
+
 __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
@@ -50,20 +57,21 @@ hipError_t launch_tac(const uint16_t* Z, const uint16_t* Mb, const uint16_t* d,
                       int M, int C, int g, uint16_t* out, hipStream_t st);
 
 // TAC fused with gate + int4 quantisation (P = NULL); valid when tac_quant_fusable.
+// bits = 4 (packed int4 codes) or 8 (int8 codes, the W8A8 variant) here and below.
 bool tac_quant_fusable(int K, int g);
 hipError_t launch_tac_quant(const uint16_t* Z, const uint16_t* Mb, const uint16_t* d, const uint8_t* state, int M,
-                            int K, int g, int dm, int du, uint8_t* Aq, float* s, hipStream_t st);
+                            int K, int g, int dm, int du, uint8_t* Aq, float* s, hipStream_t st, int bits);
 
 hipError_t launch_transform(const uint16_t* X, const uint8_t* state, const float* P,
                             int M, int K, int dm, int du, float* Xp, hipStream_t st);
 
-hipError_t launch_quant_f32(const float* x, int M, int K, uint8_t* q, float* s, hipStream_t st);
+hipError_t launch_quant_f32(const float* x, int M, int K, uint8_t* q, float* s, hipStream_t st, int bits);
 
 hipError_t launch_quant_f16(const uint16_t* x, const uint8_t* state, int M, int K, int dm, int du,
-                            uint8_t* q, float* s, hipStream_t st);
+                            uint8_t* q, float* s, hipStream_t st, int bits);
 
-size_t gemm_workspace_bytes(int M, int N, int K);
+size_t gemm_workspace_bytes(int M, int N, int K, int bits);
 hipError_t launch_gemm(const uint8_t* Aq, const float* s_a, const uint8_t* Wq, const float* s_w,
-                       int M, int N, int K, uint16_t* Y, int32_t* acc, void* ws, hipStream_t st);
+                       int M, int N, int K, uint16_t* Y, int32_t* acc, void* ws, hipStream_t st, int bits);
 
 }  // namespace sq

@@ -157,7 +157,7 @@ __device__ __forceinline__ float block_max_db(float v, float (*red)[kFusedThread
     return r;
 }
 
-template <int G>
+template <int G, int BITS>
 __global__ __launch_bounds__(kFusedThreads) void tac_quant_kernel(const uint16_t* __restrict__ Z,
                                                                   const uint16_t* __restrict__ Mb,
                                                                   const uint16_t* __restrict__ d,
@@ -208,15 +208,27 @@ __global__ __launch_bounds__(kFusedThreads) void tac_quant_kernel(const uint16_t
                 amax = fmaxf(amax, fabsf(o[r]));
             }
         }
-        const float s = block_max_db(amax, red, row & 1) / 7.0f;
+        const float s = block_max_db(amax, red, row & 1) / (BITS == 4 ? 7.0f : 127.0f);
         if (t == 0) s_out[row] = s;
         if (active) {
-            uint32_t w = 0;
-            if (s != 0.0f) {
+            if (BITS == 4) {
+                uint32_t w = 0;
+                if (s != 0.0f) {
 #pragma unroll
-                for (int q = 0; q < 8; ++q) w |= (uint32_t)(quant4(o[q], s) & 15) << (4 * q);
+                    for (int q = 0; q < 8; ++q) w |= (uint32_t)(quant4(o[q], s) & 15) << (4 * q);
+                }
+                *reinterpret_cast<uint32_t*>(Aq + (size_t)row * (K / 2) + 4 * t) = w;
+            } else {
+                uint32_t lo = 0, hi = 0;
+                if (s != 0.0f) {
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        lo |= (uint32_t)(quant8(o[q], s) & 255) << (8 * q);
+                        hi |= (uint32_t)(quant8(o[4 + q], s) & 255) << (8 * q);
+                    }
+                }
+                *reinterpret_cast<uint2*>(Aq + (size_t)row * K + 8 * t) = make_uint2(lo, hi);
             }
-            *reinterpret_cast<uint32_t*>(Aq + (size_t)row * (K / 2) + 4 * t) = w;
         }
     }
 }
@@ -226,17 +238,21 @@ __global__ __launch_bounds__(kFusedThreads) void tac_quant_kernel(const uint16_t
 bool tac_quant_fusable(int K, int g) { return g <= 16 && K % 16 == 0 && K / 8 <= kFusedThreads; }
 
 hipError_t launch_tac_quant(const uint16_t* Z, const uint16_t* Mb, const uint16_t* d, const uint8_t* state, int M,
-                            int K, int g, int dm, int du, uint8_t* Aq, float* s, hipStream_t st) {
+                            int K, int g, int dm, int du, uint8_t* Aq, float* s, hipStream_t st, int bits) {
     const int threads = ((K / 8 + kWave - 1) / kWave) * kWave;
     // enough workgroups to fill the chip, each reusing its parameters over several rows
     int rows = M / 512;
     rows = rows < 1 ? 1 : (rows > 16 ? 16 : rows);
     const dim3 grid((M + rows - 1) / rows);
-    switch (g) {
+    switch (g * (bits == 8 ? -1 : 1)) {
 #define SQ_TQ(G)                                                                                                  \
     case G:                                                                                                       \
-        hipLaunchKernelGGL(tac_quant_kernel<G>, grid, dim3(threads), 0, st, Z, Mb, d, state, M, K, dm, du, rows, \
-                           Aq, s);                                                                                \
+        hipLaunchKernelGGL((tac_quant_kernel<G, 4>), grid, dim3(threads), 0, st, Z, Mb, d, state, M, K, dm, du,  \
+                           rows, Aq, s);                                                                          \
+        break;                                                                                                    \
+    case -G:                                                                                                      \
+        hipLaunchKernelGGL((tac_quant_kernel<G, 8>), grid, dim3(threads), 0, st, Z, Mb, d, state, M, K, dm, du,  \
+                           rows, Aq, s);                                                                          \
         break;
         SQ_TQ(1)
         SQ_TQ(2)

@@ -113,3 +113,16 @@ def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     with pytest.raises(ImportError):
         L.lib()
     importlib.reload(L)
+
+
+def test_w8_entry_points_validate(lib):
+    assert lib.w8a8_gemm(FAKE, FAKE, FAKE, FAKE, 4, 16, 65536 + 64, FAKE, None, FAKE, 1 << 30, None) == L.SQ_ERR_SHAPE
+    assert b"65536" in lib.sq_last_error()
+    assert lib.w8a8_gemm(None, None, None, None, 0, 16, 64, None, None, None, 0, None) == L.SQ_OK
+    assert lib.sgat_quant_act_w8(FAKE, None, None, 4, 100, 0, 0, None, None, 0, FAKE, FAKE, None, 0, None) \
+        == L.SQ_ERR_SHAPE
+    assert lib.sgat_quantize_w8(None, 4, 64, FAKE, FAKE, None) == L.SQ_ERR_NULL
+    assert lib.sgat_prepare_weights_w8(FAKE, FAKE, 8, 64, FAKE, FAKE, None, 0, None) == L.SQ_ERR_WORKSPACE
+    assert lib.sq_gemm_w8_workspace_bytes(4096, 4096, 4096) == 0
+    # operands of 2 GiB or more are refused (32-bit buffer offsets)
+    assert lib.w4a4_gemm(FAKE, FAKE, FAKE, FAKE, 65536, 16, 65536, FAKE, None, FAKE, 1 << 40, None) == L.SQ_ERR_SHAPE

@@ -295,3 +295,84 @@ def test_empty_inputs_leave_outputs_untouched():
                  torch.ones(16, dtype=torch.float32, device="cuda"), Y=Y[:0])
     torch.cuda.synchronize()
     assert (host(Y) == 3.0).all()
+
+
+# ------------------------------------------------------------------ W8A8 (App. D)
+
+@pytest.mark.parametrize("amax", [1.0, 127.0, 0.3, 65504.0])
+def test_w8_quantiser_exhaustive_fp16(amax):
+    h = np.arange(65536, dtype=np.uint16)
+    v = h.view(np.float16)
+    v = v[np.isfinite(v) & (np.abs(v.astype(np.float32)) <= amax)]
+    K = 4096
+    n = (len(v) + K - 2) // (K - 1)
+    rows = np.zeros((n, K), np.float16)
+    rows[:, 0] = np.float16(amax)
+    flat = np.zeros(n * (K - 1), np.float16)
+    flat[:len(v)] = v
+    rows[:, 1:] = flat.reshape(n, K - 1)
+    say(f"w8 quantiser exhaustive amax={amax}")
+    Aq, s = sq.sgat_quant_act_w8(dev(rows), None, None, 0, 0)
+    rq, rs = O.quant_act_q8(rows, None, None, 0, 0)
+    assert_bits(host(s), rs, "s_a")
+    assert_bits(host(Aq), rq, "Aq")
+    Aq2, s2 = sq.sgat_quantize_w8(dev(rows.astype(np.float32)))
+    assert_bits(host(Aq2), rq, "Aq (fp32 path)")
+
+
+@pytest.mark.parametrize("withP,g", [(False, 0), (True, 0), (False, 16), (False, 128), (True, 16)])
+def test_w8_quant_act(withP, g):
+    M, K = 150, 1024
+    X, st = _x(M, K, 9)
+    P = synth.orthogonal(K, synth.rng_for(704, K)) if withP else None
+    dm, du = synth.default_band(K)
+    Mb, d = synth.tac_params(K, g, synth.rng_for(705, g)) if g else (None, None)
+    say(f"w8 quant_act P={withP} g={g}")
+    Aq, s = sq.sgat_quant_act_w8(dev(X), dev(st), dev(P) if withP else None, dm, du,
+                                 dev(Mb) if g else None, dev(d) if g else None, g)
+    rq, rs = O.quant_act_q8(X, st, P, dm, du, Mb, d, g, threads=THREADS)
+    assert_bits(host(s), rs, "s_a")
+    assert_bits(host(Aq), rq, "Aq")
+
+
+@pytest.mark.parametrize("withP", [True, False])
+def test_w8_prepare_weights(withP):
+    N, K = 200, 1024
+    W = synth.weights(N, K, synth.rng_for(706, N))
+    P = synth.orthogonal(K, synth.rng_for(707, K)) if withP else None
+    Wq, s_w = sq.sgat_prepare_weights_w8(dev(W), dev(P) if withP else None)
+    rq, rs = (O.prepare_weights_q8(W, P, threads=THREADS) if withP else O.quant_act_q8(W, None, None, 0, 0))
+    assert_bits(host(s_w), rs, "s_w")
+    assert_bits(host(Wq), rq, "Wq")
+
+
+@pytest.mark.parametrize("M,N,K", [(1, 8, 64), (16, 4096, 4096), (9, 136, 192), (33, 520, 1024), (77, 200, 192),
+                                   (300, 136, 4096), (1024, 1024, 1024), (513, 4104, 3584), (64, 512, 18944)])
+def test_w8a8_gemm_bit_exact(M, N, K):
+    rng = np.random.default_rng(10)
+    Aq = rng.integers(-128, 128, (M, K)).astype(np.int8)
+    Wq = rng.integers(-128, 128, (N, K)).astype(np.int8)
+    s_a = rng.uniform(0.01, 1, M).astype(np.float32)
+    s_w = rng.uniform(1e-5, 1e-3, N).astype(np.float32)
+    say(f"w8a8 gemm M={M} N={N} K={K}")
+    Y, acc = sq.w8a8_gemm(dev(Aq), dev(s_a), dev(Wq), dev(s_w), want_acc=True)
+    Y, acc = host(Y), host(acc)
+    rows = np.arange(M) if M * N * K <= 3e9 else np.unique(np.r_[0, M - 1, rng.choice(M, 24)])
+    rY, racc = O.gemm_q8(Aq[rows], s_a[rows], Wq, s_w, threads=THREADS)
+    assert_bits(acc[rows], racc, "acc")
+    assert_y(Y[rows], rY)
+
+
+def test_w8a8_config0_end_to_end():
+    st = synth.config_state(0)
+    t = synth.site_tensors(0, 0, st)
+    Pd = dev(t.P)
+    Wq, s_w = sq.sgat_prepare_weights_w8(dev(t.W), Pd)
+    Aq, s_a = sq.sgat_quant_act_w8(dev(t.X), dev(st), Pd, t.dm, t.du)
+    Y, acc = sq.w8a8_gemm(Aq, s_a, Wq, s_w, want_acc=True)
+    rA, rs = O.quant_act_q8(t.X, st, t.P, t.dm, t.du, threads=THREADS)
+    rW, rsw = O.prepare_weights_q8(t.W, t.P, threads=THREADS)
+    rY, racc = O.gemm_q8(rA, rs, rW, rsw, threads=THREADS)
+    for name, got, ref in (("Aq", Aq, rA), ("s_a", s_a, rs), ("Wq", Wq, rW), ("s_w", s_w, rsw), ("acc", acc, racc)):
+        assert_bits(host(got), ref, name)
+    assert_y(host(Y), rY)
