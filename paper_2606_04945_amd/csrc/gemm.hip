@@ -12,17 +12,17 @@
 // permutation is applied to A and W, and an integer sum does not depend on its
 // order, so the result is the plain dot product.
 //
-// Tiling (template): WM x WN waves, each owning TM x TN MFMA tiles of 16 x 16, so
-// a workgroup owns (16 WM TM) x (16 WN TN) outputs.  Per k step (128 codes) the
-// workgroup reads 64 packed bytes of every row of both operands with raw buffer
-// loads (out-of-range reads return 0, so no predicates in the loop), prefetching
-// the next step into registers during compute, and stages them through
-// double-buffered LDS.  UNPACK selects where nibbles become int8: when staged
-// (LDS holds int8 rows, each tile unpacked once per workgroup) or as fragments
-// leave LDS (LDS holds packed rows, each wave unpacks what it reads).  LDS rows
-// are XOR-swizzled by 16-byte chunk so the row-wise fragment reads and the
-// segment-wise stores are free of bank conflicts.  Short M splits K across
+// Tiled kernel (template): WM x WN waves, each owning TM x TN MFMA tiles of
+// 16 x 16, so a workgroup owns (16 WM TM) x (16 WN TN) outputs.  A k step is 64
+// packed bytes (128 codes) of every row of both operands.  Operand tiles go from
+// HBM straight into LDS with buffer_load ... lds (no staging registers), three
+// LDS stages deep: two k steps are in flight while a third is multiplied, with
+// one barrier per step.  LDS rows are XOR-swizzled by 16-byte chunk so the
+// fragment reads are free of bank conflicts; each wave unpacks the fragments it
+// reads.  Rows past M (or N) and the unused half of a last k step read as zero
+// through the buffer descriptors' range check.  Short M splits K across
 // workgroups; the int32 partial sums are then added exactly by a small kernel.
+// M <= 16 has a kernel of its own that streams the weights with no LDS.
 //
 // BITS = 8 is the W8A8 variant (App. D): codes are int8 already, so the same
 // tiles feed the MFMA straight from LDS with no unpacking and no scaling.
@@ -32,9 +32,13 @@ namespace sq {
 namespace {
 
 __device__ __forceinline__ v4i unpack_op(uint32_t w0, uint32_t w1) {
+    // one 64-bit shift moves the low nibbles of both words up; the nibble that
+    // crosses from w0 into w1 is cleared by the mask
+    uint64_t t = ((uint64_t)w1 << 32) | w0;
+    asm("v_lshlrev_b64 %0, 4, %1" : "=v"(t) : "v"(t));  // kept as one instruction
     v4i r;
-    r[0] = (int)((w0 << 4) & 0xF0F0F0F0u);
-    r[1] = (int)((w1 << 4) & 0xF0F0F0F0u);
+    r[0] = (int)((uint32_t)t & 0xF0F0F0F0u);
+    r[1] = (int)((uint32_t)(t >> 32) & 0xF0F0F0F0u);
     r[2] = (int)(w0 & 0xF0F0F0F0u);
     r[3] = (int)(w1 & 0xF0F0F0F0u);
     return r;
@@ -62,22 +66,6 @@ __device__ __forceinline__ int acc_value(int raw) {   // 4-bit operands carry a 
     return BITS == 8 ? raw : raw >> 8;
 }
 
-template <int WM, int WN, int TM, int TN, bool UNPACK>
-struct GemmCfg {
-    static constexpr int NT = 64 * WM * WN;          // threads
-    static constexpr int BM = 16 * WM * TM;          // rows of A per tile
-    static constexpr int BN = 16 * WN * TN;          // rows of W (output columns) per tile
-    static constexpr int SEG = kKB / 16;             // 16-byte packed segments per row per k step
-    static constexpr int AV = BM * SEG / NT;         // segments per thread
-    static constexpr int BV = BN * SEG / NT;
-    static constexpr int RB = UNPACK ? 2 * kKB : kKB;   // LDS row bytes per k step
-    static constexpr int CH = RB / 16;                  // 16-byte chunks per LDS row
-    // chunk c of LDS row r sits at chunk (c ^ swz(r)), swz(r) = index of the
-    // 128-byte line the row starts in, modulo the chunks per row: any eight
-    // consecutive rows then touch distinct 16-byte bank groups
-    static __device__ __forceinline__ int chunk(int r, int c) { return c ^ ((r / (128 / RB)) & (CH - 1)); }
-};
-
 // Raw buffer resource over [base, base + bytes): loads outside it return 0, which
 // is how rows past M (or N) and the unused half of a last k step read as zeros.
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
@@ -86,87 +74,100 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, ui
 
 constexpr uint32_t kOOB = 0x80000000u;   // an offset past any buffer this kernel builds
 
-// SPLIT == false: full K, fused epilogue.  SPLIT == true: K range of blockIdx.z,
-// raw int32 sums to part[z][M][N].
-template <int WM, int WN, int TM, int TN, bool UNPACK, bool SPLIT, int SCHED = 0, int BITS = 4>
-__global__ __launch_bounds__(64 * WM * WN) void gemm_kernel(const uint8_t* __restrict__ Aq,
-                                                           const float* __restrict__ s_a,
-                                                           const uint8_t* __restrict__ Wq,
-                                                           const float* __restrict__ s_w, int M, int N, int K,
-                                                           int ksteps_per_split, uint16_t* __restrict__ Y,
-                                                           int32_t* __restrict__ acc_out,
-                                                           int32_t* __restrict__ part) {
-    using C = GemmCfg<WM, WN, TM, TN, UNPACK>;
-    static_assert(C::BM * C::SEG % C::NT == 0 && C::BN * C::SEG % C::NT == 0, "tile loads must divide evenly");
-    static_assert(BITS == 4 || (BITS == 8 && !UNPACK && SCHED), "8-bit codes use the one-fragment loop");
-    __shared__ __attribute__((aligned(16))) uint8_t sA[2][C::BM * C::RB];
-    __shared__ __attribute__((aligned(16))) uint8_t sB[2][C::BN * C::RB];
+// Direct loads into LDS: lane i of a buffer_load ... lds lands at LDS base +
+// 16 i, so each lane fetches the 16-byte segment that belongs at its swizzled
+// slot.
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// Buffer descriptor in scalar registers: base, stride 0, size in bytes, raw
+// (untyped) buffer; offsets at or past `bytes` read as zero.
+__device__ __forceinline__ u32x4 sgpr_rsrc(const void* base, uint32_t bytes) {
+    const uint64_t a = reinterpret_cast<uint64_t>(base);
+    return u32x4{(uint32_t)a, (uint32_t)(a >> 32) & 0xFFFFu, bytes, 0x00020000u};
+}
+
+// 16 bytes per lane from buffer offset `voff` straight into LDS: lane i's bytes
+// land at LDS address `lds` + 16 i.  Issued as inline assembly so that the
+// compiler's automatic counter waits (which cannot tell the pipeline stages
+// apart and would wait for every load in flight) stay out of the loop; the
+// kernel waits for these loads itself with wait_vm.
+__device__ __forceinline__ void dma16(const u32x4& rsrc, uint32_t lds, uint32_t voff) {
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+                 :
+                 : "s"(__builtin_amdgcn_readfirstlane(lds)), "v"(voff), "s"(rsrc)
+                 : "memory", "m0");
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+    return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)p;
+}
+
+// vmcnt <= N and lgkmcnt == 0: this wave's loads older than its last N have
+// landed in LDS, and its own LDS reads are complete
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (0 << 8) | ((N >> 4) << 14));
+}
+
+template <int WM, int WN, int TM, int TN, bool SPLIT, int BITS, int OCC>
+__global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(OCC))) void gemm_tile_kernel(
+    const uint8_t* __restrict__ Aq, const float* __restrict__ s_a, const uint8_t* __restrict__ Wq,
+    const float* __restrict__ s_w, int M, int N, int K, int ksteps_per_split, uint16_t* __restrict__ Y,
+    int32_t* __restrict__ acc_out, int32_t* __restrict__ part) {
+    constexpr int NW = WM * WN;
+    constexpr int BM = 16 * WM * TM, BN = 16 * WN * TN;
+    constexpr int AB = BM * kKB, BB = BN * kKB;          // bytes of one stage
+    constexpr int SB = AB + BB;
+    constexpr int LA = AB / 1024 / NW, LB = BB / 1024 / NW;   // 1 KB loads per wave per stage
+    static_assert(LA * NW * 1024 == AB && LB * NW * 1024 == BB, "stage loads must divide evenly");
+    __shared__ __attribute__((aligned(16))) uint8_t sm[3 * SB];
 
     const int tid = threadIdx.x;
-    const int lane = tid % kWave, wave = tid / kWave;
+    const int lane = tid % kWave, wave = __builtin_amdgcn_readfirstlane(tid / kWave);
     const int wm = wave / WN, wn = wave % WN;
-    const int row0 = blockIdx.y * C::BM, col0 = blockIdx.x * C::BN;
-    const uint32_t ldb = (uint32_t)K * BITS / 8;         // bytes per row of codes
+    const uint32_t ldb = (uint32_t)K * BITS / 8;
+    const int nk_total = (int)((ldb + kKB - 1) / kKB);
+    const int nk_full = (int)(ldb / kKB);
+    const u32x4 rA = sgpr_rsrc(Aq, (uint32_t)M * ldb);
+    const u32x4 rW = sgpr_rsrc(Wq, (uint32_t)N * ldb);
+    auto swz = [](int r) { return (r >> 1) & 3; };       // 16-byte chunk swizzle of a 64-byte LDS row
 
-    const int nk_total = (int)((ldb + kKB - 1) / kKB);   // the last step may be half empty
-    const int nk_full = (int)(ldb / kKB);                // steps with every byte in range
+    const int row0 = blockIdx.y * BM, col0 = blockIdx.x * BN;
     const int kt0 = SPLIT ? blockIdx.z * ksteps_per_split : 0;
     const int kt1 = SPLIT ? min(nk_total, kt0 + ksteps_per_split) : nk_total;
 
-    const __amdgpu_buffer_rsrc_t rA = make_rsrc(Aq, (uint32_t)M * ldb);
-    const __amdgpu_buffer_rsrc_t rW = make_rsrc(Wq, (uint32_t)N * ldb);
-    // this thread's 16-byte segments: tile row e / SEG, segment e % SEG
-    uint32_t oa[C::AV], ow[C::BV];
+    // this lane's source segment for each of its loads: tile row r = 16 j + lane / 4
+    // holds, at chunk slot lane % 4, segment (lane % 4) ^ swz(r)
+    uint32_t oa[LA], ow[LB];
+    int sa_[LA], sw_[LB];
 #pragma unroll
-    for (int i = 0; i < C::AV; ++i) {
-        const int e = tid + i * C::NT, r = e / C::SEG;
-        oa[i] = row0 + r < M ? (uint32_t)(row0 + r) * ldb + (e % C::SEG) * 16 : kOOB;
+    for (int u = 0; u < LA; ++u) {
+        const int r = 16 * (wave * LA + u) + lane / 4;
+        sa_[u] = 16 * ((lane % 4) ^ swz(r));
+        oa[u] = row0 + r < M ? (uint32_t)(row0 + r) * ldb + sa_[u] : kOOB;
     }
 #pragma unroll
-    for (int i = 0; i < C::BV; ++i) {
-        const int e = tid + i * C::NT, r = e / C::SEG;
-        ow[i] = col0 + r < N ? (uint32_t)(col0 + r) * ldb + (e % C::SEG) * 16 : kOOB;
+    for (int u = 0; u < LB; ++u) {
+        const int r = 16 * (wave * LB + u) + lane / 4;
+        sw_[u] = 16 * ((lane % 4) ^ swz(r));
+        ow[u] = col0 + r < N ? (uint32_t)(col0 + r) * ldb + sw_[u] : kOOB;
     }
-
-    v4i ra[C::AV], rb[C::BV];
-    auto load = [&](int kt, bool tail) {
+    auto issue = [&](int kt, int stage) {
+        uint8_t* dA = sm + stage * SB;
+        uint8_t* dB = dA + AB;
         const uint32_t ko = (uint32_t)kt * kKB;
+        const bool tail = kt >= nk_full;
 #pragma unroll
-        for (int i = 0; i < C::AV; ++i) {
-            const int seg = ((tid + i * C::NT) % C::SEG) * 16;
-            const uint32_t o = (tail && ko + seg >= ldb) ? kOOB : oa[i] + ko;
-            ra[i] = __builtin_amdgcn_raw_buffer_load_b128(rA, (int)o, 0, 0);
+        for (int u = 0; u < LA; ++u) {
+            const uint32_t o = (tail && ko + sa_[u] >= ldb) ? kOOB : oa[u] + ko;
+            dma16(rA, lds_addr(dA + (wave * LA + u) * 1024), o);
         }
 #pragma unroll
-        for (int i = 0; i < C::BV; ++i) {
-            const int seg = ((tid + i * C::NT) % C::SEG) * 16;
-            const uint32_t o = (tail && ko + seg >= ldb) ? kOOB : ow[i] + ko;
-            rb[i] = __builtin_amdgcn_raw_buffer_load_b128(rW, (int)o, 0, 0);
+        for (int u = 0; u < LB; ++u) {
+            const uint32_t o = (tail && ko + sw_[u] >= ldb) ? kOOB : ow[u] + ko;
+            dma16(rW, lds_addr(dB + (wave * LB + u) * 1024), o);
         }
-    };
-    auto load_step = [&](int kt) {
-        if (kt < nk_full)
-            load(kt, false);
-        else
-            load(kt, true);
-    };
-    // packed segment s of row r -> LDS; with UNPACK its two int8 halves (MFMA steps
-    // h = 0, 1 of k group s) go to chunks 2s and 2s + 1
-    auto put = [&](uint8_t* base, int e, const v4i& v) {
-        const int r = e / C::SEG, s = e % C::SEG;
-        uint8_t* row = base + r * C::RB;
-        if (UNPACK) {
-            *reinterpret_cast<v4i*>(row + C::chunk(r, 2 * s) * 16) = unpack_op(v[0], v[1]);
-            *reinterpret_cast<v4i*>(row + C::chunk(r, 2 * s + 1) * 16) = unpack_op(v[2], v[3]);
-        } else {
-            *reinterpret_cast<v4i*>(row + C::chunk(r, s) * 16) = v;
-        }
-    };
-    auto stash = [&](int buf) {
-#pragma unroll
-        for (int i = 0; i < C::AV; ++i) put(sA[buf], tid + i * C::NT, ra[i]);
-#pragma unroll
-        for (int i = 0; i < C::BV; ++i) put(sB[buf], tid + i * C::NT, rb[i]);
     };
 
     v4i acc[TM][TN];
@@ -174,117 +175,93 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_kernel(const uint8_t* __res
     for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j) acc[i][j] = v4i{0, 0, 0, 0};
-
-    const int lr = lane % 16, lg = lane / 16;            // row within a 16-tile, k group
-    // a lane's fragment rows differ by multiples of 16, so swz(row) == swz(lr)
-    const int offA = ((wm * TM) * 16 + lr) * C::RB;
-    const int offB = ((wn * TN) * 16 + lr) * C::RB;
-    if (kt0 < kt1) {
-        load_step(kt0);
-        stash(0);
-        __syncthreads();
-    }
-    for (int kt = kt0; kt < kt1; ++kt) {
-        const int buf = (kt - kt0) & 1;
-        if (kt + 1 < kt1) load_step(kt + 1);
-        if (SCHED && !UNPACK) {
-            // one 16-byte fragment per tile per k step; with 4-bit codes both MFMA
-            // steps are unpacked and the scheduler interleaves the second step's
-            // unpacking with the first step's MFMAs
-            constexpr int SUBS = BITS == 4 ? 2 : 1;
-            v4i fa[TM], fb[TN];
+    const int lr = lane % 16, lg = lane / 16;
+    const int fo = (lg ^ swz(lr)) * 16;                  // this lane's fragment slot in a row
+    const int offA = ((wm * TM) * 16 + lr) * kKB + fo;
+    const int offB = AB + ((wn * TN) * 16 + lr) * kKB + fo;
+    v4i fa[TM], fb[TN];
+    auto frags = [&](const uint8_t* st) {
 #pragma unroll
-            for (int i = 0; i < TM; ++i)
-                fa[i] = *reinterpret_cast<const v4i*>(&sA[buf][offA + i * 16 * C::RB + C::chunk(lr, lg) * 16]);
+        for (int i = 0; i < TM; ++i) fa[i] = *reinterpret_cast<const v4i*>(st + offA + i * 16 * kKB);
 #pragma unroll
-            for (int j = 0; j < TN; ++j)
-                fb[j] = *reinterpret_cast<const v4i*>(&sB[buf][offB + j * 16 * C::RB + C::chunk(lr, lg) * 16]);
+        for (int j = 0; j < TN; ++j) fb[j] = *reinterpret_cast<const v4i*>(st + offB + j * 16 * kKB);
+    };
+    // B operands of one half are expanded once; each A operand just before
+    // its row of MFMAs, so that its expansion overlaps the previous row
+    auto mma = [&]() {
+        constexpr int SUBS = BITS == 4 ? 2 : 1;
 #pragma unroll
-            for (int h = 0; h < SUBS; ++h) {
-                v4i a[TM], b[TN];
+        for (int h = 0; h < SUBS; ++h) {
+            v4i b[TN];
 #pragma unroll
-                for (int i = 0; i < TM; ++i) a[i] = operand<BITS>(fa[i], h);
+            for (int j = 0; j < TN; ++j) b[j] = operand<BITS>(fb[j], h);
 #pragma unroll
-                for (int j = 0; j < TN; ++j) b[j] = operand<BITS>(fb[j], h);
+            for (int i = 0; i < TM; ++i) {
+                const v4i a = operand<BITS>(fa[i], h);
 #pragma unroll
-                for (int i = 0; i < TM; ++i)
-#pragma unroll
-                    for (int j = 0; j < TN; ++j)
-                        acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[i], b[j], acc[i][j], 0, 0, 0);
+                for (int j = 0; j < TN; ++j)   // weights as the row operand: see the epilogue
+                    acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(b[j], a, acc[i][j], 0, 0, 0);
             }
-            constexpr int nmma = TM * TN;
-            __builtin_amdgcn_sched_group_barrier(0x100, TM + TN, 0);         // fragment reads
-            if (BITS == 4) {
-                constexpr int nvalu = 6 * (TM + TN);                         // one MFMA step's unpacking
-                constexpr int per = (nvalu + nmma - 1) / nmma;
-                __builtin_amdgcn_sched_group_barrier(0x002, nvalu, 0);       // step-0 unpack
+        }
+    };
+    // acc[i][j] is the 16 x 16 block W_j A_i^T: this lane holds token row
+    // lr of A block i and the four consecutive output columns 4 lg .. 4 lg + 3
+    // of W block j, so each store is one contiguous 8-byte (fp16) or 16-byte
+    // (int32) run and the weight scales come in as one float4.
+    auto epilogue = [&]() {
 #pragma unroll
-                for (int q = 0; q < nmma; ++q) {
-                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);       // step-0 MFMA
-                    __builtin_amdgcn_sched_group_barrier(0x002, per, 0);     // step-1 unpack
+        for (int i = 0; i < TM; ++i) {
+            const int row = row0 + (wm * TM + i) * 16 + lr;
+            if (row >= M) continue;
+            const float sa = SPLIT ? 0.0f : s_a[row];
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const int col = col0 + (wn * TN + j) * 16 + lg * 4;   // N % 8 == 0: all four in range or none
+                if (col >= N) continue;
+                const int v0 = acc_value<BITS>(acc[i][j][0]), v1 = acc_value<BITS>(acc[i][j][1]);
+                const int v2 = acc_value<BITS>(acc[i][j][2]), v3 = acc_value<BITS>(acc[i][j][3]);
+                if (SPLIT) {
+                    *reinterpret_cast<int4*>(part + ((size_t)blockIdx.z * M + row) * N + col) = make_int4(v0, v1, v2, v3);
+                    continue;
+                }
+                const size_t o = (size_t)row * N + col;
+                if (acc_out) *reinterpret_cast<int4*>(acc_out + o) = make_int4(v0, v1, v2, v3);
+                if (Y) {
+                    const float4 sw = *reinterpret_cast<const float4*>(s_w + col);
+                    const uint32_t y0 = f2h(((float)v0 * sa) * sw.x), y1 = f2h(((float)v1 * sa) * sw.y);
+                    const uint32_t y2 = f2h(((float)v2 * sa) * sw.z), y3 = f2h(((float)v3 * sa) * sw.w);
+                    *reinterpret_cast<uint2*>(Y + o) = make_uint2(y0 | (y1 << 16), y2 | (y3 << 16));
                 }
             }
-            __builtin_amdgcn_sched_group_barrier(0x008, nmma, 0);            // remaining MFMAs
-        } else {
-            // k group lg of a lane covers packed bytes [16 lg, 16 lg + 16) of the row
-            // slice; MFMA step h uses 8 of them (same bytes for A and W)
-#pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                v4i a[TM], b[TN];
-                if (UNPACK) {
-#pragma unroll
-                    for (int i = 0; i < TM; ++i)
-                        a[i] = *reinterpret_cast<const v4i*>(&sA[buf][offA + i * 16 * C::RB +
-                                                                       C::chunk(lr, 2 * lg + h) * 16]);
-#pragma unroll
-                    for (int j = 0; j < TN; ++j)
-                        b[j] = *reinterpret_cast<const v4i*>(&sB[buf][offB + j * 16 * C::RB +
-                                                                       C::chunk(lr, 2 * lg + h) * 16]);
-                } else {
-#pragma unroll
-                    for (int i = 0; i < TM; ++i) {
-                        const uint2 u = *reinterpret_cast<const uint2*>(&sA[buf][offA + i * 16 * C::RB +
-                                                                                 C::chunk(lr, lg) * 16 + 8 * h]);
-                        a[i] = unpack_op(u.x, u.y);
-                    }
-#pragma unroll
-                    for (int j = 0; j < TN; ++j) {
-                        const uint2 u = *reinterpret_cast<const uint2*>(&sB[buf][offB + j * 16 * C::RB +
-                                                                                 C::chunk(lr, lg) * 16 + 8 * h]);
-                        b[j] = unpack_op(u.x, u.y);
-                    }
-                }
-#pragma unroll
-                for (int i = 0; i < TM; ++i)
-#pragma unroll
-                    for (int j = 0; j < TN; ++j)
-                        acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[i], b[j], acc[i][j], 0, 0, 0);
-            }
         }
-        if (kt + 1 < kt1) {
-            stash(buf ^ 1);
-            __syncthreads();
-        }
-    }
+    };
 
-    // D layout of a 16x16 tile: lane holds column (lane % 16), rows 4*(lane / 16) + r
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j) {
-            const int col = col0 + (wn * TN + j) * 16 + lr;
-            if (col >= N) continue;
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int row = row0 + (wm * TM + i) * 16 + lg * 4 + r;
-                if (row >= M) continue;
-                const int v = acc_value<BITS>(acc[i][j][r]);
-                if (SPLIT)
-                    part[((size_t)blockIdx.z * M + row) * N + col] = v;
-                else
-                    store_out(row, col, v, s_a, s_w, Y, acc_out, N);
-            }
-        }
+    // step kt lives in stage (kt - kt0) % 3.  At each step the loads of the
+    // step itself and of the next one are in flight; after the wait and the
+    // barrier the stage of the previous step is free for the step after next.
+    auto step = [&](int kt, int sc, int sn) {
+        asm volatile("" ::: "memory");
+        if (kt + 1 < kt1)
+            wait_vm<LA + LB>();                          // this wave's loads of step kt are done
+        else
+            wait_vm<0>();
+        // ... and every wave's.  A bare s_barrier: the workgroup fence of
+        // __syncthreads would also wait for the loads still in flight, which
+        // is the overlap this pipeline exists for.
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        frags(sm + sc * SB);
+        if (kt + 2 < kt1) issue(kt + 2, sn);             // into the stage step kt - 1 used
+        mma();
+    };
+    if (kt0 < kt1) issue(kt0, 0);
+    if (kt0 + 1 < kt1) issue(kt0 + 1, 1);
+    for (int kt = kt0; kt < kt1; kt += 3) {
+        step(kt, 0, 2);
+        if (kt + 1 < kt1) step(kt + 1, 1, 0);
+        if (kt + 2 < kt1) step(kt + 2, 2, 1);
+    }
+    epilogue();
 }
 
 // Short M (<= 64 tokens): the weights are streamed once and each is used by at
@@ -388,7 +365,7 @@ __global__ __launch_bounds__(256) void splitk_epilogue(const int32_t* __restrict
 
 // A launch plan: tile shape and K split.
 struct Plan {
-    int cfg;       // 0: 128 x 128, 1: 64 x 128, 2: 64 x 64, 3: skinny (see launch_gemm)
+    int cfg;       // 0: 256 x 128, 1: 128 x 128, 2: 64 x 64, 3: skinny, 4: 64 x 128 (see launch_gemm)
     int bm, bn;
     int splits;    // K split count actually used (1 = fused epilogue)
     int per;       // k steps per split
@@ -422,17 +399,17 @@ hipError_t launch_skinny(const Plan& p, const uint8_t* Aq, const float* s_a, con
     return hipGetLastError();
 }
 
-template <int WM, int WN, int TM, int TN, bool UNPACK, int SCHED = 0, int BITS = 4>
-hipError_t launch_cfg(const Plan& p, const uint8_t* Aq, const float* s_a, const uint8_t* Wq, const float* s_w,
-                      int M, int N, int K, uint16_t* Y, int32_t* acc, int32_t* part, hipStream_t st) {
+template <int WM, int WN, int TM, int TN, int BITS = 4, int OCC = 1>
+hipError_t launch_tiled(const Plan& p, const uint8_t* Aq, const float* s_a, const uint8_t* Wq, const float* s_w,
+                       int M, int N, int K, uint16_t* Y, int32_t* acc, int32_t* part, hipStream_t st) {
     dim3 grid((N + p.bn - 1) / p.bn, (M + p.bm - 1) / p.bm, p.splits);
     dim3 block(64 * WM * WN);
     if (p.splits == 1) {
-        hipLaunchKernelGGL((gemm_kernel<WM, WN, TM, TN, UNPACK, false, SCHED, BITS>), grid, block, 0, st, Aq, s_a, Wq, s_w, M,
+        hipLaunchKernelGGL((gemm_tile_kernel<WM, WN, TM, TN, false, BITS, OCC>), grid, block, 0, st, Aq, s_a, Wq, s_w, M,
                            N, K, p.per, Y, acc, (int32_t*)nullptr);
     } else {
-        hipLaunchKernelGGL((gemm_kernel<WM, WN, TM, TN, UNPACK, true, SCHED, BITS>), grid, block, 0, st, Aq, s_a, Wq, s_w, M, N,
-                           K, p.per, (uint16_t*)nullptr, (int32_t*)nullptr, part);
+        hipLaunchKernelGGL((gemm_tile_kernel<WM, WN, TM, TN, true, BITS, OCC>), grid, block, 0, st, Aq, s_a, Wq, s_w, M,
+                           N, K, p.per, (uint16_t*)nullptr, (int32_t*)nullptr, part);
     }
     return hipGetLastError();
 }
@@ -448,14 +425,19 @@ hipError_t finish_split(const Plan& p, int32_t* part, const float* s_a, const fl
 
 // The production plan (from measured sweeps on MI355X):
 //  - M <= 16: the skinny kernel (weight streaming, K split only for narrow N);
-//  - M <= 64: 64 x 64 tiles and a K split up to ~512 workgroups;
+//  - at least 768 tiles of 256 x 128: 256 x 128 (eight waves of 64 x 64);
 //  - at least 512 tiles of 128 x 128: 128 x 128 (four waves of 64 x 64);
-//  - otherwise 64 x 128 (four waves of 64 x 32), split along K below 512 tiles.
+//  - at most 1024 tiles of 64 x 64: 64 x 64 (four waves of 32 x 32);
+//  - otherwise 64 x 128 (four waves of 64 x 32).
+// Below 256 workgroups K is split (twice as deep for K >= 8192), keeping at
+// least 8 k steps per split.
 Plan choose_plan(int M, int N, int K, int bits) {
     const int nk = (K * bits / 8 + kKB - 1) / kKB;
-    auto splits_for = [&](int tiles) {
-        int s = tiles >= 512 ? 1 : (512 + tiles - 1) / tiles;
-        const int cap = nk / 4 > 1 ? nk / 4 : 1;       // keep at least 4 k steps per split
+    auto tiles = [&](int bm, int bn) { return ((M + bm - 1) / bm) * ((N + bn - 1) / bn); };
+    auto splits_for = [&](int t) {
+        int s = t >= 256 ? 1 : (256 + t - 1) / t;
+        if (K >= 8192) s *= 2;
+        const int cap = nk / 8 > 1 ? nk / 8 : 1;
         s = s < cap ? s : cap;
         return s < 32 ? s : 32;
     };
@@ -468,17 +450,18 @@ Plan choose_plan(int M, int N, int K, int bits) {
         s = s < cap ? s : cap;
         p = make_plan(M, N, K, 16, 64, s, bits);
         p.cfg = 3;
-    } else if (M <= 64) {
-        const int tiles = ((M + 63) / 64) * ((N + 63) / 64);
-        p = make_plan(M, N, K, 64, 64, splits_for(tiles), bits);
-        p.cfg = 2;
-    } else if (((M + 127) / 128) * ((N + 127) / 128) >= 512) {
-        p = make_plan(M, N, K, 128, 128, 1, bits);
+    } else if (tiles(256, 128) >= 768) {
+        p = make_plan(M, N, K, 256, 128, 1, bits);
         p.cfg = 0;
-    } else {
-        const int tiles = ((M + 63) / 64) * ((N + 127) / 128);
-        p = make_plan(M, N, K, 64, 128, splits_for(tiles), bits);
+    } else if (tiles(128, 128) >= 512) {
+        p = make_plan(M, N, K, 128, 128, 1, bits);
         p.cfg = 1;
+    } else if (tiles(64, 64) <= 1024) {
+        p = make_plan(M, N, K, 64, 64, splits_for(tiles(64, 64)), bits);
+        p.cfg = 2;
+    } else {
+        p = make_plan(M, N, K, 64, 128, splits_for(tiles(64, 128)), bits);
+        p.cfg = 4;
     }
     return p;
 }
@@ -495,16 +478,22 @@ hipError_t launch_gemm(const uint8_t* Aq, const float* s_a, const uint8_t* Wq, c
     const Plan p = choose_plan(M, N, K, bits);
     int32_t* part = static_cast<int32_t*>(ws);
     hipError_t e;
-    const int sel = p.cfg + (bits == 8 ? 4 : 0);
-    switch (sel) {
-        case 3: e = launch_skinny<1, 8, 4>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
-        case 2: e = launch_cfg<2, 2, 2, 2, false, 1, 4>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
-        case 1: e = launch_cfg<1, 4, 4, 2, false, 1, 4>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
-        case 0: e = launch_cfg<2, 2, 4, 4, false, 1, 4>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
-        case 7: e = launch_skinny<1, 8, 8>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
-        case 6: e = launch_cfg<2, 2, 2, 2, false, 1, 8>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
-        case 5: e = launch_cfg<1, 4, 4, 2, false, 1, 8>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
-        default: e = launch_cfg<2, 2, 4, 4, false, 1, 8>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
+    if (bits == 8) {
+        switch (p.cfg) {
+            case 3: e = launch_skinny<1, 8, 8>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
+            case 0: e = launch_tiled<4, 2, 4, 4, 8, 2>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
+            case 1: e = launch_tiled<2, 2, 4, 4, 8, 3>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
+            case 2: e = launch_tiled<2, 2, 2, 2, 8, 4>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
+            default: e = launch_tiled<1, 4, 4, 2, 8, 4>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
+        }
+    } else {
+        switch (p.cfg) {
+            case 3: e = launch_skinny<1, 8, 4>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
+            case 0: e = launch_tiled<4, 2, 4, 4, 4, 2>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
+            case 1: e = launch_tiled<2, 2, 4, 4, 4, 3>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
+            case 2: e = launch_tiled<2, 2, 2, 2, 4, 4>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
+            default: e = launch_tiled<1, 4, 4, 2, 4, 4>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
+        }
     }
     if (e != hipSuccess) return e;
     return finish_split(p, part, s_a, s_w, M, N, Y, acc, st);
