@@ -264,24 +264,25 @@ __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(OC
     epilogue();
 }
 
-// Short M (<= 64 tokens): the weights are streamed once and each is used by at
-// most 64 rows, so the kernel is bound by HBM bandwidth, not by the MFMA.  No
-// LDS and no barriers: each wave owns 16 output columns and walks its K range,
-// loading its W rows and the (L2-resident) activation rows straight into MFMA
-// operand registers with raw buffer loads, U k steps in flight per batch.  Lane
-// (c, g) reads bytes [16 g, 16 g + 16) of the 64-byte slice of row c (W) or of
-// the activation row, exactly as the tiled kernel's fragments.
-template <int TM, int U, bool SPLIT, int BITS = 4>
-__global__ __launch_bounds__(256) void gemm_skinny_kernel(const uint8_t* __restrict__ Aq,
-                                                          const float* __restrict__ s_a,
-                                                          const uint8_t* __restrict__ Wq,
-                                                          const float* __restrict__ s_w, int M, int N, int K,
-                                                          int ksteps_per_split, uint16_t* __restrict__ Y,
-                                                          int32_t* __restrict__ acc_out,
-                                                          int32_t* __restrict__ part) {
+// Short M (<= 16 tokens): the weights are streamed once and each is used by
+// at most 16 rows, so the kernel is bound by HBM bandwidth, not by the MFMA.  No
+// LDS and no barriers: each wave owns TN x 16 output columns and walks its K
+// range, loading its W rows and the (L2-resident) activation rows straight into
+// MFMA operand registers with raw buffer loads, U k steps in flight per batch;
+// an activation fragment serves TN weight fragments.  Lane (c, g) reads bytes
+// [16 g, 16 g + 16) of the 64-byte slice of row c (W) or of the activation row,
+// exactly as the tiled kernel's fragments.
+template <int TM, int U, bool SPLIT, int BITS = 4, int WPB = 1, int TN = 1>
+__global__ __launch_bounds__(64 * WPB) void gemm_skinny_kernel(const uint8_t* __restrict__ Aq,
+                                                               const float* __restrict__ s_a,
+                                                               const uint8_t* __restrict__ Wq,
+                                                               const float* __restrict__ s_w, int M, int N, int K,
+                                                               int ksteps_per_split, uint16_t* __restrict__ Y,
+                                                               int32_t* __restrict__ acc_out,
+                                                               int32_t* __restrict__ part) {
     const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
     const int lr = lane % 16, lg = lane / 16;
-    const int col0 = (blockIdx.x * 4 + wave) * 16;
+    const int col0 = (blockIdx.x * WPB + wave) * 16 * TN;
     if (col0 >= N) return;                                   // whole wave past N: nothing to do
     const uint32_t ldb = (uint32_t)K * BITS / 8;
     const int nk_total = (int)((ldb + kKB - 1) / kKB);
@@ -290,40 +291,51 @@ __global__ __launch_bounds__(256) void gemm_skinny_kernel(const uint8_t* __restr
     const __amdgpu_buffer_rsrc_t rA = make_rsrc(Aq, (uint32_t)M * ldb);
     const __amdgpu_buffer_rsrc_t rW = make_rsrc(Wq, (uint32_t)N * ldb);
     const uint32_t seg = 16 * lg;
-    const uint32_t ow = col0 + lr < N ? (uint32_t)(col0 + lr) * ldb + seg : kOOB;
-    uint32_t oa[TM];
+    uint32_t ow[TN], oa[TM];
+#pragma unroll
+    for (int t = 0; t < TN; ++t) {
+        const int c = col0 + 16 * t + lr;
+        ow[t] = c < N ? (uint32_t)c * ldb + seg : kOOB;
+    }
 #pragma unroll
     for (int i = 0; i < TM; ++i) oa[i] = 16 * i + lr < M ? (uint32_t)(16 * i + lr) * ldb + seg : kOOB;
 
-    v4i acc[TM];
+    v4i acc[TN][TM];
 #pragma unroll
-    for (int i = 0; i < TM; ++i) acc[i] = v4i{0, 0, 0, 0};
+    for (int t = 0; t < TN; ++t)
+#pragma unroll
+        for (int i = 0; i < TM; ++i) acc[t][i] = v4i{0, 0, 0, 0};
     // two register batches of U k steps: batch b + 1 is in flight while batch b is
     // multiplied (steps past the split or the row read as zeros)
-    auto issue = [&](int kb, v4i (&w)[U], v4i (&a)[U][TM]) {
+    auto issue = [&](int kb, v4i (&w)[U][TN], v4i (&a)[U][TM]) {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const uint32_t ko = (uint32_t)(kb + u) * kKB;
             const bool in = kb + u < kt1 && ko + seg < ldb;
-            w[u] = __builtin_amdgcn_raw_buffer_load_b128(rW, (int)(in ? ow + ko : kOOB), 0, 0);
+#pragma unroll
+            for (int t = 0; t < TN; ++t)
+                w[u][t] = __builtin_amdgcn_raw_buffer_load_b128(rW, (int)(in ? ow[t] + ko : kOOB), 0, 0);
 #pragma unroll
             for (int i = 0; i < TM; ++i)
                 a[u][i] = __builtin_amdgcn_raw_buffer_load_b128(rA, (int)(in ? oa[i] + ko : kOOB), 0, 0);
         }
     };
-    auto compute = [&](const v4i (&w)[U], const v4i (&a)[U][TM]) {
+    auto compute = [&](const v4i (&w)[U][TN], const v4i (&a)[U][TM]) {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
 #pragma unroll
             for (int h = 0; h < (BITS == 4 ? 2 : 1); ++h) {
-                const v4i b = operand<BITS>(w[u], h);
 #pragma unroll
-                for (int i = 0; i < TM; ++i)
-                    acc[i] = __builtin_amdgcn_mfma_i32_16x16x64_i8(operand<BITS>(a[u][i], h), b, acc[i], 0, 0, 0);
+                for (int i = 0; i < TM; ++i) {
+                    const v4i x = operand<BITS>(a[u][i], h);
+#pragma unroll
+                    for (int t = 0; t < TN; ++t)
+                        acc[t][i] = __builtin_amdgcn_mfma_i32_16x16x64_i8(x, operand<BITS>(w[u][t], h), acc[t][i], 0, 0, 0);
+                }
             }
         }
     };
-    v4i w0[U], a0[U][TM], w1[U], a1[U][TM];
+    v4i w0[U][TN], a0[U][TM], w1[U][TN], a1[U][TM];
     issue(kt0, w0, a0);
     for (int kb = kt0; kb < kt1; kb += 2 * U) {
         issue(kb + U, w1, a1);
@@ -334,20 +346,23 @@ __global__ __launch_bounds__(256) void gemm_skinny_kernel(const uint8_t* __restr
         __builtin_amdgcn_sched_barrier(0);
         compute(w1, a1);
     }
-    const int col = col0 + lr;
-    if (col >= N) return;
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
+    for (int t = 0; t < TN; ++t) {
+        const int col = col0 + 16 * t + lr;
+        if (col >= N) continue;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int row = 16 * i + 4 * lg + r;
-            if (row >= M) continue;
-            const int v = acc_value<BITS>(acc[i][r]);
-            if (SPLIT)
-                part[((size_t)blockIdx.z * M + row) * N + col] = v;
-            else
-                store_out(row, col, v, s_a, s_w, Y, acc_out, N);
-        }
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int row = 16 * i + 4 * lg + r;
+                if (row >= M) continue;
+                const int v = acc_value<BITS>(acc[t][i][r]);
+                if (SPLIT)
+                    part[((size_t)blockIdx.z * M + row) * N + col] = v;
+                else
+                    store_out(row, col, v, s_a, s_w, Y, acc_out, N);
+            }
+    }
 }
 
 // Adds the split-K partial sums (exact int32) and applies the epilogue.
@@ -365,7 +380,7 @@ __global__ __launch_bounds__(256) void splitk_epilogue(const int32_t* __restrict
 
 // A launch plan: tile shape and K split.
 struct Plan {
-    int cfg;       // 0: 256 x 128, 1: 128 x 128, 2: 64 x 64, 3: skinny, 4: 64 x 128 (see launch_gemm)
+    int cfg;       // 0: 256 x 128, 1: 128 x 128, 2: 64 x 64, 3 / 5: skinny, 4: 64 x 128 (see launch_gemm)
     int bm, bn;
     int splits;    // K split count actually used (1 = fused epilogue)
     int per;       // k steps per split
@@ -385,16 +400,17 @@ Plan make_plan(int M, int N, int K, int bm, int bn, int want_splits, int bits = 
     return p;
 }
 
-template <int TM, int U, int BITS = 4>
+template <int TM, int U, int BITS = 4, int WPB = 1, int TN = 1>
 hipError_t launch_skinny(const Plan& p, const uint8_t* Aq, const float* s_a, const uint8_t* Wq, const float* s_w,
                          int M, int N, int K, uint16_t* Y, int32_t* acc, int32_t* part, hipStream_t st) {
-    dim3 grid((N + 63) / 64, 1, p.splits);
+    constexpr int CPB = 16 * WPB * TN;                 // columns per workgroup
+    dim3 grid((N + CPB - 1) / CPB, 1, p.splits);
     if (p.splits == 1) {
-        hipLaunchKernelGGL((gemm_skinny_kernel<TM, U, false, BITS>), grid, dim3(256), 0, st, Aq, s_a, Wq, s_w, M, N, K,
-                           p.per, Y, acc, (int32_t*)nullptr);
+        hipLaunchKernelGGL((gemm_skinny_kernel<TM, U, false, BITS, WPB, TN>), grid, dim3(64 * WPB), 0, st, Aq, s_a,
+                           Wq, s_w, M, N, K, p.per, Y, acc, (int32_t*)nullptr);
     } else {
-        hipLaunchKernelGGL((gemm_skinny_kernel<TM, U, true, BITS>), grid, dim3(256), 0, st, Aq, s_a, Wq, s_w, M, N, K,
-                           p.per, (uint16_t*)nullptr, (int32_t*)nullptr, part);
+        hipLaunchKernelGGL((gemm_skinny_kernel<TM, U, true, BITS, WPB, TN>), grid, dim3(64 * WPB), 0, st, Aq, s_a,
+                           Wq, s_w, M, N, K, p.per, (uint16_t*)nullptr, (int32_t*)nullptr, part);
     }
     return hipGetLastError();
 }
@@ -424,7 +440,7 @@ hipError_t finish_split(const Plan& p, int32_t* part, const float* s_a, const fl
 }
 
 // The production plan (from measured sweeps on MI355X):
-//  - M <= 16: the skinny kernel (weight streaming, K split only for narrow N);
+//  - M <= 16: the skinny kernel (weight streaming, K split only for narrow N and long K);
 //  - at least 768 tiles of 256 x 128: 256 x 128 (eight waves of 64 x 64);
 //  - at least 512 tiles of 128 x 128: 128 x 128 (four waves of 64 x 64);
 //  - at most 1024 tiles of 64 x 64: 64 x 64 (four waves of 32 x 32);
@@ -443,13 +459,16 @@ Plan choose_plan(int M, int N, int K, int bits) {
     };
     Plan p;
     if (M <= 16) {
-        // skinny kernel: one wave per 16 columns; split K only when there are few columns
-        const int wgs = (N + 63) / 64;
-        int s = wgs >= 128 ? 1 : (256 + wgs - 1) / wgs;
+        // skinny kernel, one wave per workgroup: 32 columns per wave when that
+        // still gives at least 512 waves, else 16; K is split (up to 4 ways)
+        // only for few waves and long K
+        const bool wide = (N + 31) / 32 >= 512;
+        const int waves = (N + (wide ? 31 : 15)) / (wide ? 32 : 16);
+        int s = waves < 512 && nk >= 64 ? 4 : 1;
         const int cap = nk / 16 > 1 ? nk / 16 : 1;     // keep two batches of 8 k steps per split
         s = s < cap ? s : cap;
-        p = make_plan(M, N, K, 16, 64, s, bits);
-        p.cfg = 3;
+        p = make_plan(M, N, K, 16, wide ? 32 : 16, s, bits);
+        p.cfg = wide ? 5 : 3;
     } else if (tiles(256, 128) >= 768) {
         p = make_plan(M, N, K, 256, 128, 1, bits);
         p.cfg = 0;
@@ -480,7 +499,8 @@ hipError_t launch_gemm(const uint8_t* Aq, const float* s_a, const uint8_t* Wq, c
     hipError_t e;
     if (bits == 8) {
         switch (p.cfg) {
-            case 3: e = launch_skinny<1, 8, 8>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
+            case 3: e = launch_skinny<1, 8, 8, 1, 1>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
+            case 5: e = launch_skinny<1, 4, 8, 1, 2>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
             case 0: e = launch_tiled<4, 2, 4, 4, 8, 2>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
             case 1: e = launch_tiled<2, 2, 4, 4, 8, 3>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
             case 2: e = launch_tiled<2, 2, 2, 2, 8, 4>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
@@ -488,7 +508,8 @@ hipError_t launch_gemm(const uint8_t* Aq, const float* s_a, const uint8_t* Wq, c
         }
     } else {
         switch (p.cfg) {
-            case 3: e = launch_skinny<1, 8, 4>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
+            case 3: e = launch_skinny<1, 8, 4, 1, 1>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
+            case 5: e = launch_skinny<1, 4, 4, 1, 2>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
             case 0: e = launch_tiled<4, 2, 4, 4, 4, 2>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
             case 1: e = launch_tiled<2, 2, 4, 4, 4, 3>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
             case 2: e = launch_tiled<2, 2, 2, 2, 4, 4>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;

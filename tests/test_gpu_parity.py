@@ -145,9 +145,16 @@ def _codes(M, K, seed, lo=-7, hi=7):
     return pack_codes(q)
 
 
-@pytest.mark.parametrize("M,N,K", [(1, 8, 64), (16, 4096, 4096), (5, 4104, 4096), (9, 136, 192), (16, 24, 18944),
-                                   (16, 12288, 4096), (33, 520, 1024), (77, 200, 192), (128, 256, 512),
-                                   (300, 136, 4096), (1024, 1024, 1024), (513, 4104, 3584), (64, 512, 18944)])
+# Shapes cover every launch plan with ragged edges: the skinny kernel with 16 and
+# 32 columns per wave (with and without a K split), 64 x 64 with a K split,
+# 64 x 128, 128 x 128 and 256 x 128 tiles, and k tails of half a step.
+GEMM_SHAPES = [(1, 8, 64), (16, 4096, 4096), (5, 4104, 4096), (9, 136, 192), (16, 24, 18944),
+               (16, 12288, 4096), (16, 4096, 12288), (9, 16392, 192), (16, 32768, 256), (33, 520, 1024),
+               (77, 200, 192), (128, 256, 512), (300, 136, 4096), (300, 16384, 64), (1024, 1024, 1024),
+               (1000, 8200, 64), (2100, 12296, 64), (513, 4104, 3584), (64, 512, 18944)]
+
+
+@pytest.mark.parametrize("M,N,K", GEMM_SHAPES)
 def test_gemm_bit_exact(M, N, K):
     Aq = _codes(M, K, 1)
     Wq = _codes(N, K, 2)
@@ -180,7 +187,7 @@ def test_gemm_extreme_codes():
 def test_gemm_split_and_unsplit_agree():
     """Rows computed through the split-K path (short M) equal the same rows inside a
     tall M that takes the single-pass path."""
-    K, N = 4096, 4096
+    K, N = 12288, 4096
     Aq = _codes(2048, K, 7)
     Wq = _codes(N, K, 8)
     s_a = np.random.default_rng(9).uniform(0.1, 2, 2048).astype(np.float32)
@@ -346,8 +353,7 @@ def test_w8_prepare_weights(withP):
     assert_bits(host(Wq), rq, "Wq")
 
 
-@pytest.mark.parametrize("M,N,K", [(1, 8, 64), (16, 4096, 4096), (9, 136, 192), (33, 520, 1024), (77, 200, 192),
-                                   (300, 136, 4096), (1024, 1024, 1024), (513, 4104, 3584), (64, 512, 18944)])
+@pytest.mark.parametrize("M,N,K", GEMM_SHAPES)
 def test_w8a8_gemm_bit_exact(M, N, K):
     rng = np.random.default_rng(10)
     Aq = rng.integers(-128, 128, (M, K)).astype(np.int8)
