@@ -37,7 +37,7 @@ PEAK_INT8_TOPS = 5000.0           # dense int8 MFMA, TOP/s
 PEAK_FP32_VALU_TFLOPS = 78.6
 
 
-def recorded_traffic(kernel: str):
+def recorded_traffic(kernel: str, field: str = "traffic_bytes_per_launch"):
     """HBM bytes per launch of `kernel` from the committed counter record, or None
     when the kernel's sources have changed since the counters were taken."""
     import hashlib
@@ -51,7 +51,7 @@ def recorded_traffic(kernel: str):
         with open(path, "rb") as f:
             if hashlib.sha256(f.read()).hexdigest()[:16] != h:
                 return None
-    return rec["traffic_bytes_per_launch_step_avg"]
+    return rec.get(field)
 
 
 def parse():
@@ -63,6 +63,10 @@ def parse():
     ap.add_argument("--cpu-sample", type=int, default=384, help="tokens in the oracle timing sample")
     ap.add_argument("--only", choices=["dense", "folded", "both"], default="both")
     ap.add_argument("--no-w8", action="store_true", help="skip the W8A8 (App. D) folded-basis measurement")
+    ap.add_argument("--no-large", action="store_true",
+                    help="skip the 16384-token Dream-shaped layer set (large-token GEMM figures)")
+    ap.add_argument("--no-small", action="store_true",
+                    help="skip the 16/32/64-token denoising-step layer sets (small-token HBM figures)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain 1 GiB device copy (reference for HBM byte counters)")
     return ap.parse_args()
@@ -89,6 +93,194 @@ class Timer:
 
     def reset(self):
         self.pairs = {}
+
+
+def graph_ms(torch, fn, calls, replays=5):
+    """Median milliseconds per call of fn(i), i = 0 .. calls - 1, captured back to
+    back in one HIP graph, so that no host work sits between the launches."""
+    fn(0)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            for i in range(calls):
+                fn(i)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    ts = []
+    for _ in range(replays):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1) / calls)
+    ts.sort()
+    return ts[len(ts) // 2], g
+
+
+def large_token_block(torch, sq, synth, dev, steps, warmup):
+    """Dream-shaped layer set, 8 x 2048 tokens, folded P: per linear the gate +
+    int4 quantiser (TAC ahead of O) and the W4A4 GEMM.  Event pairs per call; the
+    kernels are long enough that the host keeps the queue full."""
+    cfg = synth.CONFIGS[2]
+    st_np = synth.config_state(2)
+    M = len(st_np)
+    state = torch.from_numpy(st_np).to(dev)
+    sites = []
+    for si, site in enumerate(cfg.sites):
+        t = synth.site_tensors(2, si, st_np, with_P=False)
+        W = torch.from_numpy(t.W).to(dev)
+        Wq, s_w = sq.sgat_prepare_weights(W, None)
+        del W
+        d = dict(name=site.name, K=site.K, N=site.N, dm=t.dm, du=t.du, X=torch.from_numpy(t.X).to(dev),
+                 Wq=Wq, s_w=s_w, Aq=torch.empty((M, site.K // 2), dtype=torch.uint8, device=dev),
+                 s_a=torch.empty((M,), dtype=torch.float32, device=dev),
+                 Y=torch.empty((M, site.N), dtype=torch.float16, device=dev))
+        if site.tac:
+            d.update(tac_M=torch.from_numpy(t.tac_M).to(dev), tac_d=torch.from_numpy(t.tac_d).to(dev), g=t.g)
+        d["qws"] = torch.empty(max(sq.quant_act_workspace_bytes(M, site.K, False, site.tac), 1), dtype=torch.uint8,
+                               device=dev)
+        d["gws"] = torch.empty(max(sq.gemm_workspace_bytes(M, site.N, site.K), 1), dtype=torch.uint8, device=dev)
+        sites.append(d)
+        del t
+    timer = Timer(torch)
+
+    def step(tm):
+        for d in sites:
+            tm.wrap("q/" + d["name"], lambda: sq.sgat_quant_act(d["X"], state, None, d["dm"], d["du"], d.get("tac_M"),
+                                                                 d.get("tac_d"), d.get("g", 0), Aq=d["Aq"],
+                                                                 s_a=d["s_a"], ws=d["qws"]))
+            tm.wrap("g/" + d["name"], lambda: sq.w4a4_gemm(d["Aq"], d["s_a"], d["Wq"], d["s_w"], Y=d["Y"],
+                                                            ws=d["gws"]))
+    for _ in range(warmup):
+        step(Timer(torch))
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        step(timer)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    per = {}
+    tot_ops = tot_ms = 0.0
+    for d in sites:
+        gms = timer.ms("g/" + d["name"])[0] / steps
+        ops = 2.0 * M * d["N"] * d["K"]
+        per[d["name"]] = {"M": M, "N": d["N"], "K": d["K"], "gemm_us": gms * 1e3, "tops": ops / gms / 1e9,
+                          "frac_int8_peak": ops / gms / 1e9 / PEAK_INT8_TOPS,
+                          "quant_act_us": timer.ms("q/" + d["name"])[0] / steps * 1e3}
+        tot_ops += ops
+        tot_ms += gms
+    dom = max(per, key=lambda n: per[n]["gemm_us"])
+    out = {"workload": "Dream-7B-shaped SGAT layer set (QKV 3584->4608, O+TAC 3584->3584, gate+up 3584->37888, "
+                       "down 18944->3584), 8 x 2048 tokens, folded P",
+           "tokens": M, "ms_per_step": ms, "tokens_per_s": M / (ms / 1e3),
+           "gemm_tops": tot_ops / tot_ms / 1e9, "gemm_frac_int8_peak": tot_ops / tot_ms / 1e9 / PEAK_INT8_TOPS,
+           "per_site": per,
+           "roofline": {"bound": "mfma", "achieved": per[dom]["tops"], "peak": PEAK_INT8_TOPS, "unit": "TOP/s",
+                        "frac": per[dom]["frac_int8_peak"],
+                        "traffic": recorded_traffic("gemm_large") if dom == "gate_up" else None,
+                        "kernel": f"w4a4 gemm ({dom})"}}
+    del sites
+    torch.cuda.empty_cache()
+    return out
+
+
+def small_token_block(torch, sq, synth, dev, token_counts=(16, 32, 64), copies=4):
+    """Denoising-step layer sets at small token counts (LLaDA shapes, step 32 of
+    64, folded P), captured in a HIP graph.  `copies` rotating sets of prepared
+    weights (4 x 108 MB) keep the 256 MB last-level cache from serving them.
+    Bytes are the algorithmic HBM traffic: fp16 activations read once, codes
+    written and read once, the packed weights and scales, the fp16 outputs."""
+    cfg = synth.CONFIGS[4]
+    st64 = synth.config_state(4, M=max(token_counts), t=32)
+    wsets = [[] for _ in range(copies)]
+    meta = []
+    for si, site in enumerate(cfg.sites):
+        t = synth.site_tensors(4, si, st64, with_P=False)
+        W = torch.from_numpy(t.W).to(dev)
+        Wq, s_w = sq.sgat_prepare_weights(W, None)
+        del W
+        for c in range(copies):
+            wsets[c].append((Wq.clone(), s_w.clone()))
+        meta.append(site)
+        del t, Wq, s_w
+    out = {}
+    dom_rec = None
+    for M in token_counts:
+        st_np = synth.config_state(4, M=M, t=32)
+        state = torch.from_numpy(st_np).to(dev)
+        sites = []
+        byts = 0
+        for si, site in enumerate(meta):
+            t = synth.site_tensors(4, si, st_np, with_W=False, with_P=False)
+            K, N = site.K, site.N
+            d = dict(name=site.name, K=K, N=N, dm=t.dm, du=t.du, X=torch.from_numpy(t.X).to(dev),
+                     Aq=torch.empty((M, K // 2), dtype=torch.uint8, device=dev),
+                     s_a=torch.empty((M,), dtype=torch.float32, device=dev),
+                     Y=torch.empty((M, N), dtype=torch.float16, device=dev))
+            tb = 0
+            if site.tac:
+                d.update(tac_M=torch.from_numpy(t.tac_M).to(dev), tac_d=torch.from_numpy(t.tac_d).to(dev), g=t.g)
+                tb = t.tac_M.nbytes + t.tac_d.nbytes
+            d["qws"] = torch.empty(max(sq.quant_act_workspace_bytes(M, K, False, site.tac), 1), dtype=torch.uint8,
+                                   device=dev)
+            d["gws"] = torch.empty(max(sq.gemm_workspace_bytes(M, N, K), 1), dtype=torch.uint8, device=dev)
+            d["gemm_bytes"] = N * K // 2 + N * 4 + M * K // 2 + M * 4 + M * N * 2
+            byts += M * K * 2 + tb + M * K // 2 + M * 4 + d["gemm_bytes"]
+            sites.append(d)
+
+        def qa(d):
+            sq.sgat_quant_act(d["X"], state, None, d["dm"], d["du"], d.get("tac_M"), d.get("tac_d"),
+                              d.get("g", 0), Aq=d["Aq"], s_a=d["s_a"], ws=d["qws"])
+
+        def step(i):
+            for d, (Wq, s_w) in zip(sites, wsets[i % copies]):
+                qa(d)
+                sq.w4a4_gemm(d["Aq"], d["s_a"], Wq, s_w, Y=d["Y"], ws=d["gws"])
+
+        step(0)
+        torch.cuda.synchronize()
+        eager = [d["Y"].clone() for d in sites]
+        ms, g = graph_ms(torch, step, copies)
+        g.replay()
+        torch.cuda.synchronize()
+        same = all(torch.equal(a, d["Y"]) for a, d in zip(eager, sites))
+        del g
+        rec = {"ms_per_step": ms, "tokens_per_s": M / (ms / 1e3), "hbm_bytes_per_step": byts,
+               "hbm_gbs": byts / ms / 1e6, "frac_hbm_peak": byts / ms / 1e6 / PEAK_HBM_GBS,
+               "graph_matches_eager": same, "gemm": {}}
+        for si, d in enumerate(sites):
+            qa(d)
+            gms, g = graph_ms(torch, lambda i, d=d, si=si: sq.w4a4_gemm(d["Aq"], d["s_a"], wsets[i % copies][si][0],
+                                                                        wsets[i % copies][si][1], Y=d["Y"],
+                                                                        ws=d["gws"]), 4 * copies)
+            del g
+            rec["gemm"][d["name"]] = {"us": gms * 1e3, "gbs": d["gemm_bytes"] / gms / 1e6,
+                                      "frac_hbm_peak": d["gemm_bytes"] / gms / 1e6 / PEAK_HBM_GBS}
+        out[str(M)] = rec
+        if M == min(token_counts):
+            dn = max(rec["gemm"], key=lambda n: rec["gemm"][n]["us"])
+            dom_rec = (dn, rec["gemm"][dn])
+        del sites
+    res = {"workload": "LLaDA-8B-shaped layer set at 16, 32 and 64 tokens (denoising step 32 of 64), folded P, "
+                       "HIP-graph replay, 4 rotating weight sets",
+           "per_tokens": out}
+    if dom_rec:
+        dn, r = dom_rec
+        res["roofline"] = {"bound": "hbm", "achieved": r["gbs"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                           "frac": r["frac_hbm_peak"],
+                           "traffic": recorded_traffic("gemm_small") if dn == "gate_up" else None,
+                           "kernel": f"w4a4 gemm ({dn}, {min(token_counts)} tokens)"}
+    del wsets
+    torch.cuda.empty_cache()
+    return res
 
 
 def main():
@@ -229,6 +421,11 @@ def main():
         out["w8"] = dict(ms=ms_w8, gemm_tops=gm_ops / gm_ms / 1e9,
                          quant_act_ms=sum(timer.ms("quant_act8/" + n)[0] for n in ops_gemm) / args.steps)
 
+    if not args.no_large:
+        out["large"] = large_token_block(torch, sq, synth, dev, max(3, args.steps // 4), 1)
+    if not args.no_small:
+        out["small"] = small_token_block(torch, sq, synth, dev)
+
     # ---------------------------------------------------------------- CPU baseline
     cpu = None
     if not args.no_cpu_baseline:
@@ -275,7 +472,8 @@ def main():
     if dense:
         ach = dense["transform_tflops"]
         res["roofline"] = {"bound": "alu", "achieved": ach, "peak": PEAK_FP32_VALU_TFLOPS, "unit": "TFLOP/s",
-                           "frac": ach / PEAK_FP32_VALU_TFLOPS, "traffic": recorded_traffic("transform"),
+                           "frac": ach / PEAK_FP32_VALU_TFLOPS,
+                           "traffic": recorded_traffic("transform", "traffic_bytes_per_launch_step_avg"),
                            "kernel": "transform (dense fp32 x P, fixed order)"}
         res["breakdown_ms"] = {k: dense[k] for k in ("transform_ms", "gemm_ms", "tac_ms", "quant_ms")}
         res["gemm"] = {"tops": dense["gemm_tops"], "frac_int8_peak": dense["gemm_tops"] / PEAK_INT8_TOPS}
@@ -294,6 +492,10 @@ def main():
         res["w8a8_folded_P"] = {"value": M / (w8["ms"] / 1e3), "unit": "tokens/s", "ms_per_step": w8["ms"],
                                 "gemm_tops": w8["gemm_tops"], "gemm_frac_int8_peak": w8["gemm_tops"] / PEAK_INT8_TOPS,
                                 "quant_act_ms": w8["quant_act_ms"]}
+    if "large" in out:
+        res["large_token"] = out["large"]
+    if "small" in out:
+        res["small_token"] = out["small"]
     if cpu:
         res["cpu_baseline"] = cpu
     print(json.dumps(res), flush=True)

@@ -33,6 +33,8 @@
  *    calling thread.
  *  - Shape rules: K % 64 == 0 and 64 <= K <= 131072; N % 8 == 0; all pointers
  *    16-byte aligned.  TAC block size g is a power of two, 1 <= g <= 128, g | C.
+ *    w4a4_gemm, w8a8_gemm, tac_apply and sgat_quant_act with TAC take at most
+ *    4194240 (65535 x 64) rows per call.
  *  - Arithmetic is fixed so that results are a unique function of the inputs:
  *    fp32 IEEE throughout (correctly rounded divide, round-to-nearest-even, no
  *    flush of subnormals); the transform accumulates k in chunks of 256 with a

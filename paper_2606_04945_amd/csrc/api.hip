@@ -26,6 +26,10 @@ int hip_status(hipError_t e, const char* what) {
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
+// Row-tiled launches put row tiles (at least 64 rows each) on the second grid
+// axis, which holds at most 65535 workgroups.
+constexpr int32_t kMaxTiledRows = 65535 * 64;
+
 constexpr size_t kAlign = 256;
 size_t round_up(size_t n) { return (n + kAlign - 1) / kAlign * kAlign; }
 
@@ -138,6 +142,8 @@ int quant_act(const uint16_t* X, const uint8_t* state, const float* P, int32_t M
     if (tac_M) {
         SQ_REQUIRE(tac_d, SQ_ERR_NULL, "%s: tac_d is required with tac_M", name);
         SQ_TRY(check_tac(K, g));
+        SQ_REQUIRE(M <= kMaxTiledRows, SQ_ERR_SHAPE, "%s: M=%d: at most %d rows per call with TAC", name, M,
+                   kMaxTiledRows);
     }
     if (M == 0) return SQ_OK;
     SQ_REQUIRE(X && Aq && s_a, SQ_ERR_NULL, "%s: X, Aq and s_a are required", name);
@@ -170,6 +176,7 @@ int gemm(const uint8_t* Aq, const float* s_a, const uint8_t* Wq, const float* s_
     SQ_TRY(check_K(K));
     SQ_REQUIRE(bits == 4 || K <= 65536, SQ_ERR_SHAPE, "%s: K=%d: 8-bit codes need K <= 65536", name, K);
     SQ_REQUIRE(M >= 0 && N >= 0, SQ_ERR_SHAPE, "M=%d N=%d: need >= 0", M, N);
+    SQ_REQUIRE(M <= kMaxTiledRows, SQ_ERR_SHAPE, "%s: M=%d: at most %d rows per call", name, M, kMaxTiledRows);
     SQ_REQUIRE(N % 8 == 0, SQ_ERR_SHAPE, "N=%d: need N %% 8 == 0", N);
     // operand rows are addressed with 32-bit buffer offsets
     const size_t row_bytes = (size_t)K * bits / 8;
@@ -254,6 +261,7 @@ int tac_apply(const uint16_t* Z, const uint16_t* tac_M, const uint16_t* tac_d, i
     SQ_TRY(check_K(C));
     SQ_TRY(check_tac(C, g));
     SQ_REQUIRE(M >= 0, SQ_ERR_SHAPE, "M=%d < 0", M);
+    SQ_REQUIRE(M <= kMaxTiledRows, SQ_ERR_SHAPE, "tac_apply: M=%d: at most %d rows per call", M, kMaxTiledRows);
     if (M == 0) return SQ_OK;
     SQ_REQUIRE(Z && tac_M && tac_d && Z_out, SQ_ERR_NULL, "tac_apply: Z, tac_M, tac_d and Z_out are required");
     SQ_REQUIRE(aligned16(Z) && aligned16(tac_M) && aligned16(tac_d) && aligned16(Z_out), SQ_ERR_ALIGN,

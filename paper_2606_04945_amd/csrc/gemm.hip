@@ -133,7 +133,11 @@ __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(OC
     const u32x4 rW = sgpr_rsrc(Wq, (uint32_t)N * ldb);
     auto swz = [](int r) { return (r >> 1) & 3; };       // 16-byte chunk swizzle of a 64-byte LDS row
 
-    const int row0 = blockIdx.y * BM, col0 = blockIdx.x * BN;
+    // groups of 8 row tiles per XCD (see xcd_tile): the workgroups an XCD runs
+    // together share 8 row tiles of A and a few column tiles of W in its L2
+    int rt, ct;
+    xcd_tile(blockIdx.x, (M + BM - 1) / BM, (N + BN - 1) / BN, 8, rt, ct);
+    const int row0 = rt * BM, col0 = ct * BN;
     const int kt0 = SPLIT ? blockIdx.z * ksteps_per_split : 0;
     const int kt1 = SPLIT ? min(nk_total, kt0 + ksteps_per_split) : nk_total;
 
@@ -418,7 +422,9 @@ hipError_t launch_skinny(const Plan& p, const uint8_t* Aq, const float* s_a, con
 template <int WM, int WN, int TM, int TN, int BITS = 4, int OCC = 1>
 hipError_t launch_tiled(const Plan& p, const uint8_t* Aq, const float* s_a, const uint8_t* Wq, const float* s_w,
                        int M, int N, int K, uint16_t* Y, int32_t* acc, int32_t* part, hipStream_t st) {
-    dim3 grid((N + p.bn - 1) / p.bn, (M + p.bm - 1) / p.bm, p.splits);
+    const size_t tiles = (size_t)((N + p.bn - 1) / p.bn) * (size_t)((M + p.bm - 1) / p.bm);
+    if (tiles > 0x7fffffffu) return hipErrorInvalidConfiguration;
+    dim3 grid((unsigned)tiles, 1, p.splits);
     dim3 block(64 * WM * WN);
     if (p.splits == 1) {
         hipLaunchKernelGGL((gemm_tile_kernel<WM, WN, TM, TN, false, BITS, OCC>), grid, block, 0, st, Aq, s_a, Wq, s_w, M,
@@ -439,20 +445,20 @@ hipError_t finish_split(const Plan& p, int32_t* part, const float* s_a, const fl
     return hipGetLastError();
 }
 
-// The production plan (from measured sweeps on MI355X):
+// The production plan (from measured sweeps on MI355X, graph-replayed with
+// rotating weights):
 //  - M <= 16: the skinny kernel (weight streaming, K split only for narrow N and long K);
 //  - at least 768 tiles of 256 x 128: 256 x 128 (eight waves of 64 x 64);
 //  - at least 512 tiles of 128 x 128: 128 x 128 (four waves of 64 x 64);
-//  - at most 1024 tiles of 64 x 64: 64 x 64 (four waves of 32 x 32);
-//  - otherwise 64 x 128 (four waves of 64 x 32).
-// Below 256 workgroups K is split (twice as deep for K >= 8192), keeping at
-// least 8 k steps per split.
+//  - at least 512 tiles of 64 x 128: 64 x 128 (four waves of 64 x 32);
+//  - otherwise 64 x 64 (four waves of 32 x 32), with K split below 256 tiles
+//    (twice as deep for K >= 8192) and kept at 8 k steps or more per split.
 Plan choose_plan(int M, int N, int K, int bits) {
     const int nk = (K * bits / 8 + kKB - 1) / kKB;
     auto tiles = [&](int bm, int bn) { return ((M + bm - 1) / bm) * ((N + bn - 1) / bn); };
     auto splits_for = [&](int t) {
         int s = t >= 256 ? 1 : (256 + t - 1) / t;
-        if (K >= 8192) s *= 2;
+        if (K >= 8192 && t <= 256) s *= 2;
         const int cap = nk / 8 > 1 ? nk / 8 : 1;
         s = s < cap ? s : cap;
         return s < 32 ? s : 32;
@@ -475,12 +481,12 @@ Plan choose_plan(int M, int N, int K, int bits) {
     } else if (tiles(128, 128) >= 512) {
         p = make_plan(M, N, K, 128, 128, 1, bits);
         p.cfg = 1;
-    } else if (tiles(64, 64) <= 1024) {
+    } else if (tiles(64, 128) >= 512) {
+        p = make_plan(M, N, K, 64, 128, 1, bits);
+        p.cfg = 4;
+    } else {
         p = make_plan(M, N, K, 64, 64, splits_for(tiles(64, 64)), bits);
         p.cfg = 2;
-    } else {
-        p = make_plan(M, N, K, 64, 128, splits_for(tiles(64, 128)), bits);
-        p.cfg = 4;
     }
     return p;
 }

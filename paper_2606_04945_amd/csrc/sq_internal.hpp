@@ -10,6 +10,26 @@ namespace sq {
 
 constexpr int kWave = 64;
 constexpr int kChunk = 256;          // transform k-chunk (fixed evaluation order)
+constexpr int kXcds = 8;             // accelerator complex dies, each with its own L2
+
+// Tile order for a one-dimensional grid of T = R x C output tiles.  Workgroup
+// dispatch goes round-robin over the XCDs (dispatch index L runs on XCD L % 8),
+// so the tiles are first split into 8 contiguous ranges, one per XCD, and
+// within a range they are visited in groups of G row tiles, row tile fastest:
+// the workgroups an XCD runs at the same time then share G row tiles and a few
+// column tiles, which its L2 serves after the first fetch.  A bijection on
+// [0, T) for any dispatch order, so only locality depends on the assumption.
+__device__ __forceinline__ void xcd_tile(int L, int R, int C, int G, int& r, int& c) {
+    const int T = R * C;
+    const int base = T / kXcds, rem = T % kXcds;
+    const int x = L % kXcds, local = L / kXcds;
+    const int v = x * base + (x < rem ? x : rem) + local;
+    const int per_group = G * C;
+    const int first = (v / per_group) * G;
+    const int gsz = R - first < G ? R - first : G;
+    r = first + (v % per_group) % gsz;
+    c = (v % per_group) / gsz;
+}
 
 typedef int v4i __attribute__((ext_vector_type(4)));
 

@@ -35,7 +35,13 @@ __global__ __launch_bounds__(kThreads) void transform_kernel(
 
     const int tid = threadIdx.x;
     const int tx = tid % 16, ty = tid / 16;
-    const int row0 = blockIdx.y * BM, col0 = blockIdx.x * kBN;
+    // up to 16 row tiles of a column tile of P run on one XCD at the same
+    // time, so that XCD's L2 fetches the column tile once per group (all of a
+    // 1024-token batch is one group) and the XCDs work on different columns
+    int rt, ct;
+    const int R = (M + BM - 1) / BM;
+    xcd_tile(blockIdx.x, R, (K + kBN - 1) / kBN, R < 16 ? R : 16, rt, ct);
+    const int row0 = rt * BM, col0 = ct * kBN;
 
     // global -> register prefetch slots
     // A: BM rows x 16 k fp16 = BM*2 16-byte vectors; thread t takes vectors t, t+256, ..
@@ -177,12 +183,13 @@ hipError_t launch_transform(const uint16_t* X, const uint8_t* state, const float
         return hipGetLastError();
     }
     const int ncol = (K + kBN - 1) / kBN;
+    if ((size_t)((M + 63) / 64) * ncol > 0x7fffffffu) return hipErrorInvalidConfiguration;
     // enough workgroups to cover the 256 CUs at least twice, else the taller tile
     if ((size_t)ncol * ((M + 127) / 128) >= 512) {
-        hipLaunchKernelGGL(transform_kernel<8>, dim3(ncol, (M + 127) / 128), dim3(kThreads), 0, st, X, state, P,
+        hipLaunchKernelGGL(transform_kernel<8>, dim3(((M + 127) / 128) * ncol), dim3(kThreads), 0, st, X, state, P,
                            M, K, dm, du, Xp);
     } else {
-        hipLaunchKernelGGL(transform_kernel<4>, dim3(ncol, (M + 63) / 64), dim3(kThreads), 0, st, X, state, P,
+        hipLaunchKernelGGL(transform_kernel<4>, dim3(((M + 63) / 64) * ncol), dim3(kThreads), 0, st, X, state, P,
                            M, K, dm, du, Xp);
     }
     return hipGetLastError();

@@ -126,3 +126,12 @@ def test_w8_entry_points_validate(lib):
     assert lib.sq_gemm_w8_workspace_bytes(4096, 4096, 4096) == 0
     # operands of 2 GiB or more are refused (32-bit buffer offsets)
     assert lib.w4a4_gemm(FAKE, FAKE, FAKE, FAKE, 65536, 16, 65536, FAKE, None, FAKE, 1 << 40, None) == L.SQ_ERR_SHAPE
+
+
+def test_row_limit_of_tiled_launches(lib):
+    big = 65535 * 64 + 1
+    assert lib.w4a4_gemm(FAKE, FAKE, FAKE, FAKE, big, 16, 64, FAKE, None, FAKE, 1 << 40, None) == L.SQ_ERR_SHAPE
+    assert b"rows" in lib.sq_last_error()
+    assert lib.tac_apply(FAKE, FAKE, FAKE, big, 64, 16, FAKE + (1 << 40), None) == L.SQ_ERR_SHAPE
+    assert lib.sgat_quant_act(FAKE, FAKE, None, big, 64, 2, 2, FAKE, FAKE, 16, FAKE, FAKE, FAKE, 1 << 40, None) \
+        == L.SQ_ERR_SHAPE
