@@ -15,7 +15,13 @@ stored dtype):
   orthogonal but costs seconds instead of minutes on the host;
 * TAC parameters: M_b = I + N(0, 0.01) per g x g block and d ~ N(0, 0.01),
   both fp16 (Eq. 17); the identity case is M_b = I, d = 0;
-* token states, uint8 [M]: 0 = unmasked, 1 = masked, with the layouts below.
+* token states, uint8 [M]: 0 = unmasked, 1 = masked, with the layouts below;
+* TAC calibration pairs (App. C), fp16 [N][C] each: a "full-precision"
+  attention output with a per-block mean and a per-block correlated covariance
+  (z = mu_b + xi L_b^T, xi ~ N(0, I), L_b lower triangular with diagonal in
+  [0.5, 1.5] and N(0, 0.2) below it), and a "quantised" counterpart drawn as a
+  generic perturbation of it: a per-channel gain 1 + N(0, 0.05), additive
+  N(0, 0.1^2) noise and a per-channel offset N(0, 0.05).
 
 Nothing here transforms, quantises or multiplies the method's operands.
 """
@@ -35,6 +41,7 @@ T_X = 3
 T_W = 4
 T_P = 5
 T_TAC = 6
+T_CALIB = 7
 
 
 def rng_for(config_id: int, tensor_id: int, *extra: int) -> np.random.Generator:
@@ -154,6 +161,24 @@ def tac_params(C: int, g: int, rng, std: float = 0.01, identity: bool = False):
     Mb = (np.eye(g)[None] + rng.standard_normal((nb, g, g)) * std).astype(np.float16)
     d = (rng.standard_normal(C) * std).astype(np.float16)
     return Mb, d
+
+
+def tac_calib_pair(N: int, C: int, g: int, rng) -> Tuple[np.ndarray, np.ndarray]:
+    """Paired (full-precision, quantised) attention outputs for TAC calibration,
+    fp16 [N][C] each; blocks of g channels are correlated within, independent
+    across."""
+    B = C // g
+    mu = rng.normal(0.0, 0.5, size=(B, g))
+    L = np.tril(rng.normal(0.0, 0.2, size=(B, g, g)), -1)
+    idx = np.arange(g)
+    L[:, idx, idx] = rng.uniform(0.5, 1.5, size=(B, g))
+    xi = rng.standard_normal((N, B, g))
+    zf = mu[None] + np.einsum("nbk,brk->nbr", xi, L)
+    zf = zf.reshape(N, C)
+    gain = 1.0 + rng.normal(0.0, 0.05, size=C)
+    off = rng.normal(0.0, 0.05, size=C)
+    zq = zf * gain[None] + rng.normal(0.0, 0.1, size=(N, C)) + off[None]
+    return zf.astype(np.float16), zq.astype(np.float16)
 
 
 def default_band(K: int) -> Tuple[int, int]:
