@@ -188,6 +188,36 @@ int w8a8_gemm(const int8_t* Aq, const float* s_a, const int8_t* Wq, const float*
               int32_t M, int32_t N, int32_t K, uint16_t* Y, int32_t* acc,
               void* ws, size_t ws_bytes, void* stream);
 
+/*
+ * tac_calibrate -- the closed-form estimate of the TAC parameters (Sec. 3.3,
+ * closed-form estimation; App. C), from paired attention outputs collected at
+ * the TAC insertion point with the quantisers off (Z_fp) and on (Z_q).  Per
+ * block b of g channels, in fp64:
+ *   mu_b = (1/N) sum_i z_i, Sigma_b = (1/N) sum_i z_i z_i^T - mu_b mu_b^T (both inputs);
+ *   lambda_b = rho max(Tr(Sigma_q) / g, eps);
+ *   M_b = Sigma_fp^(1/2) (Sigma_q + lambda_b I)^(-1/2), each power through a
+ *         symmetric eigendecomposition with eigenvalues clamped below at 1e-12;
+ *   M_b = U diag(s) V^T -> U diag((1 - eta) s + eta mean(s)) V^T   (smoothing);
+ *   M_b -> (1 - alpha) M_b + alpha I                                 (shrinkage);
+ *   d_b = mu_fp - M_b mu_q.
+ * The appendix's defaults are rho = 3e-4, eps = 1e-8, eta = 0.15, alpha = 0.55.
+ *   Z_fp, Z_q [N][C] fp16, N >= 1 tokens; C as K (C % 64 == 0); g as for TAC.
+ *   tac_M out [C/g][g][g] fp16 (M_b[r][c]), tac_d out [C] fp16: each one
+ *         round-to-nearest-even from the fp64 value; the layout tac_apply and
+ *         sgat_quant_act read.
+ *   M64 out [C/g][g][g] fp64 and d64 out [C] fp64: the unrounded values, or NULL.
+ *   ws    device workspace of at least sq_tac_calibrate_workspace_bytes(N, C, g)
+ *         (required).
+ * Sums run in a fixed order, so results depend only on the inputs; they agree
+ * with any other fp64 evaluation to rounding, not bit for bit.  Offline: run
+ * once per layer after the activation transform is fixed.
+ */
+size_t sq_tac_calibrate_workspace_bytes(int32_t N, int32_t C, int32_t g);
+int tac_calibrate(const uint16_t* Z_fp, const uint16_t* Z_q, int32_t N, int32_t C, int32_t g,
+                  double rho, double eps, double eta, double alpha,
+                  uint16_t* tac_M, uint16_t* tac_d, double* M64, double* d64,
+                  void* ws, size_t ws_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

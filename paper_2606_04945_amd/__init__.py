@@ -21,7 +21,8 @@ from ._lib import SQ_OK, StarQuantError, check, lib  # noqa: F401
 __all__ = ["sgat_prepare_weights", "sgat_transform", "sgat_quantize", "sgat_quant_act", "w4a4_gemm", "tac_apply",
            "tac_default_block", "default_band", "quant_act_workspace_bytes", "gemm_workspace_bytes",
            "prepare_weights_workspace_bytes", "StarQuantError", "lib",
-           "sgat_prepare_weights_w8", "sgat_quantize_w8", "sgat_quant_act_w8", "w8a8_gemm"]
+           "sgat_prepare_weights_w8", "sgat_quantize_w8", "sgat_quant_act_w8", "w8a8_gemm",
+           "tac_calibrate", "tac_calibrate_workspace_bytes"]
 
 
 def _ptr(t: Optional[torch.Tensor]):
@@ -218,3 +219,34 @@ def tac_apply(Z: torch.Tensor, tac_M: torch.Tensor, tac_d: torch.Tensor, g: int,
     _need(out, "out", torch.float16, (M, C))
     check(lib().tac_apply(_ptr(Z), _ptr(tac_M), _ptr(tac_d), M, C, g, _ptr(out), _stream(stream)))
     return out
+
+
+TAC_RHO, TAC_EPS, TAC_ETA, TAC_ALPHA = 3e-4, 1e-8, 0.15, 0.55   # App. C defaults
+
+
+def tac_calibrate_workspace_bytes(N: int, C: int, g: int) -> int:
+    return int(lib().sq_tac_calibrate_workspace_bytes(N, C, g))
+
+
+def tac_calibrate(Z_fp: torch.Tensor, Z_q: torch.Tensor, g: int, *, rho: float = TAC_RHO, eps: float = TAC_EPS,
+                  eta: float = TAC_ETA, alpha: float = TAC_ALPHA, want_fp64: bool = False, tac_M=None, tac_d=None,
+                  ws=None, stream=None):
+    """Closed-form TAC parameters (App. C) from paired full-precision / quantised
+    attention outputs: (tac_M fp16 [C/g, g, g], tac_d fp16 [C]) and, with
+    want_fp64, also the unrounded fp64 (M, d)."""
+    N, C = Z_fp.shape
+    _need(Z_fp, "Z_fp", torch.float16)
+    _need(Z_q, "Z_q", torch.float16, (N, C))
+    dev = Z_fp.device
+    if tac_M is None:
+        tac_M = torch.empty((C // g, g, g), dtype=torch.float16, device=dev)
+    if tac_d is None:
+        tac_d = torch.empty((C,), dtype=torch.float16, device=dev)
+    _need(tac_M, "tac_M", torch.float16, (C // g, g, g))
+    _need(tac_d, "tac_d", torch.float16, (C,))
+    M64 = torch.empty((C // g, g, g), dtype=torch.float64, device=dev) if want_fp64 else None
+    d64 = torch.empty((C,), dtype=torch.float64, device=dev) if want_fp64 else None
+    ws, wsb = _ws(tac_calibrate_workspace_bytes(N, C, g), ws, dev)
+    check(lib().tac_calibrate(_ptr(Z_fp), _ptr(Z_q), N, C, g, rho, eps, eta, alpha, _ptr(tac_M), _ptr(tac_d),
+                              _ptr(M64), _ptr(d64), _ptr(ws), wsb, _stream(stream)))
+    return (tac_M, tac_d, M64, d64) if want_fp64 else (tac_M, tac_d)

@@ -30,6 +30,9 @@ SIGNATURES = {
     "sgat_quantize_w8": (ctypes.c_int, [_p, _i32, _i32, _p, _p, _p]),
     "sgat_quant_act_w8": (ctypes.c_int, [_p, _p, _p, _i32, _i32, _i32, _i32, _p, _p, _i32, _p, _p, _p, _sz, _p]),
     "w8a8_gemm": (ctypes.c_int, [_p, _p, _p, _p, _i32, _i32, _i32, _p, _p, _p, _sz, _p]),
+    "sq_tac_calibrate_workspace_bytes": (_sz, [_i32, _i32, _i32]),
+    "tac_calibrate": (ctypes.c_int, [_p, _p, _i32, _i32, _i32, ctypes.c_double, ctypes.c_double, ctypes.c_double,
+                                     ctypes.c_double, _p, _p, _p, _p, _p, _sz, _p]),
 }
 
 

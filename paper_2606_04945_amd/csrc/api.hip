@@ -272,4 +272,30 @@ int tac_apply(const uint16_t* Z, const uint16_t* tac_M, const uint16_t* tac_d, i
     return hip_status(sq::launch_tac(Z, tac_M, tac_d, M, C, g, Z_out, static_cast<hipStream_t>(stream)), "tac");
 }
 
+size_t sq_tac_calibrate_workspace_bytes(int32_t N, int32_t C, int32_t g) {
+    if (N <= 0 || C < 64 || C % 64 || g < 1 || g > 128 || (g & (g - 1)) || C % g) return 0;
+    return sq::tac_calib_workspace_bytes(N, C, g);
+}
+
+int tac_calibrate(const uint16_t* Z_fp, const uint16_t* Z_q, int32_t N, int32_t C, int32_t g, double rho,
+                  double eps, double eta, double alpha, uint16_t* tac_M, uint16_t* tac_d, double* M64,
+                  double* d64, void* ws, size_t ws_bytes, void* stream) {
+    SQ_TRY(check_K(C));
+    SQ_TRY(check_tac(C, g));
+    SQ_REQUIRE(N >= 1, SQ_ERR_SHAPE, "tac_calibrate: N=%d: need at least one token", N);
+    SQ_REQUIRE(rho >= 0.0 && eps >= 0.0 && eta >= 0.0 && eta <= 1.0 && alpha >= 0.0 && alpha <= 1.0 &&
+                   rho < 1e300 && eps < 1e300,
+               SQ_ERR_SHAPE, "tac_calibrate: need rho, eps >= 0 (finite) and eta, alpha in [0, 1]");
+    SQ_REQUIRE(Z_fp && Z_q && tac_M && tac_d && ws, SQ_ERR_NULL,
+               "tac_calibrate: Z_fp, Z_q, tac_M, tac_d and ws are required");
+    SQ_REQUIRE(aligned16(Z_fp) && aligned16(Z_q) && aligned16(tac_M) && aligned16(tac_d) && aligned16(M64) &&
+                   aligned16(d64) && aligned16(ws),
+               SQ_ERR_ALIGN, "tac_calibrate: pointers must be 16-byte aligned");
+    const size_t need = sq::tac_calib_workspace_bytes(N, C, g);
+    SQ_REQUIRE(ws_bytes >= need, SQ_ERR_WORKSPACE, "tac_calibrate: workspace %zu B < %zu B", ws_bytes, need);
+    return hip_status(sq::launch_tac_calib(Z_fp, Z_q, N, C, g, rho, eps, eta, alpha, tac_M, tac_d, M64, d64, ws,
+                                           static_cast<hipStream_t>(stream)),
+                      "tac_calibrate");
+}
+
 }  // extern "C"

@@ -94,4 +94,10 @@ size_t gemm_workspace_bytes(int M, int N, int K, int bits);
 hipError_t launch_gemm(const uint8_t* Aq, const float* s_a, const uint8_t* Wq, const float* s_w,
                        int M, int N, int K, uint16_t* Y, int32_t* acc, void* ws, hipStream_t st, int bits);
 
+// TAC closed-form calibration (tac_calib.hip)
+size_t tac_calib_workspace_bytes(int N, int C, int g);
+hipError_t launch_tac_calib(const uint16_t* Zf, const uint16_t* Zq, int N, int C, int g, double rho, double eps,
+                            double eta, double alpha, uint16_t* tac_M, uint16_t* tac_d, double* M64, double* d64,
+                            void* ws, hipStream_t st);
+
 }  // namespace sq

@@ -1,0 +1,462 @@
+// TAC closed-form calibration (Sec. 3.3 closed-form estimation; App. C).
+//
+// From paired attention outputs Z_fp (quantisers off) and Z_q (quantisers on),
+// fp16 [N][C], per block of g channels:
+//   mu_b    = (1/N) sum_i z_i,   Sigma_b = (1/N) sum_i z_i z_i^T - mu_b mu_b^T   (both passes)
+//   lambda  = rho max(Tr(Sigma_q) / g, eps)
+//   M       = Sigma_fp^(1/2) (Sigma_q + lambda I)^(-1/2),  A^p = Q diag(max(l_i, 1e-12)^p) Q^T
+//   M_sv    = U diag((1 - eta) sigma + eta mean(sigma)) V^T,  M = U diag(sigma) V^T
+//   M_final = (1 - alpha) M_sv + alpha I,   d = mu_fp - M_final mu_q
+// stored as fp16 (one round-to-nearest-even from fp64) in the layout the TAC
+// kernels read, tac_M [C/g][g][g] (row r, column c) and tac_d [C].
+//
+// Two kernels, all arithmetic in fp64:
+//  * tac_stats_kernel: the data-parallel part.  A workgroup takes a span of
+//    channels (whole blocks, at least 64 channels so rows are read in 128-byte
+//    runs) and a chunk of tokens, stages 32 tokens at a time in LDS as fp64,
+//    and accumulates every (r, c) product of its blocks and every channel sum
+//    in registers, in token order.  Partial sums per chunk go to the
+//    workspace.
+//  * tac_finalize_kernel: one workgroup per block.  Adds the chunk partials in
+//    chunk order, forms the statistics, and runs the closed form: symmetric
+//    eigendecompositions by cyclic Jacobi with the round-robin (parallel)
+//    ordering, and the singular value decomposition of M by one-sided
+//    (Hestenes) Jacobi, whose singular values keep full relative accuracy.
+//    Matrices live in the workspace (g x g fp64, up to 128 KB each), so the
+//    workgroup's L2 holds them.
+// Results depend only on the inputs (every sum has a fixed order); they agree
+// with an fp64 LAPACK evaluation to rounding, not bit for bit.
+#include "sq_internal.hpp"
+
+namespace sq {
+namespace {
+
+constexpr int kCalThreads = 256;
+constexpr int kTileTok = 32;            // tokens staged per LDS tile
+constexpr int kMaxChunks = 16;
+constexpr int kChunkTok = 4096;         // tokens per chunk before the cap
+constexpr double kEigFloor = 1e-12;
+
+// ----------------------------------------------------------------- statistics
+
+// part layout: [pass][chunk][block][g*g second moments, then g sums]
+template <int G>
+__global__ __launch_bounds__(kCalThreads) void tac_stats_kernel(const uint16_t* __restrict__ Zf,
+                                                               const uint16_t* __restrict__ Zq, int N, int C,
+                                                               int tok_per_chunk, int chunks,
+                                                               double* __restrict__ part) {
+    constexpr int S = G > 64 ? G : 64;                   // channels per workgroup
+    constexpr int NB = S / G;                            // blocks per workgroup
+    constexpr int P = S * G;                             // (block, r, c) products
+    constexpr int PPT = (P + kCalThreads - 1) / kCalThreads;
+    constexpr int VPT = kTileTok * S / 8 / kCalThreads;  // 16-byte loads per thread per tile
+    static_assert(VPT >= 1 && VPT * 8 * kCalThreads == kTileTok * S, "tile split");
+    __shared__ double tile[kTileTok][S + 1];
+
+    const int tid = threadIdx.x;
+    const int c0 = blockIdx.x * S;
+    const int chunk = blockIdx.y;
+    const int pass = blockIdx.z;
+    const uint16_t* Z = pass == 0 ? Zf : Zq;
+    const int t0 = chunk * tok_per_chunk;
+    const int t1 = min(N, t0 + tok_per_chunk);
+
+    double acc[PPT];
+    int pr[PPT], pc[PPT];
+#pragma unroll
+    for (int k = 0; k < PPT; ++k) {
+        acc[k] = 0.0;
+        const int p = tid + k * kCalThreads;
+        const int bs = p / (G * G), rc = p % (G * G);
+        pr[k] = p < P ? bs * G + rc / G : 0;              // span-local channel of row r
+        pc[k] = p < P ? bs * G + rc % G : 0;              // and of column c
+    }
+    double sum = 0.0;                                     // channel tid's sum (tid < S)
+
+    for (int tb = t0; tb < t1; tb += kTileTok) {
+#pragma unroll
+        for (int v = 0; v < VPT; ++v) {
+            const int e = (tid + v * kCalThreads) * 8;    // element index in the tile
+            const int tt = e / S, ch = e % S;
+            const int t = tb + tt;
+            uint4 raw = make_uint4(0, 0, 0, 0);           // tokens past t1 contribute zeros
+            if (t < t1) raw = *reinterpret_cast<const uint4*>(Z + (size_t)t * C + c0 + ch);
+            const uint16_t* h = reinterpret_cast<const uint16_t*>(&raw);
+#pragma unroll
+            for (int q = 0; q < 8; ++q) tile[tt][ch + q] = (double)h2f(h[q]);
+        }
+        __syncthreads();
+        const int nt = min(kTileTok, t1 - tb);
+        for (int tt = 0; tt < nt; ++tt) {
+#pragma unroll
+            for (int k = 0; k < PPT; ++k) acc[k] = fma(tile[tt][pr[k]], tile[tt][pc[k]], acc[k]);
+            if (tid < S) sum += tile[tt][tid];
+        }
+        __syncthreads();
+    }
+    const int B = C / G;
+    const size_t stride = (size_t)G * G + G;
+    double* base = part + ((size_t)pass * chunks + chunk) * B * stride;
+#pragma unroll
+    for (int k = 0; k < PPT; ++k) {
+        const int p = tid + k * kCalThreads;
+        if (p < P) {
+            const int bs = p / (G * G), rc = p % (G * G);
+            base[(size_t)(blockIdx.x * NB + bs) * stride + rc] = acc[k];
+        }
+    }
+    if (tid < S) base[(size_t)(blockIdx.x * NB + tid / G) * stride + G * G + tid % G] = sum;
+}
+
+// ----------------------------------------------------------------- closed form
+
+// One RNE rounding of an fp64 value to fp16 bits (overflow to infinity).
+__device__ uint16_t f64_to_f16(double x) {
+    const uint64_t b = (uint64_t)__double_as_longlong(x);
+    const uint16_t sign = (uint16_t)((b >> 48) & 0x8000u);
+    const int e = (int)((b >> 52) & 0x7FF);
+    const uint64_t frac = b & 0xFFFFFFFFFFFFFull;
+    if (e == 0x7FF) return sign | 0x7C00u | (frac ? 0x200u : 0u);
+    if (e == 0) return sign;                              // zero or an fp64 subnormal
+    const uint64_t mant = frac | (1ull << 52);            // value = mant * 2^(E - 52)
+    int E = e - 1023;
+    int shift;                                            // bits dropped from mant
+    if (E >= -14) {
+        shift = 42;                                       // keep 11 bits (implicit one + 10)
+    } else {
+        shift = 28 - E;                                   // subnormal: units of 2^-24
+        if (shift > 60) return sign;                      // below half the smallest subnormal
+    }
+    uint64_t q = mant >> shift;
+    const uint64_t rem = mant & ((1ull << shift) - 1);
+    const uint64_t half = 1ull << (shift - 1);
+    if (rem > half || (rem == half && (q & 1))) ++q;
+    if (E >= -14) {
+        if (q == (1ull << 11)) {                          // mantissa carried into the exponent
+            q >>= 1;
+            ++E;
+        }
+        if (E > 15) return sign | 0x7C00u;
+        return sign | (uint16_t)((E + 15) << 10) | (uint16_t)(q & 0x3FFu);
+    }
+    return sign | (uint16_t)q;                            // q == 1024 is the smallest normal
+}
+
+__device__ int rr_player(int i, int r, int n) { return i == 0 ? 0 : 1 + (i - 1 + r) % (n - 1); }
+
+// Round-robin pair t of round r over n = g players (g even), p < q.
+__device__ void rr_pair(int t, int r, int n, int& p, int& q) {
+    const int a = rr_player(t, r, n), b = rr_player(n - 1 - t, r, n);
+    p = a < b ? a : b;
+    q = a < b ? b : a;
+}
+
+// Sum over the workgroup (fixed tree order).
+__device__ double wg_sum(double v, double* red) {
+    const int tid = threadIdx.x;
+    red[tid] = v;
+    __syncthreads();
+    for (int s = kCalThreads / 2; s > 0; s >>= 1) {
+        if (tid < s) red[tid] += red[tid + s];
+        __syncthreads();
+    }
+    const double r = red[0];
+    __syncthreads();
+    return r;
+}
+
+// Symmetric eigendecomposition of A (overwritten; eigenvalues end on its
+// diagonal), eigenvectors into the columns of V: cyclic Jacobi, round-robin.
+__device__ void jacobi_eigh(double* A, double* V, int g, double* cs, double* red) {
+    const int tid = threadIdx.x;
+    for (int e = tid; e < g * g; e += kCalThreads) V[e] = (e / g == e % g) ? 1.0 : 0.0;
+    __syncthreads();
+    if (g == 1) return;
+    const int h = g / 2;
+    for (int sweep = 0; sweep < 60; ++sweep) {
+        double off = 0.0, tot = 0.0;
+        for (int e = tid; e < g * g; e += kCalThreads) {
+            const double a2 = A[e] * A[e];
+            tot += a2;
+            if (e / g != e % g) off += a2;
+        }
+        off = wg_sum(off, red);
+        tot = wg_sum(tot, red);
+        if (!(off > 1e-30 * tot)) break;                  // also stops on a zero matrix
+        for (int r = 0; r < g - 1; ++r) {
+            if (tid < h) {
+                int p, q;
+                rr_pair(tid, r, g, p, q);
+                const double apq = A[p * g + q];
+                double c = 1.0, s = 0.0;
+                if (apq != 0.0) {
+                    const double tau = (A[q * g + q] - A[p * g + p]) / (2.0 * apq);
+                    // for |tau| beyond 1e150, tau^2 would overflow; t = 1 / (2 tau) there
+                    const double t = fabs(tau) > 1e150 ? 0.5 / tau
+                                                       : (tau >= 0.0 ? 1.0 : -1.0) / (fabs(tau) + sqrt(1.0 + tau * tau));
+                    c = 1.0 / sqrt(1.0 + t * t);
+                    s = t * c;
+                }
+                cs[2 * tid] = c;
+                cs[2 * tid + 1] = s;
+            }
+            __syncthreads();
+            for (int e = tid; e < g * h; e += kCalThreads) {      // columns: A J and V J
+                const int i = e / h, t = e % h;
+                int p, q;
+                rr_pair(t, r, g, p, q);
+                const double c = cs[2 * t], s = cs[2 * t + 1];
+                const double ap = A[i * g + p], aq = A[i * g + q];
+                A[i * g + p] = c * ap - s * aq;
+                A[i * g + q] = s * ap + c * aq;
+                const double vp = V[i * g + p], vq = V[i * g + q];
+                V[i * g + p] = c * vp - s * vq;
+                V[i * g + q] = s * vp + c * vq;
+            }
+            __syncthreads();
+            for (int e = tid; e < g * h; e += kCalThreads) {      // rows: J^T (A J)
+                const int j = e / h, t = e % h;
+                int p, q;
+                rr_pair(t, r, g, p, q);
+                const double c = cs[2 * t], s = cs[2 * t + 1];
+                const double ap = A[p * g + j], aq = A[q * g + j];
+                A[p * g + j] = c * ap - s * aq;
+                A[q * g + j] = s * ap + c * aq;
+            }
+            __syncthreads();
+        }
+    }
+}
+
+// R = V diag(max(l_i, 1e-12)^p) V^T for p = +1/2 or -1/2; l_i on the diagonal of D.
+__device__ void eig_power(const double* D, const double* V, double* R, int g, bool inverse, double* w) {
+    const int tid = threadIdx.x;
+    for (int k = tid; k < g; k += kCalThreads) {
+        const double l = fmax(D[k * g + k], kEigFloor);
+        w[k] = inverse ? 1.0 / sqrt(l) : sqrt(l);
+    }
+    __syncthreads();
+    for (int e = tid; e < g * g; e += kCalThreads) {
+        const int r = e / g, c = e % g;
+        double s = 0.0;
+        for (int k = 0; k < g; ++k) s = fma(V[r * g + k] * w[k], V[c * g + k], s);
+        R[e] = s;
+    }
+    __syncthreads();
+}
+
+// Singular value decomposition of G (g x g) by one-sided Jacobi: on return the
+// columns of G are u_j sigma_j and V holds the right singular vectors.
+__device__ void jacobi_svd(double* G, double* V, int g, double* cs, int* flag) {
+    const int tid = threadIdx.x;
+    for (int e = tid; e < g * g; e += kCalThreads) V[e] = (e / g == e % g) ? 1.0 : 0.0;
+    __syncthreads();
+    if (g == 1) return;
+    const int h = g / 2;
+    for (int sweep = 0; sweep < 60; ++sweep) {
+        if (tid == 0) *flag = 0;
+        __syncthreads();
+        for (int r = 0; r < g - 1; ++r) {
+            if (tid < h) {
+                int p, q;
+                rr_pair(tid, r, g, p, q);
+                double al = 0.0, be = 0.0, ga = 0.0;
+                for (int i = 0; i < g; ++i) {
+                    const double x = G[i * g + p], y = G[i * g + q];
+                    al = fma(x, x, al);
+                    be = fma(y, y, be);
+                    ga = fma(x, y, ga);
+                }
+                double c = 1.0, s = 0.0;
+                if (ga != 0.0 && fabs(ga) > 1e-15 * sqrt(al * be)) {
+                    const double zeta = (be - al) / (2.0 * ga);
+                    const double t = fabs(zeta) > 1e150
+                                         ? 0.5 / zeta
+                                         : (zeta >= 0.0 ? 1.0 : -1.0) / (fabs(zeta) + sqrt(1.0 + zeta * zeta));
+                    c = 1.0 / sqrt(1.0 + t * t);
+                    s = t * c;
+                    *flag = 1;
+                }
+                cs[2 * tid] = c;
+                cs[2 * tid + 1] = s;
+            }
+            __syncthreads();
+            for (int e = tid; e < g * h; e += kCalThreads) {
+                const int i = e / h, t = e % h;
+                int p, q;
+                rr_pair(t, r, g, p, q);
+                const double c = cs[2 * t], s = cs[2 * t + 1];
+                const double gp = G[i * g + p], gq = G[i * g + q];
+                G[i * g + p] = c * gp - s * gq;
+                G[i * g + q] = s * gp + c * gq;
+                const double vp = V[i * g + p], vq = V[i * g + q];
+                V[i * g + p] = c * vp - s * vq;
+                V[i * g + q] = s * vp + c * vq;
+            }
+            __syncthreads();
+        }
+        if (*flag == 0) break;
+        __syncthreads();
+    }
+}
+
+__global__ __launch_bounds__(kCalThreads) void tac_finalize_kernel(const double* __restrict__ part, int chunks,
+                                                                  int N, int C, int g, double rho, double eps,
+                                                                  double eta, double alpha, double* __restrict__ wk,
+                                                                  uint16_t* __restrict__ tac_M,
+                                                                  uint16_t* __restrict__ tac_d,
+                                                                  double* __restrict__ M64, double* __restrict__ d64) {
+    __shared__ double red[kCalThreads];
+    __shared__ double cs[128];
+    __shared__ double w[128];
+    __shared__ int flag;
+    const int tid = threadIdx.x;
+    const int b = blockIdx.x;
+    const int B = C / g;
+    const size_t gg = (size_t)g * g;
+    double* base = wk + (size_t)b * (6 * gg + 3 * g);
+    double* Sf = base;                 // Sigma_fp, then its eigenvalues
+    double* Sq = base + gg;            // Sigma_q + lambda I, then its eigenvalues
+    double* V = base + 2 * gg;         // eigenvectors / right singular vectors
+    double* R1 = base + 3 * gg;        // Sigma_fp^(1/2), later M_sv
+    double* R2 = base + 4 * gg;        // (Sigma_q + lambda I)^(-1/2)
+    double* G = base + 5 * gg;         // M, then U diag(sigma)
+    double* mu_f = base + 6 * gg;
+    double* mu_q = mu_f + g;
+    double* sig = mu_q + g;
+    const size_t stride = gg + g;
+
+    // statistics: chunk partials added in chunk order
+    for (int e = tid; e < (int)stride; e += kCalThreads) {
+        double sf = 0.0, sq = 0.0;
+        for (int k = 0; k < chunks; ++k) {
+            sf += part[((size_t)k * B + b) * stride + e];
+            sq += part[((size_t)(chunks + k) * B + b) * stride + e];
+        }
+        if (e < (int)gg) {
+            Sf[e] = sf / (double)N;
+            Sq[e] = sq / (double)N;
+        } else {
+            mu_f[e - gg] = sf / (double)N;
+            mu_q[e - gg] = sq / (double)N;
+        }
+    }
+    __syncthreads();
+    for (int e = tid; e < (int)gg; e += kCalThreads) {
+        const int r = e / g, c = e % g;
+        Sf[e] = Sf[e] - mu_f[r] * mu_f[c];
+        Sq[e] = Sq[e] - mu_q[r] * mu_q[c];
+    }
+    __syncthreads();
+    // damping
+    double tr = 0.0;
+    for (int k = tid; k < g; k += kCalThreads) tr += Sq[k * g + k];
+    tr = wg_sum(tr, red);
+    const double lam = rho * fmax(tr / g, eps);
+    for (int k = tid; k < g; k += kCalThreads) Sq[k * g + k] += lam;
+    __syncthreads();
+    // covariance matching
+    jacobi_eigh(Sf, V, g, cs, red);
+    eig_power(Sf, V, R1, g, false, w);
+    jacobi_eigh(Sq, V, g, cs, red);
+    eig_power(Sq, V, R2, g, true, w);
+    for (int e = tid; e < (int)gg; e += kCalThreads) {
+        const int r = e / g, c = e % g;
+        double s = 0.0;
+        for (int k = 0; k < g; ++k) s = fma(R1[r * g + k], R2[k * g + c], s);
+        G[e] = s;
+    }
+    __syncthreads();
+    // singular value smoothing
+    jacobi_svd(G, V, g, cs, &flag);
+    for (int j = tid; j < g; j += kCalThreads) {
+        double s = 0.0;
+        for (int i = 0; i < g; ++i) s = fma(G[i * g + j], G[i * g + j], s);
+        sig[j] = sqrt(s);
+    }
+    __syncthreads();
+    double ssum = 0.0;
+    for (int j = tid; j < g; j += kCalThreads) ssum += sig[j];
+    const double sbar = wg_sum(ssum, red) / g;
+    for (int j = tid; j < g; j += kCalThreads) {      // factor sigma'_j / sigma_j on column j of U Sigma
+        const double s = sig[j];
+        w[j] = s > 0.0 ? ((1.0 - eta) * s + eta * sbar) / s : 0.0;
+    }
+    __syncthreads();
+    for (int e = tid; e < (int)gg; e += kCalThreads) {
+        const int r = e / g, c = e % g;
+        double s = 0.0;
+        for (int k = 0; k < g; ++k) s = fma(G[r * g + k] * w[k], V[c * g + k], s);
+        // identity shrinkage
+        R1[e] = (1.0 - alpha) * s + (r == c ? alpha : 0.0);
+    }
+    __syncthreads();
+    // bias, outputs
+    for (int r = tid; r < g; r += kCalThreads) {
+        double s = 0.0;
+        for (int c = 0; c < g; ++c) s = fma(R1[r * g + c], mu_q[c], s);
+        const double d = mu_f[r] - s;
+        tac_d[b * g + r] = f64_to_f16(d);
+        if (d64) d64[b * g + r] = d;
+    }
+    for (int e = tid; e < (int)gg; e += kCalThreads) {
+        tac_M[(size_t)b * gg + e] = f64_to_f16(R1[e]);
+        if (M64) M64[(size_t)b * gg + e] = R1[e];
+    }
+}
+
+template <int G>
+hipError_t launch_stats(const uint16_t* Zf, const uint16_t* Zq, int N, int C, int per, int chunks, double* part,
+                        hipStream_t st) {
+    constexpr int S = G > 64 ? G : 64;
+    dim3 grid(C / S, chunks, 2);
+    hipLaunchKernelGGL(tac_stats_kernel<G>, grid, dim3(kCalThreads), 0, st, Zf, Zq, N, C, per, chunks, part);
+    return hipGetLastError();
+}
+
+void calib_plan(int N, int& chunks, int& per) {
+    chunks = (N + kChunkTok - 1) / kChunkTok;
+    chunks = chunks < 1 ? 1 : (chunks > kMaxChunks ? kMaxChunks : chunks);
+    per = (N + chunks - 1) / chunks;
+    chunks = (N + per - 1) / per;
+}
+
+}  // namespace
+
+size_t tac_calib_workspace_bytes(int N, int C, int g) {
+    if (N <= 0 || C <= 0 || g <= 0) return 0;
+    int chunks, per;
+    calib_plan(N, chunks, per);
+    const size_t B = (size_t)C / g, gg = (size_t)g * g;
+    const size_t part = 2 * (size_t)chunks * B * (gg + g) * sizeof(double);
+    const size_t work = B * (6 * gg + 3 * g) * sizeof(double);
+    return ((part + 255) / 256) * 256 + work;
+}
+
+hipError_t launch_tac_calib(const uint16_t* Zf, const uint16_t* Zq, int N, int C, int g, double rho, double eps,
+                            double eta, double alpha, uint16_t* tac_M, uint16_t* tac_d, double* M64, double* d64,
+                            void* ws, hipStream_t st) {
+    int chunks, per;
+    calib_plan(N, chunks, per);
+    const size_t B = (size_t)C / g, gg = (size_t)g * g;
+    double* part = static_cast<double*>(ws);
+    const size_t part_bytes = 2 * (size_t)chunks * B * (gg + g) * sizeof(double);
+    double* wk = reinterpret_cast<double*>(static_cast<uint8_t*>(ws) + ((part_bytes + 255) / 256) * 256);
+    hipError_t e;
+    switch (g) {
+        case 1: e = launch_stats<1>(Zf, Zq, N, C, per, chunks, part, st); break;
+        case 2: e = launch_stats<2>(Zf, Zq, N, C, per, chunks, part, st); break;
+        case 4: e = launch_stats<4>(Zf, Zq, N, C, per, chunks, part, st); break;
+        case 8: e = launch_stats<8>(Zf, Zq, N, C, per, chunks, part, st); break;
+        case 16: e = launch_stats<16>(Zf, Zq, N, C, per, chunks, part, st); break;
+        case 32: e = launch_stats<32>(Zf, Zq, N, C, per, chunks, part, st); break;
+        case 64: e = launch_stats<64>(Zf, Zq, N, C, per, chunks, part, st); break;
+        default: e = launch_stats<128>(Zf, Zq, N, C, per, chunks, part, st); break;
+    }
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(tac_finalize_kernel, dim3((unsigned)B), dim3(kCalThreads), 0, st, part, chunks, N, C, g, rho,
+                       eps, eta, alpha, wk, tac_M, tac_d, M64, d64);
+    return hipGetLastError();
+}
+
+}  // namespace sq

@@ -19,7 +19,8 @@ stored dtype):
 * TAC calibration pairs (App. C), fp16 [N][C] each: a "full-precision"
   attention output with a per-block mean and a per-block correlated covariance
   (z = mu_b + xi L_b^T, xi ~ N(0, I), L_b lower triangular with diagonal in
-  [0.5, 1.5] and N(0, 0.2) below it), and a "quantised" counterpart drawn as a
+  [0.5, 1.5] and N(0, 0.5^2 / g) below it, which keeps the covariance well
+  conditioned at every g), and a "quantised" counterpart drawn as a
   generic perturbation of it: a per-channel gain 1 + N(0, 0.05), additive
   N(0, 0.1^2) noise and a per-channel offset N(0, 0.05).
 
@@ -169,7 +170,7 @@ def tac_calib_pair(N: int, C: int, g: int, rng) -> Tuple[np.ndarray, np.ndarray]
     across."""
     B = C // g
     mu = rng.normal(0.0, 0.5, size=(B, g))
-    L = np.tril(rng.normal(0.0, 0.2, size=(B, g, g)), -1)
+    L = np.tril(rng.normal(0.0, 0.5 / np.sqrt(g), size=(B, g, g)), -1)
     idx = np.arange(g)
     L[:, idx, idx] = rng.uniform(0.5, 1.5, size=(B, g))
     xi = rng.standard_normal((N, B, g))

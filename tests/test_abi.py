@@ -135,3 +135,24 @@ def test_row_limit_of_tiled_launches(lib):
     assert lib.tac_apply(FAKE, FAKE, FAKE, big, 64, 16, FAKE + (1 << 40), None) == L.SQ_ERR_SHAPE
     assert lib.sgat_quant_act(FAKE, FAKE, None, big, 64, 2, 2, FAKE, FAKE, 16, FAKE, FAKE, FAKE, 1 << 40, None) \
         == L.SQ_ERR_SHAPE
+
+
+def test_tac_calibrate_validates(lib):
+    assert lib.sq_tac_calibrate_workspace_bytes(1000, 4096, 16) > 0
+    assert lib.sq_tac_calibrate_workspace_bytes(0, 4096, 16) == 0
+    ok = (3e-4, 1e-8, 0.15, 0.55)
+    big = 1 << 40
+    assert lib.tac_calibrate(FAKE, FAKE, 0, 64, 16, *ok, FAKE, FAKE, None, None, FAKE, big, None) == L.SQ_ERR_SHAPE
+    assert lib.tac_calibrate(FAKE, FAKE, 8, 64, 3, *ok, FAKE, FAKE, None, None, FAKE, big, None) == L.SQ_ERR_SHAPE
+    assert lib.tac_calibrate(FAKE, FAKE, 8, 100, 4, *ok, FAKE, FAKE, None, None, FAKE, big, None) == L.SQ_ERR_SHAPE
+    assert lib.tac_calibrate(FAKE, FAKE, 8, 64, 16, 3e-4, 1e-8, 1.5, 0.55, FAKE, FAKE, None, None, FAKE, big, None) \
+        == L.SQ_ERR_SHAPE
+    assert lib.tac_calibrate(FAKE, FAKE, 8, 64, 16, -1.0, 1e-8, 0.1, 0.5, FAKE, FAKE, None, None, FAKE, big, None) \
+        == L.SQ_ERR_SHAPE
+    assert lib.tac_calibrate(FAKE, None, 8, 64, 16, *ok, FAKE, FAKE, None, None, FAKE, big, None) == L.SQ_ERR_NULL
+    assert lib.tac_calibrate(FAKE, FAKE, 8, 64, 16, *ok, FAKE, FAKE, None, None, None, big, None) == L.SQ_ERR_NULL
+    assert lib.tac_calibrate(FAKE, FAKE, 8, 64, 16, *ok, FAKE + 8, FAKE, None, None, FAKE, big, None) \
+        == L.SQ_ERR_ALIGN
+    need = lib.sq_tac_calibrate_workspace_bytes(8, 64, 16)
+    assert lib.tac_calibrate(FAKE, FAKE, 8, 64, 16, *ok, FAKE, FAKE, None, None, FAKE, need - 1, None) \
+        == L.SQ_ERR_WORKSPACE
