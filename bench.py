@@ -67,6 +67,7 @@ def parse():
                     help="skip the 16384-token Dream-shaped layer set (large-token GEMM figures)")
     ap.add_argument("--no-small", action="store_true",
                     help="skip the 16/32/64-token denoising-step layer sets (small-token HBM figures)")
+    ap.add_argument("--no-calib", action="store_true", help="skip the TAC calibration timing")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain 1 GiB device copy (reference for HBM byte counters)")
     return ap.parse_args()
@@ -283,6 +284,35 @@ def small_token_block(torch, sq, synth, dev, token_counts=(16, 32, 64), copies=4
     return res
 
 
+def tac_calibration_block(torch, sq, synth, dev, N=8192, C=4096, reps=5):
+    """TAC closed-form calibration (App. C, offline) on 8192 paired tokens of width
+    4096, at the default block size 16 and at 128: call time and the rate at which
+    it consumes the two fp16 inputs (the statistics pass reads each once)."""
+    out = {}
+    for g in (16, 128):
+        zf, zq = synth.tac_calib_pair(N, C, g, synth.rng_for(3, synth.T_CALIB, N, C, g))
+        Zf, Zq = torch.from_numpy(zf).to(dev), torch.from_numpy(zq).to(dev)
+        ws = torch.empty(sq.tac_calibrate_workspace_bytes(N, C, g), dtype=torch.uint8, device=dev)
+        tM = torch.empty((C // g, g, g), dtype=torch.float16, device=dev)
+        td = torch.empty((C,), dtype=torch.float16, device=dev)
+        sq.tac_calibrate(Zf, Zq, g, tac_M=tM, tac_d=td, ws=ws)
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            sq.tac_calibrate(Zf, Zq, g, tac_M=tM, tac_d=td, ws=ws)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        byts = 2 * N * C * 2
+        out[f"g{g}"] = {"ms_per_call": ms, "input_gbs": byts / ms / 1e6,
+                        "stats_fp64_gflop": 4.0 * N * C * g / 1e9}
+        del Zf, Zq, ws
+    return {"workload": f"TAC calibration, {N} paired tokens x {C} channels, fp64 statistics and closed form",
+            "per_block_size": out}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -425,6 +455,8 @@ def main():
         out["large"] = large_token_block(torch, sq, synth, dev, max(3, args.steps // 4), 1)
     if not args.no_small:
         out["small"] = small_token_block(torch, sq, synth, dev)
+    if not args.no_calib:
+        out["calib"] = tac_calibration_block(torch, sq, synth, dev)
 
     # ---------------------------------------------------------------- CPU baseline
     cpu = None
@@ -496,6 +528,8 @@ def main():
         res["large_token"] = out["large"]
     if "small" in out:
         res["small_token"] = out["small"]
+    if "calib" in out:
+        res["tac_calibration"] = out["calib"]
     if cpu:
         res["cpu_baseline"] = cpu
     print(json.dumps(res), flush=True)

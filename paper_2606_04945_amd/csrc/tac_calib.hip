@@ -22,8 +22,8 @@
 //    eigendecompositions by cyclic Jacobi with the round-robin (parallel)
 //    ordering, and the singular value decomposition of M by one-sided
 //    (Hestenes) Jacobi, whose singular values keep full relative accuracy.
-//    Matrices live in the workspace (g x g fp64, up to 128 KB each), so the
-//    workgroup's L2 holds them.
+//    Matrices live in the workspace (g x g fp64, up to 128 KB each); the two
+//    a Jacobi iteration updates every round are staged in LDS for g <= 64.
 // Results depend only on the inputs (every sum has a fixed order); they agree
 // with an fp64 LAPACK evaluation to rounding, not bit for bit.
 #include "sq_internal.hpp"
@@ -33,9 +33,10 @@ namespace {
 
 constexpr int kCalThreads = 256;
 constexpr int kTileTok = 32;            // tokens staged per LDS tile
-constexpr int kMaxChunks = 16;
-constexpr int kChunkTok = 4096;         // tokens per chunk before the cap
+constexpr int kMaxChunks = 64;
+constexpr int kChunkTok = 128;          // tokens per chunk before the caps
 constexpr double kEigFloor = 1e-12;
+constexpr int kLdsBlock = 64;          // largest g whose Jacobi matrices stay in LDS
 
 // ----------------------------------------------------------------- statistics
 
@@ -310,10 +311,25 @@ __global__ __launch_bounds__(kCalThreads) void tac_finalize_kernel(const double*
     __shared__ double cs[128];
     __shared__ double w[128];
     __shared__ int flag;
+    extern __shared__ double lds_mats[];               // 2 g^2 doubles when g <= 64
     const int tid = threadIdx.x;
     const int b = blockIdx.x;
     const int B = C / g;
     const size_t gg = (size_t)g * g;
+    // the Jacobi iterations touch their two matrices every round: in LDS when
+    // they fit, else in the workspace
+    const bool local = g <= kLdsBlock;
+    auto stage_in = [&](const double* src) {
+        for (int e = tid; e < (int)gg; e += kCalThreads) lds_mats[e] = src[e];
+        __syncthreads();
+    };
+    auto stage_out = [&](double* a, double* v) {
+        for (int e = tid; e < (int)gg; e += kCalThreads) {
+            a[e] = lds_mats[e];
+            v[e] = lds_mats[gg + e];
+        }
+        __syncthreads();
+    };
     double* base = wk + (size_t)b * (6 * gg + 3 * g);
     double* Sf = base;                 // Sigma_fp, then its eigenvalues
     double* Sq = base + gg;            // Sigma_q + lambda I, then its eigenvalues
@@ -356,9 +372,21 @@ __global__ __launch_bounds__(kCalThreads) void tac_finalize_kernel(const double*
     for (int k = tid; k < g; k += kCalThreads) Sq[k * g + k] += lam;
     __syncthreads();
     // covariance matching
-    jacobi_eigh(Sf, V, g, cs, red);
+    if (local) {
+        stage_in(Sf);
+        jacobi_eigh(lds_mats, lds_mats + gg, g, cs, red);
+        stage_out(Sf, V);
+    } else {
+        jacobi_eigh(Sf, V, g, cs, red);
+    }
     eig_power(Sf, V, R1, g, false, w);
-    jacobi_eigh(Sq, V, g, cs, red);
+    if (local) {
+        stage_in(Sq);
+        jacobi_eigh(lds_mats, lds_mats + gg, g, cs, red);
+        stage_out(Sq, V);
+    } else {
+        jacobi_eigh(Sq, V, g, cs, red);
+    }
     eig_power(Sq, V, R2, g, true, w);
     for (int e = tid; e < (int)gg; e += kCalThreads) {
         const int r = e / g, c = e % g;
@@ -368,7 +396,13 @@ __global__ __launch_bounds__(kCalThreads) void tac_finalize_kernel(const double*
     }
     __syncthreads();
     // singular value smoothing
-    jacobi_svd(G, V, g, cs, &flag);
+    if (local) {
+        stage_in(G);
+        jacobi_svd(lds_mats, lds_mats + gg, g, cs, &flag);
+        stage_out(G, V);
+    } else {
+        jacobi_svd(G, V, g, cs, &flag);
+    }
     for (int j = tid; j < g; j += kCalThreads) {
         double s = 0.0;
         for (int i = 0; i < g; ++i) s = fma(G[i * g + j], G[i * g + j], s);
@@ -414,9 +448,15 @@ hipError_t launch_stats(const uint16_t* Zf, const uint16_t* Zq, int N, int C, in
     return hipGetLastError();
 }
 
-void calib_plan(int N, int& chunks, int& per) {
+// Token chunks: about 128 tokens each, at most 64, and at most what keeps the
+// partial sums under 64 MB.
+void calib_plan(int N, int C, int g, int& chunks, int& per) {
+    const size_t per_chunk = 2 * ((size_t)C / g) * ((size_t)g * g + g) * sizeof(double);
+    const size_t cap_bytes = (size_t)64 << 20;
+    int cap = (int)(cap_bytes / per_chunk);
+    cap = cap < 1 ? 1 : (cap > kMaxChunks ? kMaxChunks : cap);
     chunks = (N + kChunkTok - 1) / kChunkTok;
-    chunks = chunks < 1 ? 1 : (chunks > kMaxChunks ? kMaxChunks : chunks);
+    chunks = chunks < 1 ? 1 : (chunks > cap ? cap : chunks);
     per = (N + chunks - 1) / chunks;
     chunks = (N + per - 1) / per;
 }
@@ -426,7 +466,7 @@ void calib_plan(int N, int& chunks, int& per) {
 size_t tac_calib_workspace_bytes(int N, int C, int g) {
     if (N <= 0 || C <= 0 || g <= 0) return 0;
     int chunks, per;
-    calib_plan(N, chunks, per);
+    calib_plan(N, C, g, chunks, per);
     const size_t B = (size_t)C / g, gg = (size_t)g * g;
     const size_t part = 2 * (size_t)chunks * B * (gg + g) * sizeof(double);
     const size_t work = B * (6 * gg + 3 * g) * sizeof(double);
@@ -437,7 +477,7 @@ hipError_t launch_tac_calib(const uint16_t* Zf, const uint16_t* Zq, int N, int C
                             double eta, double alpha, uint16_t* tac_M, uint16_t* tac_d, double* M64, double* d64,
                             void* ws, hipStream_t st) {
     int chunks, per;
-    calib_plan(N, chunks, per);
+    calib_plan(N, C, g, chunks, per);
     const size_t B = (size_t)C / g, gg = (size_t)g * g;
     double* part = static_cast<double*>(ws);
     const size_t part_bytes = 2 * (size_t)chunks * B * (gg + g) * sizeof(double);
@@ -454,8 +494,9 @@ hipError_t launch_tac_calib(const uint16_t* Zf, const uint16_t* Zq, int N, int C
         default: e = launch_stats<128>(Zf, Zq, N, C, per, chunks, part, st); break;
     }
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(tac_finalize_kernel, dim3((unsigned)B), dim3(kCalThreads), 0, st, part, chunks, N, C, g, rho,
-                       eps, eta, alpha, wk, tac_M, tac_d, M64, d64);
+    const size_t lds = g <= kLdsBlock ? 2 * gg * sizeof(double) : 0;
+    hipLaunchKernelGGL(tac_finalize_kernel, dim3((unsigned)B), dim3(kCalThreads), lds, st, part, chunks, N, C, g,
+                       rho, eps, eta, alpha, wk, tac_M, tac_d, M64, d64);
     return hipGetLastError();
 }
 

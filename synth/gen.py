@@ -173,9 +173,8 @@ def tac_calib_pair(N: int, C: int, g: int, rng) -> Tuple[np.ndarray, np.ndarray]
     L = np.tril(rng.normal(0.0, 0.5 / np.sqrt(g), size=(B, g, g)), -1)
     idx = np.arange(g)
     L[:, idx, idx] = rng.uniform(0.5, 1.5, size=(B, g))
-    xi = rng.standard_normal((N, B, g))
-    zf = mu[None] + np.einsum("nbk,brk->nbr", xi, L)
-    zf = zf.reshape(N, C)
+    xi = rng.standard_normal((B, N, g))
+    zf = (mu[:, None, :] + np.matmul(xi, L.transpose(0, 2, 1))).transpose(1, 0, 2).reshape(N, C)
     gain = 1.0 + rng.normal(0.0, 0.05, size=C)
     off = rng.normal(0.0, 0.05, size=C)
     zq = zf * gain[None] + rng.normal(0.0, 0.1, size=(N, C)) + off[None]
