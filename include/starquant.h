@@ -212,6 +212,25 @@ int w8a8_gemm(const int8_t* Aq, const float* s_a, const int8_t* Wq, const float*
  * with any other fp64 evaluation to rounding, not bit for bit.  Offline: run
  * once per layer after the activation transform is fixed.
  */
+/*
+ * Fast activation transform on the fp16 matrix cores (the matrix-core form of
+ * Eq. 11).  The basis is split once: v = 2^14 P, hi = fp16(v), lo = fp16(v - hi),
+ * stored as Ps [K][2K] fp16 with Ps[j][k] = hi(P[k][j]) and Ps[j][K + k] =
+ * lo(P[k][j]) (4 K^2 bytes, the size of P itself).  sgat_transform_fast then
+ * computes x' = 2^-14 ([x, x] . Ps^T) with fp32 accumulation and the gate of
+ * sgat_transform; the result differs from the exact x P by at most
+ * 2^-14 (sum_k |x_k||v_kj - hi_kj - lo_kj| + gamma_2K sum_k |x_k|(|hi_kj| + |lo_kj|)),
+ * gamma_n = n u / (1 - n u), u = 2^-23.  It is not bit-identical to
+ * sgat_transform, whose fixed order defines the codes; codes quantised from it
+ * can differ where a value lies within that bound of a rounding boundary.
+ *   sgat_split_basis:    P [K][K] fp32 in, Ps [K][2K] fp16 out; K^2 4 bytes < 2 GiB.
+ *   sgat_transform_fast: X [M][K] fp16, state [M] or NULL (no gate), Ps from
+ *                        sgat_split_basis, Xp out [M][K] fp32; X under 2 GiB.
+ */
+int sgat_split_basis(const float* P, int32_t K, uint16_t* Ps, void* stream);
+int sgat_transform_fast(const uint16_t* X, const uint8_t* state, const uint16_t* Ps, int32_t M, int32_t K,
+                        int32_t d_m, int32_t d_u, float* Xp, void* stream);
+
 size_t sq_tac_calibrate_workspace_bytes(int32_t N, int32_t C, int32_t g);
 int tac_calibrate(const uint16_t* Z_fp, const uint16_t* Z_q, int32_t N, int32_t C, int32_t g,
                   double rho, double eps, double eta, double alpha,

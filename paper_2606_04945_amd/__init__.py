@@ -22,7 +22,7 @@ __all__ = ["sgat_prepare_weights", "sgat_transform", "sgat_quantize", "sgat_quan
            "tac_default_block", "default_band", "quant_act_workspace_bytes", "gemm_workspace_bytes",
            "prepare_weights_workspace_bytes", "StarQuantError", "lib",
            "sgat_prepare_weights_w8", "sgat_quantize_w8", "sgat_quant_act_w8", "w8a8_gemm",
-           "tac_calibrate", "tac_calibrate_workspace_bytes"]
+           "tac_calibrate", "tac_calibrate_workspace_bytes", "sgat_split_basis", "sgat_transform_fast"]
 
 
 def _ptr(t: Optional[torch.Tensor]):
@@ -250,3 +250,32 @@ def tac_calibrate(Z_fp: torch.Tensor, Z_q: torch.Tensor, g: int, *, rho: float =
     check(lib().tac_calibrate(_ptr(Z_fp), _ptr(Z_q), N, C, g, rho, eps, eta, alpha, _ptr(tac_M), _ptr(tac_d),
                               _ptr(M64), _ptr(d64), _ptr(ws), wsb, _stream(stream)))
     return (tac_M, tac_d, M64, d64) if want_fp64 else (tac_M, tac_d)
+
+
+def sgat_split_basis(P: torch.Tensor, *, out=None, stream=None):
+    """fp16 hi / lo split of 2^14 P, transposed: Ps [K, 2K] for sgat_transform_fast."""
+    K = P.shape[0]
+    _need(P, "P", torch.float32, (K, K))
+    if out is None:
+        out = torch.empty((K, 2 * K), dtype=torch.float16, device=P.device)
+    _need(out, "out", torch.float16, (K, 2 * K))
+    check(lib().sgat_split_basis(_ptr(P), K, _ptr(out), _stream(stream)))
+    return out
+
+
+def sgat_transform_fast(X: torch.Tensor, state: Optional[torch.Tensor], Ps: torch.Tensor,
+                        d_m: Optional[int] = None, d_u: Optional[int] = None, *, out=None, stream=None):
+    """x' = x P G_s on the fp16 matrix cores (within a stated bound of the exact
+    product; not bit-identical to sgat_transform).  fp32 out."""
+    M, K = X.shape
+    _need(X, "X", torch.float16)
+    _need(state, "state", torch.uint8, (M,), optional=True)
+    _need(Ps, "Ps", torch.float16, (K, 2 * K))
+    dm0, du0 = default_band(K)
+    d_m = dm0 if d_m is None else d_m
+    d_u = du0 if d_u is None else d_u
+    if out is None:
+        out = torch.empty((M, K), dtype=torch.float32, device=X.device)
+    _need(out, "out", torch.float32, (M, K))
+    check(lib().sgat_transform_fast(_ptr(X), _ptr(state), _ptr(Ps), M, K, d_m, d_u, _ptr(out), _stream(stream)))
+    return out

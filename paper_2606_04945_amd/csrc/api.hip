@@ -298,4 +298,30 @@ int tac_calibrate(const uint16_t* Z_fp, const uint16_t* Z_q, int32_t N, int32_t 
                       "tac_calibrate");
 }
 
+int sgat_split_basis(const float* P, int32_t K, uint16_t* Ps, void* stream) {
+    SQ_TRY(check_K(K));
+    SQ_REQUIRE((size_t)K * K * 4 < (1u << 31), SQ_ERR_SHAPE,
+               "sgat_split_basis: K=%d: the split basis (4 K^2 bytes) must be under 2 GiB", K);
+    SQ_REQUIRE(P && Ps, SQ_ERR_NULL, "sgat_split_basis: P and Ps are required");
+    SQ_REQUIRE(aligned16(P) && aligned16(Ps), SQ_ERR_ALIGN, "sgat_split_basis: pointers must be 16-byte aligned");
+    return hip_status(sq::launch_split_basis(P, K, Ps, static_cast<hipStream_t>(stream)), "split_basis");
+}
+
+int sgat_transform_fast(const uint16_t* X, const uint8_t* state, const uint16_t* Ps, int32_t M, int32_t K,
+                        int32_t d_m, int32_t d_u, float* Xp, void* stream) {
+    SQ_TRY(check_K(K));
+    SQ_TRY(check_band(K, d_m, d_u));
+    SQ_REQUIRE(M >= 0, SQ_ERR_SHAPE, "M=%d < 0", M);
+    SQ_REQUIRE((size_t)K * K * 4 < (1u << 31), SQ_ERR_SHAPE,
+               "sgat_transform_fast: K=%d: the split basis (4 K^2 bytes) must be under 2 GiB", K);
+    SQ_REQUIRE((size_t)M * K * 2 < (1u << 31), SQ_ERR_SHAPE,
+               "sgat_transform_fast: X must be under 2 GiB (M=%d K=%d)", M, K);
+    if (M == 0) return SQ_OK;
+    SQ_REQUIRE(X && Ps && Xp, SQ_ERR_NULL, "sgat_transform_fast: X, Ps and Xp are required");
+    SQ_REQUIRE(aligned16(X) && aligned16(Ps) && aligned16(Xp), SQ_ERR_ALIGN,
+               "sgat_transform_fast: X, Ps and Xp must be 16-byte aligned");
+    return hip_status(sq::launch_transform_fast(X, state, Ps, M, K, d_m, d_u, Xp, static_cast<hipStream_t>(stream)),
+                      "transform_fast");
+}
+
 }  // extern "C"

@@ -100,4 +100,9 @@ hipError_t launch_tac_calib(const uint16_t* Zf, const uint16_t* Zq, int N, int C
                             double eta, double alpha, uint16_t* tac_M, uint16_t* tac_d, double* M64, double* d64,
                             void* ws, hipStream_t st);
 
+// Fast transform on the fp16 MFMA (transform_fast.hip)
+hipError_t launch_split_basis(const float* P, int K, uint16_t* Ps, hipStream_t st);
+hipError_t launch_transform_fast(const uint16_t* X, const uint8_t* state, const uint16_t* Ps, int M, int K, int dm,
+                                 int du, float* Xp, hipStream_t st);
+
 }  // namespace sq
