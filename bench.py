@@ -32,6 +32,7 @@ sys.path.insert(0, ROOT)
 # MI355X published peaks
 PEAK_HBM_GBS = 8000.0
 PEAK_INT8_TOPS = 5000.0           # dense int8 MFMA, TOP/s
+PEAK_FP16_TFLOPS = 2500.0         # dense fp16 MFMA, TFLOP/s
 # fp32 FMA on the VALU without packed-fp32 instructions (the library is built
 # without them): 256 CU x 4 SIMD x 16 lanes x 2 flop x 2.4 GHz
 PEAK_FP32_VALU_TFLOPS = 78.6
@@ -68,6 +69,7 @@ def parse():
     ap.add_argument("--no-small", action="store_true",
                     help="skip the 16/32/64-token denoising-step layer sets (small-token HBM figures)")
     ap.add_argument("--no-calib", action="store_true", help="skip the TAC calibration timing")
+    ap.add_argument("--no-fast", action="store_true", help="skip the dense step with the matrix-core transform")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain 1 GiB device copy (reference for HBM byte counters)")
     return ap.parse_args()
@@ -378,6 +380,18 @@ def main():
             tm.wrap("gemm/" + d["site"].name,
                     lambda: sq.w4a4_gemm(d["Aq"], d["s_a"], d["Wq"], d["s_w"], Y=d["Y"], ws=d["gws"]))
 
+    def step_dense_fast(tm):
+        for d in sites:
+            src = d["X"]
+            if d["z"] is not None:
+                tm.wrap("tac", lambda: sq.tac_apply(d["X"], d["tac_M"], d["tac_d"], d["g"], out=d["z"]))
+                src = d["z"]
+            tm.wrap("ftransform/" + d["site"].name,
+                    lambda: sq.sgat_transform_fast(src, state, d["Ps"], d["dm"], d["du"], out=d["xp"]))
+            tm.wrap("quant", lambda: sq.sgat_quantize(d["xp"], Aq=d["Aq"], s=d["s_a"]))
+            tm.wrap("gemm/" + d["site"].name,
+                    lambda: sq.w4a4_gemm(d["Aq"], d["s_a"], d["Wq"], d["s_w"], Y=d["Y"], ws=d["gws"]))
+
     def step_folded(tm, it):
         ws = wcopies[it % len(wcopies)]
         for d, (Wq, s_w) in zip(sites, ws):
@@ -425,6 +439,24 @@ def main():
                             gemm_ms=gm_ms / args.steps, gemm_tops=gm_ops / gm_ms / 1e9,
                             tac_ms=timer.ms("tac")[0] / args.steps, quant_ms=timer.ms("quant")[0] / args.steps,
                             per_site_transform_ms={n: timer.ms("transform/" + n)[0] / args.steps for n in flops_tr})
+    if args.only in ("dense", "both") and not args.no_fast:
+        for d in sites:
+            d["Ps"] = sq.sgat_split_basis(d["P"])
+        # codes of one step through each transform, compared
+        step_dense(Timer(torch))
+        torch.cuda.synchronize()
+        canon = [(d["Aq"].clone(), d["s_a"].clone()) for d in sites]
+        step_dense_fast(Timer(torch))
+        torch.cuda.synchronize()
+        flips = sum(int(((a ^ d["Aq"]) & 0x0F).ne(0).sum() + ((a ^ d["Aq"]) & 0xF0).ne(0).sum())
+                    for (a, _), d in zip(canon, sites))
+        ncodes = sum(d["Aq"].numel() * 2 for d in sites)
+        ms_f = run(lambda tm, i: step_dense_fast(tm), args.steps, args.warmup)
+        tr_ms = sum(timer.ms("ftransform/" + n)[0] for n in flops_tr)
+        tr_flop = sum(flops_tr.values()) * args.steps
+        out["dense_fast"] = dict(ms=ms_f, transform_ms=tr_ms / args.steps, transform_tflops=tr_flop / tr_ms / 1e9,
+                                 code_flips=flips, codes=ncodes)
+        del canon
     if args.only in ("folded", "both"):
         ms_fold = run(step_folded, args.steps, args.warmup)
         gm_ms = sum(timer.ms("gemm/" + n)[0] for n in ops_gemm)
@@ -524,6 +556,15 @@ def main():
         res["w8a8_folded_P"] = {"value": M / (w8["ms"] / 1e3), "unit": "tokens/s", "ms_per_step": w8["ms"],
                                 "gemm_tops": w8["gemm_tops"], "gemm_frac_int8_peak": w8["gemm_tops"] / PEAK_INT8_TOPS,
                                 "quant_act_ms": w8["quant_act_ms"]}
+    if "dense_fast" in out:
+        f = out["dense_fast"]
+        res["dense_P_fast_transform"] = {
+            "value": M / (f["ms"] / 1e3), "unit": "tokens/s", "ms_per_step": f["ms"],
+            "transform_ms": f["transform_ms"],
+            "roofline": {"bound": "mfma", "achieved": f["transform_tflops"], "peak": PEAK_FP16_TFLOPS,
+                         "unit": "TFLOP/s", "frac": f["transform_tflops"] / PEAK_FP16_TFLOPS, "traffic": None,
+                         "kernel": "transform on the fp16 MFMA (hi + lo split: executes 2x the algorithmic flops)"},
+            "codes_differing_from_fixed_order": f["code_flips"], "codes": f["codes"]}
     if "large" in out:
         res["large_token"] = out["large"]
     if "small" in out:

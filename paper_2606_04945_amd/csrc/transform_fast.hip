@@ -15,7 +15,7 @@
 // codes are defined by, this one trades that for the matrix cores.
 //
 // The kernel is the GEMM's three-stage direct-to-LDS pipeline on fp16
-// operands: 128 x 128 (or 64 x 64) output tiles, four waves, one
+// operands: 128 x 128, 64 x 128 or 64 x 64 output tiles, four waves, one
 // v_mfma_f32_16x16x32_f16 per 16 x 16 tile and k step of 32, the gate applied
 // in the epilogue, fp32 out.
 #include "tile_common.hpp"
@@ -165,11 +165,15 @@ hipError_t launch_split_basis(const float* P, int K, uint16_t* Ps, hipStream_t s
 hipError_t launch_transform_fast(const uint16_t* X, const uint8_t* state, const uint16_t* Ps, int M, int K, int dm,
                                  int du, float* Xp, hipStream_t st) {
     const size_t t128 = (size_t)((M + 127) / 128) * (size_t)((K + 127) / 128);
+    const size_t t64x128 = (size_t)((M + 63) / 64) * (size_t)((K + 127) / 128);
     const size_t t64 = (size_t)((M + 63) / 64) * (size_t)((K + 63) / 64);
     if (t64 > 0x7fffffffu) return hipErrorInvalidConfiguration;
     if (t128 >= 512) {
         hipLaunchKernelGGL((transform_mfma_kernel<2, 2, 4, 4>), dim3((unsigned)t128), dim3(256), 0, st, X, state, Ps,
                            M, K, dm, du, Xp);
+    } else if (t64x128 >= 512) {
+        hipLaunchKernelGGL((transform_mfma_kernel<1, 4, 4, 2>), dim3((unsigned)t64x128), dim3(256), 0, st, X, state,
+                           Ps, M, K, dm, du, Xp);
     } else {
         hipLaunchKernelGGL((transform_mfma_kernel<2, 2, 2, 2>), dim3((unsigned)t64), dim3(256), 0, st, X, state, Ps,
                            M, K, dm, du, Xp);
