@@ -7,8 +7,8 @@
 // byte: for a packed dword w, (w << 4) & 0xF0F0F0F0 holds the even-k codes and
 // w & 0xF0F0F0F0 the odd-k codes, each as the int8 value 16*q, with no sign
 // extension step.  With both operands scaled by 16 the MFMA sums 256*qa*qw
-// exactly (|sum| <= 256 * 64 * K < 2^31 for K <= 131072), and >> 8 recovers the
-// integer dot product.  Even and odd k land in different registers; the same
+// exactly, and >> 8 recovers the integer dot product (see acc_value for the one
+// sum, +2^23 at K = 131072, whose scaled value wraps).  Even and odd k land in different registers; the same
 // permutation is applied to A and W, and an integer sum does not depend on its
 // order, so the result is the plain dot product.
 //
@@ -63,7 +63,11 @@ __device__ __forceinline__ v4i operand(const v4i& raw, int h) {
 }
 template <int BITS>
 __device__ __forceinline__ int acc_value(int raw) {   // 4-bit operands carry a factor 16 each
-    return BITS == 8 ? raw : raw >> 8;
+    // 4-bit: the dot product lies in [-56 K, 64 K] (codes in [-8, 7]), so 256 x it
+    // fits in int32 except at +2^31, reached only when every product is
+    // (-8)(-8) at K = 131072; that wraps to INT_MIN, which no in-range sum
+    // produces, and stands for +2^23
+    return BITS == 8 ? raw : (raw == INT32_MIN ? (1 << 23) : raw >> 8);
 }
 
 template <int WM, int WN, int TM, int TN, bool SPLIT, int BITS, int OCC>

@@ -66,7 +66,7 @@ def test_zero_rows_and_tiny_scales():
 
 # ------------------------------------------------------------------ folded basis (P = NULL)
 
-@pytest.mark.parametrize("M,K", [(1, 64), (3, 512), (77, 4096), (130, 3584), (64, 18944)])
+@pytest.mark.parametrize("M,K", [(1, 64), (3, 512), (77, 4096), (130, 3584), (64, 18944), (3, 131072)])
 @pytest.mark.parametrize("layout", ["random", "all_masked", "none_masked", "alternating"])
 def test_quant_act_folded(M, K, layout):
     st = None if layout == "random" else synth.state_edge(M, layout)
@@ -77,6 +77,21 @@ def test_quant_act_folded(M, K, layout):
     ref_q, ref_s = O.quant_act(X, st, None, dm, du)
     assert_bits(host(s), ref_s, "s_a")
     assert_bits(host(Aq), ref_q, "Aq")
+
+
+@pytest.mark.parametrize("K", [24576, 32768, 131072])
+def test_quantize_rows_longer_than_the_register_tile(K):
+    """Rows above 12 x 256 vectors of 8 are read twice instead of held (the reload path)."""
+    x = np.random.default_rng(K).standard_normal((3, K)).astype(np.float32)
+    x[1, 5] = 40.0
+    Aq, s = sq.sgat_quantize(dev(x))
+    rq, rs, _ = O.quant_rows(x)
+    assert_bits(host(s), rs, "s")
+    assert_bits(host(Aq), rq, "Aq")
+    Aq8, s8 = sq.sgat_quantize_w8(dev(x))
+    rq8, rs8 = O.quant_rows_q8(x)
+    assert_bits(host(s8), rs8, "s8")
+    assert_bits(host(Aq8), rq8, "Aq8")
 
 
 def test_quant_act_folded_no_gate_and_custom_bands():
@@ -182,6 +197,42 @@ def test_gemm_extreme_codes():
     assert_bits(host(acc), (q @ w.T).astype(np.int32), "acc")
     rY, _ = O.gemm(Aq, s_a, Wq, s_w)
     assert_y(host(Y), rY)
+
+
+@pytest.mark.parametrize("M,N", [(1, 8), (3, 16), (130, 136)])
+def test_gemm_at_the_largest_K(M, N):
+    """K = 131072: random codes, and the one extreme sum (every product (-8)(-8), so
+    the dot product is 2^23 and its x256 scaled form is 2^31) on row 0 / column 0."""
+    K = 131072
+    rng = np.random.default_rng(11 + M)
+    q = rng.integers(-8, 8, (M, K))
+    w = rng.integers(-8, 8, (N, K))
+    q[0, :] = -8
+    w[0, :] = -8
+    Aq, Wq = pack_codes(q), pack_codes(w)
+    s_a = rng.uniform(0.5, 1, M).astype(np.float32)
+    s_w = rng.uniform(1e-8, 1e-7, N).astype(np.float32)
+    say(f"gemm largest K M={M} N={N} ws={sq.gemm_workspace_bytes(M, N, K)}")
+    Y, acc = sq.w4a4_gemm(dev(Aq), dev(s_a), dev(Wq), dev(s_w), want_acc=True)
+    ref = q.astype(np.int64) @ w.T.astype(np.int64)
+    assert ref[0, 0] == 1 << 23
+    assert_bits(host(acc), ref.astype(np.int32), "acc")
+    rY, racc = O.gemm(Aq, s_a, Wq, s_w, threads=THREADS)
+    assert_bits(racc, ref.astype(np.int32), "oracle acc")
+    assert_y(host(Y), rY)
+
+
+def test_w8a8_gemm_at_the_largest_K():
+    K, M, N = 65536, 3, 16
+    q = np.full((M, K), -128, np.int8)
+    w = np.full((N, K), -128, np.int8)
+    q[1:] = np.random.default_rng(12).integers(-128, 128, (M - 1, K))
+    s_a = np.ones(M, np.float32)
+    s_w = np.full(N, 1e-9, np.float32)
+    Y, acc = sq.w8a8_gemm(dev(q), dev(s_a), dev(w), dev(s_w), want_acc=True)
+    ref = q.astype(np.int64) @ w.T.astype(np.int64)
+    assert ref[0, 0] == 1 << 30
+    assert_bits(host(acc), ref.astype(np.int32), "acc")
 
 
 def test_gemm_split_and_unsplit_agree():
