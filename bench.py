@@ -286,6 +286,53 @@ def small_token_block(torch, sq, synth, dev, token_counts=(16, 32, 64), copies=4
     return res
 
 
+def tac_oproj_block(torch, sq, synth, dev, steps=5):
+    """TAC (32 blocks of 128) on 8 x 2048 attention outputs of width 4096, then the
+    gate + int4 quantiser and the 4096 -> 4096 W4A4 GEMM (folded P).  TAC at
+    g = 128 runs as its own kernel (the fused form covers g <= 16)."""
+    st_np = synth.config_state(3)
+    M = len(st_np)
+    state = torch.from_numpy(st_np).to(dev)
+    t = synth.site_tensors(3, 0, st_np, with_P=False)
+    K, N, g = t.site.K, t.site.N, t.g
+    W = torch.from_numpy(t.W).to(dev)
+    Wq, s_w = sq.sgat_prepare_weights(W, None)
+    del W
+    X = torch.from_numpy(t.X).to(dev)
+    tM, td = torch.from_numpy(t.tac_M).to(dev), torch.from_numpy(t.tac_d).to(dev)
+    Z = torch.empty_like(X)
+    Aq = torch.empty((M, K // 2), dtype=torch.uint8, device=dev)
+    s_a = torch.empty((M,), dtype=torch.float32, device=dev)
+    Y = torch.empty((M, N), dtype=torch.float16, device=dev)
+    gws = torch.empty(max(sq.gemm_workspace_bytes(M, N, K), 1), dtype=torch.uint8, device=dev)
+    timer = Timer(torch)
+
+    def step(tm):
+        tm.wrap("tac", lambda: sq.tac_apply(X, tM, td, g, out=Z))
+        tm.wrap("q", lambda: sq.sgat_quant_act(Z, state, None, t.dm, t.du, Aq=Aq, s_a=s_a))
+        tm.wrap("g", lambda: sq.w4a4_gemm(Aq, s_a, Wq, s_w, Y=Y, ws=gws))
+    step(Timer(torch))
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        step(timer)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    tac_ms = timer.ms("tac")[0] / steps
+    g_ms = timer.ms("g")[0] / steps
+    tac_flop = 2.0 * M * K * g
+    return {"workload": f"TAC g = {g} + O projection {K}->{N}, 8 x 2048 tokens, folded P",
+            "tokens": M, "ms_per_step": ms, "tokens_per_s": M / (ms / 1e3),
+            "tac_ms": tac_ms, "quant_ms": timer.ms("q")[0] / steps, "gemm_ms": g_ms,
+            "gemm_frac_int8_peak": 2.0 * M * N * K / g_ms / 1e9 / PEAK_INT8_TOPS,
+            "roofline": {"bound": "alu", "achieved": tac_flop / tac_ms / 1e9, "peak": PEAK_FP32_VALU_TFLOPS,
+                         "unit": "TFLOP/s", "frac": tac_flop / tac_ms / 1e9 / PEAK_FP32_VALU_TFLOPS,
+                         "traffic": None, "kernel": f"tac (g = {g})"}}
+
+
 def tac_calibration_block(torch, sq, synth, dev, N=8192, C=4096, reps=5):
     """TAC closed-form calibration (App. C, offline) on 8192 paired tokens of width
     4096, at the default block size 16 and at 128: call time and the rate at which
@@ -487,6 +534,8 @@ def main():
         out["large"] = large_token_block(torch, sq, synth, dev, max(3, args.steps // 4), 1)
     if not args.no_small:
         out["small"] = small_token_block(torch, sq, synth, dev)
+    if not args.no_large:
+        out["tac_oproj"] = tac_oproj_block(torch, sq, synth, dev)
     if not args.no_calib:
         out["calib"] = tac_calibration_block(torch, sq, synth, dev)
 
@@ -569,6 +618,8 @@ def main():
         res["large_token"] = out["large"]
     if "small" in out:
         res["small_token"] = out["small"]
+    if "tac_oproj" in out:
+        res["tac_oproj"] = out["tac_oproj"]
     if "calib" in out:
         res["tac_calibration"] = out["calib"]
     if cpu:

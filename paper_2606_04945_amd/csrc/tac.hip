@@ -7,7 +7,8 @@
 // kernel is a register-tiled batched SGEMM: a workgroup owns TT tokens x CW
 // channels (CW = max(g, 64) so a span holds whole blocks), stages the span's
 // block matrices and the token tile through LDS as fp32, and each thread keeps
-// 8 tokens x 4 channels of accumulators.
+// 8 tokens x 8 channels of accumulators (8 x 4 when g < 8), so each pair of
+// LDS reads feeds 64 (32) fused multiply-adds.
 #include "sq_internal.hpp"
 
 namespace sq {
@@ -15,14 +16,15 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kTPT = 8;   // tokens per thread
-constexpr int kCPT = 4;   // channels per thread
-constexpr int kCC = 32;   // block-matrix columns staged per pass
 
-template <int CW>
+// CPT channels per thread (8, or 4 for g < 8); CC block-matrix columns staged per pass
+template <int CW, int CPT>
 __global__ __launch_bounds__(kThreads) void tac_kernel(const uint16_t* __restrict__ Z,
                                                        const uint16_t* __restrict__ Mb,
                                                        const uint16_t* __restrict__ d, int M, int C,
                                                        int g, uint16_t* __restrict__ out) {
+    constexpr int kCPT = CPT;
+    constexpr int kCC = CW == 128 ? 16 : 32;
     constexpr int CG = CW / kCPT;            // channel groups per span
     constexpr int TG = kThreads / CG;        // token groups
     constexpr int TT = TG * kTPT;            // tokens per tile
@@ -49,7 +51,7 @@ __global__ __launch_bounds__(kThreads) void tac_kernel(const uint16_t* __restric
     __syncthreads();
 
     const int cg = tid % CG, tg = tid / CG;
-    const int ch0 = cg * kCPT;               // first of this thread's 4 channels (span-local)
+    const int ch0 = cg * kCPT;               // first of this thread's channels (span-local)
     float acc[kTPT][kCPT];
 #pragma unroll
     for (int t = 0; t < kTPT; ++t)
@@ -68,14 +70,18 @@ __global__ __launch_bounds__(kThreads) void tac_kernel(const uint16_t* __restric
         }
         __syncthreads();
         if (g >= kCPT) {
-            const int base = (ch0 / g) * g;  // block start, shared by the 4 channels
+            const int base = (ch0 / g) * g;  // block start, shared by the thread's channels
             for (int c = 0; c < cc; ++c) {
-                const float4 mv = *reinterpret_cast<const float4*>(msT + c * MP + ch0);
+                float m[kCPT];
+#pragma unroll
+                for (int q = 0; q < kCPT; q += 4) {
+                    const float4 mv = *reinterpret_cast<const float4*>(msT + c * MP + ch0 + q);
+                    m[q] = mv.x, m[q + 1] = mv.y, m[q + 2] = mv.z, m[q + 3] = mv.w;
+                }
                 const float* zr = zsT + (base + c0 + c) * ZP + tg * kTPT;
                 const float4 z0 = *reinterpret_cast<const float4*>(zr);
                 const float4 z1 = *reinterpret_cast<const float4*>(zr + 4);
                 const float zv[8] = {z0.x, z0.y, z0.z, z0.w, z1.x, z1.y, z1.z, z1.w};
-                const float m[4] = {mv.x, mv.y, mv.z, mv.w};
 #pragma unroll
                 for (int t = 0; t < kTPT; ++t)
 #pragma unroll
@@ -103,22 +109,30 @@ __global__ __launch_bounds__(kThreads) void tac_kernel(const uint16_t* __restric
     for (int t = 0; t < kTPT; ++t) {
         const int tok = tok0 + tg * kTPT + t;
         if (tok >= M) break;
-        ushort4 o;
-        o.x = f2h(acc[t][0] + dv[0]);
-        o.y = f2h(acc[t][1] + dv[1]);
-        o.z = f2h(acc[t][2] + dv[2]);
-        o.w = f2h(acc[t][3] + dv[3]);
-        *reinterpret_cast<ushort4*>(out + (size_t)tok * C + span0 + ch0) = o;
+#pragma unroll
+        for (int q = 0; q < kCPT; q += 4) {
+            ushort4 o;
+            o.x = f2h(acc[t][q] + dv[q]);
+            o.y = f2h(acc[t][q + 1] + dv[q + 1]);
+            o.z = f2h(acc[t][q + 2] + dv[q + 2]);
+            o.w = f2h(acc[t][q + 3] + dv[q + 3]);
+            *reinterpret_cast<ushort4*>(out + (size_t)tok * C + span0 + ch0 + q) = o;
+        }
     }
 }
 
-template <int CW>
+template <int CW, int CPT>
 hipError_t launch_cw(const uint16_t* Z, const uint16_t* Mb, const uint16_t* d, int M, int C, int g,
                      uint16_t* out, hipStream_t st) {
-    constexpr int CG = CW / kCPT, TT = (kThreads / CG) * kTPT;
-    const size_t lds = sizeof(float) * ((size_t)CW * (TT + 4) + (size_t)kCC * (CW + 4));
+    constexpr int CG = CW / CPT, TT = (kThreads / CG) * kTPT;
+    constexpr int CC = CW == 128 ? 16 : 32;
+    const size_t lds = sizeof(float) * ((size_t)CW * (TT + 4) + (size_t)CC * (CW + 4));
+    static const hipError_t attr =             // above the 64 KB default for dynamic LDS
+        hipFuncSetAttribute(reinterpret_cast<const void*>(&tac_kernel<CW, CPT>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (attr != hipSuccess) return attr;
     dim3 grid(C / CW, (M + TT - 1) / TT);
-    hipLaunchKernelGGL(tac_kernel<CW>, grid, dim3(kThreads), lds, st, Z, Mb, d, M, C, g, out);
+    hipLaunchKernelGGL((tac_kernel<CW, CPT>), grid, dim3(kThreads), lds, st, Z, Mb, d, M, C, g, out);
     return hipGetLastError();
 }
 
@@ -126,8 +140,9 @@ hipError_t launch_cw(const uint16_t* Z, const uint16_t* Mb, const uint16_t* d, i
 
 hipError_t launch_tac(const uint16_t* Z, const uint16_t* Mb, const uint16_t* d, int M, int C, int g,
                       uint16_t* out, hipStream_t st) {
-    if (g <= 64) return launch_cw<64>(Z, Mb, d, M, C, g, out, st);
-    return launch_cw<128>(Z, Mb, d, M, C, g, out, st);
+    if (g < 8) return launch_cw<64, 4>(Z, Mb, d, M, C, g, out, st);
+    if (g <= 64) return launch_cw<64, 8>(Z, Mb, d, M, C, g, out, st);
+    return launch_cw<128, 8>(Z, Mb, d, M, C, g, out, st);
 }
 
 }  // namespace sq
