@@ -24,7 +24,8 @@ __global__ __launch_bounds__(kThreads) void tac_kernel(const uint16_t* __restric
                                                        const uint16_t* __restrict__ d, int M, int C,
                                                        int g, uint16_t* __restrict__ out) {
     constexpr int kCPT = CPT;
-    constexpr int kCC = CW == 128 ? 16 : 32;
+    constexpr int kCC = CW == 128 ? 8 : 16;
+    constexpr int MPT = CW * kCC / kThreads; // block-matrix values each thread stages per pass
     constexpr int CG = CW / kCPT;            // channel groups per span
     constexpr int TG = kThreads / CG;        // token groups
     constexpr int TT = TG * kTPT;            // tokens per tile
@@ -32,7 +33,7 @@ __global__ __launch_bounds__(kThreads) void tac_kernel(const uint16_t* __restric
     constexpr int MP = CW + 4;               // padded row of the transposed block tile
     extern __shared__ float smem[];
     float* zsT = smem;                       // [CW][ZP]   zsT[ch][tok]
-    float* msT = smem + CW * ZP;             // [kCC][MP]  msT[c-c0][ch] = M_{blk(ch)}[ch%g][c]
+    float* msT = smem + CW * ZP;             // [2][kCC][MP]  msT[c-c0][ch] = M_{blk(ch)}[ch%g][c]
 
     const int tid = threadIdx.x;
     const int span0 = blockIdx.x * CW;       // first channel of this span
@@ -48,7 +49,6 @@ __global__ __launch_bounds__(kThreads) void tac_kernel(const uint16_t* __restric
 #pragma unroll
         for (int q = 0; q < 8; ++q) zsT[(v * 8 + q) * ZP + t] = h2f(h[q]);
     }
-    __syncthreads();
 
     const int cg = tid % CG, tg = tid / CG;
     const int ch0 = cg * kCPT;               // first of this thread's channels (span-local)
@@ -58,24 +58,42 @@ __global__ __launch_bounds__(kThreads) void tac_kernel(const uint16_t* __restric
 #pragma unroll
         for (int q = 0; q < kCPT; ++q) acc[t][q] = 0.0f;
 
-    // the block matrices are staged kCC columns c at a time; every accumulator
-    // still sees c in ascending order
+    // the block matrices are staged kCC columns c at a time, double-buffered:
+    // the next pass's values are loaded into registers while this pass
+    // computes; every accumulator still sees c in ascending order
     const int cc = g < kCC ? g : kCC;
-    for (int c0 = 0; c0 < g; c0 += cc) {
-        __syncthreads();
-        for (int e = tid; e < CW * cc; e += kThreads) {
+    const int npass = g / cc;
+    uint16_t pre[MPT];
+    auto load_pass = [&](int c0) {
+#pragma unroll
+        for (int i = 0; i < MPT; ++i) {
+            const int e = tid + i * kThreads;
             const int ch = e / cc, c = e % cc;
             // tac_M is [C/g][g][g] == [C][g]: row (span0 + ch), column c0 + c
-            msT[c * MP + ch] = h2f(Mb[(size_t)(span0 + ch) * g + c0 + c]);
+            pre[i] = e < CW * cc ? Mb[(size_t)(span0 + ch) * g + c0 + c] : (uint16_t)0;
         }
-        __syncthreads();
-        if (g >= kCPT) {
+    };
+    auto store_pass = [&](float* buf) {
+#pragma unroll
+        for (int i = 0; i < MPT; ++i) {
+            const int e = tid + i * kThreads;
+            if (e < CW * cc) buf[(e % cc) * MP + e / cc] = h2f(pre[i]);
+        }
+    };
+    load_pass(0);
+    store_pass(msT);
+    __syncthreads();                         // token tile and first pass staged
+    for (int p = 0; p < npass; ++p) {
+        const int c0 = p * cc;
+        const float* ms = msT + (p & 1) * kCC * MP;
+        if (p + 1 < npass) load_pass(c0 + cc);
+        if (CPT == 8 || g >= kCPT) {         // CPT == 8 is launched for g >= 8 only
             const int base = (ch0 / g) * g;  // block start, shared by the thread's channels
             for (int c = 0; c < cc; ++c) {
                 float m[kCPT];
 #pragma unroll
                 for (int q = 0; q < kCPT; q += 4) {
-                    const float4 mv = *reinterpret_cast<const float4*>(msT + c * MP + ch0 + q);
+                    const float4 mv = *reinterpret_cast<const float4*>(ms + c * MP + ch0 + q);
                     m[q] = mv.x, m[q + 1] = mv.y, m[q + 2] = mv.z, m[q + 3] = mv.w;
                 }
                 const float* zr = zsT + (base + c0 + c) * ZP + tg * kTPT;
@@ -87,19 +105,21 @@ __global__ __launch_bounds__(kThreads) void tac_kernel(const uint16_t* __restric
 #pragma unroll
                     for (int q = 0; q < kCPT; ++q) acc[t][q] = __builtin_fmaf(m[q], zv[t], acc[t][q]);
             }
-        } else {
+        } else if constexpr (CPT == 4) {
             // g in {1, 2}: the thread's channels lie in different blocks
 #pragma unroll
             for (int q = 0; q < kCPT; ++q) {
                 const int ch = ch0 + q, base = (ch / g) * g;
                 for (int c = 0; c < cc; ++c) {
-                    const float m = msT[c * MP + ch];
+                    const float m = ms[c * MP + ch];
 #pragma unroll
                     for (int t = 0; t < kTPT; ++t)
                         acc[t][q] = __builtin_fmaf(m, zsT[(base + c0 + c) * ZP + tg * kTPT + t], acc[t][q]);
                 }
             }
         }
+        if (p + 1 < npass) store_pass(msT + ((p + 1) & 1) * kCC * MP);
+        __syncthreads();                     // next buffer filled; this one free for p + 2
     }
 
     float dv[kCPT];
@@ -125,8 +145,8 @@ template <int CW, int CPT>
 hipError_t launch_cw(const uint16_t* Z, const uint16_t* Mb, const uint16_t* d, int M, int C, int g,
                      uint16_t* out, hipStream_t st) {
     constexpr int CG = CW / CPT, TT = (kThreads / CG) * kTPT;
-    constexpr int CC = CW == 128 ? 16 : 32;
-    const size_t lds = sizeof(float) * ((size_t)CW * (TT + 4) + (size_t)CC * (CW + 4));
+    constexpr int CC = CW == 128 ? 8 : 16;
+    const size_t lds = sizeof(float) * ((size_t)CW * (TT + 4) + 2 * (size_t)CC * (CW + 4));
     static const hipError_t attr =             // above the 64 KB default for dynamic LDS
         hipFuncSetAttribute(reinterpret_cast<const void*>(&tac_kernel<CW, CPT>),
                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
