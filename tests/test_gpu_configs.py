@@ -96,8 +96,39 @@ def test_dream_layer_set(si):
 
 
 @pytest.mark.timeout(600)
-def test_dream_layer_set_folded_gate_up():
-    run_site(2, 2, synth.config_state(2), folded=True)
+@pytest.mark.parametrize("si", [1, 2], ids=["o_tac_fused", "gate_up"])
+def test_dream_layer_set_folded(si):
+    """Folded P at 8 x 2048 tokens: the O projection runs TAC (g = 16) fused into the
+    quantiser; gate+up is the widest GEMM of the set."""
+    run_site(2, si, synth.config_state(2), folded=True)
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("si", range(4), ids=[s.name for s in synth.CONFIGS[1].sites])
+def test_llada_layer_set_w8a8(si):
+    """The W8A8 variant (App. D) of every linear of the LLaDA-shaped set, folded P."""
+    st = synth.config_state(1)
+    t = synth.site_tensors(1, si, st, with_P=False)
+    K, N, M = t.site.K, t.site.N, len(st)
+    say(f"w8a8 config 1 site {t.site.name} M={M} K={K} N={N}")
+    tM = dev(t.tac_M) if t.tac_M is not None else None
+    td = dev(t.tac_d) if t.tac_d is not None else None
+    Wq, s_w = sq.sgat_prepare_weights_w8(dev(t.W), None)
+    Aq, s_a = sq.sgat_quant_act_w8(dev(t.X), dev(st), None, t.dm, t.du, tM, td, t.g)
+    Y, acc = sq.w8a8_gemm(Aq, s_a, Wq, s_w, want_acc=True)
+    torch.cuda.synchronize()
+    rows = sample_rows(st, 6, 3000 + si)
+    cols = np.unique(np.r_[0, N - 1, np.random.default_rng(4000 + si).choice(N, 8, replace=False)])
+    rq, rs = O.quant_act_q8(t.X[rows], st[rows], None, t.dm, t.du, t.tac_M, t.tac_d, t.g, threads=THREADS)
+    wq, ws = O.prepare_weights_q8(t.W[cols], None)
+    ry, racc = O.gemm_q8(rq, rs, wq, ws)
+    assert_bits(host(s_a)[rows], rs, "s_a rows")
+    assert_bits(host(Aq)[rows], rq, "Aq rows")
+    assert_bits(host(Wq)[cols], wq, "Wq rows")
+    ri = torch.from_numpy(rows).cuda()
+    ci = torch.from_numpy(cols).cuda()
+    assert_bits(host(acc.index_select(0, ri).index_select(1, ci)), racc, "acc samples")
+    assert_y(host(Y.index_select(0, ri).index_select(1, ci)), ry)
 
 
 @pytest.mark.timeout(600)
