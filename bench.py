@@ -70,6 +70,7 @@ def parse():
                     help="skip the 16/32/64-token denoising-step layer sets (small-token HBM figures)")
     ap.add_argument("--no-calib", action="store_true", help="skip the TAC calibration timing")
     ap.add_argument("--no-fast", action="store_true", help="skip the dense step with the matrix-core transform")
+    ap.add_argument("--no-sweep", action="store_true", help="skip the GEMM token-count sweep")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain 1 GiB device copy (reference for HBM byte counters)")
     return ap.parse_args()
@@ -284,6 +285,48 @@ def small_token_block(torch, sq, synth, dev, token_counts=(16, 32, 64), copies=4
     del wsets
     torch.cuda.empty_cache()
     return res
+
+
+def sweep_block(torch, sq, synth, dev, token_counts=(16, 64, 256, 1024, 4096, 16384), copies=4):
+    """Denoising-step sweep over token counts (LLaDA shapes, step 32 of 64, folded P):
+    the W4A4 GEMM of every linear, graph-replayed with rotating weights, as
+    achieved TOP/s and algorithmic GB/s, from memory-bound to compute-bound."""
+    cfg = synth.CONFIGS[4]
+    st_max = synth.config_state(4, M=max(token_counts), t=32)
+    wsets, meta = [[] for _ in range(copies)], []
+    for si, site in enumerate(cfg.sites):
+        t = synth.site_tensors(4, si, st_max[:16], with_P=False)
+        W = torch.from_numpy(t.W).to(dev)
+        Wq, s_w = sq.sgat_prepare_weights(W, None)
+        del W
+        for c in range(copies):
+            wsets[c].append((Wq.clone(), s_w.clone()))
+        meta.append(site)
+        del t, Wq, s_w
+    out = {}
+    for M in token_counts:
+        rec = {}
+        for si, site in enumerate(meta):
+            K, N = site.K, site.N
+            g = torch.Generator(device="cpu").manual_seed(M * 10 + si)
+            Aq = torch.randint(0, 256, (M, K // 2), dtype=torch.uint8, generator=g).to(dev)
+            s_a = (torch.rand(M, generator=g) + 0.5).to(dev)
+            Y = torch.empty((M, N), dtype=torch.float16, device=dev)
+            gws = torch.empty(max(sq.gemm_workspace_bytes(M, N, K), 1), dtype=torch.uint8, device=dev)
+            calls = 4 * copies if M <= 1024 else copies
+            ms, gr = graph_ms(torch, lambda i: sq.w4a4_gemm(Aq, s_a, wsets[i % copies][si][0],
+                                                            wsets[i % copies][si][1], Y=Y, ws=gws), calls)
+            del gr
+            ops = 2.0 * M * N * K
+            byts = N * K // 2 + N * 4 + M * K // 2 + M * 4 + M * N * 2
+            rec[site.name] = {"us": ms * 1e3, "tops": ops / ms / 1e9, "frac_int8_peak": ops / ms / 1e9 / PEAK_INT8_TOPS,
+                              "gbs": byts / ms / 1e6, "frac_hbm_peak": byts / ms / 1e6 / PEAK_HBM_GBS}
+            del Aq, s_a, Y, gws
+        out[str(M)] = rec
+    del wsets
+    torch.cuda.empty_cache()
+    return {"workload": "W4A4 GEMMs of the LLaDA-shaped layer set, token counts 16 ... 16384, graph-replayed, "
+                        "4 rotating weight sets", "per_tokens": out}
 
 
 def tac_oproj_block(torch, sq, synth, dev, steps=5):
@@ -536,6 +579,8 @@ def main():
         out["small"] = small_token_block(torch, sq, synth, dev)
     if not args.no_large:
         out["tac_oproj"] = tac_oproj_block(torch, sq, synth, dev)
+    if not args.no_sweep:
+        out["sweep"] = sweep_block(torch, sq, synth, dev)
     if not args.no_calib:
         out["calib"] = tac_calibration_block(torch, sq, synth, dev)
 
@@ -620,6 +665,8 @@ def main():
         res["small_token"] = out["small"]
     if "tac_oproj" in out:
         res["tac_oproj"] = out["tac_oproj"]
+    if "sweep" in out:
+        res["token_sweep_gemm"] = out["sweep"]
     if "calib" in out:
         res["tac_calibration"] = out["calib"]
     if cpu:
