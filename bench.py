@@ -373,7 +373,8 @@ def tac_oproj_block(torch, sq, synth, dev, steps=5):
             "gemm_frac_int8_peak": 2.0 * M * N * K / g_ms / 1e9 / PEAK_INT8_TOPS,
             "roofline": {"bound": "alu", "achieved": tac_flop / tac_ms / 1e9, "peak": PEAK_FP32_VALU_TFLOPS,
                          "unit": "TFLOP/s", "frac": tac_flop / tac_ms / 1e9 / PEAK_FP32_VALU_TFLOPS,
-                         "traffic": None, "kernel": f"tac (g = {g})"}}
+                         "traffic": recorded_traffic("tac_g128") if g == 128 else None,
+                         "kernel": f"tac (g = {g})"}}
 
 
 def tac_calibration_block(torch, sq, synth, dev, N=8192, C=4096, reps=5):
@@ -656,7 +657,8 @@ def main():
             "value": M / (f["ms"] / 1e3), "unit": "tokens/s", "ms_per_step": f["ms"],
             "transform_ms": f["transform_ms"],
             "roofline": {"bound": "mfma", "achieved": f["transform_tflops"], "peak": PEAK_FP16_TFLOPS,
-                         "unit": "TFLOP/s", "frac": f["transform_tflops"] / PEAK_FP16_TFLOPS, "traffic": None,
+                         "unit": "TFLOP/s", "frac": f["transform_tflops"] / PEAK_FP16_TFLOPS,
+                         "traffic": recorded_traffic("transform_fast", "traffic_bytes_per_launch_step_avg"),
                          "kernel": "transform on the fp16 MFMA (hi + lo split: executes 2x the algorithmic flops)"},
             "codes_differing_from_fixed_order": f["code_flips"], "codes": f["codes"]}
     if "large" in out:
