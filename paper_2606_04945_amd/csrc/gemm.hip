@@ -20,9 +20,10 @@
 // one barrier per step.  LDS rows are XOR-swizzled by 16-byte chunk so the
 // fragment reads are free of bank conflicts; each wave unpacks the fragments it
 // reads.  Rows past M (or N) and the unused half of a last k step read as zero
-// through the buffer descriptors' range check.  Short M splits K across
-// workgroups; the int32 partial sums are then added exactly by a small kernel.
-// M <= 16 has a kernel of its own that streams the weights with no LDS.
+// through the buffer descriptors' range check.  Few tiles (M of 17 to a few
+// hundred) split K across workgroups; the int32 partial sums are then added
+// exactly by a small kernel.
+// M <= 16 has kernels of their own that stream the weights into registers.
 //
 // BITS = 8 is the W8A8 variant (App. D): codes are int8 already, so the same
 // tiles feed the MFMA straight from LDS with no unpacking and no scaling.
@@ -228,105 +229,194 @@ __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(OC
     epilogue();
 }
 
-// Short M (<= 16 tokens): the weights are streamed once and each is used by
-// at most 16 rows, so the kernel is bound by HBM bandwidth, not by the MFMA.  No
-// LDS and no barriers: each wave owns TN x 16 output columns and walks its K
-// range, loading its W rows and the (L2-resident) activation rows straight into
-// MFMA operand registers with raw buffer loads, U k steps in flight per batch;
-// an activation fragment serves TN weight fragments.  Lane (c, g) reads bytes
-// [16 g, 16 g + 16) of the 64-byte slice of row c (W) or of the activation row,
-// exactly as the tiled kernel's fragments.
-template <int TM, int U, bool SPLIT, int BITS = 4, int WPB = 1, int TN = 1>
-__global__ __launch_bounds__(64 * WPB) void gemm_skinny_kernel(const uint8_t* __restrict__ Aq,
-                                                               const float* __restrict__ s_a,
-                                                               const uint8_t* __restrict__ Wq,
-                                                               const float* __restrict__ s_w, int M, int N, int K,
-                                                               int ksteps_per_split, uint16_t* __restrict__ Y,
-                                                               int32_t* __restrict__ acc_out,
-                                                               int32_t* __restrict__ part) {
-    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+// Short M (<= 16 tokens): every weight is used by at most 16 rows, so these
+// kernels are bound by streaming the weights from HBM, not by the MFMA.  One
+// 16-row MFMA tile covers all the tokens; each wave owns 16 output columns and
+// loads its weight fragments straight into registers (lane (c, g) reads bytes
+// [16 g, 16 g + 16) of the 64-byte slice of row c, the tiled kernel's fragment
+// order).  The k offset of a load rides in the scalar offset, so issuing a load
+// costs no vector instruction; a ring of D batches of U k steps keeps D - 1
+// batches in flight while one is multiplied.  There is no branch between a
+// batch's loads and their use: a conditional exit there lets the compiler sink
+// the loads past the other batch's multiply, which serialises memory and MFMA.
+//
+// Zeros: k steps past the row read as zero weights (in-range row offset plus an
+// out-of-range scalar offset), and the activation bytes past the end of a row
+// (the second half of a last, half-filled k step) read as zero activations, so
+// a product that mixes in a neighbouring row's bytes is always a product with
+// zero.  Rows past M and columns past N are clamped to the last valid one and
+// their outputs are not stored.  The dequantisation scales are fetched while
+// the weights stream, so the epilogue waits on no load.
+
+// Scalar offset of k step kt: past the last step, one that no buffer reaches.
+__device__ __forceinline__ int step_offset(int kt, int nk) { return kt < nk ? kt * kKB : (int)kOOB; }
+
+// Epilogue of the short-M kernels: lane (c, g) holds rows 4 g .. 4 g + 3 of
+// output column col.
+template <int BITS>
+__device__ __forceinline__ void skinny_store(const v4i& acc, int lg, int col, int M, int N, const float (&sav)[4],
+                                             float swv, uint16_t* __restrict__ Y, int32_t* __restrict__ acc_out) {
+    if (col >= N) return;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int row = 4 * lg + r;
+        if (row >= M) continue;
+        const int v = acc_value<BITS>(acc[r]);
+        const size_t o = (size_t)row * N + col;
+        if (acc_out) acc_out[o] = v;
+        if (Y) Y[o] = f2h(((float)v * sav[r]) * swv);
+    }
+}
+
+// KW waves share one group of 16 columns and take turns over k, batch by batch
+// (wave w multiplies batches w, w + KW, ...); their partial sums meet in LDS.
+// Activation fragments come from global memory (they stay in L2: every
+// workgroup reads the same M x K codes).  The K split gives narrow layers
+// enough waves to keep HBM busy.
+template <int U, int KW, int BITS>
+__global__ __launch_bounds__(64 * KW) void gemm_skinny_kernel(const uint8_t* __restrict__ Aq,
+                                                              const float* __restrict__ s_a,
+                                                              const uint8_t* __restrict__ Wq,
+                                                              const float* __restrict__ s_w, int M, int N, int K,
+                                                              uint16_t* __restrict__ Y, int32_t* __restrict__ acc_out) {
+    constexpr int D = 2;
+    __shared__ v4i red[KW > 1 ? KW - 1 : 1][kWave];
+    const int lane = threadIdx.x % kWave, wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int lr = lane % 16, lg = lane / 16;
-    const int col0 = (blockIdx.x * WPB + wave) * 16 * TN;
-    if (col0 >= N) return;                                   // whole wave past N: nothing to do
+    const int col = blockIdx.x * 16 + lr;
     const uint32_t ldb = (uint32_t)K * BITS / 8;
-    const int nk_total = (int)((ldb + kKB - 1) / kKB);
-    const int kt0 = SPLIT ? blockIdx.z * ksteps_per_split : 0;
-    const int kt1 = SPLIT ? min(nk_total, kt0 + ksteps_per_split) : nk_total;
+    const int nk = (int)((ldb + kKB - 1) / kKB);
+    const int nb = (nk + U - 1) / U;
     const __amdgpu_buffer_rsrc_t rA = make_rsrc(Aq, (uint32_t)M * ldb);
     const __amdgpu_buffer_rsrc_t rW = make_rsrc(Wq, (uint32_t)N * ldb);
     const uint32_t seg = 16 * lg;
-    uint32_t ow[TN], oa[TM];
+    const uint32_t ow = (uint32_t)min(col, N - 1) * ldb + seg;
+    const uint32_t oa = (uint32_t)min(lr, M - 1) * ldb + seg;
+    const uint32_t alim = ldb > seg ? ldb - seg : 0;   // this lane's activation bytes end here
+    auto issue = [&](int b, v4i (&w)[U], v4i (&a)[U]) {
 #pragma unroll
-    for (int t = 0; t < TN; ++t) {
-        const int c = col0 + 16 * t + lr;
-        ow[t] = c < N ? (uint32_t)c * ldb + seg : kOOB;
+        for (int u = 0; u < U; ++u) {
+            const int kt = b * U + u;
+            const int so = step_offset(kt, nk);
+            w[u] = __builtin_amdgcn_raw_buffer_load_b128(rW, (int)ow, so, 0);
+            a[u] = __builtin_amdgcn_raw_buffer_load_b128(rA, (uint32_t)kt * kKB < alim ? (int)oa : (int)kOOB, so, 0);
+        }
+    };
+    v4i acc = v4i{0, 0, 0, 0};
+    auto compute = [&](const v4i (&w)[U], const v4i (&a)[U]) {
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int h = 0; h < (BITS == 4 ? 2 : 1); ++h)
+                acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(operand<BITS>(a[u], h), operand<BITS>(w[u], h), acc, 0,
+                                                            0, 0);
+    };
+    v4i w[D][U], a[D][U];
+    issue(wave, w[0], a[0]);
+    float sav[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) sav[r] = s_a[min(4 * lg + r, M - 1)];
+    const float swv = s_w[min(col, N - 1)];
+    int b = wave;
+    do {
+        issue(b + KW, w[1], a[1]);
+        __builtin_amdgcn_sched_barrier(0);
+        compute(w[0], a[0]);
+        __builtin_amdgcn_sched_barrier(0);
+        issue(b + 2 * KW, w[0], a[0]);
+        __builtin_amdgcn_sched_barrier(0);
+        compute(w[1], a[1]);
+        __builtin_amdgcn_sched_barrier(0);
+        b += 2 * KW;
+    } while (b < nb);
+    if (KW > 1) {
+        if (wave > 0) red[wave - 1][lane] = acc;
+        __syncthreads();
+        if (wave > 0) return;
+#pragma unroll
+        for (int r = 0; r < KW - 1; ++r) acc += red[r][lane];
     }
-#pragma unroll
-    for (int i = 0; i < TM; ++i) oa[i] = 16 * i + lr < M ? (uint32_t)(16 * i + lr) * ldb + seg : kOOB;
+    skinny_store<BITS>(acc, lg, col, M, N, sav, swv, Y, acc_out);
+}
 
-    v4i acc[TN][TM];
+// Wide layers, 4-bit codes: the workgroup's waves (blockDim.x / 64 of them)
+// each stream their own 16 columns, and the M x K activation codes are staged
+// once per workgroup in LDS, already expanded to MFMA operands
+// ([k step][half][lane][16 B]), instead of being fetched and expanded by every
+// wave.  Staging: a direct-to-LDS copy of the packed codes (zero past M and K),
+// then one expansion pass split over the waves.  The weight ring is issued
+// before the copy is waited on, so the first batches are already in flight.
+constexpr int kSharedU = 2, kSharedD = 4;
+constexpr int kSharedMaxSteps = 32;                 // K <= 4096: 96 KB of LDS
+constexpr int kSharedMaxWaves = 16;
+
+__global__ __launch_bounds__(64 * kSharedMaxWaves) void gemm_skinny_shared_kernel(
+    const uint8_t* __restrict__ Aq, const float* __restrict__ s_a, const uint8_t* __restrict__ Wq,
+    const float* __restrict__ s_w, int M, int N, int K, uint16_t* __restrict__ Y, int32_t* __restrict__ acc_out) {
+    constexpr int U = kSharedU, D = kSharedD;
+    extern __shared__ __attribute__((aligned(16))) uint8_t sm[];
+    const int nw = blockDim.x / kWave;
+    const int lane = threadIdx.x % kWave, wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int lr = lane % 16, lg = lane / 16;
+    const int col = (blockIdx.x * nw + wave) * 16 + lr;
+    const uint32_t ldb = (uint32_t)K / 2;
+    const int nk = (int)((ldb + kKB - 1) / kKB);
+    const int nb = (nk + U - 1) / U;
+    uint8_t* raw = sm;                   // nk x 1 KB: packed activation fragments
+    uint8_t* ops = sm + nk * 1024;       // nk x 2 KB: expanded operands
+    const u32x4 rA = sgpr_rsrc(Aq, (uint32_t)M * ldb);
+    const __amdgpu_buffer_rsrc_t rW = make_rsrc(Wq, (uint32_t)N * ldb);
+    const uint32_t seg = 16 * lg;
+    for (int s = wave; s < nk; s += nw) {
+        const uint32_t ko = (uint32_t)s * kKB;
+        dma16(rA, lds_addr(raw + s * 1024), (lr < M && ko + seg < ldb) ? (uint32_t)lr * ldb + ko + seg : kOOB);
+    }
+    const uint32_t ow = (uint32_t)min(col, N - 1) * ldb + seg;
+    auto issue = [&](int b, v4i (&w)[U]) {
 #pragma unroll
-    for (int t = 0; t < TN; ++t)
-#pragma unroll
-        for (int i = 0; i < TM; ++i) acc[t][i] = v4i{0, 0, 0, 0};
-    // two register batches of U k steps: batch b + 1 is in flight while batch b is
-    // multiplied (steps past the split or the row read as zeros)
-    auto issue = [&](int kb, v4i (&w)[U][TN], v4i (&a)[U][TM]) {
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const uint32_t ko = (uint32_t)(kb + u) * kKB;
-            const bool in = kb + u < kt1 && ko + seg < ldb;
-#pragma unroll
-            for (int t = 0; t < TN; ++t)
-                w[u][t] = __builtin_amdgcn_raw_buffer_load_b128(rW, (int)(in ? ow[t] + ko : kOOB), 0, 0);
-#pragma unroll
-            for (int i = 0; i < TM; ++i)
-                a[u][i] = __builtin_amdgcn_raw_buffer_load_b128(rA, (int)(in ? oa[i] + ko : kOOB), 0, 0);
-        }
+        for (int u = 0; u < U; ++u)
+            w[u] = __builtin_amdgcn_raw_buffer_load_b128(rW, (int)ow, step_offset(b * U + u, nk), 0);
     };
-    auto compute = [&](const v4i (&w)[U][TN], const v4i (&a)[U][TM]) {
+    v4i w[D][U];
+#pragma unroll
+    for (int d = 0; d < D - 1; ++d) issue(d, w[d]);
+    wait_vm<(D - 1) * U>();              // this wave's copies have landed (its weight loads may not have)
+    __builtin_amdgcn_s_barrier();        // ... and every wave's
+    asm volatile("" ::: "memory");
+    for (int s = wave; s < nk; s += nw) {
+        const v4i r = *reinterpret_cast<const v4i*>(raw + s * 1024 + lane * 16);
+        *reinterpret_cast<v4i*>(ops + (2 * s) * 1024 + lane * 16) = operand<4>(r, 0);
+        *reinterpret_cast<v4i*>(ops + (2 * s + 1) * 1024 + lane * 16) = operand<4>(r, 1);
+    }
+    __syncthreads();
+    float sav[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) sav[r] = s_a[min(4 * lg + r, M - 1)];
+    const float swv = s_w[min(col, N - 1)];
+    v4i acc = v4i{0, 0, 0, 0};
+    auto compute = [&](int b, const v4i (&wb)[U]) {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
+            const int kt = min(b * U + u, nk - 1);      // past the end the weights read as zero
 #pragma unroll
-            for (int h = 0; h < (BITS == 4 ? 2 : 1); ++h) {
-#pragma unroll
-                for (int i = 0; i < TM; ++i) {
-                    const v4i x = operand<BITS>(a[u][i], h);
-#pragma unroll
-                    for (int t = 0; t < TN; ++t)
-                        acc[t][i] = __builtin_amdgcn_mfma_i32_16x16x64_i8(x, operand<BITS>(w[u][t], h), acc[t][i], 0, 0, 0);
-                }
+            for (int h = 0; h < 2; ++h) {
+                const v4i x = *reinterpret_cast<const v4i*>(ops + (2 * kt + h) * 1024 + lane * 16);
+                acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(x, operand<4>(wb[u], h), acc, 0, 0, 0);
             }
         }
     };
-    v4i w0[U][TN], a0[U][TM], w1[U][TN], a1[U][TM];
-    issue(kt0, w0, a0);
-    for (int kb = kt0; kb < kt1; kb += 2 * U) {
-        issue(kb + U, w1, a1);
-        __builtin_amdgcn_sched_barrier(0);
-        compute(w0, a0);
-        if (kb + U >= kt1) break;
-        issue(kb + 2 * U, w0, a0);
-        __builtin_amdgcn_sched_barrier(0);
-        compute(w1, a1);
-    }
+    int b = 0;
+    do {
 #pragma unroll
-    for (int t = 0; t < TN; ++t) {
-        const int col = col0 + 16 * t + lr;
-        if (col >= N) continue;
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int row = 16 * i + 4 * lg + r;
-                if (row >= M) continue;
-                const int v = acc_value<BITS>(acc[t][i][r]);
-                if (SPLIT)
-                    part[((size_t)blockIdx.z * M + row) * N + col] = v;
-                else
-                    store_out(row, col, v, s_a, s_w, Y, acc_out, N);
-            }
-    }
+        for (int d = 0; d < D; ++d) {
+            issue(b + d + D - 1, w[(d + D - 1) % D]);
+            __builtin_amdgcn_sched_barrier(0);
+            compute(b + d, w[d]);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        b += D;
+    } while (b < nb);
+    skinny_store<4>(acc, lg, col, M, N, sav, swv, Y, acc_out);
 }
 
 // Adds the split-K partial sums (exact int32) and applies the epilogue.
@@ -344,10 +434,12 @@ __global__ __launch_bounds__(256) void splitk_epilogue(const int32_t* __restrict
 
 // A launch plan: tile shape and K split.
 struct Plan {
-    int cfg;       // 0: 256 x 128, 1: 128 x 128, 2: 64 x 64, 3 / 5: skinny, 4: 64 x 128 (see launch_gemm)
+    int cfg;       // 0: 256 x 128, 1: 128 x 128, 2: 64 x 64, 4: 64 x 128, 3: short M, K split in the
+                   // workgroup, 5: short M, activations shared in LDS (see launch_gemm)
     int bm, bn;
-    int splits;    // K split count actually used (1 = fused epilogue)
+    int splits;    // K split count across workgroups actually used (1 = fused epilogue)
     int per;       // k steps per split
+    int waves;     // cfg 3: waves sharing a column group over k; cfg 5: waves per workgroup
 };
 
 Plan make_plan(int M, int N, int K, int bm, int bn, int want_splits, int bits = 4) {
@@ -355,6 +447,7 @@ Plan make_plan(int M, int N, int K, int bm, int bn, int want_splits, int bits = 
     (void)N;
     Plan p;
     p.cfg = -1;
+    p.waves = 1;
     p.bm = bm;
     p.bn = bn;
     const int nk = (K * bits / 8 + kKB - 1) / kKB;
@@ -364,18 +457,26 @@ Plan make_plan(int M, int N, int K, int bm, int bn, int want_splits, int bits = 
     return p;
 }
 
-template <int TM, int U, int BITS = 4, int WPB = 1, int TN = 1>
-hipError_t launch_skinny(const Plan& p, const uint8_t* Aq, const float* s_a, const uint8_t* Wq, const float* s_w,
-                         int M, int N, int K, uint16_t* Y, int32_t* acc, int32_t* part, hipStream_t st) {
-    constexpr int CPB = 16 * WPB * TN;                 // columns per workgroup
-    dim3 grid((N + CPB - 1) / CPB, 1, p.splits);
-    if (p.splits == 1) {
-        hipLaunchKernelGGL((gemm_skinny_kernel<TM, U, false, BITS, WPB, TN>), grid, dim3(64 * WPB), 0, st, Aq, s_a,
-                           Wq, s_w, M, N, K, p.per, Y, acc, (int32_t*)nullptr);
-    } else {
-        hipLaunchKernelGGL((gemm_skinny_kernel<TM, U, true, BITS, WPB, TN>), grid, dim3(64 * WPB), 0, st, Aq, s_a,
-                           Wq, s_w, M, N, K, p.per, (uint16_t*)nullptr, (int32_t*)nullptr, part);
-    }
+template <int U, int KW, int BITS>
+hipError_t launch_skinny(const uint8_t* Aq, const float* s_a, const uint8_t* Wq, const float* s_w, int M, int N,
+                         int K, uint16_t* Y, int32_t* acc, hipStream_t st) {
+    hipLaunchKernelGGL((gemm_skinny_kernel<U, KW, BITS>), dim3((N + 15) / 16), dim3(64 * KW), 0, st, Aq, s_a, Wq, s_w,
+                       M, N, K, Y, acc);
+    return hipGetLastError();
+}
+
+hipError_t launch_skinny_shared(int waves, const uint8_t* Aq, const float* s_a, const uint8_t* Wq, const float* s_w,
+                                int M, int N, int K, uint16_t* Y, int32_t* acc, hipStream_t st) {
+    const int nk = (K / 2 + kKB - 1) / kKB;
+    const size_t lds = (size_t)nk * 3 * 1024;
+    static const hipError_t attr =     // above the 64 KB default for dynamic LDS
+        hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_skinny_shared_kernel),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, kSharedMaxSteps * 3 * 1024);
+    if (attr != hipSuccess) return attr;
+    if (nk > kSharedMaxSteps || waves < 1 || waves > kSharedMaxWaves) return hipErrorInvalidConfiguration;
+    const int groups = (N + 15) / 16;
+    hipLaunchKernelGGL(gemm_skinny_shared_kernel, dim3((groups + waves - 1) / waves), dim3(64 * waves), lds, st, Aq,
+                       s_a, Wq, s_w, M, N, K, Y, acc);
     return hipGetLastError();
 }
 
@@ -396,6 +497,17 @@ hipError_t launch_tiled(const Plan& p, const uint8_t* Aq, const float* s_a, cons
     return hipGetLastError();
 }
 
+template <int BITS>
+hipError_t skinny_kw(int kw, const uint8_t* Aq, const float* s_a, const uint8_t* Wq, const float* s_w, int M, int N,
+                     int K, uint16_t* Y, int32_t* acc, hipStream_t st) {
+    switch (kw) {
+        case 1: return launch_skinny<8, 1, BITS>(Aq, s_a, Wq, s_w, M, N, K, Y, acc, st);
+        case 2: return launch_skinny<8, 2, BITS>(Aq, s_a, Wq, s_w, M, N, K, Y, acc, st);
+        case 4: return launch_skinny<4, 4, BITS>(Aq, s_a, Wq, s_w, M, N, K, Y, acc, st);
+        default: return launch_skinny<4, 8, BITS>(Aq, s_a, Wq, s_w, M, N, K, Y, acc, st);
+    }
+}
+
 hipError_t finish_split(const Plan& p, int32_t* part, const float* s_a, const float* s_w, int M, int N, uint16_t* Y,
                         int32_t* acc, hipStream_t st) {
     if (p.splits == 1) return hipSuccess;
@@ -407,7 +519,8 @@ hipError_t finish_split(const Plan& p, int32_t* part, const float* s_a, const fl
 
 // The production plan (from measured sweeps on MI355X, graph-replayed with
 // rotating weights):
-//  - M <= 16: the skinny kernel (weight streaming, K split only for narrow N and long K);
+//  - M <= 16: the short-M kernels (weight streaming; activations shared in LDS
+//    for wide 4-bit layers, K split inside the workgroup otherwise);
 //  - at least 768 tiles of 256 x 128: 256 x 128 (eight waves of 64 x 64);
 //  - at least 512 tiles of 128 x 128: 128 x 128 (four waves of 64 x 64);
 //  - at least 512 tiles of 64 x 128: 64 x 128 (four waves of 64 x 32);
@@ -425,16 +538,21 @@ Plan choose_plan(int M, int N, int K, int bits) {
     };
     Plan p;
     if (M <= 16) {
-        // skinny kernel, one wave per workgroup: 32 columns per wave when that
-        // still gives at least 512 waves, else 16; K is split (up to 4 ways)
-        // only for few waves and long K
-        const bool wide = (N + 31) / 32 >= 512;
-        const int waves = (N + (wide ? 31 : 15)) / (wide ? 32 : 16);
-        int s = waves < 512 && nk >= 64 ? 4 : 1;
-        const int cap = nk / 16 > 1 ? nk / 16 : 1;     // keep two batches of 8 k steps per split
-        s = s < cap ? s : cap;
-        p = make_plan(M, N, K, 16, wide ? 32 : 16, s, bits);
-        p.cfg = wide ? 5 : 3;
+        // one wave per 16 columns.  Wide 4-bit layers with K <= 4096 share the
+        // staged activations among ceil(groups / 256) waves per workgroup (one
+        // workgroup per CU); the rest split K inside the workgroup, the more
+        // ways the fewer column groups there are, keeping two batches per wave
+        const int groups = (N + 15) / 16;
+        p = make_plan(M, N, K, 16, 16, 1, bits);
+        if (bits == 4 && groups >= 768 && nk <= kSharedMaxSteps) {
+            p.cfg = 5;
+            p.waves = (groups + 255) / 256 < kSharedMaxWaves ? (groups + 255) / 256 : kSharedMaxWaves;
+        } else {
+            int kw = groups >= 1024 ? 1 : groups >= 256 ? 2 : groups >= 128 ? 4 : 8;
+            while (kw > 1 && (nk + (kw <= 2 ? 8 : 4) - 1) / (kw <= 2 ? 8 : 4) < 2 * kw) kw /= 2;
+            p.cfg = 3;
+            p.waves = kw;
+        }
     } else if (tiles(256, 128) >= 768) {
         p = make_plan(M, N, K, 256, 128, 1, bits);
         p.cfg = 0;
@@ -465,8 +583,7 @@ hipError_t launch_gemm(const uint8_t* Aq, const float* s_a, const uint8_t* Wq, c
     hipError_t e;
     if (bits == 8) {
         switch (p.cfg) {
-            case 3: e = launch_skinny<1, 8, 8, 1, 1>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
-            case 5: e = launch_skinny<1, 4, 8, 1, 2>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
+            case 3: e = skinny_kw<8>(p.waves, Aq, s_a, Wq, s_w, M, N, K, Y, acc, st); break;
             case 0: e = launch_tiled<4, 2, 4, 4, 8, 2>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
             case 1: e = launch_tiled<2, 2, 4, 4, 8, 3>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
             case 2: e = launch_tiled<2, 2, 2, 2, 8, 4>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
@@ -474,8 +591,8 @@ hipError_t launch_gemm(const uint8_t* Aq, const float* s_a, const uint8_t* Wq, c
         }
     } else {
         switch (p.cfg) {
-            case 3: e = launch_skinny<1, 8, 4, 1, 1>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
-            case 5: e = launch_skinny<1, 4, 4, 1, 2>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
+            case 3: e = skinny_kw<4>(p.waves, Aq, s_a, Wq, s_w, M, N, K, Y, acc, st); break;
+            case 5: e = launch_skinny_shared(p.waves, Aq, s_a, Wq, s_w, M, N, K, Y, acc, st); break;
             case 0: e = launch_tiled<4, 2, 4, 4, 4, 2>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
             case 1: e = launch_tiled<2, 2, 4, 4, 4, 3>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
             case 2: e = launch_tiled<2, 2, 2, 2, 4, 4>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;

@@ -163,8 +163,13 @@ def _codes(M, K, seed, lo=-7, hi=7):
 # Shapes cover every launch plan with ragged edges: the skinny kernel with 16 and
 # 32 columns per wave (with and without a K split), 64 x 64 with a K split,
 # 64 x 128, 128 x 128 and 256 x 128 tiles, and k tails of half a step.
+# every launch plan: short M (activations shared in LDS: wide 4-bit layers with K <= 4096,
+# including a half last k step and a partial last workgroup; K split inside the
+# workgroup 1, 2, 4 or 8 ways), the tiled shapes and the split-K path
 GEMM_SHAPES = [(1, 8, 64), (16, 4096, 4096), (5, 4104, 4096), (9, 136, 192), (16, 24, 18944),
                (16, 12288, 4096), (16, 4096, 12288), (9, 16392, 192), (16, 32768, 256), (33, 520, 1024),
+               (16, 24576, 4096), (7, 37888, 3584), (3, 12304, 4032), (1, 12288, 64), (16, 16392, 8192),
+               (11, 2056, 4160),
                (77, 200, 192), (128, 256, 512), (300, 136, 4096), (300, 16384, 64), (1024, 1024, 1024),
                (1000, 8200, 64), (2100, 12296, 64), (513, 4104, 3584), (64, 512, 18944)]
 
@@ -236,17 +241,18 @@ def test_w8a8_gemm_at_the_largest_K():
 
 
 def test_gemm_split_and_unsplit_agree():
-    """Rows computed through the split-K path (short M) equal the same rows inside a
-    tall M that takes the single-pass path."""
+    """Rows computed through the split-K path (few tiles) and through the short-M
+    kernels equal the same rows inside a tall M that takes the single-pass path."""
     K, N = 12288, 4096
     Aq = _codes(2048, K, 7)
     Wq = _codes(N, K, 8)
     s_a = np.random.default_rng(9).uniform(0.1, 2, 2048).astype(np.float32)
     s_w = np.random.default_rng(10).uniform(1e-3, 2e-3, N).astype(np.float32)
-    assert sq.gemm_workspace_bytes(16, N, K) > 0 and sq.gemm_workspace_bytes(2048, N, K) == 0
+    assert sq.gemm_workspace_bytes(32, N, K) > 0 and sq.gemm_workspace_bytes(2048, N, K) == 0
     big = host(sq.w4a4_gemm(dev(Aq), dev(s_a), dev(Wq), dev(s_w)))
-    small = host(sq.w4a4_gemm(dev(Aq[:16]), dev(s_a[:16]), dev(Wq), dev(s_w)))
-    assert_bits(small, big[:16], "split vs unsplit")
+    for m in (32, 16):
+        small = host(sq.w4a4_gemm(dev(Aq[:m]), dev(s_a[:m]), dev(Wq), dev(s_w)))
+        assert_bits(small, big[:m], f"{m} rows vs the single-pass rows")
 
 
 # ------------------------------------------------------------------ TAC
