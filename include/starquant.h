@@ -231,6 +231,30 @@ int sgat_split_basis(const float* P, int32_t K, uint16_t* Ps, void* stream);
 int sgat_transform_fast(const uint16_t* X, const uint8_t* state, const uint16_t* Ps, int32_t M, int32_t K,
                         int32_t d_m, int32_t d_u, float* Xp, void* stream);
 
+/*
+ * int4 codes on the FP6 matrix cores: the same GEMM (Eq. 5 / Eq. 13) with both
+ * operands re-encoded as 6-bit floats.  In e3m2 (sign, 3 exponent bits with
+ * bias 3, 2 mantissa bits; OCP Microscaling Formats v1.0 FP6 E3M2) every code
+ * -8..7 is exact, products are integers of magnitude <= 64 and sums of up to
+ * 131072 of them are integers below 2^24, so the matrix cores' fp32
+ * accumulation is exact: acc and Y equal w4a4_gemm's bit for bit.
+ * Operand layout (A and W alike): per row, the K codes padded with zero codes to
+ * whole blocks of 128; block b takes 96 bytes at 96 b; chunk c of it (codes
+ * 128 b + 32 c .. + 31) is the 192-bit little-endian string with code j in bits
+ * 6 j .. 6 j + 5, its bytes 0..15 stored at 96 b + 16 c and bytes 16..23 at
+ * 96 b + 64 + 8 c.  Rows are sq_fp6_row_bytes(K) = 96 ceil(K / 128) bytes.
+ *   sq_fp6_row_bytes: bytes per operand row, 0 for an invalid K.
+ *   sq_codes_to_fp6:  codes [R][K/2] packed int4 (the sgat_* layout) in, out
+ *                     [R][sq_fp6_row_bytes(K)] (must not overlap codes); under 2 GiB.
+ *   w4a4_gemm_fp6:    A6 [M][row bytes], W6 [N][row bytes], s_a [M], s_w [N];
+ *                     Y [M][N] fp16 and / or acc [M][N] int32 out; N % 8 == 0;
+ *                     operands under 2 GiB; no workspace.
+ */
+size_t sq_fp6_row_bytes(int32_t K);
+int sq_codes_to_fp6(const uint8_t* codes, int32_t R, int32_t K, uint8_t* out, void* stream);
+int w4a4_gemm_fp6(const uint8_t* A6, const float* s_a, const uint8_t* W6, const float* s_w,
+                  int32_t M, int32_t N, int32_t K, uint16_t* Y, int32_t* acc, void* stream);
+
 size_t sq_tac_calibrate_workspace_bytes(int32_t N, int32_t C, int32_t g);
 int tac_calibrate(const uint16_t* Z_fp, const uint16_t* Z_q, int32_t N, int32_t C, int32_t g,
                   double rho, double eps, double eta, double alpha,

@@ -22,7 +22,8 @@ __all__ = ["sgat_prepare_weights", "sgat_transform", "sgat_quantize", "sgat_quan
            "tac_default_block", "default_band", "quant_act_workspace_bytes", "gemm_workspace_bytes",
            "prepare_weights_workspace_bytes", "StarQuantError", "lib",
            "sgat_prepare_weights_w8", "sgat_quantize_w8", "sgat_quant_act_w8", "w8a8_gemm",
-           "tac_calibrate", "tac_calibrate_workspace_bytes", "sgat_split_basis", "sgat_transform_fast"]
+           "tac_calibrate", "tac_calibrate_workspace_bytes", "sgat_split_basis", "sgat_transform_fast",
+           "fp6_row_bytes", "codes_to_fp6", "w4a4_gemm_fp6"]
 
 
 def _ptr(t: Optional[torch.Tensor]):
@@ -206,6 +207,48 @@ def w4a4_gemm(Aq: torch.Tensor, s_a: torch.Tensor, Wq: torch.Tensor, s_w: torch.
 
 def w8a8_gemm(Aq, s_a, Wq, s_w, **kw):
     return w4a4_gemm(Aq, s_a, Wq, s_w, bits=8, **kw)
+
+
+def fp6_row_bytes(K: int) -> int:
+    """Bytes per row of an FP6 operand of K codes (96 per block of 128)."""
+    n = int(lib().sq_fp6_row_bytes(K))
+    if n == 0:
+        raise ValueError(f"K={K}: need 64 <= K <= 131072 and K % 64 == 0")
+    return n
+
+
+def codes_to_fp6(codes: torch.Tensor, *, out=None, stream=None):
+    """Packed int4 codes [R, K/2] -> the FP6 (e3m2) operand layout [R, fp6_row_bytes(K)]."""
+    R, Kh = codes.shape
+    K = 2 * Kh
+    _need(codes, "codes", torch.uint8)
+    rb = fp6_row_bytes(K)
+    if out is None:
+        out = torch.empty((R, rb), dtype=torch.uint8, device=codes.device)
+    _need(out, "out", torch.uint8, (R, rb))
+    check(lib().sq_codes_to_fp6(_ptr(codes), R, K, _ptr(out), _stream(stream)))
+    return out
+
+
+def w4a4_gemm_fp6(A6: torch.Tensor, s_a: torch.Tensor, W6: torch.Tensor, s_w: torch.Tensor, K: int, *, Y=None,
+                  acc=None, want_Y: bool = True, want_acc: bool = False, stream=None):
+    """The W4A4 GEMM (Eq. 13) on FP6 operands (codes_to_fp6 layout) and the FP6
+    matrix cores; bit-identical to w4a4_gemm.  Returns Y, or (Y, acc)."""
+    M, N = A6.shape[0], W6.shape[0]
+    rb = fp6_row_bytes(K)
+    _need(A6, "A6", torch.uint8, (M, rb))
+    _need(W6, "W6", torch.uint8, (N, rb))
+    _need(s_a, "s_a", torch.float32, (M,))
+    _need(s_w, "s_w", torch.float32, (N,))
+    if Y is None and want_Y:
+        Y = torch.empty((M, N), dtype=torch.float16, device=A6.device)
+    if acc is None and want_acc:
+        acc = torch.empty((M, N), dtype=torch.int32, device=A6.device)
+    _need(Y, "Y", torch.float16, (M, N), optional=True)
+    _need(acc, "acc", torch.int32, (M, N), optional=True)
+    check(lib().w4a4_gemm_fp6(_ptr(A6), _ptr(s_a), _ptr(W6), _ptr(s_w), M, N, K, _ptr(Y), _ptr(acc),
+                              _stream(stream)))
+    return (Y, acc) if want_acc else Y
 
 
 def tac_apply(Z: torch.Tensor, tac_M: torch.Tensor, tac_d: torch.Tensor, g: int, *, out=None, stream=None):

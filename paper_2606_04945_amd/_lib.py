@@ -32,6 +32,9 @@ SIGNATURES = {
     "w8a8_gemm": (ctypes.c_int, [_p, _p, _p, _p, _i32, _i32, _i32, _p, _p, _p, _sz, _p]),
     "sgat_split_basis": (ctypes.c_int, [_p, _i32, _p, _p]),
     "sgat_transform_fast": (ctypes.c_int, [_p, _p, _p, _i32, _i32, _i32, _i32, _p, _p]),
+    "sq_fp6_row_bytes": (_sz, [_i32]),
+    "sq_codes_to_fp6": (ctypes.c_int, [_p, _i32, _i32, _p, _p]),
+    "w4a4_gemm_fp6": (ctypes.c_int, [_p, _p, _p, _p, _i32, _i32, _i32, _p, _p, _p]),
     "sq_tac_calibrate_workspace_bytes": (_sz, [_i32, _i32, _i32]),
     "tac_calibrate": (ctypes.c_int, [_p, _p, _i32, _i32, _i32, ctypes.c_double, ctypes.c_double, ctypes.c_double,
                                      ctypes.c_double, _p, _p, _p, _p, _p, _sz, _p]),

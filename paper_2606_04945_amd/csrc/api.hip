@@ -272,6 +272,43 @@ int tac_apply(const uint16_t* Z, const uint16_t* tac_M, const uint16_t* tac_d, i
     return hip_status(sq::launch_tac(Z, tac_M, tac_d, M, C, g, Z_out, static_cast<hipStream_t>(stream)), "tac");
 }
 
+size_t sq_fp6_row_bytes(int32_t K) {
+    if (K < 64 || K > 131072 || K % 64) return 0;
+    return sq::fp6_row_bytes(K);
+}
+
+int sq_codes_to_fp6(const uint8_t* codes, int32_t R, int32_t K, uint8_t* out, void* stream) {
+    SQ_TRY(check_K(K));
+    SQ_REQUIRE(R >= 0, SQ_ERR_SHAPE, "sq_codes_to_fp6: R=%d < 0", R);
+    SQ_REQUIRE((size_t)R * sq::fp6_row_bytes(K) < (1u << 31), SQ_ERR_SHAPE,
+               "sq_codes_to_fp6: the FP6 operand must be under 2 GiB (R=%d K=%d)", R, K);
+    if (R == 0) return SQ_OK;
+    SQ_REQUIRE(codes && out, SQ_ERR_NULL, "sq_codes_to_fp6: codes and out are required");
+    SQ_REQUIRE(aligned16(codes) && aligned16(out), SQ_ERR_ALIGN, "sq_codes_to_fp6: pointers must be 16-byte aligned");
+    const uintptr_t a0 = (uintptr_t)codes, a1 = a0 + (size_t)R * K / 2;
+    const uintptr_t b0 = (uintptr_t)out, b1 = b0 + (size_t)R * sq::fp6_row_bytes(K);
+    SQ_REQUIRE(a1 <= b0 || b1 <= a0, SQ_ERR_SHAPE, "sq_codes_to_fp6: out overlaps codes");
+    return hip_status(sq::launch_codes_to_fp6(codes, R, K, out, static_cast<hipStream_t>(stream)), "codes_to_fp6");
+}
+
+int w4a4_gemm_fp6(const uint8_t* A6, const float* s_a, const uint8_t* W6, const float* s_w, int32_t M, int32_t N,
+                  int32_t K, uint16_t* Y, int32_t* acc, void* stream) {
+    SQ_TRY(check_K(K));
+    SQ_REQUIRE(M >= 0 && N >= 0, SQ_ERR_SHAPE, "M=%d N=%d: need >= 0", M, N);
+    SQ_REQUIRE(N % 8 == 0, SQ_ERR_SHAPE, "N=%d: need N %% 8 == 0", N);
+    const size_t rb = sq::fp6_row_bytes(K);
+    SQ_REQUIRE((size_t)M * rb < (1u << 31) && (size_t)N * rb < (1u << 31), SQ_ERR_SHAPE,
+               "w4a4_gemm_fp6: each operand must be under 2 GiB (M=%d N=%d K=%d)", M, N, K);
+    if (M == 0 || N == 0) return SQ_OK;
+    SQ_REQUIRE(A6 && s_a && W6 && s_w && (Y || acc), SQ_ERR_NULL,
+               "w4a4_gemm_fp6: A6, s_a, W6, s_w and one of Y / acc are required");
+    SQ_REQUIRE(aligned16(A6) && aligned16(s_a) && aligned16(W6) && aligned16(s_w) && aligned16(Y) &&
+                   aligned16(acc),
+               SQ_ERR_ALIGN, "w4a4_gemm_fp6: pointers must be 16-byte aligned");
+    return hip_status(sq::launch_gemm_fp6(A6, s_a, W6, s_w, M, N, K, Y, acc, static_cast<hipStream_t>(stream)),
+                      "gemm_fp6");
+}
+
 size_t sq_tac_calibrate_workspace_bytes(int32_t N, int32_t C, int32_t g) {
     if (N <= 0 || C < 64 || C % 64 || g < 1 || g > 128 || (g & (g - 1)) || C % g) return 0;
     return sq::tac_calib_workspace_bytes(N, C, g);

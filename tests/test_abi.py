@@ -157,3 +157,23 @@ def test_tac_calibrate_validates(lib):
     need = lib.sq_tac_calibrate_workspace_bytes(8, 64, 16)
     assert lib.tac_calibrate(FAKE, FAKE, 8, 64, 16, *ok, FAKE, FAKE, None, None, FAKE, need - 1, None) \
         == L.SQ_ERR_WORKSPACE
+
+
+def test_fp6_entry_points_validate(lib):
+    assert lib.sq_fp6_row_bytes(64) == 96 and lib.sq_fp6_row_bytes(128) == 96
+    assert lib.sq_fp6_row_bytes(3584) == 96 * 28 and lib.sq_fp6_row_bytes(4160) == 96 * 33
+    assert lib.sq_fp6_row_bytes(100) == 0 and lib.sq_fp6_row_bytes(0) == 0
+    # K, N % 8, NULL, alignment
+    assert lib.w4a4_gemm_fp6(FAKE, FAKE, FAKE, FAKE, 4, 16, 100, FAKE, None, None) == L.SQ_ERR_SHAPE
+    assert lib.w4a4_gemm_fp6(FAKE, FAKE, FAKE, FAKE, 4, 12, 128, FAKE, None, None) == L.SQ_ERR_SHAPE
+    assert lib.w4a4_gemm_fp6(FAKE, FAKE, FAKE, FAKE, 4, 16, 128, None, None, None) == L.SQ_ERR_NULL
+    assert lib.w4a4_gemm_fp6(FAKE + 8, FAKE, FAKE, FAKE, 4, 16, 128, FAKE, None, None) == L.SQ_ERR_ALIGN
+    assert lib.w4a4_gemm_fp6(None, None, None, None, 0, 16, 128, None, None, None) == L.SQ_OK
+    # operands over 2 GiB
+    assert lib.w4a4_gemm_fp6(FAKE, FAKE, FAKE, FAKE, 1 << 20, 16, 4096, FAKE, None, None) == L.SQ_ERR_SHAPE
+    # conversion: K, NULL, alignment, overlap
+    assert lib.sq_codes_to_fp6(FAKE, 4, 96, FAKE + (1 << 20), None) == L.SQ_ERR_SHAPE
+    assert lib.sq_codes_to_fp6(None, 4, 128, FAKE, None) == L.SQ_ERR_NULL
+    assert lib.sq_codes_to_fp6(FAKE, 4, 128, FAKE + 8, None) == L.SQ_ERR_ALIGN
+    assert lib.sq_codes_to_fp6(FAKE, 4, 128, FAKE + 64, None) == L.SQ_ERR_SHAPE
+    assert lib.sq_codes_to_fp6(None, 0, 128, None, None) == L.SQ_OK

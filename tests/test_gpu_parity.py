@@ -160,9 +160,6 @@ def _codes(M, K, seed, lo=-7, hi=7):
     return pack_codes(q)
 
 
-# Shapes cover every launch plan with ragged edges: the skinny kernel with 16 and
-# 32 columns per wave (with and without a K split), 64 x 64 with a K split,
-# 64 x 128, 128 x 128 and 256 x 128 tiles, and k tails of half a step.
 # every launch plan: short M (activations shared in LDS: wide 4-bit layers with K <= 4096,
 # including a half last k step and a partial last workgroup; K split inside the
 # workgroup 1, 2, 4 or 8 ways), the tiled shapes and the split-K path
