@@ -99,6 +99,17 @@ class Timer:
         self.pairs = {}
 
 
+LLC_DEFEAT_BYTES = 800 << 20     # weight copies cycled per timing: over 3x the 256 MB last-level cache
+
+
+def rotating_copies(Wq, s_w, floor=4):
+    """(Wq, s_w) followed by enough clones that one pass over them streams at
+    least LLC_DEFEAT_BYTES, so that no call finds its weights in the last-level
+    cache."""
+    n = max(floor, -(-LLC_DEFEAT_BYTES // (Wq.numel() * Wq.element_size() + s_w.numel() * 4)))
+    return [(Wq, s_w)] + [(Wq.clone(), s_w.clone()) for _ in range(n - 1)]
+
+
 def graph_ms(torch, fn, calls, replays=5):
     """Median milliseconds per call of fn(i), i = 0 .. calls - 1, captured back to
     back in one HIP graph, so that no host work sits between the launches."""
@@ -196,10 +207,11 @@ def large_token_block(torch, sq, synth, dev, steps, warmup):
     return out
 
 
-def small_token_block(torch, sq, synth, dev, token_counts=(16, 32, 64), copies=4):
+def small_token_block(torch, sq, synth, dev, token_counts=(16, 32, 64), copies=8):
     """Denoising-step layer sets at small token counts (LLaDA shapes, step 32 of
     64, folded P), captured in a HIP graph.  `copies` rotating sets of prepared
-    weights (4 x 108 MB) keep the 256 MB last-level cache from serving them.
+    weights (8 x 108 MB) keep the 256 MB last-level cache from serving them; each
+    GEMM timed on its own cycles through at least 800 MB of its weights.
     Bytes are the algorithmic HBM traffic: fp16 activations read once, codes
     written and read once, the packed weights and scales, the fp16 outputs."""
     cfg = synth.CONFIGS[4]
@@ -262,10 +274,11 @@ def small_token_block(torch, sq, synth, dev, token_counts=(16, 32, 64), copies=4
                "graph_matches_eager": same, "gemm": {}}
         for si, d in enumerate(sites):
             qa(d)
-            gms, g = graph_ms(torch, lambda i, d=d, si=si: sq.w4a4_gemm(d["Aq"], d["s_a"], wsets[i % copies][si][0],
-                                                                        wsets[i % copies][si][1], Y=d["Y"],
-                                                                        ws=d["gws"]), 4 * copies)
-            del g
+            rot = rotating_copies(*wsets[0][si])
+            gms, g = graph_ms(torch, lambda i, d=d, rot=rot: sq.w4a4_gemm(d["Aq"], d["s_a"], rot[i % len(rot)][0],
+                                                                          rot[i % len(rot)][1], Y=d["Y"],
+                                                                          ws=d["gws"]), 2 * len(rot))
+            del g, rot
             rec["gemm"][d["name"]] = {"us": gms * 1e3, "gbs": d["gemm_bytes"] / gms / 1e6,
                                       "frac_hbm_peak": d["gemm_bytes"] / gms / 1e6 / PEAK_HBM_GBS}
         out[str(M)] = rec
@@ -274,7 +287,7 @@ def small_token_block(torch, sq, synth, dev, token_counts=(16, 32, 64), copies=4
             dom_rec = (dn, rec["gemm"][dn])
         del sites
     res = {"workload": "LLaDA-8B-shaped layer set at 16, 32 and 64 tokens (denoising step 32 of 64), folded P, "
-                       "HIP-graph replay, 4 rotating weight sets",
+                       "HIP-graph replay, 8 rotating weight sets (per-GEMM timings: >= 800 MB of rotating weights)",
            "per_tokens": out}
     if dom_rec:
         dn, r = dom_rec
@@ -287,7 +300,7 @@ def small_token_block(torch, sq, synth, dev, token_counts=(16, 32, 64), copies=4
     return res
 
 
-def sweep_block(torch, sq, synth, dev, token_counts=(16, 64, 256, 1024, 4096, 16384), copies=4):
+def sweep_block(torch, sq, synth, dev, token_counts=(16, 64, 256, 1024, 4096, 16384), copies=1):
     """Denoising-step sweep over token counts (LLaDA shapes, step 32 of 64, folded P):
     the W4A4 GEMM of every linear, graph-replayed with rotating weights, as
     achieved TOP/s and algorithmic GB/s, from memory-bound to compute-bound."""
@@ -303,6 +316,7 @@ def sweep_block(torch, sq, synth, dev, token_counts=(16, 64, 256, 1024, 4096, 16
             wsets[c].append((Wq.clone(), s_w.clone()))
         meta.append(site)
         del t, Wq, s_w
+    rots = [rotating_copies(*wsets[0][si]) for si in range(len(meta))]
     out = {}
     for M in token_counts:
         rec = {}
@@ -313,9 +327,10 @@ def sweep_block(torch, sq, synth, dev, token_counts=(16, 64, 256, 1024, 4096, 16
             s_a = (torch.rand(M, generator=g) + 0.5).to(dev)
             Y = torch.empty((M, N), dtype=torch.float16, device=dev)
             gws = torch.empty(max(sq.gemm_workspace_bytes(M, N, K), 1), dtype=torch.uint8, device=dev)
-            calls = 4 * copies if M <= 1024 else copies
-            ms, gr = graph_ms(torch, lambda i: sq.w4a4_gemm(Aq, s_a, wsets[i % copies][si][0],
-                                                            wsets[i % copies][si][1], Y=Y, ws=gws), calls)
+            rot = rots[si]
+            calls = 2 * len(rot) if M <= 1024 else len(rot)
+            ms, gr = graph_ms(torch, lambda i: sq.w4a4_gemm(Aq, s_a, rot[i % len(rot)][0],
+                                                            rot[i % len(rot)][1], Y=Y, ws=gws), calls)
             del gr
             ops = 2.0 * M * N * K
             byts = N * K // 2 + N * 4 + M * K // 2 + M * 4 + M * N * 2
@@ -323,10 +338,10 @@ def sweep_block(torch, sq, synth, dev, token_counts=(16, 64, 256, 1024, 4096, 16
                               "gbs": byts / ms / 1e6, "frac_hbm_peak": byts / ms / 1e6 / PEAK_HBM_GBS}
             del Aq, s_a, Y, gws
         out[str(M)] = rec
-    del wsets
+    del wsets, rots
     torch.cuda.empty_cache()
     return {"workload": "W4A4 GEMMs of the LLaDA-shaped layer set, token counts 16 ... 16384, graph-replayed, "
-                        "4 rotating weight sets", "per_tokens": out}
+                        ">= 800 MB of rotating weights per GEMM", "per_tokens": out}
 
 
 def tac_oproj_block(torch, sq, synth, dev, steps=5):
@@ -453,9 +468,12 @@ def main():
             K, N = d["K"], d["N"]
             d["Aq8"] = torch.empty((M, K), dtype=torch.int8, device=dev)
             d["gws8"] = torch.empty(max(sq.gemm_workspace_bytes(M, N, K, 8), 1), dtype=torch.uint8, device=dev)
-    # three rotating copies of the prepared weights for the folded-basis run, so
-    # that the 256 MB MALL cannot hold a whole layer set's weights between steps
-    wcopies = [[(d["Wq"].clone(), d["s_w"].clone()) for d in sites] for _ in range(3)]
+    # rotating copies of the prepared weights for the folded-basis runs (8 x 108 MB
+    # of 4-bit, 4 x 216 MB of 8-bit codes), so that the 256 MB last-level cache
+    # cannot hold a layer set's weights from one step to the next
+    wcopies = [[(d["Wq"].clone(), d["s_w"].clone()) for d in sites] for _ in range(8)]
+    w8copies = ([[(d["Wq8"].clone(), d["s_w8"].clone()) for d in sites] for _ in range(4)]
+                if not args.no_w8 else [])
     torch.cuda.synchronize()
     timer = Timer(torch)
 
@@ -494,13 +512,13 @@ def main():
                     lambda: sq.w4a4_gemm(d["Aq"], d["s_a"], Wq, s_w, Y=d["Y"], ws=d["gws"]))
 
     def step_w8(tm, it):
-        for d in sites:
+        for d, (Wq8, s_w8) in zip(sites, w8copies[it % len(w8copies)]):
             tm.wrap("quant_act8/" + d["site"].name,
                     lambda: sq.sgat_quant_act_w8(d["X"], state, None, d["dm"], d["du"], d.get("tac_M"),
                                                  d.get("tac_d"), d.get("g", 0), Aq=d["Aq8"], s_a=d["s_a"],
                                                  ws=d["qws"]))
             tm.wrap("gemm8/" + d["site"].name,
-                    lambda: sq.w8a8_gemm(d["Aq8"], d["s_a"], d["Wq8"], d["s_w8"], Y=d["Y"], ws=d["gws8"]))
+                    lambda: sq.w8a8_gemm(d["Aq8"], d["s_a"], Wq8, s_w8, Y=d["Y"], ws=d["gws8"]))
 
     def run(step, steps, warmup):
         for i in range(warmup):
