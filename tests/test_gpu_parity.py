@@ -162,11 +162,12 @@ def _codes(M, K, seed, lo=-7, hi=7):
 
 # every launch plan: short M (activations shared in LDS: wide 4-bit layers with K <= 4096,
 # including a half last k step and a partial last workgroup; K split inside the
-# workgroup 1, 2, 4 or 8 ways), the tiled shapes and the split-K path
+# workgroup 1, 2, 4 or 8 ways), the tiled shapes with ragged last tiles and the
+# split-K path
 GEMM_SHAPES = [(1, 8, 64), (16, 4096, 4096), (5, 4104, 4096), (9, 136, 192), (16, 24, 18944),
                (16, 12288, 4096), (16, 4096, 12288), (9, 16392, 192), (16, 32768, 256), (33, 520, 1024),
                (16, 24576, 4096), (7, 37888, 3584), (3, 12304, 4032), (1, 12288, 64), (16, 16392, 8192),
-               (11, 2056, 4160),
+               (11, 2056, 4160), (4096, 8200, 192), (4096, 8200, 4160),
                (77, 200, 192), (128, 256, 512), (300, 136, 4096), (300, 16384, 64), (1024, 1024, 1024),
                (1000, 8200, 64), (2100, 12296, 64), (513, 4104, 3584), (64, 512, 18944)]
 
