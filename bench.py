@@ -33,6 +33,7 @@ sys.path.insert(0, ROOT)
 PEAK_HBM_GBS = 8000.0
 PEAK_INT8_TOPS = 5000.0           # dense int8 MFMA, TOP/s
 PEAK_FP16_TFLOPS = 2500.0         # dense fp16 MFMA, TFLOP/s
+PEAK_FP6_TFLOPS = 10100.0         # dense FP6 / FP4 MFMA, TFLOP/s
 # fp32 FMA on the VALU without packed-fp32 instructions (the library is built
 # without them): 256 CU x 4 SIMD x 16 lanes x 2 flop x 2.4 GHz
 PEAK_FP32_VALU_TFLOPS = 78.6
@@ -193,6 +194,7 @@ def large_token_block(torch, sq, synth, dev, steps, warmup):
         tot_ops += ops
         tot_ms += gms
     dom = max(per, key=lambda n: per[n]["gemm_us"])
+    fp6 = fp6_variant(torch, sq, sites, state, M, steps, warmup)
     out = {"workload": "Dream-7B-shaped SGAT layer set (QKV 3584->4608, O+TAC 3584->3584, gate+up 3584->37888, "
                        "down 18944->3584), 8 x 2048 tokens, folded P",
            "tokens": M, "ms_per_step": ms, "tokens_per_s": M / (ms / 1e3),
@@ -201,10 +203,63 @@ def large_token_block(torch, sq, synth, dev, steps, warmup):
            "roofline": {"bound": "mfma", "achieved": per[dom]["tops"], "peak": PEAK_INT8_TOPS, "unit": "TOP/s",
                         "frac": per[dom]["frac_int8_peak"],
                         "traffic": recorded_traffic("gemm_large") if dom == "gate_up" else None,
-                        "kernel": f"w4a4 gemm ({dom})"}}
+                        "kernel": f"w4a4 gemm ({dom})"},
+           "fp6": fp6}
     del sites
     torch.cuda.empty_cache()
     return out
+
+
+def fp6_variant(torch, sq, sites, state, M, steps, warmup):
+    """The same layer set with the codes carried as e3m2 on the FP6 matrix cores:
+    per linear the gate + int4 quantiser, the conversion of the activation codes
+    to the FP6 operand layout, and the GEMM on FP6 operands (weights converted
+    once, offline).  Its outputs are checked equal to the int4 path's."""
+    ref = {d["name"]: d["Y"].clone() for d in sites}
+    for d in sites:
+        d["W6"] = sq.codes_to_fp6(d["Wq"])
+        d["A6"] = torch.empty((M, sq.fp6_row_bytes(d["K"])), dtype=torch.uint8, device=d["Aq"].device)
+        d["Y6"] = torch.empty_like(d["Y"])
+    timer = Timer(torch)
+
+    def step(tm):
+        for d in sites:
+            tm.wrap("q/" + d["name"], lambda: sq.sgat_quant_act(d["X"], state, None, d["dm"], d["du"], d.get("tac_M"),
+                                                                 d.get("tac_d"), d.get("g", 0), Aq=d["Aq"],
+                                                                 s_a=d["s_a"], ws=d["qws"]))
+            tm.wrap("c/" + d["name"], lambda: sq.codes_to_fp6(d["Aq"], out=d["A6"]))
+            tm.wrap("g/" + d["name"], lambda: sq.w4a4_gemm_fp6(d["A6"], d["s_a"], d["W6"], d["s_w"], d["K"],
+                                                                Y=d["Y6"]))
+    for _ in range(warmup):
+        step(Timer(torch))
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        step(timer)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    per, tot_ops, tot_ms = {}, 0.0, 0.0
+    for d in sites:
+        gms = timer.ms("g/" + d["name"])[0] / steps
+        ops = 2.0 * M * d["N"] * d["K"]
+        per[d["name"]] = {"gemm_us": gms * 1e3, "tops": ops / gms / 1e9,
+                          "frac_fp6_peak": ops / gms / 1e9 / PEAK_FP6_TFLOPS,
+                          "frac_int8_peak": ops / gms / 1e9 / PEAK_INT8_TOPS,
+                          "convert_us": timer.ms("c/" + d["name"])[0] / steps * 1e3}
+        tot_ops += ops
+        tot_ms += gms
+    same = all(torch.equal(ref[d["name"]], d["Y6"]) for d in sites)
+    dom = max(per, key=lambda n: per[n]["gemm_us"])
+    for d in sites:
+        del d["W6"], d["A6"], d["Y6"]
+    return {"ms_per_step": ms, "tokens_per_s": M / (ms / 1e3), "gemm_tops": tot_ops / tot_ms / 1e9,
+            "per_site": per, "outputs_equal_int4_path": same,
+            "roofline": {"bound": "mfma", "achieved": per[dom]["tops"], "peak": PEAK_FP6_TFLOPS, "unit": "TFLOP/s",
+                         "frac": per[dom]["frac_fp6_peak"], "traffic": None,
+                         "kernel": f"w4a4 gemm on FP6 operands ({dom})"}}
 
 
 def small_token_block(torch, sq, synth, dev, token_counts=(16, 32, 64), copies=8):
