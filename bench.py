@@ -195,6 +195,8 @@ def large_token_block(torch, sq, synth, dev, steps, warmup):
         tot_ms += gms
     dom = max(per, key=lambda n: per[n]["gemm_us"])
     fp6 = fp6_variant(torch, sq, sites, state, M, steps, warmup)
+    for d in sites:      # context: the vendor library's int8 GEMM (torch._int_mm) at the same shape
+        per[d["name"]]["vendor_int8_gemm_us"] = vendor_int8_us(torch, M, d["N"], d["K"], d["X"].device)
     out = {"workload": "Dream-7B-shaped SGAT layer set (QKV 3584->4608, O+TAC 3584->3584, gate+up 3584->37888, "
                        "down 18944->3584), 8 x 2048 tokens, folded P",
            "tokens": M, "ms_per_step": ms, "tokens_per_s": M / (ms / 1e3),
@@ -208,6 +210,29 @@ def large_token_block(torch, sq, synth, dev, steps, warmup):
     del sites
     torch.cuda.empty_cache()
     return out
+
+
+def vendor_int8_us(torch, M, N, K, dev, reps=5):
+    """Microseconds per call of the vendor library's int8 GEMM (torch._int_mm,
+    int32 out) on int8 operands of the same shape: a reference point only."""
+    g = torch.Generator(device="cpu").manual_seed(M + N + K)
+    A = torch.randint(-8, 8, (M, K), dtype=torch.int8, generator=g).to(dev)
+    B = torch.randint(-8, 8, (N, K), dtype=torch.int8, generator=g).to(dev)
+    try:
+        torch._int_mm(A, B.t())
+    except (RuntimeError, AttributeError):
+        return None
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        torch._int_mm(A, B.t())
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) / reps * 1e3
+    del A, B
+    return us
 
 
 def fp6_variant(torch, sq, sites, state, M, steps, warmup):
