@@ -78,7 +78,7 @@ size_t sq_quant_act_workspace_bytes(int32_t M, int32_t K, int32_t has_P, int32_t
 size_t sq_prepare_weights_workspace_bytes(int32_t N, int32_t K, int32_t has_P);
 
 /* Device workspace, in bytes, that w4a4_gemm needs for this shape (split-K
- * partial sums for short M); 0 means ws may be NULL. */
+ * partial sums when few output tiles meet a long K); 0 means ws may be NULL. */
 size_t sq_gemm_workspace_bytes(int32_t M, int32_t N, int32_t K);
 
 /* The same for w8a8_gemm. */

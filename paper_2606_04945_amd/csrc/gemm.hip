@@ -23,7 +23,7 @@
 // through the buffer descriptors' range check.  Few tiles (M of 17 to a few
 // hundred) split K across workgroups; the int32 partial sums are then added
 // exactly by a small kernel.
-// M <= 16 has kernels of their own that stream the weights into registers.
+// M <= 48 has kernels of their own that stream the weights into registers.
 //
 // BITS = 8 is the W8A8 variant (App. D): codes are int8 already, so the same
 // tiles feed the MFMA straight from LDS with no unpacking and no scaling.
@@ -251,15 +251,16 @@ __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(OC
 // Scalar offset of k step kt: past the last step, one that no buffer reaches.
 __device__ __forceinline__ int step_offset(int kt, int nk) { return kt < nk ? kt * kKB : (int)kOOB; }
 
-// Epilogue of the short-M kernels: lane (c, g) holds rows 4 g .. 4 g + 3 of
+// Epilogue of the short-M kernels: lane (c, g) holds rows row0 + 4 g .. + 3 of
 // output column col.
 template <int BITS>
-__device__ __forceinline__ void skinny_store(const v4i& acc, int lg, int col, int M, int N, const float (&sav)[4],
-                                             float swv, uint16_t* __restrict__ Y, int32_t* __restrict__ acc_out) {
+__device__ __forceinline__ void skinny_store(const v4i& acc, int row0, int lg, int col, int M, int N,
+                                             const float (&sav)[4], float swv, uint16_t* __restrict__ Y,
+                                             int32_t* __restrict__ acc_out) {
     if (col >= N) return;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-        const int row = 4 * lg + r;
+        const int row = row0 + 4 * lg + r;
         if (row >= M) continue;
         const int v = acc_value<BITS>(acc[r]);
         const size_t o = (size_t)row * N + col;
@@ -268,19 +269,24 @@ __device__ __forceinline__ void skinny_store(const v4i& acc, int lg, int col, in
     }
 }
 
+// Short-M kernels cover M <= 16 TM tokens with TM row tiles of 16, TM <= 3: at
+// four row tiles the activation unpacking outweighs what the kernels save over
+// the tiled one.
+constexpr int kShortMaxTiles = 3;
+
 // KW waves share one group of 16 columns and take turns over k, batch by batch
 // (wave w multiplies batches w, w + KW, ...); their partial sums meet in LDS.
 // Activation fragments come from global memory (they stay in L2: every
 // workgroup reads the same M x K codes).  The K split gives narrow layers
 // enough waves to keep HBM busy.
-template <int U, int KW, int BITS>
+template <int U, int KW, int TM, int BITS>
 __global__ __launch_bounds__(64 * KW) void gemm_skinny_kernel(const uint8_t* __restrict__ Aq,
                                                               const float* __restrict__ s_a,
                                                               const uint8_t* __restrict__ Wq,
                                                               const float* __restrict__ s_w, int M, int N, int K,
                                                               uint16_t* __restrict__ Y, int32_t* __restrict__ acc_out) {
     constexpr int D = 2;
-    __shared__ v4i red[KW > 1 ? KW - 1 : 1][kWave];
+    __shared__ v4i red[KW > 1 ? KW - 1 : 1][TM][kWave];
     const int lane = threadIdx.x % kWave, wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int lr = lane % 16, lg = lane / 16;
     const int col = blockIdx.x * 16 + lr;
@@ -291,31 +297,43 @@ __global__ __launch_bounds__(64 * KW) void gemm_skinny_kernel(const uint8_t* __r
     const __amdgpu_buffer_rsrc_t rW = make_rsrc(Wq, (uint32_t)N * ldb);
     const uint32_t seg = 16 * lg;
     const uint32_t ow = (uint32_t)min(col, N - 1) * ldb + seg;
-    const uint32_t oa = (uint32_t)min(lr, M - 1) * ldb + seg;
+    uint32_t oa[TM];
+#pragma unroll
+    for (int i = 0; i < TM; ++i) oa[i] = (uint32_t)min(16 * i + lr, M - 1) * ldb + seg;
     const uint32_t alim = ldb > seg ? ldb - seg : 0;   // this lane's activation bytes end here
-    auto issue = [&](int b, v4i (&w)[U], v4i (&a)[U]) {
+    auto issue = [&](int b, v4i (&w)[U], v4i (&a)[U][TM]) {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int kt = b * U + u;
             const int so = step_offset(kt, nk);
+            const bool in = (uint32_t)kt * kKB < alim;
             w[u] = __builtin_amdgcn_raw_buffer_load_b128(rW, (int)ow, so, 0);
-            a[u] = __builtin_amdgcn_raw_buffer_load_b128(rA, (uint32_t)kt * kKB < alim ? (int)oa : (int)kOOB, so, 0);
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+                a[u][i] = __builtin_amdgcn_raw_buffer_load_b128(rA, in ? (int)oa[i] : (int)kOOB, so, 0);
         }
     };
-    v4i acc = v4i{0, 0, 0, 0};
-    auto compute = [&](const v4i (&w)[U], const v4i (&a)[U]) {
+    v4i acc[TM];
+#pragma unroll
+    for (int i = 0; i < TM; ++i) acc[i] = v4i{0, 0, 0, 0};
+    auto compute = [&](const v4i (&w)[U], const v4i (&a)[U][TM]) {
 #pragma unroll
         for (int u = 0; u < U; ++u)
 #pragma unroll
-            for (int h = 0; h < (BITS == 4 ? 2 : 1); ++h)
-                acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(operand<BITS>(a[u], h), operand<BITS>(w[u], h), acc, 0,
-                                                            0, 0);
-    };
-    v4i w[D][U], a[D][U];
-    issue(wave, w[0], a[0]);
-    float sav[4];
+            for (int h = 0; h < (BITS == 4 ? 2 : 1); ++h) {
+                const v4i wop = operand<BITS>(w[u], h);
 #pragma unroll
-    for (int r = 0; r < 4; ++r) sav[r] = s_a[min(4 * lg + r, M - 1)];
+                for (int i = 0; i < TM; ++i)
+                    acc[i] = __builtin_amdgcn_mfma_i32_16x16x64_i8(operand<BITS>(a[u][i], h), wop, acc[i], 0, 0, 0);
+            }
+    };
+    v4i w[D][U], a[D][U][TM];
+    issue(wave, w[0], a[0]);
+    float sav[TM][4];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) sav[i][r] = s_a[min(16 * i + 4 * lg + r, M - 1)];
     const float swv = s_w[min(col, N - 1)];
     int b = wave;
     do {
@@ -330,30 +348,40 @@ __global__ __launch_bounds__(64 * KW) void gemm_skinny_kernel(const uint8_t* __r
         b += 2 * KW;
     } while (b < nb);
     if (KW > 1) {
-        if (wave > 0) red[wave - 1][lane] = acc;
+        if (wave > 0) {
+#pragma unroll
+            for (int i = 0; i < TM; ++i) red[wave - 1][i][lane] = acc[i];
+        }
         __syncthreads();
         if (wave > 0) return;
 #pragma unroll
-        for (int r = 0; r < KW - 1; ++r) acc += red[r][lane];
+        for (int r = 0; r < KW - 1; ++r)
+#pragma unroll
+            for (int i = 0; i < TM; ++i) acc[i] += red[r][i][lane];
     }
-    skinny_store<BITS>(acc, lg, col, M, N, sav, swv, Y, acc_out);
+#pragma unroll
+    for (int i = 0; i < TM; ++i) skinny_store<BITS>(acc[i], 16 * i, lg, col, M, N, sav[i], swv, Y, acc_out);
 }
 
 // Wide layers, 4-bit codes: the workgroup's waves (blockDim.x / 64 of them)
 // each stream their own 16 columns, and the M x K activation codes are staged
-// once per workgroup in LDS, already expanded to MFMA operands
-// ([k step][half][lane][16 B]), instead of being fetched and expanded by every
-// wave.  Staging: a direct-to-LDS copy of the packed codes (zero past M and K),
-// then one expansion pass split over the waves.  The weight ring is issued
-// before the copy is waited on, so the first batches are already in flight.
+// once per workgroup in LDS by a direct-to-LDS copy (zero past M and K), instead
+// of being fetched by every wave.  With one row tile (M <= 16) they are then
+// expanded once, by all waves together, to MFMA operands ([k step][half][lane]
+// [16 B]); with more row tiles each wave expands its fragments as it multiplies
+// (the expanded copy would not fit).  The weight ring is issued before the copy
+// is waited on, so the first batches are already in flight.
 constexpr int kSharedU = 2, kSharedD = 4;
-constexpr int kSharedMaxSteps = 32;                 // K <= 4096: 96 KB of LDS
+constexpr int kSharedMaxSteps = 32;                 // one row tile, K <= 4096: 96 KB of LDS
+constexpr int kSharedMaxTileSteps = 128;            // more row tiles: row tiles x k steps <= 128 (128 KB)
 constexpr int kSharedMaxWaves = 16;
 
+template <int TM>
 __global__ __launch_bounds__(64 * kSharedMaxWaves) void gemm_skinny_shared_kernel(
     const uint8_t* __restrict__ Aq, const float* __restrict__ s_a, const uint8_t* __restrict__ Wq,
     const float* __restrict__ s_w, int M, int N, int K, uint16_t* __restrict__ Y, int32_t* __restrict__ acc_out) {
     constexpr int U = kSharedU, D = kSharedD;
+    constexpr bool kExpand = TM == 1;
     extern __shared__ __attribute__((aligned(16))) uint8_t sm[];
     const int nw = blockDim.x / kWave;
     const int lane = threadIdx.x % kWave, wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
@@ -362,14 +390,15 @@ __global__ __launch_bounds__(64 * kSharedMaxWaves) void gemm_skinny_shared_kerne
     const uint32_t ldb = (uint32_t)K / 2;
     const int nk = (int)((ldb + kKB - 1) / kKB);
     const int nb = (nk + U - 1) / U;
-    uint8_t* raw = sm;                   // nk x 1 KB: packed activation fragments
-    uint8_t* ops = sm + nk * 1024;       // nk x 2 KB: expanded operands
+    uint8_t* raw = sm;                   // [TM][nk] x 1 KB: packed activation fragments
+    uint8_t* ops = sm + nk * 1024;       // one row tile: nk x 2 KB of expanded operands
     const u32x4 rA = sgpr_rsrc(Aq, (uint32_t)M * ldb);
     const __amdgpu_buffer_rsrc_t rW = make_rsrc(Wq, (uint32_t)N * ldb);
     const uint32_t seg = 16 * lg;
-    for (int s = wave; s < nk; s += nw) {
-        const uint32_t ko = (uint32_t)s * kKB;
-        dma16(rA, lds_addr(raw + s * 1024), (lr < M && ko + seg < ldb) ? (uint32_t)lr * ldb + ko + seg : kOOB);
+    for (int p = wave; p < TM * nk; p += nw) {
+        const int row = 16 * (p / nk) + lr;
+        const uint32_t ko = (uint32_t)(p % nk) * kKB;
+        dma16(rA, lds_addr(raw + p * 1024), (row < M && ko + seg < ldb) ? (uint32_t)row * ldb + ko + seg : kOOB);
     }
     const uint32_t ow = (uint32_t)min(col, N - 1) * ldb + seg;
     auto issue = [&](int b, v4i (&w)[U]) {
@@ -383,25 +412,41 @@ __global__ __launch_bounds__(64 * kSharedMaxWaves) void gemm_skinny_shared_kerne
     wait_vm<(D - 1) * U>();              // this wave's copies have landed (its weight loads may not have)
     __builtin_amdgcn_s_barrier();        // ... and every wave's
     asm volatile("" ::: "memory");
-    for (int s = wave; s < nk; s += nw) {
-        const v4i r = *reinterpret_cast<const v4i*>(raw + s * 1024 + lane * 16);
-        *reinterpret_cast<v4i*>(ops + (2 * s) * 1024 + lane * 16) = operand<4>(r, 0);
-        *reinterpret_cast<v4i*>(ops + (2 * s + 1) * 1024 + lane * 16) = operand<4>(r, 1);
+    if (kExpand) {
+        for (int s = wave; s < nk; s += nw) {
+            const v4i r = *reinterpret_cast<const v4i*>(raw + s * 1024 + lane * 16);
+            *reinterpret_cast<v4i*>(ops + (2 * s) * 1024 + lane * 16) = operand<4>(r, 0);
+            *reinterpret_cast<v4i*>(ops + (2 * s + 1) * 1024 + lane * 16) = operand<4>(r, 1);
+        }
+        __syncthreads();
     }
-    __syncthreads();
-    float sav[4];
+    float sav[TM][4];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) sav[r] = s_a[min(4 * lg + r, M - 1)];
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) sav[i][r] = s_a[min(16 * i + 4 * lg + r, M - 1)];
     const float swv = s_w[min(col, N - 1)];
-    v4i acc = v4i{0, 0, 0, 0};
+    v4i acc[TM];
+#pragma unroll
+    for (int i = 0; i < TM; ++i) acc[i] = v4i{0, 0, 0, 0};
     auto compute = [&](int b, const v4i (&wb)[U]) {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int kt = min(b * U + u, nk - 1);      // past the end the weights read as zero
+            v4i ar[TM];
+            if (!kExpand) {
+#pragma unroll
+                for (int i = 0; i < TM; ++i) ar[i] = *reinterpret_cast<const v4i*>(raw + (i * nk + kt) * 1024 + lane * 16);
+            }
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
-                const v4i x = *reinterpret_cast<const v4i*>(ops + (2 * kt + h) * 1024 + lane * 16);
-                acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(x, operand<4>(wb[u], h), acc, 0, 0, 0);
+                const v4i wop = operand<4>(wb[u], h);
+#pragma unroll
+                for (int i = 0; i < TM; ++i) {
+                    const v4i x = kExpand ? *reinterpret_cast<const v4i*>(ops + (2 * kt + h) * 1024 + lane * 16)
+                                          : operand<4>(ar[i], h);
+                    acc[i] = __builtin_amdgcn_mfma_i32_16x16x64_i8(x, wop, acc[i], 0, 0, 0);
+                }
             }
         }
     };
@@ -416,7 +461,8 @@ __global__ __launch_bounds__(64 * kSharedMaxWaves) void gemm_skinny_shared_kerne
         }
         b += D;
     } while (b < nb);
-    skinny_store<4>(acc, lg, col, M, N, sav, swv, Y, acc_out);
+#pragma unroll
+    for (int i = 0; i < TM; ++i) skinny_store<4>(acc[i], 16 * i, lg, col, M, N, sav[i], swv, Y, acc_out);
 }
 
 // Adds the split-K partial sums (exact int32) and applies the epilogue.
@@ -457,27 +503,45 @@ Plan make_plan(int M, int N, int K, int bm, int bn, int want_splits, int bits = 
     return p;
 }
 
-template <int U, int KW, int BITS>
+template <int U, int KW, int TM, int BITS>
 hipError_t launch_skinny(const uint8_t* Aq, const float* s_a, const uint8_t* Wq, const float* s_w, int M, int N,
                          int K, uint16_t* Y, int32_t* acc, hipStream_t st) {
-    hipLaunchKernelGGL((gemm_skinny_kernel<U, KW, BITS>), dim3((N + 15) / 16), dim3(64 * KW), 0, st, Aq, s_a, Wq, s_w,
-                       M, N, K, Y, acc);
+    hipLaunchKernelGGL((gemm_skinny_kernel<U, KW, TM, BITS>), dim3((N + 15) / 16), dim3(64 * KW), 0, st, Aq, s_a, Wq,
+                       s_w, M, N, K, Y, acc);
+    return hipGetLastError();
+}
+
+// Bytes of dynamic LDS the shared-activation kernel needs, 0 if it cannot run.
+size_t shared_lds_bytes(int tiles, int nk) {
+    if (tiles == 1) return nk <= kSharedMaxSteps ? (size_t)nk * 3 * 1024 : 0;
+    return tiles * nk <= kSharedMaxTileSteps ? (size_t)tiles * nk * 1024 : 0;
+}
+
+template <int TM>
+hipError_t launch_skinny_shared_tm(int waves, const uint8_t* Aq, const float* s_a, const uint8_t* Wq,
+                                   const float* s_w, int M, int N, int K, uint16_t* Y, int32_t* acc, hipStream_t st) {
+    const int nk = (K / 2 + kKB - 1) / kKB;
+    const size_t lds = shared_lds_bytes(TM, nk);
+    static const hipError_t attr =     // above the 64 KB default for dynamic LDS
+        hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_skinny_shared_kernel<TM>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)(TM == 1 ? kSharedMaxSteps * 3 * 1024 : kSharedMaxTileSteps * 1024));
+    if (attr != hipSuccess) return attr;
+    if (lds == 0 || waves < 1 || waves > kSharedMaxWaves) return hipErrorInvalidConfiguration;
+    const int groups = (N + 15) / 16;
+    hipLaunchKernelGGL((gemm_skinny_shared_kernel<TM>), dim3((groups + waves - 1) / waves), dim3(64 * waves), lds,
+                       st, Aq, s_a, Wq, s_w, M, N, K, Y, acc);
     return hipGetLastError();
 }
 
 hipError_t launch_skinny_shared(int waves, const uint8_t* Aq, const float* s_a, const uint8_t* Wq, const float* s_w,
                                 int M, int N, int K, uint16_t* Y, int32_t* acc, hipStream_t st) {
-    const int nk = (K / 2 + kKB - 1) / kKB;
-    const size_t lds = (size_t)nk * 3 * 1024;
-    static const hipError_t attr =     // above the 64 KB default for dynamic LDS
-        hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_skinny_shared_kernel),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, kSharedMaxSteps * 3 * 1024);
-    if (attr != hipSuccess) return attr;
-    if (nk > kSharedMaxSteps || waves < 1 || waves > kSharedMaxWaves) return hipErrorInvalidConfiguration;
-    const int groups = (N + 15) / 16;
-    hipLaunchKernelGGL(gemm_skinny_shared_kernel, dim3((groups + waves - 1) / waves), dim3(64 * waves), lds, st, Aq,
-                       s_a, Wq, s_w, M, N, K, Y, acc);
-    return hipGetLastError();
+    switch ((M + 15) / 16) {
+        case 1: return launch_skinny_shared_tm<1>(waves, Aq, s_a, Wq, s_w, M, N, K, Y, acc, st);
+        case 2: return launch_skinny_shared_tm<2>(waves, Aq, s_a, Wq, s_w, M, N, K, Y, acc, st);
+        case 3: return launch_skinny_shared_tm<3>(waves, Aq, s_a, Wq, s_w, M, N, K, Y, acc, st);
+        default: return hipErrorInvalidConfiguration;
+    }
 }
 
 template <int WM, int WN, int TM, int TN, int BITS = 4, int OCC = 1>
@@ -497,14 +561,29 @@ hipError_t launch_tiled(const Plan& p, const uint8_t* Aq, const float* s_a, cons
     return hipGetLastError();
 }
 
+template <int TM, int BITS>
+hipError_t skinny_kw_tm(int kw, const uint8_t* Aq, const float* s_a, const uint8_t* Wq, const float* s_w, int M, int N,
+                        int K, uint16_t* Y, int32_t* acc, hipStream_t st) {
+    // two register batches of U k steps in flight: 8 steps per batch for one row
+    // tile and up to two waves per column group, 4 for four or eight waves, 2 for
+    // more row tiles (each step holds TM + 1 fragments)
+    constexpr int U1 = TM == 1 ? 8 : 2, U4 = TM == 1 ? 4 : 2;
+    switch (kw) {
+        case 1: return launch_skinny<U1, 1, TM, BITS>(Aq, s_a, Wq, s_w, M, N, K, Y, acc, st);
+        case 2: return launch_skinny<U1, 2, TM, BITS>(Aq, s_a, Wq, s_w, M, N, K, Y, acc, st);
+        case 4: return launch_skinny<U4, 4, TM, BITS>(Aq, s_a, Wq, s_w, M, N, K, Y, acc, st);
+        default: return launch_skinny<U4, 8, TM, BITS>(Aq, s_a, Wq, s_w, M, N, K, Y, acc, st);
+    }
+}
+
 template <int BITS>
 hipError_t skinny_kw(int kw, const uint8_t* Aq, const float* s_a, const uint8_t* Wq, const float* s_w, int M, int N,
                      int K, uint16_t* Y, int32_t* acc, hipStream_t st) {
-    switch (kw) {
-        case 1: return launch_skinny<8, 1, BITS>(Aq, s_a, Wq, s_w, M, N, K, Y, acc, st);
-        case 2: return launch_skinny<8, 2, BITS>(Aq, s_a, Wq, s_w, M, N, K, Y, acc, st);
-        case 4: return launch_skinny<4, 4, BITS>(Aq, s_a, Wq, s_w, M, N, K, Y, acc, st);
-        default: return launch_skinny<4, 8, BITS>(Aq, s_a, Wq, s_w, M, N, K, Y, acc, st);
+    switch ((M + 15) / 16) {
+        case 1: return skinny_kw_tm<1, BITS>(kw, Aq, s_a, Wq, s_w, M, N, K, Y, acc, st);
+        case 2: return skinny_kw_tm<2, BITS>(kw, Aq, s_a, Wq, s_w, M, N, K, Y, acc, st);
+        case 3: return skinny_kw_tm<3, BITS>(kw, Aq, s_a, Wq, s_w, M, N, K, Y, acc, st);
+        default: return hipErrorInvalidConfiguration;
     }
 }
 
@@ -519,7 +598,7 @@ hipError_t finish_split(const Plan& p, int32_t* part, const float* s_a, const fl
 
 // The production plan (from measured sweeps on MI355X, graph-replayed with
 // rotating weights):
-//  - M <= 16: the short-M kernels (weight streaming; activations shared in LDS
+//  - M <= 48: the short-M kernels (weight streaming; activations shared in LDS
 //    for wide 4-bit layers, K split inside the workgroup otherwise);
 //  - at least 768 tiles of 256 x 128: 256 x 128 (eight waves of 64 x 64);
 //  - at least 512 tiles of 128 x 128: 128 x 128 (four waves of 64 x 64);
@@ -537,19 +616,22 @@ Plan choose_plan(int M, int N, int K, int bits) {
         return s < 32 ? s : 32;
     };
     Plan p;
-    if (M <= 16) {
-        // one wave per 16 columns.  Wide 4-bit layers with K <= 4096 share the
-        // staged activations among ceil(groups / 256) waves per workgroup (one
-        // workgroup per CU); the rest split K inside the workgroup, the more
-        // ways the fewer column groups there are, keeping two batches per wave
+    if (M <= 16 * kShortMaxTiles) {
+        // one wave per 16 columns, all M <= 48 tokens in its MFMA row tiles.  Wide
+        // 4-bit layers whose activation codes fit in LDS share them among
+        // ceil(groups / 256) waves per workgroup (one workgroup per CU); the rest
+        // split K inside the workgroup, the more ways the fewer column groups
+        // there are, keeping two batches per wave
         const int groups = (N + 15) / 16;
-        p = make_plan(M, N, K, 16, 16, 1, bits);
-        if (bits == 4 && groups >= 768 && nk <= kSharedMaxSteps) {
+        const int tm = (M + 15) / 16;
+        p = make_plan(M, N, K, 16 * tm, 16, 1, bits);
+        if (bits == 4 && groups >= 768 && shared_lds_bytes(tm, nk) > 0) {
             p.cfg = 5;
             p.waves = (groups + 255) / 256 < kSharedMaxWaves ? (groups + 255) / 256 : kSharedMaxWaves;
         } else {
+            const int u1 = tm == 1 ? 8 : 2, u4 = tm == 1 ? 4 : 2;
             int kw = groups >= 1024 ? 1 : groups >= 256 ? 2 : groups >= 128 ? 4 : 8;
-            while (kw > 1 && (nk + (kw <= 2 ? 8 : 4) - 1) / (kw <= 2 ? 8 : 4) < 2 * kw) kw /= 2;
+            while (kw > 1 && (nk + (kw <= 2 ? u1 : u4) - 1) / (kw <= 2 ? u1 : u4) < 2 * kw) kw /= 2;
             p.cfg = 3;
             p.waves = kw;
         }

@@ -45,8 +45,8 @@ def test_helpers(lib):
     assert lib.sq_prepare_weights_workspace_bytes(64, 512, 1) == 64 * 512 * 4
     assert lib.sq_prepare_weights_workspace_bytes(64, 512, 0) == 0
     assert lib.sq_gemm_workspace_bytes(4096, 4096, 4096) == 0      # no split at large M
-    assert lib.sq_gemm_workspace_bytes(32, 4096, 12288) > 0        # split-K across workgroups: few tiles, long K
-    assert lib.sq_gemm_workspace_bytes(16, 4096, 12288) == 0       # M <= 16 splits K inside the workgroup
+    assert lib.sq_gemm_workspace_bytes(96, 4096, 12288) > 0        # split-K across workgroups: few tiles, long K
+    assert lib.sq_gemm_workspace_bytes(48, 4096, 12288) == 0       # M <= 48 splits K inside the workgroup
 
 
 FAKE = 1 << 20          # a 16-byte aligned non-null address; never dereferenced on these paths
@@ -86,8 +86,8 @@ def test_null_alignment_workspace(lib):
         == L.SQ_ERR_WORKSPACE
     assert lib.w4a4_gemm(FAKE, FAKE, FAKE, FAKE, 4, 12, 64, FAKE, None, None, 0, None) == L.SQ_ERR_SHAPE   # N % 8
     assert lib.w4a4_gemm(FAKE, FAKE, FAKE, FAKE, 4, 16, 64, None, None, None, 0, None) == L.SQ_ERR_NULL
-    wneed = lib.sq_gemm_workspace_bytes(32, 4096, 12288)
-    assert lib.w4a4_gemm(FAKE, FAKE, FAKE, FAKE, 32, 4096, 12288, FAKE, None, None, 0, None) == L.SQ_ERR_WORKSPACE
+    wneed = lib.sq_gemm_workspace_bytes(96, 4096, 12288)
+    assert lib.w4a4_gemm(FAKE, FAKE, FAKE, FAKE, 96, 4096, 12288, FAKE, None, None, 0, None) == L.SQ_ERR_WORKSPACE
     assert wneed > 0
     assert lib.sgat_prepare_weights(FAKE, FAKE, 8, 64, FAKE, FAKE, None, 0, None) == L.SQ_ERR_WORKSPACE
     assert lib.sgat_transform(FAKE, None, FAKE + 4, 8, 64, 0, 0, FAKE, None) == L.SQ_ERR_ALIGN

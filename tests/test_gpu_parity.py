@@ -160,14 +160,15 @@ def _codes(M, K, seed, lo=-7, hi=7):
     return pack_codes(q)
 
 
-# every launch plan: short M (activations shared in LDS: wide 4-bit layers with K <= 4096,
-# including a half last k step and a partial last workgroup; K split inside the
-# workgroup 1, 2, 4 or 8 ways), the tiled shapes with ragged last tiles and the
-# split-K path
+# every launch plan: short M, 1 to 3 row tiles of 16 (activations shared in LDS for
+# wide 4-bit layers, expanded once for one row tile, per wave for more; a half
+# last k step and a partial last workgroup; K split inside the workgroup 1, 2, 4
+# or 8 ways), the tiled shapes with ragged last tiles and the split-K path
 GEMM_SHAPES = [(1, 8, 64), (16, 4096, 4096), (5, 4104, 4096), (9, 136, 192), (16, 24, 18944),
                (16, 12288, 4096), (16, 4096, 12288), (9, 16392, 192), (16, 32768, 256), (33, 520, 1024),
                (16, 24576, 4096), (7, 37888, 3584), (3, 12304, 4032), (1, 12288, 64), (16, 16392, 8192),
                (11, 2056, 4160), (4096, 8200, 192), (4096, 8200, 4160),
+               (64, 24576, 4096), (48, 12304, 4032), (20, 16384, 8192), (64, 16392, 8192), (40, 4104, 12288),
                (77, 200, 192), (128, 256, 512), (300, 136, 4096), (300, 16384, 64), (1024, 1024, 1024),
                (1000, 8200, 64), (2100, 12296, 64), (513, 4104, 3584), (64, 512, 18944)]
 
@@ -246,9 +247,9 @@ def test_gemm_split_and_unsplit_agree():
     Wq = _codes(N, K, 8)
     s_a = np.random.default_rng(9).uniform(0.1, 2, 2048).astype(np.float32)
     s_w = np.random.default_rng(10).uniform(1e-3, 2e-3, N).astype(np.float32)
-    assert sq.gemm_workspace_bytes(32, N, K) > 0 and sq.gemm_workspace_bytes(2048, N, K) == 0
+    assert sq.gemm_workspace_bytes(96, N, K) > 0 and sq.gemm_workspace_bytes(2048, N, K) == 0
     big = host(sq.w4a4_gemm(dev(Aq), dev(s_a), dev(Wq), dev(s_w)))
-    for m in (32, 16):
+    for m in (96, 48, 16):
         small = host(sq.w4a4_gemm(dev(Aq[:m]), dev(s_a[:m]), dev(Wq), dev(s_w)))
         assert_bits(small, big[:m], f"{m} rows vs the single-pass rows")
 
