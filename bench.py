@@ -153,7 +153,8 @@ def large_token_block(torch, sq, synth, dev, steps, warmup):
         Wq, s_w = sq.sgat_prepare_weights(W, None)
         del W
         d = dict(name=site.name, K=site.K, N=site.N, dm=t.dm, du=t.du, X=torch.from_numpy(t.X).to(dev),
-                 Wq=Wq, s_w=s_w, Aq=torch.empty((M, site.K // 2), dtype=torch.uint8, device=dev),
+                 Wq=Wq, Wf=sq.weights_to_frag(Wq), s_w=s_w,
+                 Aq=torch.empty((M, site.K // 2), dtype=torch.uint8, device=dev),
                  s_a=torch.empty((M,), dtype=torch.float32, device=dev),
                  Y=torch.empty((M, site.N), dtype=torch.float16, device=dev))
         if site.tac:
@@ -170,8 +171,8 @@ def large_token_block(torch, sq, synth, dev, steps, warmup):
             tm.wrap("q/" + d["name"], lambda: sq.sgat_quant_act(d["X"], state, None, d["dm"], d["du"], d.get("tac_M"),
                                                                  d.get("tac_d"), d.get("g", 0), Aq=d["Aq"],
                                                                  s_a=d["s_a"], ws=d["qws"]))
-            tm.wrap("g/" + d["name"], lambda: sq.w4a4_gemm(d["Aq"], d["s_a"], d["Wq"], d["s_w"], Y=d["Y"],
-                                                            ws=d["gws"]))
+            tm.wrap("g/" + d["name"], lambda: sq.w4a4_gemm_frag(d["Aq"], d["s_a"], d["Wf"], d["s_w"], Y=d["Y"],
+                                                                 ws=d["gws"]))
     for _ in range(warmup):
         step(Timer(torch))
     torch.cuda.synchronize()
@@ -302,11 +303,12 @@ def small_token_block(torch, sq, synth, dev, token_counts=(16, 32, 64), copies=8
         t = synth.site_tensors(4, si, st64, with_P=False)
         W = torch.from_numpy(t.W).to(dev)
         Wq, s_w = sq.sgat_prepare_weights(W, None)
-        del W
+        Wf = sq.weights_to_frag(Wq)
+        del W, Wq
         for c in range(copies):
-            wsets[c].append((Wq.clone(), s_w.clone()))
+            wsets[c].append((Wf.clone(), s_w.clone()))
         meta.append(site)
-        del t, Wq, s_w
+        del t, Wf, s_w
     out = {}
     dom_rec = None
     for M in token_counts:
@@ -337,9 +339,9 @@ def small_token_block(torch, sq, synth, dev, token_counts=(16, 32, 64), copies=8
                               d.get("g", 0), Aq=d["Aq"], s_a=d["s_a"], ws=d["qws"])
 
         def step(i):
-            for d, (Wq, s_w) in zip(sites, wsets[i % copies]):
+            for d, (Wf, s_w) in zip(sites, wsets[i % copies]):
                 qa(d)
-                sq.w4a4_gemm(d["Aq"], d["s_a"], Wq, s_w, Y=d["Y"], ws=d["gws"])
+                sq.w4a4_gemm_frag(d["Aq"], d["s_a"], Wf, s_w, Y=d["Y"], ws=d["gws"])
 
         step(0)
         torch.cuda.synchronize()
@@ -355,9 +357,10 @@ def small_token_block(torch, sq, synth, dev, token_counts=(16, 32, 64), copies=8
         for si, d in enumerate(sites):
             qa(d)
             rot = rotating_copies(*wsets[0][si])
-            gms, g = graph_ms(torch, lambda i, d=d, rot=rot: sq.w4a4_gemm(d["Aq"], d["s_a"], rot[i % len(rot)][0],
-                                                                          rot[i % len(rot)][1], Y=d["Y"],
-                                                                          ws=d["gws"]), 2 * len(rot))
+            gms, g = graph_ms(torch, lambda i, d=d, rot=rot: sq.w4a4_gemm_frag(d["Aq"], d["s_a"],
+                                                                               rot[i % len(rot)][0],
+                                                                               rot[i % len(rot)][1], Y=d["Y"],
+                                                                               ws=d["gws"]), 2 * len(rot))
             del g, rot
             rec["gemm"][d["name"]] = {"us": gms * 1e3, "gbs": d["gemm_bytes"] / gms / 1e6,
                                       "frac_hbm_peak": d["gemm_bytes"] / gms / 1e6 / PEAK_HBM_GBS}
@@ -391,11 +394,12 @@ def sweep_block(torch, sq, synth, dev, token_counts=(16, 64, 256, 1024, 4096, 16
         t = synth.site_tensors(4, si, st_max[:16], with_P=False)
         W = torch.from_numpy(t.W).to(dev)
         Wq, s_w = sq.sgat_prepare_weights(W, None)
-        del W
+        Wf = sq.weights_to_frag(Wq)
+        del W, Wq
         for c in range(copies):
-            wsets[c].append((Wq.clone(), s_w.clone()))
+            wsets[c].append((Wf.clone(), s_w.clone()))
         meta.append(site)
-        del t, Wq, s_w
+        del t, Wf, s_w
     rots = [rotating_copies(*wsets[0][si]) for si in range(len(meta))]
     out = {}
     for M in token_counts:
@@ -409,8 +413,8 @@ def sweep_block(torch, sq, synth, dev, token_counts=(16, 64, 256, 1024, 4096, 16
             gws = torch.empty(max(sq.gemm_workspace_bytes(M, N, K), 1), dtype=torch.uint8, device=dev)
             rot = rots[si]
             calls = 2 * len(rot) if M <= 1024 else len(rot)
-            ms, gr = graph_ms(torch, lambda i: sq.w4a4_gemm(Aq, s_a, rot[i % len(rot)][0],
-                                                            rot[i % len(rot)][1], Y=Y, ws=gws), calls)
+            ms, gr = graph_ms(torch, lambda i: sq.w4a4_gemm_frag(Aq, s_a, rot[i % len(rot)][0],
+                                                                 rot[i % len(rot)][1], Y=Y, ws=gws), calls)
             del gr
             ops = 2.0 * M * N * K
             byts = N * K // 2 + N * 4 + M * K // 2 + M * 4 + M * N * 2
@@ -435,7 +439,8 @@ def tac_oproj_block(torch, sq, synth, dev, steps=5):
     K, N, g = t.site.K, t.site.N, t.g
     W = torch.from_numpy(t.W).to(dev)
     Wq, s_w = sq.sgat_prepare_weights(W, None)
-    del W
+    Wf = sq.weights_to_frag(Wq)
+    del W, Wq
     X = torch.from_numpy(t.X).to(dev)
     tM, td = torch.from_numpy(t.tac_M).to(dev), torch.from_numpy(t.tac_d).to(dev)
     Z = torch.empty_like(X)
@@ -448,7 +453,7 @@ def tac_oproj_block(torch, sq, synth, dev, steps=5):
     def step(tm):
         tm.wrap("tac", lambda: sq.tac_apply(X, tM, td, g, out=Z))
         tm.wrap("q", lambda: sq.sgat_quant_act(Z, state, None, t.dm, t.du, Aq=Aq, s_a=s_a))
-        tm.wrap("g", lambda: sq.w4a4_gemm(Aq, s_a, Wq, s_w, Y=Y, ws=gws))
+        tm.wrap("g", lambda: sq.w4a4_gemm_frag(Aq, s_a, Wf, s_w, Y=Y, ws=gws))
     step(Timer(torch))
     torch.cuda.synchronize()
     e0 = torch.cuda.Event(enable_timing=True)
@@ -532,6 +537,7 @@ def main():
     # offline weight preparation (Eq. 12), outside the timed region
     for d in sites:
         d["Wq"], d["s_w"] = sq.sgat_prepare_weights(d["W"], d["P"])
+        d["Wf"] = sq.weights_to_frag(d["Wq"])
         K, N = d["K"], d["N"]
         d["z"] = torch.empty((M, K), dtype=torch.float16, device=dev) if "tac_M" in d else None
         d["xp"] = torch.empty((M, K), dtype=torch.float32, device=dev)
@@ -551,7 +557,7 @@ def main():
     # rotating copies of the prepared weights for the folded-basis runs (8 x 108 MB
     # of 4-bit, 4 x 216 MB of 8-bit codes), so that the 256 MB last-level cache
     # cannot hold a layer set's weights from one step to the next
-    wcopies = [[(d["Wq"].clone(), d["s_w"].clone()) for d in sites] for _ in range(8)]
+    wcopies = [[(d["Wf"].clone(), d["s_w"].clone()) for d in sites] for _ in range(8)]
     w8copies = ([[(d["Wq8"].clone(), d["s_w8"].clone()) for d in sites] for _ in range(4)]
                 if not args.no_w8 else [])
     torch.cuda.synchronize()
@@ -567,7 +573,7 @@ def main():
                     lambda: sq.sgat_transform(src, state, d["P"], d["dm"], d["du"], out=d["xp"]))
             tm.wrap("quant", lambda: sq.sgat_quantize(d["xp"], Aq=d["Aq"], s=d["s_a"]))
             tm.wrap("gemm/" + d["site"].name,
-                    lambda: sq.w4a4_gemm(d["Aq"], d["s_a"], d["Wq"], d["s_w"], Y=d["Y"], ws=d["gws"]))
+                    lambda: sq.w4a4_gemm_frag(d["Aq"], d["s_a"], d["Wf"], d["s_w"], Y=d["Y"], ws=d["gws"]))
 
     def step_dense_fast(tm):
         for d in sites:
@@ -579,17 +585,17 @@ def main():
                     lambda: sq.sgat_transform_fast(src, state, d["Ps"], d["dm"], d["du"], out=d["xp"]))
             tm.wrap("quant", lambda: sq.sgat_quantize(d["xp"], Aq=d["Aq"], s=d["s_a"]))
             tm.wrap("gemm/" + d["site"].name,
-                    lambda: sq.w4a4_gemm(d["Aq"], d["s_a"], d["Wq"], d["s_w"], Y=d["Y"], ws=d["gws"]))
+                    lambda: sq.w4a4_gemm_frag(d["Aq"], d["s_a"], d["Wf"], d["s_w"], Y=d["Y"], ws=d["gws"]))
 
     def step_folded(tm, it):
         ws = wcopies[it % len(wcopies)]
-        for d, (Wq, s_w) in zip(sites, ws):
+        for d, (Wf, s_w) in zip(sites, ws):
             tm.wrap("quant_act/" + d["site"].name,
                     lambda: sq.sgat_quant_act(d["X"], state, None, d["dm"], d["du"], d.get("tac_M"),
                                               d.get("tac_d"), d.get("g", 0), Aq=d["Aq"], s_a=d["s_a"],
                                               ws=d["qws"]))
             tm.wrap("gemm/" + d["site"].name,
-                    lambda: sq.w4a4_gemm(d["Aq"], d["s_a"], Wq, s_w, Y=d["Y"], ws=d["gws"]))
+                    lambda: sq.w4a4_gemm_frag(d["Aq"], d["s_a"], Wf, s_w, Y=d["Y"], ws=d["gws"]))
 
     def step_w8(tm, it):
         for d, (Wq8, s_w8) in zip(sites, w8copies[it % len(w8copies)]):
@@ -721,6 +727,8 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "int4xint4->int32 GEMM, fp32 transform, fp16 I/O",
         "data": "synthetic (seeded; random-init weights and orthogonal bases)",
+        "weights": "int4 codes in fragment order (sq_weights_to_frag, once, outside the timed region); W8A8 and "
+                   "FP6 variants in their own layouts",
         "config": {"workload": "LLaDA-8B-shaped SGAT layer set (QKV, O+TAC g=16, gate+up, down), "
                                "1024 tokens, dense online P" if dense else
                                "LLaDA-8B-shaped SGAT layer set, 1024 tokens, folded P",

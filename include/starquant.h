@@ -255,6 +255,33 @@ int sq_codes_to_fp6(const uint8_t* codes, int32_t R, int32_t K, uint8_t* out, vo
 int w4a4_gemm_fp6(const uint8_t* A6, const float* s_a, const uint8_t* W6, const float* s_w,
                   int32_t M, int32_t N, int32_t K, uint16_t* Y, int32_t* acc, void* stream);
 
+/*
+ * Fragment-ordered weights: the same GEMM (Eq. 13; Eq. 5) with the packed int4
+ * weights stored in the order the GEMM kernels read them.  The weights are
+ * fixed after sgat_prepare_weights (Eq. 12), so they can be reordered once,
+ * offline; a load of 16 weight rows then reads one contiguous 1 KB block, which
+ * the memory system serves faster than 16 runs of 64 bytes (decode-sized M,
+ * where the GEMM streams the weights from HBM).
+ * Layout: rows in groups of 16 (the last group padded with zero rows), k in
+ * steps of 128 codes (64 bytes of a row; the last step padded with zero codes);
+ * with G = ceil(N / 16), block (g, t) is 1024 bytes at (t G + g) 1024, and
+ * within it the 16 bytes at 16 (16 j + r) are bytes 64 t + 16 j .. 64 t + 16 j
+ * + 15 of row 16 g + r (j = 0..3, r = 0..15).  Every byte of Wq appears exactly
+ * once.
+ *   sq_frag_weight_bytes: G ceil(K / 128) 1024, 0 for an invalid K.
+ *   sq_weights_to_frag:   Wq [N][K/2] (the sgat_prepare_weights layout) in, Wf
+ *                         [sq_frag_weight_bytes(N, K)] out (must not overlap
+ *                         Wq); under 2 GiB.  Any N >= 0.
+ *   w4a4_gemm_frag:       as w4a4_gemm with Wf in place of Wq: same arguments,
+ *                         rules and workspace (sq_gemm_workspace_bytes); acc and
+ *                         Y equal w4a4_gemm's bit for bit.
+ */
+size_t sq_frag_weight_bytes(int32_t N, int32_t K);
+int sq_weights_to_frag(const uint8_t* Wq, int32_t N, int32_t K, uint8_t* Wf, void* stream);
+int w4a4_gemm_frag(const uint8_t* Aq, const float* s_a, const uint8_t* Wf, const float* s_w,
+                   int32_t M, int32_t N, int32_t K, uint16_t* Y, int32_t* acc,
+                   void* ws, size_t ws_bytes, void* stream);
+
 size_t sq_tac_calibrate_workspace_bytes(int32_t N, int32_t C, int32_t g);
 int tac_calibrate(const uint16_t* Z_fp, const uint16_t* Z_q, int32_t N, int32_t C, int32_t g,
                   double rho, double eps, double eta, double alpha,

@@ -23,7 +23,8 @@ __all__ = ["sgat_prepare_weights", "sgat_transform", "sgat_quantize", "sgat_quan
            "prepare_weights_workspace_bytes", "StarQuantError", "lib",
            "sgat_prepare_weights_w8", "sgat_quantize_w8", "sgat_quant_act_w8", "w8a8_gemm",
            "tac_calibrate", "tac_calibrate_workspace_bytes", "sgat_split_basis", "sgat_transform_fast",
-           "fp6_row_bytes", "codes_to_fp6", "w4a4_gemm_fp6"]
+           "fp6_row_bytes", "codes_to_fp6", "w4a4_gemm_fp6",
+           "frag_weight_bytes", "weights_to_frag", "w4a4_gemm_frag"]
 
 
 def _ptr(t: Optional[torch.Tensor]):
@@ -248,6 +249,51 @@ def w4a4_gemm_fp6(A6: torch.Tensor, s_a: torch.Tensor, W6: torch.Tensor, s_w: to
     _need(acc, "acc", torch.int32, (M, N), optional=True)
     check(lib().w4a4_gemm_fp6(_ptr(A6), _ptr(s_a), _ptr(W6), _ptr(s_w), M, N, K, _ptr(Y), _ptr(acc),
                               _stream(stream)))
+    return (Y, acc) if want_acc else Y
+
+
+def frag_weight_bytes(N: int, K: int) -> int:
+    """Bytes of the fragment-ordered weights of an N x K int4 matrix (1 KB per
+    16 rows and k step of 128 codes)."""
+    n = int(lib().sq_frag_weight_bytes(N, K))
+    if n == 0 and N > 0:
+        raise ValueError(f"K={K}: need 64 <= K <= 131072 and K % 64 == 0")
+    return n
+
+
+def weights_to_frag(Wq: torch.Tensor, *, out=None, stream=None):
+    """Packed int4 weights [N, K/2] -> fragment order [ceil(K/128), ceil(N/16), 1024] (uint8)."""
+    N, Kh = Wq.shape
+    K = 2 * Kh
+    _need(Wq, "Wq", torch.uint8)
+    shape = ((K + 127) // 128, (N + 15) // 16, 1024)
+    frag_weight_bytes(N, K)
+    if out is None:
+        out = torch.empty(shape, dtype=torch.uint8, device=Wq.device)
+    _need(out, "out", torch.uint8, shape)
+    check(lib().sq_weights_to_frag(_ptr(Wq), N, K, _ptr(out), _stream(stream)))
+    return out
+
+
+def w4a4_gemm_frag(Aq: torch.Tensor, s_a: torch.Tensor, Wf: torch.Tensor, s_w: torch.Tensor, *, Y=None, acc=None,
+                   want_Y: bool = True, want_acc: bool = False, ws=None, stream=None):
+    """w4a4_gemm (Eq. 13) with the weights in fragment order (weights_to_frag);
+    N is s_w's length.  Bit-identical to w4a4_gemm.  Returns Y, or (Y, acc)."""
+    M, Kc = Aq.shape
+    N, K = s_w.shape[0], 2 * Kc
+    _need(Aq, "Aq", torch.uint8)
+    _need(Wf, "Wf", torch.uint8, ((K + 127) // 128, (N + 15) // 16, 1024))
+    _need(s_a, "s_a", torch.float32, (M,))
+    _need(s_w, "s_w", torch.float32, (N,))
+    if Y is None and want_Y:
+        Y = torch.empty((M, N), dtype=torch.float16, device=Aq.device)
+    if acc is None and want_acc:
+        acc = torch.empty((M, N), dtype=torch.int32, device=Aq.device)
+    _need(Y, "Y", torch.float16, (M, N), optional=True)
+    _need(acc, "acc", torch.int32, (M, N), optional=True)
+    ws, wsb = _ws(gemm_workspace_bytes(M, N, K), ws, Aq.device)
+    check(lib().w4a4_gemm_frag(_ptr(Aq), _ptr(s_a), _ptr(Wf), _ptr(s_w), M, N, K, _ptr(Y), _ptr(acc), _ptr(ws), wsb,
+                               _stream(stream)))
     return (Y, acc) if want_acc else Y
 
 

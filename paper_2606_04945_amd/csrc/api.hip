@@ -309,6 +309,46 @@ int w4a4_gemm_fp6(const uint8_t* A6, const float* s_a, const uint8_t* W6, const 
                       "gemm_fp6");
 }
 
+size_t sq_frag_weight_bytes(int32_t N, int32_t K) {
+    if (N < 0 || K < 64 || K > 131072 || K % 64) return 0;
+    return sq::frag_weight_bytes(N, K);
+}
+
+int sq_weights_to_frag(const uint8_t* Wq, int32_t N, int32_t K, uint8_t* Wf, void* stream) {
+    SQ_TRY(check_K(K));
+    SQ_REQUIRE(N >= 0, SQ_ERR_SHAPE, "sq_weights_to_frag: N=%d < 0", N);
+    SQ_REQUIRE(sq::frag_weight_bytes(N, K) < (1u << 31), SQ_ERR_SHAPE,
+               "sq_weights_to_frag: the fragment-ordered weights must be under 2 GiB (N=%d K=%d)", N, K);
+    if (N == 0) return SQ_OK;
+    SQ_REQUIRE(Wq && Wf, SQ_ERR_NULL, "sq_weights_to_frag: Wq and Wf are required");
+    SQ_REQUIRE(aligned16(Wq) && aligned16(Wf), SQ_ERR_ALIGN, "sq_weights_to_frag: pointers must be 16-byte aligned");
+    const uintptr_t a0 = (uintptr_t)Wq, a1 = a0 + (size_t)N * K / 2;
+    const uintptr_t b0 = (uintptr_t)Wf, b1 = b0 + sq::frag_weight_bytes(N, K);
+    SQ_REQUIRE(a1 <= b0 || b1 <= a0, SQ_ERR_SHAPE, "sq_weights_to_frag: Wf overlaps Wq");
+    return hip_status(sq::launch_weights_to_frag(Wq, N, K, Wf, static_cast<hipStream_t>(stream)), "weights_to_frag");
+}
+
+int w4a4_gemm_frag(const uint8_t* Aq, const float* s_a, const uint8_t* Wf, const float* s_w, int32_t M, int32_t N,
+                   int32_t K, uint16_t* Y, int32_t* acc, void* ws, size_t ws_bytes, void* stream) {
+    SQ_TRY(check_K(K));
+    SQ_REQUIRE(M >= 0 && N >= 0, SQ_ERR_SHAPE, "M=%d N=%d: need >= 0", M, N);
+    SQ_REQUIRE(M <= kMaxTiledRows, SQ_ERR_SHAPE, "w4a4_gemm_frag: M=%d: at most %d rows per call", M, kMaxTiledRows);
+    SQ_REQUIRE(N % 8 == 0, SQ_ERR_SHAPE, "N=%d: need N %% 8 == 0", N);
+    SQ_REQUIRE((size_t)M * K / 2 < (1u << 31) && sq::frag_weight_bytes(N, K) < (1u << 31), SQ_ERR_SHAPE,
+               "w4a4_gemm_frag: each operand must be under 2 GiB (M=%d N=%d K=%d)", M, N, K);
+    if (M == 0 || N == 0) return SQ_OK;
+    SQ_REQUIRE(Aq && s_a && Wf && s_w && (Y || acc), SQ_ERR_NULL,
+               "w4a4_gemm_frag: Aq, s_a, Wf, s_w and one of Y / acc are required");
+    SQ_REQUIRE(aligned16(Aq) && aligned16(s_a) && aligned16(Wf) && aligned16(s_w) && aligned16(Y) &&
+                   aligned16(acc) && aligned16(ws),
+               SQ_ERR_ALIGN, "w4a4_gemm_frag: pointers must be 16-byte aligned");
+    const size_t need = sq_gemm_workspace_bytes(M, N, K);
+    SQ_REQUIRE(ws_bytes >= need && (need == 0 || ws), SQ_ERR_WORKSPACE, "w4a4_gemm_frag: workspace %zu B < %zu B",
+               ws_bytes, need);
+    return hip_status(
+        sq::launch_gemm_frag(Aq, s_a, Wf, s_w, M, N, K, Y, acc, ws, static_cast<hipStream_t>(stream)), "gemm_frag");
+}
+
 size_t sq_tac_calibrate_workspace_bytes(int32_t N, int32_t C, int32_t g) {
     if (N <= 0 || C < 64 || C % 64 || g < 1 || g > 128 || (g & (g - 1)) || C % g) return 0;
     return sq::tac_calib_workspace_bytes(N, C, g);

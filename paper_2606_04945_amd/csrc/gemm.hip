@@ -71,7 +71,7 @@ __device__ __forceinline__ int acc_value(int raw) {   // 4-bit operands carry a 
     return BITS == 8 ? raw : (raw == INT32_MIN ? (1 << 23) : raw >> 8);
 }
 
-template <int WM, int WN, int TM, int TN, bool SPLIT, int BITS, int OCC>
+template <int WM, int WN, int TM, int TN, bool SPLIT, int BITS, int OCC, bool WF = false>
 __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(OCC))) void gemm_tile_kernel(
     const uint8_t* __restrict__ Aq, const float* __restrict__ s_a, const uint8_t* __restrict__ Wq,
     const float* __restrict__ s_w, int M, int N, int K, int ksteps_per_split, uint16_t* __restrict__ Y,
@@ -91,7 +91,8 @@ __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(OC
     const int nk_total = (int)((ldb + kKB - 1) / kKB);
     const int nk_full = (int)(ldb / kKB);
     const u32x4 rA = sgpr_rsrc(Aq, (uint32_t)M * ldb);
-    const u32x4 rW = sgpr_rsrc(Wq, (uint32_t)N * ldb);
+    const int ngrp = (N + 15) / 16;                     // WF: fragment-ordered weights, 16-row groups
+    const u32x4 rW = sgpr_rsrc(Wq, WF ? (uint32_t)ngrp * nk_total * 1024 : (uint32_t)N * ldb);
     auto swz = [](int r) { return (r >> 1) & 3; };       // 16-byte chunk swizzle of a 64-byte LDS row
 
     // groups of 8 row tiles per XCD (see xcd_tile): the workgroups an XCD runs
@@ -116,7 +117,12 @@ __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(OC
     for (int u = 0; u < LB; ++u) {
         const int r = 16 * (wave * LB + u) + lane / 4;
         sw_[u] = 16 * ((lane % 4) ^ swz(r));
-        ow[u] = col0 + r < N ? (uint32_t)(col0 + r) * ldb + sw_[u] : kOOB;
+        if (WF) {   // one 1 KB block per k step, copied as it is: lane l fetches bytes 16 l .. 16 l + 15
+            const int g = (col0 + r) / 16;
+            ow[u] = g < ngrp ? (uint32_t)g * 1024 + (uint32_t)lane * 16 : kOOB;
+        } else {
+            ow[u] = col0 + r < N ? (uint32_t)(col0 + r) * ldb + sw_[u] : kOOB;
+        }
     }
     auto issue = [&](int kt, int stage) {
         uint8_t* dA = sm + stage * SB;
@@ -130,7 +136,8 @@ __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(OC
         }
 #pragma unroll
         for (int u = 0; u < LB; ++u) {
-            const uint32_t o = (tail && ko + sw_[u] >= ldb) ? kOOB : ow[u] + ko;
+            // fragment-ordered weights are zero-padded to whole k steps
+            const uint32_t o = WF ? ow[u] + (uint32_t)kt * ngrp * 1024 : (tail && ko + sw_[u] >= ldb) ? kOOB : ow[u] + ko;
             dma16(rW, lds_addr(dB + (wave * LB + u) * 1024), o);
         }
     };
@@ -143,7 +150,8 @@ __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(OC
     const int lr = lane % 16, lg = lane / 16;
     const int fo = (lg ^ swz(lr)) * 16;                  // this lane's fragment slot in a row
     const int offA = ((wm * TM) * 16 + lr) * kKB + fo;
-    const int offB = AB + ((wn * TN) * 16 + lr) * kKB + fo;
+    // fragment-ordered weights sit in LDS in fragment order: lane l's 16 bytes at 16 l
+    const int offB = WF ? AB + (wn * TN) * 1024 + lane * 16 : AB + ((wn * TN) * 16 + lr) * kKB + fo;
     v4i fa[TM], fb[TN];
     auto frags = [&](const uint8_t* st) {
 #pragma unroll
@@ -465,6 +473,152 @@ __global__ __launch_bounds__(64 * kSharedMaxWaves) void gemm_skinny_shared_kerne
     for (int i = 0; i < TM; ++i) skinny_store<4>(acc[i], 16 * i, lg, col, M, N, sav[i], swv, Y, acc_out);
 }
 
+// Short M on fragment-ordered weights.  The weights of 16 columns at one k step
+// are one 1 KB block in the MFMA fragment order (lane l's 16 bytes at 16 l), the
+// blocks of one k step side by side, so every weight load of a wave reads 1 KB
+// of consecutive bytes and neighbouring waves read neighbouring blocks
+// (row-major weights give 16 runs of 64 bytes per load, which the memory system
+// serves markedly slower), with the non-temporal hint, as nothing reuses them.  A workgroup holds CG column groups
+// times KW waves that take turns over k (wave w of a group multiplies batches
+// w, w + KW, ...; partial sums meet in LDS).  Activation fragments are staged
+// once per workgroup in LDS (ALDS) or, for narrow layers whose few column
+// groups leave each workgroup little weight to stream, read from L2 by each
+// wave, which does not wait for a whole-workgroup copy before its first
+// multiply.  A ring of D batches of U k steps keeps D - 1 batches in flight;
+// zero handling and epilogue as in the kernels above; the weights past K and
+// past N read as zero from the layout's own padding.
+constexpr int kFragNT = 2;                             // buffer-load cache policy: non-temporal
+constexpr size_t kFragMaxLds = 160 * 1024;
+
+template <int TM, int KW, bool ALDS, int U, int D>
+__global__ __launch_bounds__(ALDS ? 1024 : 512) void gemm_short_frag_kernel(
+    const uint8_t* __restrict__ Aq, const float* __restrict__ s_a, const uint8_t* __restrict__ Wf,
+    const float* __restrict__ s_w, int M, int N, int K, uint16_t* __restrict__ Y, int32_t* __restrict__ acc_out) {
+    extern __shared__ __attribute__((aligned(16))) uint8_t sm[];
+    const int CG = blockDim.x / kWave / KW;
+    const int lane = threadIdx.x % kWave, wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int cgi = wave % CG, kw = wave / CG;
+    const int lr = lane % 16, lg = lane / 16;
+    const int ngrp = (N + 15) / 16;
+    const int grp = blockIdx.x * CG + cgi;
+    const int col = grp * 16 + lr;
+    const uint32_t ldb = (uint32_t)K / 2;
+    const int nk = (int)((ldb + kKB - 1) / kKB);
+    const int nb = (nk + U - 1) / U;
+    const uint32_t seg = 16 * lg;
+    uint8_t* raw = sm;                                         // ALDS: [TM][nk] x 1 KB of activation fragments
+    v4i* red = reinterpret_cast<v4i*>(sm + (ALDS ? (size_t)TM * nk * 1024 : 0));   // [KW - 1][CG][TM][lane]
+    const __amdgpu_buffer_rsrc_t rW = make_rsrc(Wf, (uint32_t)ngrp * nk * 1024);
+    const __amdgpu_buffer_rsrc_t rA = make_rsrc(Aq, (uint32_t)M * ldb);
+    if (ALDS) {
+        const u32x4 rAs = sgpr_rsrc(Aq, (uint32_t)M * ldb);
+        for (int p = wave; p < TM * nk; p += blockDim.x / kWave) {
+            const int row = 16 * (p / nk) + lr;
+            const uint32_t ko = (uint32_t)(p % nk) * kKB;
+            dma16(rAs, lds_addr(raw + p * 1024), (row < M && ko + seg < ldb) ? (uint32_t)row * ldb + ko + seg : kOOB);
+        }
+    }
+    uint32_t oa[TM];
+#pragma unroll
+    for (int i = 0; i < TM; ++i) oa[i] = (uint32_t)min(16 * i + lr, M - 1) * ldb + seg;
+    const uint32_t alim = ldb > seg ? ldb - seg : 0;   // this lane's activation bytes end here
+    const uint32_t ow = (uint32_t)min(grp, ngrp - 1) * 1024 + lane * 16;
+    const int kstride = ngrp * 1024;                   // bytes from one k step to the next
+    auto issue = [&](int b, v4i (&w)[U], v4i (&a)[U][TM]) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int kt = b * U + u;
+            w[u] = __builtin_amdgcn_raw_buffer_load_b128(rW, (int)ow, kt < nk ? kt * kstride : (int)kOOB, kFragNT);
+            if (!ALDS) {
+                const bool in = (uint32_t)kt * kKB < alim;
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+                    a[u][i] = __builtin_amdgcn_raw_buffer_load_b128(rA, in ? (int)oa[i] : (int)kOOB, step_offset(kt, nk), 0);
+            }
+        }
+    };
+    v4i w[D][U];
+    v4i a[ALDS ? 1 : D][U][TM];
+#pragma unroll
+    for (int d = 0; d < D - 1; ++d) issue(kw + d * KW, w[d], a[ALDS ? 0 : d]);
+    if (ALDS) {
+        wait_vm<(D - 1) * U>();          // this wave's copies have landed (its weight loads may not have)
+        __builtin_amdgcn_s_barrier();    // ... and every wave's
+        asm volatile("" ::: "memory");
+    }
+    float sav[TM][4];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) sav[i][r] = s_a[min(16 * i + 4 * lg + r, M - 1)];
+    const float swv = s_w[min(col, N - 1)];
+    v4i acc[TM];
+#pragma unroll
+    for (int i = 0; i < TM; ++i) acc[i] = v4i{0, 0, 0, 0};
+    auto compute = [&](int b, const v4i (&wb)[U], const v4i (&ab)[U][TM]) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int kt = min(b * U + u, nk - 1);      // past the end the weights read as zero
+            v4i ar[TM];
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+                ar[i] = ALDS ? *reinterpret_cast<const v4i*>(raw + (i * nk + kt) * 1024 + lane * 16) : ab[u][i];
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const v4i wop = operand<4>(wb[u], h);
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+                    acc[i] = __builtin_amdgcn_mfma_i32_16x16x64_i8(operand<4>(ar[i], h), wop, acc[i], 0, 0, 0);
+            }
+        }
+    };
+    int b = kw;
+    do {
+#pragma unroll
+        for (int d = 0; d < D; ++d) {
+            issue(b + (d + D - 1) * KW, w[(d + D - 1) % D], a[ALDS ? 0 : (d + D - 1) % D]);
+            __builtin_amdgcn_sched_barrier(0);
+            compute(b + d * KW, w[d], a[ALDS ? 0 : d]);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        b += D * KW;
+    } while (b < nb);
+    if (KW > 1) {
+        if (kw > 0) {
+#pragma unroll
+            for (int i = 0; i < TM; ++i) red[(((kw - 1) * CG + cgi) * TM + i) * kWave + lane] = acc[i];
+        }
+        __syncthreads();
+        if (kw > 0) return;
+#pragma unroll
+        for (int r = 0; r < KW - 1; ++r)
+#pragma unroll
+            for (int i = 0; i < TM; ++i) acc[i] += red[((r * CG + cgi) * TM + i) * kWave + lane];
+    }
+#pragma unroll
+    for (int i = 0; i < TM; ++i) skinny_store<4>(acc[i], 16 * i, lg, col, M, N, sav[i], swv, Y, acc_out);
+}
+
+// Packed int4 weights [N][K/2] -> fragment order: one thread per 16-byte unit
+// (k step t, group g, lane l) = bytes 64 t + 16 (l / 16) .. + 15 of row
+// 16 g + l % 16, zero past N and past the row.
+__global__ __launch_bounds__(256) void weights_to_frag_kernel(const uint8_t* __restrict__ Wq, int N, int K,
+                                                              uint8_t* __restrict__ Wf) {
+    const uint32_t ldb = (uint32_t)K / 2;
+    const uint32_t nk = (ldb + kKB - 1) / kKB;
+    const uint32_t ngrp = (uint32_t)(N + 15) / 16;
+    const size_t units = (size_t)ngrp * nk * kWave;
+    for (size_t e = (size_t)blockIdx.x * 256 + threadIdx.x; e < units; e += (size_t)gridDim.x * 256) {
+        const uint32_t l = (uint32_t)(e % kWave);
+        const size_t tg = e / kWave;
+        const uint32_t g = (uint32_t)(tg % ngrp), t = (uint32_t)(tg / ngrp);
+        const uint32_t row = 16 * g + l % 16, byte = t * kKB + 16 * (l / 16);
+        v4i v = v4i{0, 0, 0, 0};
+        if (row < (uint32_t)N && byte < ldb) v = *reinterpret_cast<const v4i*>(Wq + (size_t)row * ldb + byte);
+        *reinterpret_cast<v4i*>(Wf + e * 16) = v;
+    }
+}
+
 // Adds the split-K partial sums (exact int32) and applies the epilogue.
 __global__ __launch_bounds__(256) void splitk_epilogue(const int32_t* __restrict__ part, int splits,
                                                        const float* __restrict__ s_a,
@@ -481,11 +635,16 @@ __global__ __launch_bounds__(256) void splitk_epilogue(const int32_t* __restrict
 // A launch plan: tile shape and K split.
 struct Plan {
     int cfg;       // 0: 256 x 128, 1: 128 x 128, 2: 64 x 64, 4: 64 x 128, 3: short M, K split in the
-                   // workgroup, 5: short M, activations shared in LDS (see launch_gemm)
+                   // workgroup, 5: short M, activations shared in LDS (see launch_gemm), 6: short M on
+                   // fragment-ordered weights (see launch_gemm_frag)
     int bm, bn;
     int splits;    // K split count across workgroups actually used (1 = fused epilogue)
     int per;       // k steps per split
-    int waves;     // cfg 3: waves sharing a column group over k; cfg 5: waves per workgroup
+    int waves;     // cfg 3: waves sharing a column group over k; cfg 5: waves per workgroup;
+                   // cfg 6: column groups per workgroup
+    int kw;        // cfg 6: waves per column group, taking turns over k
+    bool alds;     // cfg 6: activation fragments staged in LDS (else read from L2)
+    int u, d;      // cfg 6: k steps per batch, batches in the register ring
 };
 
 Plan make_plan(int M, int N, int K, int bm, int bn, int want_splits, int bits = 4) {
@@ -494,6 +653,10 @@ Plan make_plan(int M, int N, int K, int bm, int bn, int want_splits, int bits = 
     Plan p;
     p.cfg = -1;
     p.waves = 1;
+    p.kw = 1;
+    p.alds = false;
+    p.u = 2;
+    p.d = 4;
     p.bm = bm;
     p.bn = bn;
     const int nk = (K * bits / 8 + kKB - 1) / kKB;
@@ -544,7 +707,7 @@ hipError_t launch_skinny_shared(int waves, const uint8_t* Aq, const float* s_a, 
     }
 }
 
-template <int WM, int WN, int TM, int TN, int BITS = 4, int OCC = 1>
+template <int WM, int WN, int TM, int TN, int BITS = 4, int OCC = 1, bool WF = false>
 hipError_t launch_tiled(const Plan& p, const uint8_t* Aq, const float* s_a, const uint8_t* Wq, const float* s_w,
                        int M, int N, int K, uint16_t* Y, int32_t* acc, int32_t* part, hipStream_t st) {
     const size_t tiles = (size_t)((N + p.bn - 1) / p.bn) * (size_t)((M + p.bm - 1) / p.bm);
@@ -552,13 +715,68 @@ hipError_t launch_tiled(const Plan& p, const uint8_t* Aq, const float* s_a, cons
     dim3 grid((unsigned)tiles, 1, p.splits);
     dim3 block(64 * WM * WN);
     if (p.splits == 1) {
-        hipLaunchKernelGGL((gemm_tile_kernel<WM, WN, TM, TN, false, BITS, OCC>), grid, block, 0, st, Aq, s_a, Wq, s_w, M,
-                           N, K, p.per, Y, acc, (int32_t*)nullptr);
+        hipLaunchKernelGGL((gemm_tile_kernel<WM, WN, TM, TN, false, BITS, OCC, WF>), grid, block, 0, st, Aq, s_a, Wq,
+                           s_w, M, N, K, p.per, Y, acc, (int32_t*)nullptr);
     } else {
-        hipLaunchKernelGGL((gemm_tile_kernel<WM, WN, TM, TN, true, BITS, OCC>), grid, block, 0, st, Aq, s_a, Wq, s_w, M,
-                           N, K, p.per, (uint16_t*)nullptr, (int32_t*)nullptr, part);
+        hipLaunchKernelGGL((gemm_tile_kernel<WM, WN, TM, TN, true, BITS, OCC, WF>), grid, block, 0, st, Aq, s_a, Wq,
+                           s_w, M, N, K, p.per, (uint16_t*)nullptr, (int32_t*)nullptr, part);
     }
     return hipGetLastError();
+}
+
+// Dynamic LDS of the fragment-ordered short-M kernel.
+size_t frag_lds_bytes(int tm, int nk, int kw, int cg, bool alds) {
+    return (alds ? (size_t)tm * nk * 1024 : 0) + (kw > 1 ? (size_t)(kw - 1) * cg * tm * 1024 : 0);
+}
+
+template <int TM, int KW, bool ALDS, int U, int D>
+hipError_t launch_short_frag_t(const Plan& p, const uint8_t* Aq, const float* s_a, const uint8_t* Wf,
+                               const float* s_w, int M, int N, int K, uint16_t* Y, int32_t* acc, hipStream_t st) {
+    const int nk = (K / 2 + kKB - 1) / kKB;
+    const size_t lds = frag_lds_bytes(TM, nk, KW, p.waves, ALDS);
+    static const hipError_t attr =     // above the 64 KB default for dynamic LDS
+        hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_short_frag_kernel<TM, KW, ALDS, U, D>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)kFragMaxLds);
+    if (attr != hipSuccess) return attr;
+    if (lds > kFragMaxLds || p.waves < 1 || p.waves * KW > (ALDS ? 16 : 8)) return hipErrorInvalidConfiguration;
+    const int groups = (N + 15) / 16;
+    hipLaunchKernelGGL((gemm_short_frag_kernel<TM, KW, ALDS, U, D>), dim3((groups + p.waves - 1) / p.waves),
+                       dim3(64 * p.waves * KW), lds, st, Aq, s_a, Wf, s_w, M, N, K, Y, acc);
+    return hipGetLastError();
+}
+
+// The (waves per group, activation staging, batch, ring) combinations the plan uses.
+template <int TM>
+hipError_t launch_short_frag_tm(const Plan& p, const uint8_t* Aq, const float* s_a, const uint8_t* Wf,
+                                const float* s_w, int M, int N, int K, uint16_t* Y, int32_t* acc, hipStream_t st) {
+    if (p.alds) {
+        if (p.d != 4) return hipErrorInvalidConfiguration;
+        switch (p.kw * 4 + p.u) {
+            case 5: return launch_short_frag_t<TM, 1, true, 1, 4>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, st);
+            case 6: return launch_short_frag_t<TM, 1, true, 2, 4>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, st);
+            case 9: return launch_short_frag_t<TM, 2, true, 1, 4>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, st);
+            case 10: return launch_short_frag_t<TM, 2, true, 2, 4>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, st);
+            default: return hipErrorInvalidConfiguration;
+        }
+    }
+    if (p.u != 2) return hipErrorInvalidConfiguration;
+    switch (p.kw * 8 + p.d) {
+        case 12: return launch_short_frag_t<TM, 1, false, 2, 4>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, st);
+        case 20: return launch_short_frag_t<TM, 2, false, 2, 4>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, st);
+        case 34: return launch_short_frag_t<TM, 4, false, 2, 2>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, st);
+        case 36: return launch_short_frag_t<TM, 4, false, 2, 4>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, st);
+        default: return hipErrorInvalidConfiguration;
+    }
+}
+
+hipError_t launch_short_frag(const Plan& p, const uint8_t* Aq, const float* s_a, const uint8_t* Wf, const float* s_w,
+                             int M, int N, int K, uint16_t* Y, int32_t* acc, hipStream_t st) {
+    switch ((M + 15) / 16) {
+        case 1: return launch_short_frag_tm<1>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, st);
+        case 2: return launch_short_frag_tm<2>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, st);
+        case 3: return launch_short_frag_tm<3>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, st);
+        default: return hipErrorInvalidConfiguration;
+    }
 }
 
 template <int TM, int BITS>
@@ -651,7 +869,82 @@ Plan choose_plan(int M, int N, int K, int bits) {
     return p;
 }
 
+// Fragment-ordered weights, M <= 48 (from graph-replayed sweeps with rotating
+// weights): at most about one workgroup per CU.  Wide layers (>= 1024 column
+// groups): one wave per column group, activations in LDS; mid-width (>= 384):
+// two waves per column group, activations in LDS; 257-383 groups: two waves per
+// group, two groups per workgroup, activations in LDS (one group per workgroup
+// would leave some CUs twice the work of the rest); up to 256: four waves per
+// column group, one group per workgroup, activations from L2, a ring of two
+// batches from 17 tokens on.  Batches of two k steps, or of one where that
+// leaves fewer zero-weight k steps in the last pass of the ring.  At least two
+// batches per wave.
+Plan choose_frag_short(int M, int N, int K) {
+    const int nk = (K / 2 + kKB - 1) / kKB, nb = (nk + 1) / 2;
+    const int groups = (N + 15) / 16, tm = (M + 15) / 16;
+    Plan p = make_plan(M, N, K, 16 * tm, 16, 1, 4);
+    p.cfg = 6;
+    int kw, cg;
+    bool alds;
+    if (groups >= 1024) {
+        kw = 1, cg = (groups + 255) / 256, alds = true;
+    } else if (groups >= 384) {
+        kw = 2, cg = tm == 1 ? (groups + 255) / 256 : (groups + 191) / 192, alds = true;
+    } else if (groups > 256) {
+        kw = 2, cg = 2, alds = true;
+    } else {
+        kw = 4, cg = 1, alds = false;
+    }
+    while (kw > 1 && nb < 2 * kw) kw /= 2;
+    const int cg0 = cg;
+    if (alds) {   // staged activations that do not fit in LDS are read from L2 instead
+        cg = cg < 16 / kw ? cg : 16 / kw;
+        while (cg > 1 && frag_lds_bytes(tm, nk, kw, cg, true) > kFragMaxLds) --cg;
+        alds = frag_lds_bytes(tm, nk, kw, cg, true) <= kFragMaxLds;
+    }
+    if (!alds) cg = cg0 < 8 / kw ? cg0 : 8 / kw;
+    p.waves = cg;
+    p.kw = kw;
+    p.alds = alds;
+    p.d = !alds && kw == 4 && tm > 1 ? 2 : 4;
+    // k steps a wave multiplies past the end: its batches rounded up to whole passes of the ring
+    auto waste = [&](int u) {
+        const int batches = (nk + u - 1) / u, per_wave = (batches + kw - 1) / kw;
+        return (((per_wave + p.d - 1) / p.d) * p.d * kw - batches) * u;
+    };
+    p.u = alds && waste(1) < waste(2) ? 1 : 2;
+    return p;
+}
+
 }  // namespace
+
+size_t frag_weight_bytes(int N, int K) {
+    return (size_t)((N + 15) / 16) * (size_t)((K / 2 + kKB - 1) / kKB) * 1024;
+}
+
+hipError_t launch_weights_to_frag(const uint8_t* Wq, int N, int K, uint8_t* Wf, hipStream_t st) {
+    const size_t units = frag_weight_bytes(N, K) / 16;
+    const size_t blocks = (units + 255) / 256;
+    hipLaunchKernelGGL(weights_to_frag_kernel, dim3((unsigned)(blocks < 16384 ? blocks : 16384)), dim3(256), 0, st, Wq,
+                       N, K, Wf);
+    return hipGetLastError();
+}
+
+hipError_t launch_gemm_frag(const uint8_t* Aq, const float* s_a, const uint8_t* Wf, const float* s_w, int M, int N,
+                            int K, uint16_t* Y, int32_t* acc, void* ws, hipStream_t st) {
+    if (M <= 16 * kShortMaxTiles) return launch_short_frag(choose_frag_short(M, N, K), Aq, s_a, Wf, s_w, M, N, K, Y, acc, st);
+    const Plan p = choose_plan(M, N, K, 4);   // the tiled plans of row-major weights
+    int32_t* part = static_cast<int32_t*>(ws);
+    hipError_t e;
+    switch (p.cfg) {
+        case 0: e = launch_tiled<4, 2, 4, 4, 4, 2, true>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, part, st); break;
+        case 1: e = launch_tiled<2, 2, 4, 4, 4, 3, true>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, part, st); break;
+        case 2: e = launch_tiled<2, 2, 2, 2, 4, 4, true>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, part, st); break;
+        default: e = launch_tiled<1, 4, 4, 2, 4, 4, true>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, part, st); break;
+    }
+    if (e != hipSuccess) return e;
+    return finish_split(p, part, s_a, s_w, M, N, Y, acc, st);
+}
 
 size_t gemm_workspace_bytes(int M, int N, int K, int bits) {
     const Plan p = choose_plan(M, N, K, bits);

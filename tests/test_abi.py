@@ -177,3 +177,34 @@ def test_fp6_entry_points_validate(lib):
     assert lib.sq_codes_to_fp6(FAKE, 4, 128, FAKE + 8, None) == L.SQ_ERR_ALIGN
     assert lib.sq_codes_to_fp6(FAKE, 4, 128, FAKE + 64, None) == L.SQ_ERR_SHAPE
     assert lib.sq_codes_to_fp6(None, 0, 128, None, None) == L.SQ_OK
+
+
+def test_frag_entry_points_validate(lib):
+    # ceil(N / 16) ceil(K / 128) 1024
+    assert lib.sq_frag_weight_bytes(16, 128) == 1024 and lib.sq_frag_weight_bytes(24, 192) == 2 * 2 * 1024
+    assert lib.sq_frag_weight_bytes(24576, 4096) == 1536 * 32 * 1024 and lib.sq_frag_weight_bytes(0, 128) == 0
+    assert lib.sq_frag_weight_bytes(16, 100) == 0 and lib.sq_frag_weight_bytes(-1, 128) == 0
+    # GEMM: K, N % 8, NULL, alignment, workspace, empty, over 2 GiB
+    args = (FAKE, FAKE, FAKE, FAKE)
+    assert lib.w4a4_gemm_frag(*args, 4, 16, 100, FAKE, None, None, 0, None) == L.SQ_ERR_SHAPE
+    assert lib.w4a4_gemm_frag(*args, 4, 12, 128, FAKE, None, None, 0, None) == L.SQ_ERR_SHAPE
+    assert lib.w4a4_gemm_frag(*args, -1, 16, 128, FAKE, None, None, 0, None) == L.SQ_ERR_SHAPE
+    assert lib.w4a4_gemm_frag(*args, 4, 16, 128, None, None, None, 0, None) == L.SQ_ERR_NULL
+    assert lib.w4a4_gemm_frag(FAKE, FAKE, None, FAKE, 4, 16, 128, FAKE, None, None, 0, None) == L.SQ_ERR_NULL
+    assert lib.w4a4_gemm_frag(FAKE, FAKE, FAKE + 8, FAKE, 4, 16, 128, FAKE, None, None, 0, None) == L.SQ_ERR_ALIGN
+    assert lib.w4a4_gemm_frag(None, None, None, None, 0, 16, 128, None, None, None, 0, None) == L.SQ_OK
+    assert lib.w4a4_gemm_frag(*args, 1 << 20, 16, 4096, FAKE, None, None, 0, None) == L.SQ_ERR_SHAPE
+    assert lib.w4a4_gemm_frag(*args, 4, 1 << 20, 4096, FAKE, None, None, 0, None) == L.SQ_ERR_SHAPE
+    need = lib.sq_gemm_workspace_bytes(96, 4096, 4096)
+    assert need > 0
+    assert lib.w4a4_gemm_frag(*args, 96, 4096, 4096, FAKE, None, None, need - 1, None) == L.SQ_ERR_WORKSPACE
+    assert lib.w4a4_gemm_frag(*args, 96, 4096, 4096, FAKE, None, None, need, None) == L.SQ_ERR_WORKSPACE
+    # conversion: K, N, NULL, alignment, overlap, empty, over 2 GiB
+    assert lib.sq_weights_to_frag(FAKE, 16, 96, FAKE + (1 << 20), None) == L.SQ_ERR_SHAPE
+    assert lib.sq_weights_to_frag(FAKE, -16, 128, FAKE + (1 << 20), None) == L.SQ_ERR_SHAPE
+    assert lib.sq_weights_to_frag(None, 16, 128, FAKE, None) == L.SQ_ERR_NULL
+    assert lib.sq_weights_to_frag(FAKE, 16, 128, FAKE + 8, None) == L.SQ_ERR_ALIGN
+    assert lib.sq_weights_to_frag(FAKE, 16, 128, FAKE + 512, None) == L.SQ_ERR_SHAPE
+    assert lib.sq_weights_to_frag(FAKE + 512, 16, 128, FAKE, None) == L.SQ_ERR_SHAPE
+    assert lib.sq_weights_to_frag(None, 0, 128, None, None) == L.SQ_OK
+    assert lib.sq_weights_to_frag(FAKE, 1 << 20, 4096, FAKE + (1 << 40), None) == L.SQ_ERR_SHAPE
