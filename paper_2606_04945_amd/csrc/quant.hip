@@ -7,13 +7,16 @@
 // clamp(rint(x_j / s), -128, 127), one signed byte per code.
 //
 // One 256-thread workgroup per row: coalesced 16-byte loads held in registers,
-// a wavefront max reduction plus one LDS exchange across the four waves, then
+// all issued before the first is used (buffer loads, whose range check reads
+// past the row, and the state of a call without one, as zero, so no branch
+// separates them and a row costs one memory round trip however long it is), a
+// wavefront max reduction plus one LDS exchange across the four waves, then
 // quantise-and-pack straight from the registers.  Two input forms:
 //   quant_f16: fp16 rows already in the P basis, with the SGAT gate applied on
 //              the fly (state select, Eq. 9-11) -- the folded-basis hot path;
 //   quant_f32: fp32 rows from the dense transform (already gated).
 // Rows longer than NV*256 vectors are read twice instead of held.
-#include "sq_internal.hpp"
+#include "tile_common.hpp"
 
 namespace sq {
 namespace {
@@ -80,14 +83,23 @@ __global__ __launch_bounds__(kThreads) void quant_f16_kernel(const uint16_t* __r
     uint8_t* qr = Aq + (size_t)row * (K * BITS / 8);
     float amax = 0.0f;
     if constexpr (NV > 0) {
+        const bool gated = state != nullptr;
+        const __amdgpu_buffer_rsrc_t rX = make_rsrc(xr, (uint32_t)K * 2);
+        const __amdgpu_buffer_rsrc_t rS = make_rsrc(state, gated ? (uint32_t)row + 1 : 0u);
+        v4i raw[NV];
+#pragma unroll
+        for (int i = 0; i < NV; ++i)
+            raw[i] = __builtin_amdgcn_raw_buffer_load_b128(rX, ((int)threadIdx.x + i * kThreads) * 16, 0, 0);
+        const bool masked = __builtin_amdgcn_raw_buffer_load_b8(rS, row, 0, 0) != 0;
         float x[NV][8];
 #pragma unroll
         for (int i = 0; i < NV; ++i) {
             const int v = threadIdx.x + i * kThreads;
-            if (v < nvec) {
-                load_f16x8(xr + v * 8, state, row, v * 8, K, dm, du, x[i]);
+            const uint16_t* h = reinterpret_cast<const uint16_t*>(&raw[i]);
 #pragma unroll
-                for (int q = 0; q < 8; ++q) amax = fmaxf(amax, fabsf(x[i][q]));
+            for (int q = 0; q < 8; ++q) {
+                x[i][q] = (!gated | kept_sel(v * 8 + q, K, dm, du, masked)) ? h2f(h[q]) : 0.0f;
+                amax = fmaxf(amax, fabsf(x[i][q]));
             }
         }
         const float s = block_max(amax, red) / qmaxf<BITS>();
@@ -129,16 +141,23 @@ __global__ __launch_bounds__(kThreads) void quant_f32_kernel(const float* __rest
         x[0] = a.x, x[1] = a.y, x[2] = a.z, x[3] = a.w, x[4] = b.x, x[5] = b.y, x[6] = b.z, x[7] = b.w;
     };
     if constexpr (NV > 0) {
+        const __amdgpu_buffer_rsrc_t rX = make_rsrc(xr, (uint32_t)K * 4);
+        v4i raw[NV][2];
+#pragma unroll
+        for (int i = 0; i < NV; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+                raw[i][j] = __builtin_amdgcn_raw_buffer_load_b128(rX, ((int)threadIdx.x + i * kThreads) * 32 + 16 * j,
+                                                                  0, 0);
         float x[NV][8];
 #pragma unroll
-        for (int i = 0; i < NV; ++i) {
-            const int v = threadIdx.x + i * kThreads;
-            if (v < nvec) {
-                ld(v, x[i]);
+        for (int i = 0; i < NV; ++i)
 #pragma unroll
-                for (int q = 0; q < 8; ++q) amax = fmaxf(amax, fabsf(x[i][q]));
+            for (int q = 0; q < 8; ++q) {
+                const int b = raw[i][q / 4][q % 4];   // copied out first: a bit cast of a vector element reads element 0
+                x[i][q] = __builtin_bit_cast(float, b);
+                amax = fmaxf(amax, fabsf(x[i][q]));
             }
-        }
         const float s = block_max(amax, red) / qmaxf<BITS>();
         if (threadIdx.x == 0) s_out[row] = s;
 #pragma unroll

@@ -51,6 +51,12 @@ __device__ __forceinline__ bool kept(int j, int K, int dm, int du, bool masked) 
     return j < m_lo || (j < u_lo ? masked : !masked);
 }
 
+// The same without control flow (bitwise on the comparisons), for use between
+// loads that must all be in flight together.
+__device__ __forceinline__ bool kept_sel(int j, int K, int dm, int du, bool masked) {
+    return (j < K - dm - du) | ((j < K - du) == masked);
+}
+
 // Symmetric int4 code of x for scale s (s > 0): clamp(rint(x / s), -8, 7).
 // `/` is the correctly rounded fp32 divide (built without fast-math).
 __device__ __forceinline__ int quant4(float x, float s) {

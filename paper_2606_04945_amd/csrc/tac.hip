@@ -9,7 +9,7 @@
 // block matrices and the token tile through LDS as fp32, and each thread keeps
 // 8 tokens x 8 channels of accumulators (8 x 4 when g < 8), so each pair of
 // LDS reads feeds 64 (32) fused multiply-adds.
-#include "sq_internal.hpp"
+#include "tile_common.hpp"
 
 namespace sq {
 namespace {
@@ -206,32 +206,50 @@ __global__ __launch_bounds__(kFusedThreads) void tac_quant_kernel(const uint16_t
     const bool active = 8 * t < K;
     const int c0 = 8 * t;                               // first output channel of this thread
     const int z0 = (c0 / ZW) * ZW;                      // first input channel it reads
-    float m[8][G];                                      // tac_M viewed as [K][G]: rows c0 .. c0 + 7
-    float dv[8];
-    if (active) {
-#pragma unroll
-        for (int r = 0; r < 8; ++r) {
-#pragma unroll
-            for (int c = 0; c < G; ++c) m[r][c] = h2f(Mb[(size_t)(c0 + r) * G + c]);
-            dv[r] = h2f(d[c0 + r]);
-        }
-    }
     const int row_begin = blockIdx.x * rows_per_wg;
     const int row_end = min(M, row_begin + rows_per_wg);
+    // A row's inputs (its activations and state byte) are requested before the
+    // previous row's work, the first row's around the block parameters, so these
+    // fetches overlap instead of following one another.  Buffer loads: inactive
+    // threads and a call without states read zeros, with no branch.
+    const bool gated = state != nullptr;
+    const __amdgpu_buffer_rsrc_t rS = make_rsrc(state, gated ? (uint32_t)M : 0u);
+    v4i zr[ZW / 8];
+    uint32_t sb = 0;
+    auto fetch_z = [&](int row) {
+        const __amdgpu_buffer_rsrc_t rz = make_rsrc(Z + (size_t)row * K, (uint32_t)K * 2);
+#pragma unroll
+        for (int v = 0; v < ZW / 8; ++v)
+            zr[v] = __builtin_amdgcn_raw_buffer_load_b128(rz, active ? (z0 + 8 * v) * 2 : (int)kOOB, 0, 0);
+    };
+    auto fetch_s = [&](int row) { sb = __builtin_amdgcn_raw_buffer_load_b8(rS, row, 0, 0); };
+    if (row_begin < row_end) fetch_z(row_begin);
+    float m[8][G];                                      // tac_M viewed as [K][G]: rows c0 .. c0 + 7
+    float dv[8];
+    const int cm = active ? c0 : 0;                     // inactive threads read the first rows, unused
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+#pragma unroll
+        for (int c = 0; c < G; ++c) m[r][c] = h2f(Mb[(size_t)(cm + r) * G + c]);
+        dv[r] = h2f(d[cm + r]);
+    }
+    if (row_begin < row_end) fetch_s(row_begin);
     for (int row = row_begin; row < row_end; ++row) {
         float o[8];
         float amax = 0.0f;
+        float z[ZW];
+#pragma unroll
+        for (int v = 0; v < ZW / 8; ++v) {
+            const uint16_t* h = reinterpret_cast<const uint16_t*>(&zr[v]);
+#pragma unroll
+            for (int i = 0; i < 8; ++i) z[8 * v + i] = h2f(h[i]);
+        }
+        const bool masked = sb != 0;
+        if (row + 1 < row_end) {
+            fetch_z(row + 1);
+            fetch_s(row + 1);
+        }
         if (active) {
-            float z[ZW];
-            const uint4* src = reinterpret_cast<const uint4*>(Z + (size_t)row * K + z0);
-#pragma unroll
-            for (int v = 0; v < ZW / 8; ++v) {
-                const uint4 q = src[v];
-                const uint16_t* h = reinterpret_cast<const uint16_t*>(&q);
-#pragma unroll
-                for (int i = 0; i < 8; ++i) z[8 * v + i] = h2f(h[i]);
-            }
-            const bool masked = state ? state[row] != 0 : false;
 #pragma unroll
             for (int r = 0; r < 8; ++r) {
                 const int base = ((c0 - z0 + r) / G) * G;   // block start within z[]
@@ -239,7 +257,7 @@ __global__ __launch_bounds__(kFusedThreads) void tac_quant_kernel(const uint16_t
 #pragma unroll
                 for (int c = 0; c < G; ++c) acc = __builtin_fmaf(m[r][c], z[base + c], acc);
                 const float v = h2f(f2h(acc + dv[r]));  // TAC output, materialised as fp16
-                o[r] = (!state || kept(c0 + r, K, dm, du, masked)) ? v : 0.0f;
+                o[r] = (!gated | kept_sel(c0 + r, K, dm, du, masked)) ? v : 0.0f;
                 amax = fmaxf(amax, fabsf(o[r]));
             }
         }

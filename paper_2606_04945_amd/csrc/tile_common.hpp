@@ -1,7 +1,7 @@
 // Building blocks shared by the MFMA tile kernels (the W4A4 / W8A8 GEMM and the
-// MFMA transform): buffer descriptors whose range check turns out-of-range
-// reads into zeros, direct global-to-LDS loads, and the counter wait the
-// three-stage pipelines use.
+// MFMA transform) and the quantisers: buffer descriptors whose range check turns
+// out-of-range reads into zeros, direct global-to-LDS loads, and the counter
+// wait the three-stage pipelines use.
 #pragma once
 #include "sq_internal.hpp"
 
