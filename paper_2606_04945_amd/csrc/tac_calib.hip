@@ -23,7 +23,8 @@
 //    ordering, and the singular value decomposition of M by one-sided
 //    (Hestenes) Jacobi, whose singular values keep full relative accuracy.
 //    Matrices live in the workspace (g x g fp64, up to 128 KB each); the two
-//    a Jacobi iteration updates every round are staged in LDS for g <= 64.
+//    a Jacobi iteration updates every round are staged in LDS for g <= 64, and
+//    for g = 128 the rotated matrix sits in LDS and the vectors in registers.
 // Results depend only on the inputs (every sum has a fixed order); they agree
 // with an fp64 LAPACK evaluation to rounding, not bit for bit.
 #include "sq_internal.hpp"
@@ -301,6 +302,221 @@ __device__ void jacobi_svd(double* G, double* V, int g, double* cs, int* flag) {
     }
 }
 
+// g = 128: two g x g fp64 matrices (256 KB) do not fit in LDS together, and
+// updating them in global memory made every round a chain of dependent memory
+// round trips.  The matrix the rotations act on two-sidedly (A) or whose
+// columns they combine (G) stays in LDS; the vector matrix V lives in registers,
+// each row split over a lane pair: lane 2 i + h holds half h of row i.  V's
+// columns are kept in round-robin *position* order (position k holds column
+// rr_player(k, r)), half 0 holding positions 0 .. g/2 - 1 at index k and half 1
+// positions g - 1 .. g/2 at index k (position g - 1 - k), so that every round's
+// pair t (positions t and g - 1 - t) sits at index t in both lanes and all
+// register indices are static.  Between rounds positions 1 .. g - 1 shift
+// cyclically by one.  After a whole sweep (g - 1 rounds) position order is
+// column order again, and the sweep loops only stop at sweep boundaries.
+// Rotations and sums are those of jacobi_eigh and jacobi_svd; only where the
+// data lives differs (and, for the SVD, the column sums are split four ways and
+// added in a fixed order).
+constexpr int kRegBlock = 128;
+
+// The value held by the other lane of this lane's pair (lanes 2 i, 2 i + 1).
+__device__ __forceinline__ double pair_swap(double x) {
+    const unsigned long long u = (unsigned long long)__double_as_longlong(x);
+    const int lo = __builtin_amdgcn_mov_dpp((int)(unsigned)u, 0xB1, 0xF, 0xF, false);   // quad_perm [1, 0, 3, 2]
+    const int hi = __builtin_amdgcn_mov_dpp((int)(unsigned)(u >> 32), 0xB1, 0xF, 0xF, false);
+    return __longlong_as_double((long long)(((unsigned long long)(unsigned)hi << 32) | (unsigned)lo));
+}
+
+// Half h of row i of the identity, in position order at the start of a sweep.
+template <int G>
+__device__ __forceinline__ void half_identity(double (&v)[G / 2], int i, bool h1) {
+#pragma unroll
+    for (int k = 0; k < G / 2; ++k) v[k] = (h1 ? G - 1 - k : k) == i ? 1.0 : 0.0;
+}
+
+template <int G>
+__device__ __forceinline__ void store_half(const double (&v)[G / 2], double* Vout, int i, bool h1) {
+#pragma unroll
+    for (int k = 0; k < G / 2; ++k) Vout[i * G + (h1 ? G - 1 - k : k)] = v[k];
+}
+
+// One round on the lane pair's row: pair t holds columns (a, b) = (rr_player(t),
+// rr_player(g - 1 - t)); with p = min(a, b) the rotation is (v_p, v_q) <- (c v_p
+// - s v_q, s v_p + c v_q), the same map on (v_a, v_b) with s negated when a > b;
+// sg[t] holds that signed s.  Then the shift to the next round's positions.
+template <int G>
+__device__ __forceinline__ void rotate_pairs(double (&v)[G / 2], bool h1, const double* cs, const double* sg) {
+    constexpr int H = G / 2, CH = 8;
+    static_assert(H % CH == 0, "chunks of pairs");
+    // chunks of pairs, so that the rotation parameters are read as they are used
+    // and do not all sit in registers at once
+#pragma unroll
+    for (int t0 = 0; t0 < H; t0 += CH) {
+#pragma unroll
+        for (int t = t0; t < t0 + CH; ++t) {
+            const double c = cs[2 * t], sp = sg[t];
+            const double mine = v[t], other = pair_swap(mine);
+            v[t] = h1 ? sp * other + c * mine : c * mine - sp * other;
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    // half 0 moves down one index and takes position g/2 from its partner's
+    // last index; half 1 moves up one index and takes position 1 from its
+    // partner's index 1; position 0 stays.  In place, in ascending index order,
+    // carrying the old value of the previous index for half 1.
+    const double from_hi = pair_swap(v[H - 1]), from_lo = pair_swap(v[1]);
+    double prev = v[0];
+    v[0] = h1 ? from_lo : v[0];
+#pragma unroll
+    for (int k = 1; k < H - 1; ++k) {
+        const double cur = v[k];
+        v[k] = h1 ? prev : v[k + 1];
+        prev = cur;
+    }
+    v[H - 1] = h1 ? prev : from_hi;
+}
+
+// Symmetric eigendecomposition, A in LDS (eigenvalues end on its diagonal),
+// eigenvectors into the columns of Vout (global), V by lane-pair rows as above.  One two-sided update per
+// round over 2 x 2 blocks: block (t1, t2) takes rows (p1, q1) and columns (p2,
+// q2), rotated first by columns (A J) then by rows (J^T), the order and
+// arithmetic of jacobi_eigh's two passes.
+template <int G>
+__device__ __forceinline__ void jacobi_eigh_reg(double* A, double* Vout, double* cs, double* sg, int* pq, double* red) {
+    constexpr int H = G / 2;
+    static_assert(2 * G <= kCalThreads, "a lane pair per row");
+    const int tid = threadIdx.x;
+    const int row = tid / 2;
+    const bool h1 = tid & 1;
+    double v[H];
+    half_identity<G>(v, row, h1);
+    for (int sweep = 0; sweep < 60; ++sweep) {
+        double off = 0.0, tot = 0.0;
+        for (int e = tid; e < G * G; e += kCalThreads) {
+            const double a2 = A[e] * A[e];
+            tot += a2;
+            if (e / G != e % G) off += a2;
+        }
+        off = wg_sum(off, red);
+        tot = wg_sum(tot, red);
+        if (!(off > 1e-30 * tot)) break;                  // also stops on a zero matrix
+        for (int r = 0; r < G - 1; ++r) {
+            if (tid < H) {
+                int p, q;
+                rr_pair(tid, r, G, p, q);
+                const double apq = A[p * G + q];
+                double c = 1.0, s = 0.0;
+                if (apq != 0.0) {
+                    const double tau = (A[q * G + q] - A[p * G + p]) / (2.0 * apq);
+                    const double t = fabs(tau) > 1e150 ? 0.5 / tau
+                                                       : (tau >= 0.0 ? 1.0 : -1.0) / (fabs(tau) + sqrt(1.0 + tau * tau));
+                    c = 1.0 / sqrt(1.0 + t * t);
+                    s = t * c;
+                }
+                cs[2 * tid] = c;
+                cs[2 * tid + 1] = s;
+                sg[tid] = rr_player(tid, r, G) == p ? s : -s;
+                pq[2 * tid] = p;
+                pq[2 * tid + 1] = q;
+            }
+            __syncthreads();
+#pragma unroll 2
+            for (int blk = tid; blk < H * H; blk += kCalThreads) {
+                const int t1 = blk / H, t2 = blk % H;
+                const int p1 = pq[2 * t1], q1 = pq[2 * t1 + 1], p2 = pq[2 * t2], q2 = pq[2 * t2 + 1];
+                const double c1 = cs[2 * t1], s1 = cs[2 * t1 + 1], c2 = cs[2 * t2], s2 = cs[2 * t2 + 1];
+                const double a00 = A[p1 * G + p2], a01 = A[p1 * G + q2], a10 = A[q1 * G + p2], a11 = A[q1 * G + q2];
+                const double b00 = c2 * a00 - s2 * a01, b01 = s2 * a00 + c2 * a01;   // columns: A J
+                const double b10 = c2 * a10 - s2 * a11, b11 = s2 * a10 + c2 * a11;
+                A[p1 * G + p2] = c1 * b00 - s1 * b10;                                  // rows: J^T (A J)
+                A[q1 * G + p2] = s1 * b00 + c1 * b10;
+                A[p1 * G + q2] = c1 * b01 - s1 * b11;
+                A[q1 * G + q2] = s1 * b01 + c1 * b11;
+            }
+            rotate_pairs<G>(v, h1, cs, sg);
+            __syncthreads();
+        }
+    }
+    store_half<G>(v, Vout, row, h1);
+    __syncthreads();
+}
+
+// One-sided Jacobi SVD of Gm (g x g, in LDS): on return its columns are
+// u_j sigma_j and Vout (global) holds the right singular vectors.  Each pair's
+// three column sums are split over four threads (rows i = 4 k + j ... ) and
+// added in the fixed order (s0 + s1) + (s2 + s3).
+template <int G>
+__device__ __forceinline__ void jacobi_svd_reg(double* Gm, double* Vout, double* cs, double* sg, int* flag) {
+    constexpr int H = G / 2;
+    static_assert(4 * H <= kCalThreads && 2 * G <= kCalThreads, "four threads per pair, a lane pair per row");
+    const int tid = threadIdx.x;
+    const int row = tid / 2;
+    const bool h1 = tid & 1;
+    double v[H];
+    half_identity<G>(v, row, h1);
+    for (int sweep = 0; sweep < 60; ++sweep) {
+        if (tid == 0) *flag = 0;
+        __syncthreads();
+        for (int r = 0; r < G - 1; ++r) {
+            const int t = tid / 4, j = tid % 4;
+            int p = 0, q = 1;
+            double al = 0.0, be = 0.0, ga = 0.0;
+            if (t < H) {
+                rr_pair(t, r, G, p, q);
+#pragma unroll 4
+                for (int i = j; i < G; i += 4) {
+                    const double x = Gm[i * G + p], y = Gm[i * G + q];
+                    al = fma(x, x, al);
+                    be = fma(y, y, be);
+                    ga = fma(x, y, ga);
+                }
+            }
+            // lanes 4 t .. 4 t + 3 are consecutive in one wave: (s0 + s1) + (s2 + s3)
+            al += __shfl_xor(al, 1);
+            be += __shfl_xor(be, 1);
+            ga += __shfl_xor(ga, 1);
+            al += __shfl_xor(al, 2);
+            be += __shfl_xor(be, 2);
+            ga += __shfl_xor(ga, 2);
+            if (t < H && j == 0) {
+                double c = 1.0, s = 0.0;
+                if (ga != 0.0 && fabs(ga) > 1e-15 * sqrt(al * be)) {
+                    const double zeta = (be - al) / (2.0 * ga);
+                    const double tt = fabs(zeta) > 1e150
+                                          ? 0.5 / zeta
+                                          : (zeta >= 0.0 ? 1.0 : -1.0) / (fabs(zeta) + sqrt(1.0 + zeta * zeta));
+                    c = 1.0 / sqrt(1.0 + tt * tt);
+                    s = tt * c;
+                    *flag = 1;
+                }
+                cs[2 * t] = c;
+                cs[2 * t + 1] = s;
+                sg[t] = rr_player(t, r, G) == p ? s : -s;
+            }
+            __syncthreads();
+#pragma unroll 2
+            for (int e = tid; e < G * H; e += kCalThreads) {
+                const int i = e / H, tt = e % H;
+                int pp, qq;
+                rr_pair(tt, r, G, pp, qq);
+                const double c = cs[2 * tt], s = cs[2 * tt + 1];
+                const double gp = Gm[i * G + pp], gq = Gm[i * G + qq];
+                Gm[i * G + pp] = c * gp - s * gq;
+                Gm[i * G + qq] = s * gp + c * gq;
+            }
+            rotate_pairs<G>(v, h1, cs, sg);
+            __syncthreads();
+        }
+        if (*flag == 0) break;
+        __syncthreads();
+    }
+    store_half<G>(v, Vout, row, h1);
+    __syncthreads();
+}
+
+// REG: g = 128, the Jacobi matrix in LDS and V in registers (see jacobi_eigh_reg);
+// otherwise both Jacobi matrices in LDS for g <= 64, in the workspace above.
+template <bool REG>
 __global__ __launch_bounds__(kCalThreads) void tac_finalize_kernel(const double* __restrict__ part, int chunks,
                                                                   int N, int C, int g, double rho, double eps,
                                                                   double eta, double alpha, double* __restrict__ wk,
@@ -310,15 +526,17 @@ __global__ __launch_bounds__(kCalThreads) void tac_finalize_kernel(const double*
     __shared__ double red[kCalThreads];
     __shared__ double cs[128];
     __shared__ double w[128];
+    __shared__ double sg[64];
+    __shared__ int pq[128];
     __shared__ int flag;
-    extern __shared__ double lds_mats[];               // 2 g^2 doubles when g <= 64
+    extern __shared__ double lds_mats[];               // 2 g^2 doubles when g <= 64, g^2 for REG
     const int tid = threadIdx.x;
     const int b = blockIdx.x;
     const int B = C / g;
     const size_t gg = (size_t)g * g;
     // the Jacobi iterations touch their two matrices every round: in LDS when
     // they fit, else in the workspace
-    const bool local = g <= kLdsBlock;
+    const bool local = !REG && g <= kLdsBlock;
     auto stage_in = [&](const double* src) {
         for (int e = tid; e < (int)gg; e += kCalThreads) lds_mats[e] = src[e];
         __syncthreads();
@@ -328,6 +546,10 @@ __global__ __launch_bounds__(kCalThreads) void tac_finalize_kernel(const double*
             a[e] = lds_mats[e];
             v[e] = lds_mats[gg + e];
         }
+        __syncthreads();
+    };
+    auto stage_out_a = [&](double* a) {               // REG: V was written by the solver
+        for (int e = tid; e < (int)gg; e += kCalThreads) a[e] = lds_mats[e];
         __syncthreads();
     };
     double* base = wk + (size_t)b * (6 * gg + 3 * g);
@@ -372,7 +594,11 @@ __global__ __launch_bounds__(kCalThreads) void tac_finalize_kernel(const double*
     for (int k = tid; k < g; k += kCalThreads) Sq[k * g + k] += lam;
     __syncthreads();
     // covariance matching
-    if (local) {
+    if (REG) {
+        stage_in(Sf);
+        jacobi_eigh_reg<kRegBlock>(lds_mats, V, cs, sg, pq, red);
+        stage_out_a(Sf);
+    } else if (local) {
         stage_in(Sf);
         jacobi_eigh(lds_mats, lds_mats + gg, g, cs, red);
         stage_out(Sf, V);
@@ -380,7 +606,11 @@ __global__ __launch_bounds__(kCalThreads) void tac_finalize_kernel(const double*
         jacobi_eigh(Sf, V, g, cs, red);
     }
     eig_power(Sf, V, R1, g, false, w);
-    if (local) {
+    if (REG) {
+        stage_in(Sq);
+        jacobi_eigh_reg<kRegBlock>(lds_mats, V, cs, sg, pq, red);
+        stage_out_a(Sq);
+    } else if (local) {
         stage_in(Sq);
         jacobi_eigh(lds_mats, lds_mats + gg, g, cs, red);
         stage_out(Sq, V);
@@ -396,7 +626,11 @@ __global__ __launch_bounds__(kCalThreads) void tac_finalize_kernel(const double*
     }
     __syncthreads();
     // singular value smoothing
-    if (local) {
+    if (REG) {
+        stage_in(G);
+        jacobi_svd_reg<kRegBlock>(lds_mats, V, cs, sg, &flag);
+        stage_out_a(G);
+    } else if (local) {
         stage_in(G);
         jacobi_svd(lds_mats, lds_mats + gg, g, cs, &flag);
         stage_out(G, V);
@@ -494,9 +728,18 @@ hipError_t launch_tac_calib(const uint16_t* Zf, const uint16_t* Zq, int N, int C
         default: e = launch_stats<128>(Zf, Zq, N, C, per, chunks, part, st); break;
     }
     if (e != hipSuccess) return e;
+    if (g == kRegBlock) {
+        static const hipError_t attr =     // above the 64 KB default for dynamic LDS
+            hipFuncSetAttribute(reinterpret_cast<const void*>(&tac_finalize_kernel<true>),
+                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)(gg * sizeof(double)));
+        if (attr != hipSuccess) return attr;
+        hipLaunchKernelGGL(tac_finalize_kernel<true>, dim3((unsigned)B), dim3(kCalThreads), gg * sizeof(double), st,
+                           part, chunks, N, C, g, rho, eps, eta, alpha, wk, tac_M, tac_d, M64, d64);
+        return hipGetLastError();
+    }
     const size_t lds = g <= kLdsBlock ? 2 * gg * sizeof(double) : 0;
-    hipLaunchKernelGGL(tac_finalize_kernel, dim3((unsigned)B), dim3(kCalThreads), lds, st, part, chunks, N, C, g,
-                       rho, eps, eta, alpha, wk, tac_M, tac_d, M64, d64);
+    hipLaunchKernelGGL(tac_finalize_kernel<false>, dim3((unsigned)B), dim3(kCalThreads), lds, st, part, chunks, N, C,
+                       g, rho, eps, eta, alpha, wk, tac_M, tac_d, M64, d64);
     return hipGetLastError();
 }
 
