@@ -36,22 +36,27 @@ __device__ __forceinline__ float block_max(float v, float* red) {
 
 // 8 values -> their codes, stored at code index 8v of the row: 4 bytes (4-bit)
 // or 8 bytes (8-bit)
+// (y = 1 / s, see quant_codes8)
 template <int BITS>
-__device__ __forceinline__ void store8(uint8_t* row, int v, const float* x, float s) {
+__device__ __forceinline__ void store8(uint8_t* row, int v, const float* x, float s, float y) {
     if (BITS == 4) {
         uint32_t out = 0;
         if (s != 0.0f) {
+            int c[8];
+            quant_codes8<7>(x, s, y, c);
 #pragma unroll
-            for (int q = 0; q < 8; ++q) out |= (uint32_t)(quant4(x[q], s) & 15) << (4 * q);
+            for (int q = 0; q < 8; ++q) out |= (uint32_t)(c[q] & 15) << (4 * q);
         }
         reinterpret_cast<uint32_t*>(row)[v] = out;
     } else {
         uint32_t lo = 0, hi = 0;
         if (s != 0.0f) {
+            int c[8];
+            quant_codes8<127>(x, s, y, c);
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
-                lo |= (uint32_t)(quant8(x[q], s) & 255) << (8 * q);
-                hi |= (uint32_t)(quant8(x[4 + q], s) & 255) << (8 * q);
+                lo |= (uint32_t)(c[q] & 255) << (8 * q);
+                hi |= (uint32_t)(c[4 + q] & 255) << (8 * q);
             }
         }
         reinterpret_cast<uint2*>(row)[v] = make_uint2(lo, hi);
@@ -103,11 +108,12 @@ __global__ __launch_bounds__(kThreads) void quant_f16_kernel(const uint16_t* __r
             }
         }
         const float s = block_max(amax, red) / qmaxf<BITS>();
+        const float y = s != 0.0f ? 1.0f / s : 0.0f;
         if (threadIdx.x == 0) s_out[row] = s;
 #pragma unroll
         for (int i = 0; i < NV; ++i) {
             const int v = threadIdx.x + i * kThreads;
-            if (v < nvec) store8<BITS>(qr, v, x[i], s);
+            if (v < nvec) store8<BITS>(qr, v, x[i], s, y);
         }
     } else {
         float x[8];
@@ -117,10 +123,11 @@ __global__ __launch_bounds__(kThreads) void quant_f16_kernel(const uint16_t* __r
             for (int q = 0; q < 8; ++q) amax = fmaxf(amax, fabsf(x[q]));
         }
         const float s = block_max(amax, red) / qmaxf<BITS>();
+        const float y = s != 0.0f ? 1.0f / s : 0.0f;
         if (threadIdx.x == 0) s_out[row] = s;
         for (int v = threadIdx.x; v < nvec; v += kThreads) {
             load_f16x8(xr + v * 8, state, row, v * 8, K, dm, du, x);
-            store8<BITS>(qr, v, x, s);
+            store8<BITS>(qr, v, x, s, y);
         }
     }
 }
@@ -159,11 +166,12 @@ __global__ __launch_bounds__(kThreads) void quant_f32_kernel(const float* __rest
                 amax = fmaxf(amax, fabsf(x[i][q]));
             }
         const float s = block_max(amax, red) / qmaxf<BITS>();
+        const float y = s != 0.0f ? 1.0f / s : 0.0f;
         if (threadIdx.x == 0) s_out[row] = s;
 #pragma unroll
         for (int i = 0; i < NV; ++i) {
             const int v = threadIdx.x + i * kThreads;
-            if (v < nvec) store8<BITS>(qr, v, x[i], s);
+            if (v < nvec) store8<BITS>(qr, v, x[i], s, y);
         }
     } else {
         float x[8];
@@ -173,10 +181,11 @@ __global__ __launch_bounds__(kThreads) void quant_f32_kernel(const float* __rest
             for (int q = 0; q < 8; ++q) amax = fmaxf(amax, fabsf(x[q]));
         }
         const float s = block_max(amax, red) / qmaxf<BITS>();
+        const float y = s != 0.0f ? 1.0f / s : 0.0f;
         if (threadIdx.x == 0) s_out[row] = s;
         for (int v = threadIdx.x; v < nvec; v += kThreads) {
             ld(v, x);
-            store8<BITS>(qr, v, x, s);
+            store8<BITS>(qr, v, x, s, y);
         }
     }
 }

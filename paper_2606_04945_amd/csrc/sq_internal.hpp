@@ -72,6 +72,42 @@ __device__ __forceinline__ int quant8(float x, float s) {
     return (int)r;
 }
 
+// The same code as quant4 (QMAX = 7) or quant8 (QMAX = 127), given also
+// y = 1 / s correctly rounded, with a multiply in place of most divides.  y and
+// the product x y each round once, and fl(x / s) once, so x y is within
+// 3 2^-24 |x / s| of fl(x / s).  Where the clamp does not decide the code,
+// |x / s| < QMAX + 2, so the two are less than half of kNear (2^-18, resp.
+// 2^-14) apart; when x y is farther than kNear from every half-integer both lie
+// between the same two half-integers and rint gives the same integer.  Where
+// the clamp decides it, both roundings land beyond the same end of the range.
+// Only the remaining x take the divide, and so do NaN and infinite products
+// (the comparison is written to be false for NaN), which covers y = inf from a
+// subnormal s and non-finite inputs.  Eight codes at a time, with one (rarely
+// taken) branch for the group.
+template <int QMAX>
+__device__ __forceinline__ void quant_codes8(const float* x, float s, float y, int* code) {
+    constexpr float kNear = QMAX == 7 ? 0x1p-18f : 0x1p-14f;
+    static_assert(QMAX == 7 || QMAX == 127, "4- or 8-bit codes");
+    float r[8];
+    bool near = false;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+        const float q0 = x[q] * y;
+        r[q] = __builtin_rintf(q0);
+        near |= !(0.5f - fabsf(q0 - r[q]) > kNear);
+    }
+    if (__builtin_expect(near, 0)) {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            const float q0 = x[q] * y;
+            if (!(0.5f - fabsf(q0 - r[q]) > kNear)) r[q] = __builtin_rintf(x[q] / s);
+        }
+    }
+    constexpr float lo = -(QMAX + 1.0f), hi = (float)QMAX;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) code[q] = (int)(r[q] < lo ? lo : (r[q] > hi ? hi : r[q]));
+}
+
 __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));

@@ -262,22 +262,27 @@ __global__ __launch_bounds__(kFusedThreads) void tac_quant_kernel(const uint16_t
             }
         }
         const float s = block_max_db(amax, red, row & 1) / (BITS == 4 ? 7.0f : 127.0f);
+        const float y = s != 0.0f ? 1.0f / s : 0.0f;
         if (t == 0) s_out[row] = s;
         if (active) {
             if (BITS == 4) {
                 uint32_t w = 0;
                 if (s != 0.0f) {
+                    int c[8];
+                    quant_codes8<7>(o, s, y, c);
 #pragma unroll
-                    for (int q = 0; q < 8; ++q) w |= (uint32_t)(quant4(o[q], s) & 15) << (4 * q);
+                    for (int q = 0; q < 8; ++q) w |= (uint32_t)(c[q] & 15) << (4 * q);
                 }
                 *reinterpret_cast<uint32_t*>(Aq + (size_t)row * (K / 2) + 4 * t) = w;
             } else {
                 uint32_t lo = 0, hi = 0;
                 if (s != 0.0f) {
+                    int c[8];
+                    quant_codes8<127>(o, s, y, c);
 #pragma unroll
                     for (int q = 0; q < 4; ++q) {
-                        lo |= (uint32_t)(quant8(o[q], s) & 255) << (8 * q);
-                        hi |= (uint32_t)(quant8(o[4 + q], s) & 255) << (8 * q);
+                        lo |= (uint32_t)(c[q] & 255) << (8 * q);
+                        hi |= (uint32_t)(c[4 + q] & 255) << (8 * q);
                     }
                 }
                 *reinterpret_cast<uint2*>(Aq + (size_t)row * K + 8 * t) = make_uint2(lo, hi);
