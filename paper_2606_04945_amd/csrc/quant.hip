@@ -16,6 +16,12 @@
 //              the fly (state select, Eq. 9-11) -- the folded-basis hot path;
 //   quant_f32: fp32 rows from the dense transform (already gated).
 // Rows longer than NV*256 vectors are read twice instead of held.
+//
+// Few rows (decode-sized batches) would leave most of the chip idle with one
+// workgroup per row, and each lane's chain of NV vectors then sets the time.
+// There the quantisers run `slices` workgroups per row: each reads the whole row
+// and forms the same absmax (max is exact and order-free, so every slice
+// derives the identical s), and quantises only its own vector of each lane.
 #include "tile_common.hpp"
 
 namespace sq {
@@ -79,10 +85,10 @@ __device__ __forceinline__ void load_f16x8(const uint16_t* p, const uint8_t* sta
 template <int NV, int BITS>
 __global__ __launch_bounds__(kThreads) void quant_f16_kernel(const uint16_t* __restrict__ X,
                                                              const uint8_t* __restrict__ state, int K, int dm,
-                                                             int du, uint8_t* __restrict__ Aq,
+                                                             int du, int slices, uint8_t* __restrict__ Aq,
                                                              float* __restrict__ s_out) {
     __shared__ float red[kThreads / kWave];
-    const int row = blockIdx.x;
+    const int row = blockIdx.x / slices, slice = blockIdx.x % slices;
     const int nvec = K / 8;
     const uint16_t* xr = X + (size_t)row * K;
     uint8_t* qr = Aq + (size_t)row * (K * BITS / 8);
@@ -109,11 +115,11 @@ __global__ __launch_bounds__(kThreads) void quant_f16_kernel(const uint16_t* __r
         }
         const float s = block_max(amax, red) / qmaxf<BITS>();
         const float y = s != 0.0f ? 1.0f / s : 0.0f;
-        if (threadIdx.x == 0) s_out[row] = s;
+        if (threadIdx.x == 0 && slice == 0) s_out[row] = s;
 #pragma unroll
         for (int i = 0; i < NV; ++i) {
             const int v = threadIdx.x + i * kThreads;
-            if (v < nvec) store8<BITS>(qr, v, x[i], s, y);
+            if ((slices == 1 || i == slice) && v < nvec) store8<BITS>(qr, v, x[i], s, y);
         }
     } else {
         float x[8];
@@ -134,10 +140,10 @@ __global__ __launch_bounds__(kThreads) void quant_f16_kernel(const uint16_t* __r
 
 // fp32 input (already gated); NV vectors of 8 floats per thread (NV == 0: reload).
 template <int NV, int BITS>
-__global__ __launch_bounds__(kThreads) void quant_f32_kernel(const float* __restrict__ X, int K,
+__global__ __launch_bounds__(kThreads) void quant_f32_kernel(const float* __restrict__ X, int K, int slices,
                                                              uint8_t* __restrict__ Aq, float* __restrict__ s_out) {
     __shared__ float red[kThreads / kWave];
-    const int row = blockIdx.x;
+    const int row = blockIdx.x / slices, slice = blockIdx.x % slices;
     const int nvec = K / 8;
     const float* xr = X + (size_t)row * K;
     uint8_t* qr = Aq + (size_t)row * (K * BITS / 8);
@@ -167,11 +173,11 @@ __global__ __launch_bounds__(kThreads) void quant_f32_kernel(const float* __rest
             }
         const float s = block_max(amax, red) / qmaxf<BITS>();
         const float y = s != 0.0f ? 1.0f / s : 0.0f;
-        if (threadIdx.x == 0) s_out[row] = s;
+        if (threadIdx.x == 0 && slice == 0) s_out[row] = s;
 #pragma unroll
         for (int i = 0; i < NV; ++i) {
             const int v = threadIdx.x + i * kThreads;
-            if (v < nvec) store8<BITS>(qr, v, x[i], s, y);
+            if ((slices == 1 || i == slice) && v < nvec) store8<BITS>(qr, v, x[i], s, y);
         }
     } else {
         float x[8];
@@ -196,16 +202,25 @@ hipError_t by_nv(int K, A... args) {
     if (per <= 1) return Launch<1, BITS>::run(args...);
     if (per <= 2) return Launch<2, BITS>::run(args...);
     if (per <= 4) return Launch<4, BITS>::run(args...);
+    if (per <= 6) return Launch<6, BITS>::run(args...);
     if (per <= 8) return Launch<8, BITS>::run(args...);
     if (per <= 12) return Launch<12, BITS>::run(args...);
     return Launch<0, BITS>::run(args...);
 }
 
+// The quantisers split each row over one workgroup per vector of a lane while
+// that gives at most this many workgroups (M x slices); past it the repeated
+// reads of each row cost more than the shorter chains gain
+constexpr long kSplitWorkgroups = 768;
+
 template <int NV, int BITS>
 struct LaunchF16 {
     static hipError_t run(const uint16_t* x, const uint8_t* state, int M, int K, int dm, int du, uint8_t* q,
                           float* s, hipStream_t st) {
-        hipLaunchKernelGGL((quant_f16_kernel<NV, BITS>), dim3(M), dim3(kThreads), 0, st, x, state, K, dm, du, q, s);
+        const int per = (K / 8 + kThreads - 1) / kThreads;
+        const int slices = NV > 1 && (long)M * per <= kSplitWorkgroups ? per : 1;
+        hipLaunchKernelGGL((quant_f16_kernel<NV, BITS>), dim3(M * slices), dim3(kThreads), 0, st, x, state, K, dm,
+                           du, slices, q, s);
         return hipGetLastError();
     }
 };
@@ -213,7 +228,9 @@ struct LaunchF16 {
 template <int NV, int BITS>
 struct LaunchF32 {
     static hipError_t run(const float* x, int M, int K, uint8_t* q, float* s, hipStream_t st) {
-        hipLaunchKernelGGL((quant_f32_kernel<NV, BITS>), dim3(M), dim3(kThreads), 0, st, x, K, q, s);
+        const int per = (K / 8 + kThreads - 1) / kThreads;
+        const int slices = NV > 1 && (long)M * per <= kSplitWorkgroups ? per : 1;
+        hipLaunchKernelGGL((quant_f32_kernel<NV, BITS>), dim3(M * slices), dim3(kThreads), 0, st, x, K, slices, q, s);
         return hipGetLastError();
     }
 };

@@ -66,7 +66,11 @@ def test_zero_rows_and_tiny_scales():
 
 # ------------------------------------------------------------------ folded basis (P = NULL)
 
-@pytest.mark.parametrize("M,K", [(1, 64), (3, 512), (77, 4096), (130, 3584), (64, 18944), (3, 131072)])
+# while rows x vectors per lane <= 768 a row spans one workgroup per vector of
+# a lane: (77, 4096), (130, 3584), (5, 6144), (16, 12288), (64, 18944);
+# (129, 12288) takes one workgroup per row
+@pytest.mark.parametrize("M,K", [(1, 64), (3, 512), (77, 4096), (130, 3584), (5, 6144), (16, 12288),
+                                 (129, 12288), (64, 18944), (3, 131072)])
 @pytest.mark.parametrize("layout", ["random", "all_masked", "none_masked", "alternating"])
 def test_quant_act_folded(M, K, layout):
     st = None if layout == "random" else synth.state_edge(M, layout)
@@ -381,6 +385,24 @@ def test_w8_quantiser_exhaustive_fp16(amax):
     assert_bits(host(Aq), rq, "Aq")
     Aq2, s2 = sq.sgat_quantize_w8(dev(rows.astype(np.float32)))
     assert_bits(host(Aq2), rq, "Aq (fp32 path)")
+
+
+@pytest.mark.parametrize("M,K", [(16, 12288), (3, 6144), (384, 4096), (385, 4096)])
+def test_w8_quant_act_short_batches(M, K):
+    """8-bit codes on the row-split path (rows x vectors per lane <= 768) and
+    just past it, fp16 and fp32 inputs."""
+    X, st = _x(M, K, 10)
+    dm, du = synth.default_band(K)
+    say(f"w8 quant_act short M={M} K={K}")
+    Aq, s = sq.sgat_quant_act_w8(dev(X), dev(st), None, dm, du)
+    rq, rs = O.quant_act_q8(X, st, None, dm, du)
+    assert_bits(host(s), rs, "s_a")
+    assert_bits(host(Aq), rq, "Aq")
+    x32 = X.astype(np.float32)
+    Aq2, s2 = sq.sgat_quantize_w8(dev(x32))
+    rq2, rs2 = O.quant_rows_q8(x32)
+    assert_bits(host(s2), rs2, "s (fp32 path)")
+    assert_bits(host(Aq2), rq2, "Aq (fp32 path)")
 
 
 @pytest.mark.parametrize("withP,g", [(False, 0), (True, 0), (False, 16), (False, 128), (True, 16)])
