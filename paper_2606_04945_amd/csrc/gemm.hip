@@ -685,10 +685,10 @@ hipError_t launch_skinny_shared_tm(int waves, const uint8_t* Aq, const float* s_
                                    const float* s_w, int M, int N, int K, uint16_t* Y, int32_t* acc, hipStream_t st) {
     const int nk = (K / 2 + kKB - 1) / kKB;
     const size_t lds = shared_lds_bytes(TM, nk);
-    static const hipError_t attr =     // above the 64 KB default for dynamic LDS
-        hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_skinny_shared_kernel<TM>),
-                            hipFuncAttributeMaxDynamicSharedMemorySize,
-                            (int)(TM == 1 ? kSharedMaxSteps * 3 * 1024 : kSharedMaxTileSteps * 1024));
+    static std::atomic<int> lds_set[kMaxDevices];   // above the 64 KB default for dynamic LDS
+    const hipError_t attr =
+        allow_dynamic_lds(reinterpret_cast<const void*>(&gemm_skinny_shared_kernel<TM>),
+                          (int)(TM == 1 ? kSharedMaxSteps * 3 * 1024 : kSharedMaxTileSteps * 1024), lds_set);
     if (attr != hipSuccess) return attr;
     if (lds == 0 || waves < 1 || waves > kSharedMaxWaves) return hipErrorInvalidConfiguration;
     const int groups = (N + 15) / 16;
@@ -734,9 +734,9 @@ hipError_t launch_short_frag_t(const Plan& p, const uint8_t* Aq, const float* s_
                                const float* s_w, int M, int N, int K, uint16_t* Y, int32_t* acc, hipStream_t st) {
     const int nk = (K / 2 + kKB - 1) / kKB;
     const size_t lds = frag_lds_bytes(TM, nk, KW, p.waves, ALDS);
-    static const hipError_t attr =     // above the 64 KB default for dynamic LDS
-        hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_short_frag_kernel<TM, KW, ALDS, U, D>),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)kFragMaxLds);
+    static std::atomic<int> lds_set[kMaxDevices];   // above the 64 KB default for dynamic LDS
+    const hipError_t attr = allow_dynamic_lds(
+        reinterpret_cast<const void*>(&gemm_short_frag_kernel<TM, KW, ALDS, U, D>), (int)kFragMaxLds, lds_set);
     if (attr != hipSuccess) return attr;
     if (lds > kFragMaxLds || p.waves < 1 || p.waves * KW > (ALDS ? 16 : 8)) return hipErrorInvalidConfiguration;
     const int groups = (N + 15) / 16;

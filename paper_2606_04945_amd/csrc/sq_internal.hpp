@@ -6,6 +6,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <atomic>
+
 namespace sq {
 
 constexpr int kWave = 64;
@@ -112,6 +114,23 @@ __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
     return v;
+}
+
+// Raises kernel `fn`'s dynamic-LDS limit to `bytes` on the current device, once
+// per device.  The attribute belongs to the device that is current when it is
+// set, so a process that drives several GPUs needs it on each; `done` is the
+// caller's per-device flag array (static storage, kMaxDevices entries).  A
+// failed call is not remembered: the next launch tries again.
+constexpr int kMaxDevices = 64;
+inline hipError_t allow_dynamic_lds(const void* fn, int bytes, std::atomic<int>* done) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    if (done[dev].load(std::memory_order_acquire)) return hipSuccess;
+    e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+    if (e == hipSuccess) done[dev].store(1, std::memory_order_release);
+    return e;
 }
 
 // ---- launchers (each returns hipError_t of the launch) ----

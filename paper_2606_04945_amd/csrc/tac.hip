@@ -147,9 +147,8 @@ hipError_t launch_cw(const uint16_t* Z, const uint16_t* Mb, const uint16_t* d, i
     constexpr int CG = CW / CPT, TT = (kThreads / CG) * kTPT;
     constexpr int CC = CW == 128 ? 8 : 16;
     const size_t lds = sizeof(float) * ((size_t)CW * (TT + 4) + 2 * (size_t)CC * (CW + 4));
-    static const hipError_t attr =             // above the 64 KB default for dynamic LDS
-        hipFuncSetAttribute(reinterpret_cast<const void*>(&tac_kernel<CW, CPT>),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    static std::atomic<int> lds_set[kMaxDevices];   // above the 64 KB default for dynamic LDS
+    const hipError_t attr = allow_dynamic_lds(reinterpret_cast<const void*>(&tac_kernel<CW, CPT>), (int)lds, lds_set);
     if (attr != hipSuccess) return attr;
     dim3 grid(C / CW, (M + TT - 1) / TT);
     hipLaunchKernelGGL((tac_kernel<CW, CPT>), grid, dim3(kThreads), lds, st, Z, Mb, d, M, C, g, out);
@@ -180,6 +179,7 @@ namespace sq {
 namespace {
 
 constexpr int kFusedThreads = 512;
+typedef _Float16 v8h __attribute__((ext_vector_type(8)));
 
 __device__ __forceinline__ float block_max_db(float v, float (*red)[kFusedThreads / kWave], int parity) {
     v = wave_max(v);
@@ -202,6 +202,9 @@ __global__ __launch_bounds__(kFusedThreads) void tac_quant_kernel(const uint16_t
                                                                   float* __restrict__ s_out) {
     constexpr int ZW = G > 8 ? G : 8;                   // input channels a thread reads (whole blocks)
     __shared__ float red[2][kFusedThreads / kWave];
+    // staging of the block-matrix rows (G >= 4): per wave, TPP slots of 16 G + 16 bytes
+    constexpr int kStage = G >= 4 ? (G == 16 ? 32 : 64) * (16 * G + 16) : 16;
+    __shared__ __attribute__((aligned(16))) uint8_t pstage[kFusedThreads / kWave * kStage];
     const int t = threadIdx.x;
     const bool active = 8 * t < K;
     const int c0 = 8 * t;                               // first output channel of this thread
@@ -224,15 +227,65 @@ __global__ __launch_bounds__(kFusedThreads) void tac_quant_kernel(const uint16_t
     };
     auto fetch_s = [&](int row) { sb = __builtin_amdgcn_raw_buffer_load_b8(rS, row, 0, 0); };
     if (row_begin < row_end) fetch_z(row_begin);
-    float m[8][G];                                      // tac_M viewed as [K][G]: rows c0 .. c0 + 7
+    // tac_M viewed as [K][G]: this thread's rows c0 .. c0 + 7 are 8 G fp16
+    // values, held as G vectors of 8 (element r G + c of the run = row r,
+    // column c) and widened to fp32 where they are used
+    v8h mh[G];
     float dv[8];
     const int cm = active ? c0 : 0;                     // inactive threads read the first rows, unused
+    if constexpr (G >= 4) {
+        // A thread's rows are PB = 16 G contiguous bytes at PB t, so loaded
+        // directly the lanes of one 16-byte load would touch up to 64 cache
+        // lines.  Instead each wave loads its 64 runs with whole-wave
+        // contiguous 16-byte loads, writes them to per-thread LDS slots padded
+        // by 16 bytes (so the 16-byte reads below are free of bank conflicts),
+        // and each thread reads its own slot back; for G = 16 in two passes of
+        // 32 threads, the second pass's loads in flight during the first's
+        // LDS traffic.  A wave's LDS accesses are performed in order, so only
+        // the compiler has to be kept from reordering them (the fences).
+        constexpr int PB = 16 * G, NC = PB / 16, SLOT = PB + 16;
+        constexpr int TPP = G == 16 ? 32 : 64;          // threads per pass
+        constexpr int PASSES = kWave / TPP;
+        constexpr int LOADS = TPP * NC / kWave;         // 16-byte loads per lane per pass
+        const int wave = t / kWave, lane = t % kWave;
+        uint8_t* stage = pstage + wave * (TPP * SLOT);
+        const __amdgpu_buffer_rsrc_t rM = make_rsrc(Mb, (uint32_t)K * G * 2);
+        const int slab = wave * kWave * NC;             // first chunk of this wave's runs
+        auto load_pass = [&](int p, v4i* ch) {
 #pragma unroll
-    for (int r = 0; r < 8; ++r) {
+            for (int i = 0; i < LOADS; ++i)
+                ch[i] = __builtin_amdgcn_raw_buffer_load_b128(rM, (slab + p * TPP * NC + i * kWave + lane) * 16, 0, 0);
+        };
+        auto wave_sync = [] {
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        };
+        v4i ch[PASSES][LOADS];
+        load_pass(0, ch[0]);
 #pragma unroll
-        for (int c = 0; c < G; ++c) m[r][c] = h2f(Mb[(size_t)(cm + r) * G + c]);
-        dv[r] = h2f(d[cm + r]);
+        for (int p = 0; p < PASSES; ++p) {
+#pragma unroll
+            for (int i = 0; i < LOADS; ++i) {
+                const int c = i * kWave + lane;         // chunk of this pass: thread c / NC, piece c % NC
+                *reinterpret_cast<v4i*>(stage + (c / NC) * SLOT + (c % NC) * 16) = ch[p][i];
+            }
+            if (p + 1 < PASSES) load_pass(p + 1, ch[p + 1]);
+            wave_sync();
+            if (lane / TPP == p) {
+#pragma unroll
+                for (int j = 0; j < NC; ++j)
+                    mh[j] = *reinterpret_cast<const v8h*>(stage + (lane - p * TPP) * SLOT + j * 16);
+            }
+            wave_sync();
+        }
+    } else {
+        // runs of 16 or 32 bytes: the lanes of a load already cover whole lines
+#pragma unroll
+        for (int j = 0; j < G; ++j) mh[j] = *reinterpret_cast<const v8h*>(Mb + (size_t)cm * G + 8 * j);
     }
+#pragma unroll
+    for (int r = 0; r < 8; ++r) dv[r] = h2f(d[cm + r]);
     if (row_begin < row_end) fetch_s(row_begin);
     for (int row = row_begin; row < row_end; ++row) {
         float o[8];
@@ -255,7 +308,10 @@ __global__ __launch_bounds__(kFusedThreads) void tac_quant_kernel(const uint16_t
                 const int base = ((c0 - z0 + r) / G) * G;   // block start within z[]
                 float acc = 0.0f;
 #pragma unroll
-                for (int c = 0; c < G; ++c) acc = __builtin_fmaf(m[r][c], z[base + c], acc);
+                for (int c = 0; c < G; ++c) {
+                    const int e = r * G + c;
+                    acc = __builtin_fmaf((float)mh[e / 8][e % 8], z[base + c], acc);
+                }
                 const float v = h2f(f2h(acc + dv[r]));  // TAC output, materialised as fp16
                 o[r] = (!gated | kept_sel(c0 + r, K, dm, du, masked)) ? v : 0.0f;
                 amax = fmaxf(amax, fabsf(o[r]));

@@ -729,9 +729,9 @@ hipError_t launch_tac_calib(const uint16_t* Zf, const uint16_t* Zq, int N, int C
     }
     if (e != hipSuccess) return e;
     if (g == kRegBlock) {
-        static const hipError_t attr =     // above the 64 KB default for dynamic LDS
-            hipFuncSetAttribute(reinterpret_cast<const void*>(&tac_finalize_kernel<true>),
-                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)(gg * sizeof(double)));
+        static std::atomic<int> lds_set[kMaxDevices];   // above the 64 KB default for dynamic LDS
+        const hipError_t attr = allow_dynamic_lds(reinterpret_cast<const void*>(&tac_finalize_kernel<true>),
+                                                  (int)(gg * sizeof(double)), lds_set);
         if (attr != hipSuccess) return attr;
         hipLaunchKernelGGL(tac_finalize_kernel<true>, dim3((unsigned)B), dim3(kCalThreads), gg * sizeof(double), st,
                            part, chunks, N, C, g, rho, eps, eta, alpha, wk, tac_M, tac_d, M64, d64);
