@@ -129,6 +129,18 @@ __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(OC
         uint8_t* dB = dA + AB;
         const uint32_t ko = (uint32_t)kt * kKB;
         const bool tail = kt >= nk_full;
+        if (WF && !tail) {
+            // Whole k steps of fragment-ordered weights: the k offsets ride in
+            // the scalar offset (no vector instruction per load).  Every access
+            // of a row below M stays inside that row, and rows past M (and
+            // weight groups past N) carry an out-of-range vector offset.
+#pragma unroll
+            for (int u = 0; u < LA; ++u) dma16s(rA, lds_addr(dA + (wave * LA + u) * 1024), oa[u], ko);
+#pragma unroll
+            for (int u = 0; u < LB; ++u)
+                dma16s(rW, lds_addr(dB + (wave * LB + u) * 1024), ow[u], (uint32_t)kt * ngrp * 1024);
+            return;
+        }
 #pragma unroll
         for (int u = 0; u < LA; ++u) {
             const uint32_t o = (tail && ko + sa_[u] >= ldb) ? kOOB : oa[u] + ko;

@@ -41,6 +41,19 @@ __device__ __forceinline__ void dma16(const u32x4& rsrc, uint32_t lds, uint32_t 
                  : "memory", "m0");
 }
 
+// The same with a wave-uniform offset `soff` in the scalar-offset field, added
+// to voff, so a k-step offset costs no vector instruction.  Callers keep every
+// in-range lane's voff + soff inside the buffer and put the out-of-range lanes'
+// voff itself past it, so the result does not depend on whether the range
+// check counts soff.
+__device__ __forceinline__ void dma16s(const u32x4& rsrc, uint32_t lds, uint32_t voff, uint32_t soff) {
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+                 :
+                 : "s"(__builtin_amdgcn_readfirstlane(lds)), "v"(voff), "s"(rsrc),
+                   "s"(__builtin_amdgcn_readfirstlane(soff))
+                 : "memory", "m0");
+}
+
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
     return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)p;
 }
