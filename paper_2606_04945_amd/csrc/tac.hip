@@ -89,21 +89,38 @@ __global__ __launch_bounds__(kThreads) void tac_kernel(const uint16_t* __restric
         if (p + 1 < npass) load_pass(c0 + cc);
         if (CPT == 8 || g >= kCPT) {         // CPT == 8 is launched for g >= 8 only
             const int base = (ch0 / g) * g;  // block start, shared by the thread's channels
-            for (int c = 0; c < cc; ++c) {
-                float m[kCPT];
-#pragma unroll
-                for (int q = 0; q < kCPT; q += 4) {
-                    const float4 mv = *reinterpret_cast<const float4*>(ms + c * MP + ch0 + q);
-                    m[q] = mv.x, m[q + 1] = mv.y, m[q + 2] = mv.z, m[q + 3] = mv.w;
-                }
+            // column c: the thread's kCPT block-matrix values and kTPT inputs
+            auto fetch = [&](int c, float4 (&r)[4]) {
+                r[0] = *reinterpret_cast<const float4*>(ms + c * MP + ch0);
+                r[1] = *reinterpret_cast<const float4*>(ms + c * MP + ch0 + 4);
                 const float* zr = zsT + (base + c0 + c) * ZP + tg * kTPT;
-                const float4 z0 = *reinterpret_cast<const float4*>(zr);
-                const float4 z1 = *reinterpret_cast<const float4*>(zr + 4);
-                const float zv[8] = {z0.x, z0.y, z0.z, z0.w, z1.x, z1.y, z1.z, z1.w};
+                r[2] = *reinterpret_cast<const float4*>(zr);
+                r[3] = *reinterpret_cast<const float4*>(zr + 4);
+            };
+            auto madd = [&](const float4 (&r)[4]) {
+                const float m[8] = {r[0].x, r[0].y, r[0].z, r[0].w, r[1].x, r[1].y, r[1].z, r[1].w};
+                const float zv[8] = {r[2].x, r[2].y, r[2].z, r[2].w, r[3].x, r[3].y, r[3].z, r[3].w};
 #pragma unroll
                 for (int t = 0; t < kTPT; ++t)
 #pragma unroll
                     for (int q = 0; q < kCPT; ++q) acc[t][q] = __builtin_fmaf(m[q], zv[t], acc[t][q]);
+            };
+            if (cc == kCC) {
+                // a full pass (g >= kCC), unrolled with the next column's LDS
+                // reads issued ahead of this column's multiply-adds
+                float4 r[2][4];
+                fetch(0, r[0]);
+#pragma unroll
+                for (int c = 0; c < kCC; ++c) {
+                    if (c + 1 < kCC) fetch(c + 1, r[(c + 1) & 1]);
+                    madd(r[c & 1]);
+                }
+            } else {
+                for (int c = 0; c < cc; ++c) {
+                    float4 r[4];
+                    fetch(c, r);
+                    madd(r);
+                }
             }
         } else if constexpr (CPT == 4) {
             // g in {1, 2}: the thread's channels lie in different blocks
