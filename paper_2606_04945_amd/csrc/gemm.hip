@@ -193,18 +193,33 @@ __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(OC
     // lr of A block i and the four consecutive output columns 4 lg .. 4 lg + 3
     // of W block j, so each store is one contiguous 8-byte (fp16) or 16-byte
     // (int32) run and the weight scales come in as one float4.
-    auto epilogue = [&]() {
+    // The dequantisation scales of all of this lane's rows and columns are
+    // requested together before any is used (indices clamped into range, so no
+    // branch separates the loads): one memory round trip per tile rather than
+    // one per 16 x 16 block.  Below K = 131072 the scaled sum 256 x dot cannot
+    // wrap, so the shift alone recovers the dot product (acc_value's special
+    // case is only needed at the largest K).
+    auto epilogue = [&](auto NOWRAP) {
+        float sa[TM];
+        float4 sw[TN];
+        if (!SPLIT && Y) {
+#pragma unroll
+            for (int i = 0; i < TM; ++i) sa[i] = s_a[min(row0 + (wm * TM + i) * 16 + lr, M - 1)];
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+                sw[j] = *reinterpret_cast<const float4*>(s_w + min(col0 + (wn * TN + j) * 16 + lg * 4, N - 4));
+        }
+        auto value = [](int raw) { return decltype(NOWRAP)::value && BITS == 4 ? raw >> 8 : acc_value<BITS>(raw); };
 #pragma unroll
         for (int i = 0; i < TM; ++i) {
             const int row = row0 + (wm * TM + i) * 16 + lr;
             if (row >= M) continue;
-            const float sa = SPLIT ? 0.0f : s_a[row];
 #pragma unroll
             for (int j = 0; j < TN; ++j) {
                 const int col = col0 + (wn * TN + j) * 16 + lg * 4;   // N % 8 == 0: all four in range or none
                 if (col >= N) continue;
-                const int v0 = acc_value<BITS>(acc[i][j][0]), v1 = acc_value<BITS>(acc[i][j][1]);
-                const int v2 = acc_value<BITS>(acc[i][j][2]), v3 = acc_value<BITS>(acc[i][j][3]);
+                const int v0 = value(acc[i][j][0]), v1 = value(acc[i][j][1]);
+                const int v2 = value(acc[i][j][2]), v3 = value(acc[i][j][3]);
                 if (SPLIT) {
                     *reinterpret_cast<int4*>(part + ((size_t)blockIdx.z * M + row) * N + col) = make_int4(v0, v1, v2, v3);
                     continue;
@@ -212,9 +227,8 @@ __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(OC
                 const size_t o = (size_t)row * N + col;
                 if (acc_out) *reinterpret_cast<int4*>(acc_out + o) = make_int4(v0, v1, v2, v3);
                 if (Y) {
-                    const float4 sw = *reinterpret_cast<const float4*>(s_w + col);
-                    const uint32_t y0 = f2h(((float)v0 * sa) * sw.x), y1 = f2h(((float)v1 * sa) * sw.y);
-                    const uint32_t y2 = f2h(((float)v2 * sa) * sw.z), y3 = f2h(((float)v3 * sa) * sw.w);
+                    const uint32_t y0 = f2h(((float)v0 * sa[i]) * sw[j].x), y1 = f2h(((float)v1 * sa[i]) * sw[j].y);
+                    const uint32_t y2 = f2h(((float)v2 * sa[i]) * sw[j].z), y3 = f2h(((float)v3 * sa[i]) * sw[j].w);
                     *reinterpret_cast<uint2*>(Y + o) = make_uint2(y0 | (y1 << 16), y2 | (y3 << 16));
                 }
             }
@@ -246,7 +260,10 @@ __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(OC
         if (kt + 1 < kt1) step(kt + 1, 1, 0);
         if (kt + 2 < kt1) step(kt + 2, 2, 1);
     }
-    epilogue();
+    if (K < 131072)
+        epilogue(std::true_type{});
+    else
+        epilogue(std::false_type{});
 }
 
 // Short M (<= 16 tokens): every weight is used by at most 16 rows, so these
