@@ -202,12 +202,25 @@ __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(OC
         if (kt + 2 < nk) step(kt + 2, 2, 1);
     }
     // acc[i][j] is the 32 x 32 block W_j A_i^T: element 4 q + e of this lane is
-    // output column 8 q + 4 lg + e of W block j for token row lr of A block i
+    // output column 8 q + 4 lg + e of W block j for token row lr of A block i.
+    // All of the lane's row and weight scales are requested before any is used
+    // (indices clamped into range, so no branch separates the loads).
+    float sa[TM];
+    float4 sw[TN][4];
+    if (Y) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i) sa[i] = s_a[min(row0 + (wm * TM + i) * 32 + lr, M - 1)];
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                sw[j][q] = *reinterpret_cast<const float4*>(
+                    s_w + min(col0 + (wn * TN + j) * 32 + 8 * q + 4 * lg, N - 4));
+    }
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
         const int row = row0 + (wm * TM + i) * 32 + lr;
         if (row >= M) continue;
-        const float sa = s_a[row];
 #pragma unroll
         for (int j = 0; j < TN; ++j)
 #pragma unroll
@@ -220,9 +233,9 @@ __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(OC
                 const size_t o = (size_t)row * N + col;
                 if (acc_out) *reinterpret_cast<int4*>(acc_out + o) = make_int4(v0, v1, v2, v3);
                 if (Y) {
-                    const float4 sw = *reinterpret_cast<const float4*>(s_w + col);
-                    const uint32_t y0 = f2h(((float)v0 * sa) * sw.x), y1 = f2h(((float)v1 * sa) * sw.y);
-                    const uint32_t y2 = f2h(((float)v2 * sa) * sw.z), y3 = f2h(((float)v3 * sa) * sw.w);
+                    const float4 w = sw[j][q];
+                    const uint32_t y0 = f2h(((float)v0 * sa[i]) * w.x), y1 = f2h(((float)v1 * sa[i]) * w.y);
+                    const uint32_t y2 = f2h(((float)v2 * sa[i]) * w.z), y3 = f2h(((float)v3 * sa[i]) * w.w);
                     *reinterpret_cast<uint2*>(Y + o) = make_uint2(y0 | (y1 << 16), y2 | (y3 << 16));
                 }
             }
