@@ -257,8 +257,8 @@ __global__ __launch_bounds__(kFusedThreads) void tac_quant_kernel(const uint16_t
         // contiguous 16-byte loads, writes them to per-thread LDS slots padded
         // by 16 bytes (so the 16-byte reads below are free of bank conflicts),
         // and each thread reads its own slot back; for G = 16 in two passes of
-        // 32 threads, the second pass's loads in flight during the first's
-        // LDS traffic.  A wave's LDS accesses are performed in order, so only
+        // 32 threads, one after the other so that only one pass's loads hold
+        // registers.  A wave's LDS accesses are performed in order, so only
         // the compiler has to be kept from reordering them (the fences).
         constexpr int PB = 16 * G, NC = PB / 16, SLOT = PB + 16;
         constexpr int TPP = G == 16 ? 32 : 64;          // threads per pass
@@ -278,16 +278,15 @@ __global__ __launch_bounds__(kFusedThreads) void tac_quant_kernel(const uint16_t
             __builtin_amdgcn_wave_barrier();
             __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
         };
-        v4i ch[PASSES][LOADS];
-        load_pass(0, ch[0]);
 #pragma unroll
         for (int p = 0; p < PASSES; ++p) {
+            v4i ch[LOADS];
+            load_pass(p, ch);
 #pragma unroll
             for (int i = 0; i < LOADS; ++i) {
                 const int c = i * kWave + lane;         // chunk of this pass: thread c / NC, piece c % NC
-                *reinterpret_cast<v4i*>(stage + (c / NC) * SLOT + (c % NC) * 16) = ch[p][i];
+                *reinterpret_cast<v4i*>(stage + (c / NC) * SLOT + (c % NC) * 16) = ch[i];
             }
-            if (p + 1 < PASSES) load_pass(p + 1, ch[p + 1]);
             wave_sync();
             if (lane / TPP == p) {
 #pragma unroll
@@ -305,6 +304,11 @@ __global__ __launch_bounds__(kFusedThreads) void tac_quant_kernel(const uint16_t
     for (int r = 0; r < 8; ++r) dv[r] = h2f(d[cm + r]);
     if (row_begin < row_end) fetch_s(row_begin);
     for (int row = row_begin; row < row_end; ++row) {
+        // keeps the block rows packed as fp16 (the multiply-adds widen them):
+        // hoisting their conversion out of the loop would hold 8 G fp32
+        // registers and leave room for fewer waves
+#pragma unroll
+        for (int j = 0; j < G; ++j) asm volatile("" : "+v"(mh[j]));
         float o[8];
         float amax = 0.0f;
         float z[ZW];
