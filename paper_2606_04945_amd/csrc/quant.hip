@@ -102,16 +102,30 @@ __global__ __launch_bounds__(kThreads) void quant_f16_kernel(const uint16_t* __r
         for (int i = 0; i < NV; ++i)
             raw[i] = __builtin_amdgcn_raw_buffer_load_b128(rX, ((int)threadIdx.x + i * kThreads) * 16, 0, 0);
         const bool masked = __builtin_amdgcn_raw_buffer_load_b8(rS, row, 0, 0) != 0;
+        // The gate keeps columns [0, lim0) and [lim1, K) of this row (a masked
+        // row drops its u-band, an unmasked one its m-band), so nearly every
+        // vector of 8 is kept or dropped whole; only a vector that straddles a
+        // band edge is gated column by column.
+        const int lim0 = gated ? (masked ? K - du : K - dm - du) : K;
+        const int lim1 = masked ? K : K - du;
         float x[NV][8];
 #pragma unroll
         for (int i = 0; i < NV; ++i) {
             const int v = threadIdx.x + i * kThreads;
+            const int lo = v * 8;
             const uint16_t* h = reinterpret_cast<const uint16_t*>(&raw[i]);
+            if ((lo + 8 <= lim0) | (lo >= lim1)) {
 #pragma unroll
-            for (int q = 0; q < 8; ++q) {
-                x[i][q] = (!gated | kept_sel(v * 8 + q, K, dm, du, masked)) ? h2f(h[q]) : 0.0f;
-                amax = fmaxf(amax, fabsf(x[i][q]));
+                for (int q = 0; q < 8; ++q) x[i][q] = h2f(h[q]);
+            } else if ((lo >= lim0) & (lo + 8 <= lim1)) {
+#pragma unroll
+                for (int q = 0; q < 8; ++q) x[i][q] = 0.0f;
+            } else {
+#pragma unroll
+                for (int q = 0; q < 8; ++q) x[i][q] = (lo + q < lim0) | (lo + q >= lim1) ? h2f(h[q]) : 0.0f;
             }
+#pragma unroll
+            for (int q = 0; q < 8; ++q) amax = fmaxf(amax, fabsf(x[i][q]));
         }
         const float s = block_max(amax, red) / qmaxf<BITS>();
         const float y = s != 0.0f ? 1.0f / s : 0.0f;
