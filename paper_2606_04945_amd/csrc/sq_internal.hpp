@@ -105,9 +105,11 @@ __device__ __forceinline__ void quant_codes8(const float* x, float s, float y, i
             if (!(0.5f - fabsf(q0 - r[q]) > kNear)) r[q] = __builtin_rintf(x[q] / s);
         }
     }
+    // clamp with one median-of-three (identical to the two-sided clamp for
+    // every finite value; it also maps a NaN from non-finite input to a code)
     constexpr float lo = -(QMAX + 1.0f), hi = (float)QMAX;
 #pragma unroll
-    for (int q = 0; q < 8; ++q) code[q] = (int)(r[q] < lo ? lo : (r[q] > hi ? hi : r[q]));
+    for (int q = 0; q < 8; ++q) code[q] = (int)__builtin_amdgcn_fmed3f(r[q], lo, hi);
 }
 
 __device__ __forceinline__ float wave_max(float v) {
