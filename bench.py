@@ -142,13 +142,13 @@ def large_token_block(torch, sq, synth, dev, steps, warmup):
     """Dream-shaped layer set, 8 x 2048 tokens, folded P: per linear the gate +
     int4 quantiser (TAC ahead of O) and the W4A4 GEMM.  Event pairs per call; the
     kernels are long enough that the host keeps the queue full."""
-    cfg = synth.CONFIGS[2]
-    st_np = synth.config_state(2)
+    cfg = synth.CONFIGS[synth.DREAM]
+    st_np = synth.config_state(synth.DREAM)
     M = len(st_np)
     state = torch.from_numpy(st_np).to(dev)
     sites = []
     for si, site in enumerate(cfg.sites):
-        t = synth.site_tensors(2, si, st_np, with_P=False)
+        t = synth.site_tensors(synth.DREAM, si, st_np, with_P=False)
         W = torch.from_numpy(t.W).to(dev)
         Wq, s_w = sq.sgat_prepare_weights(W, None)
         del W
@@ -295,12 +295,12 @@ def small_token_block(torch, sq, synth, dev, token_counts=(16, 32, 64), copies=8
     GEMM timed on its own cycles through at least 800 MB of its weights.
     Bytes are the algorithmic HBM traffic: fp16 activations read once, codes
     written and read once, the packed weights and scales, the fp16 outputs."""
-    cfg = synth.CONFIGS[4]
-    st64 = synth.config_state(4, M=max(token_counts), t=32)
+    cfg = synth.CONFIGS[synth.LLADA_SWEEP]
+    st64 = synth.config_state(synth.LLADA_SWEEP, M=max(token_counts), t=32)
     wsets = [[] for _ in range(copies)]
     meta = []
     for si, site in enumerate(cfg.sites):
-        t = synth.site_tensors(4, si, st64, with_P=False)
+        t = synth.site_tensors(synth.LLADA_SWEEP, si, st64, with_P=False)
         W = torch.from_numpy(t.W).to(dev)
         Wq, s_w = sq.sgat_prepare_weights(W, None)
         Wf = sq.weights_to_frag(Wq)
@@ -312,12 +312,12 @@ def small_token_block(torch, sq, synth, dev, token_counts=(16, 32, 64), copies=8
     out = {}
     dom_rec = None
     for M in token_counts:
-        st_np = synth.config_state(4, M=M, t=32)
+        st_np = synth.config_state(synth.LLADA_SWEEP, M=M, t=32)
         state = torch.from_numpy(st_np).to(dev)
         sites = []
         byts = 0
         for si, site in enumerate(meta):
-            t = synth.site_tensors(4, si, st_np, with_W=False, with_P=False)
+            t = synth.site_tensors(synth.LLADA_SWEEP, si, st_np, with_W=False, with_P=False)
             K, N = site.K, site.N
             d = dict(name=site.name, K=K, N=N, dm=t.dm, du=t.du, X=torch.from_numpy(t.X).to(dev),
                      Aq=torch.empty((M, K // 2), dtype=torch.uint8, device=dev),
@@ -387,11 +387,11 @@ def sweep_block(torch, sq, synth, dev, token_counts=(16, 64, 256, 1024, 4096, 16
     """Denoising-step sweep over token counts (LLaDA shapes, step 32 of 64, folded P):
     the W4A4 GEMM of every linear, graph-replayed with rotating weights, as
     achieved TOP/s and algorithmic GB/s, from memory-bound to compute-bound."""
-    cfg = synth.CONFIGS[4]
-    st_max = synth.config_state(4, M=max(token_counts), t=32)
+    cfg = synth.CONFIGS[synth.LLADA_SWEEP]
+    st_max = synth.config_state(synth.LLADA_SWEEP, M=max(token_counts), t=32)
     wsets, meta = [[] for _ in range(copies)], []
     for si, site in enumerate(cfg.sites):
-        t = synth.site_tensors(4, si, st_max[:16], with_P=False)
+        t = synth.site_tensors(synth.LLADA_SWEEP, si, st_max[:16], with_P=False)
         W = torch.from_numpy(t.W).to(dev)
         Wq, s_w = sq.sgat_prepare_weights(W, None)
         Wf = sq.weights_to_frag(Wq)
@@ -432,10 +432,10 @@ def tac_oproj_block(torch, sq, synth, dev, steps=5):
     """TAC (32 blocks of 128) on 8 x 2048 attention outputs of width 4096, then the
     gate + int4 quantiser and the 4096 -> 4096 W4A4 GEMM (folded P).  TAC at
     g = 128 runs as its own kernel (the fused form covers g <= 16)."""
-    st_np = synth.config_state(3)
+    st_np = synth.config_state(synth.TAC_OPROJ)
     M = len(st_np)
     state = torch.from_numpy(st_np).to(dev)
-    t = synth.site_tensors(3, 0, st_np, with_P=False)
+    t = synth.site_tensors(synth.TAC_OPROJ, 0, st_np, with_P=False)
     K, N, g = t.site.K, t.site.N, t.g
     W = torch.from_numpy(t.W).to(dev)
     Wq, s_w = sq.sgat_prepare_weights(W, None)
@@ -518,14 +518,14 @@ def main():
     sq.lib()                                    # raises if the HIP library is missing
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    cfg = synth.CONFIGS[1]
+    cfg = synth.CONFIGS[synth.LLADA]
     M = cfg.M
-    state_np = synth.config_state(1)
+    state_np = synth.config_state(synth.LLADA)
     state = torch.from_numpy(state_np).to(dev)
     t0 = time.time()
     sites = []
     for si, site in enumerate(cfg.sites):
-        t = synth.site_tensors(1, si, state_np)
+        t = synth.site_tensors(synth.LLADA, si, state_np)
         d = dict(site=site, K=site.K, N=site.N, dm=t.dm, du=t.du,
                  X=torch.from_numpy(t.X).to(dev), P=torch.from_numpy(t.P).to(dev),
                  W=torch.from_numpy(t.W).to(dev))

@@ -222,6 +222,9 @@ LLADA_SITES = (Site("qkv", 4096, 12288), Site("o", 4096, 4096, tac=True),
 DREAM_SITES = (Site("qkv", 3584, 4608), Site("o", 3584, 3584, tac=True),
                Site("gate_up", 3584, 37888), Site("down", 18944, 3584))
 
+# workload ids (each id also keys its seeded generators)
+SINGLE_LINEAR, LLADA, DREAM, TAC_OPROJ, LLADA_SWEEP = 0, 1, 2, 3, 4
+
 CONFIGS: Dict[int, Config] = {
     0: Config(0, "single SGAT W4A4 linear, 128 tokens, K=N=512", 128,
               (Site("linear", 512, 512),), outliers=4),

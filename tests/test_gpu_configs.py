@@ -83,16 +83,16 @@ def run_site(cid, si, state, *, g=None, folded=False, n_rows=6, n_cols=8, tac_id
 
 
 @pytest.mark.timeout(600)
-@pytest.mark.parametrize("si", range(4), ids=[s.name for s in synth.CONFIGS[1].sites])
+@pytest.mark.parametrize("si", range(4), ids=[s.name for s in synth.CONFIGS[synth.LLADA].sites])
 @pytest.mark.parametrize("folded", [False, True], ids=["denseP", "foldedP"])
 def test_llada_layer_set(si, folded):
-    run_site(1, si, synth.config_state(1), folded=folded)
+    run_site(synth.LLADA, si, synth.config_state(synth.LLADA), folded=folded)
 
 
 @pytest.mark.timeout(900)
-@pytest.mark.parametrize("si", range(4), ids=[s.name for s in synth.CONFIGS[2].sites])
+@pytest.mark.parametrize("si", range(4), ids=[s.name for s in synth.CONFIGS[synth.DREAM].sites])
 def test_dream_layer_set(si):
-    run_site(2, si, synth.config_state(2), n_rows=4, n_cols=6)
+    run_site(synth.DREAM, si, synth.config_state(synth.DREAM), n_rows=4, n_cols=6)
 
 
 @pytest.mark.timeout(600)
@@ -100,15 +100,15 @@ def test_dream_layer_set(si):
 def test_dream_layer_set_folded(si):
     """Folded P at 8 x 2048 tokens: the O projection runs TAC (g = 16) fused into the
     quantiser; gate+up is the widest GEMM of the set."""
-    run_site(2, si, synth.config_state(2), folded=True)
+    run_site(synth.DREAM, si, synth.config_state(synth.DREAM), folded=True)
 
 
 @pytest.mark.timeout(600)
-@pytest.mark.parametrize("si", range(4), ids=[s.name for s in synth.CONFIGS[1].sites])
+@pytest.mark.parametrize("si", range(4), ids=[s.name for s in synth.CONFIGS[synth.LLADA].sites])
 def test_llada_layer_set_w8a8(si):
     """The W8A8 variant (App. D) of every linear of the LLaDA-shaped set, folded P."""
-    st = synth.config_state(1)
-    t = synth.site_tensors(1, si, st, with_P=False)
+    st = synth.config_state(synth.LLADA)
+    t = synth.site_tensors(synth.LLADA, si, st, with_P=False)
     K, N, M = t.site.K, t.site.N, len(st)
     say(f"w8a8 config 1 site {t.site.name} M={M} K={K} N={N}")
     tM = dev(t.tac_M) if t.tac_M is not None else None
@@ -136,15 +136,15 @@ def test_llada_layer_set_w8a8(si):
 def test_tac_oproj_g128(folded):
     """TAC (32 blocks of 128) on 8 x 2048 tokens, then SGAT quantise, then the
     4096 -> 4096 GEMM."""
-    run_site(3, 0, synth.config_state(3), folded=folded)
+    run_site(synth.TAC_OPROJ, 0, synth.config_state(synth.TAC_OPROJ), folded=folded)
 
 
 @pytest.mark.timeout(600)
 def test_tac_oproj_identity_blocks_is_plain_sgat():
     """With identity blocks and zero bias the TAC + O-projection equals the same layer
     without TAC, bit for bit."""
-    st = synth.config_state(3)
-    t = synth.site_tensors(3, 0, st, tac_identity=True, with_W=False, with_P=False)
+    st = synth.config_state(synth.TAC_OPROJ)
+    t = synth.site_tensors(synth.TAC_OPROJ, 0, st, tac_identity=True, with_W=False, with_P=False)
     Xd = dev(t.X)
     a = sq.sgat_quant_act(Xd, dev(st), None, t.dm, t.du, dev(t.tac_M), dev(t.tac_d), t.g)
     b = sq.sgat_quant_act(Xd, dev(st), None, t.dm, t.du)
@@ -160,9 +160,9 @@ SWEEP = [16, 32, 64, 256, 1024, 4096, 16384]
 def test_denoise_sweep_token_counts(M):
     """Denoising-step sweep: each token count through every linear of the LLaDA set
     (folded P, the per-step GEMM path), at step t = 32, sampled rows vs the oracle."""
-    st = synth.config_state(4, M=M, t=32)
+    st = synth.config_state(synth.LLADA_SWEEP, M=M, t=32)
     for si in range(4):
-        run_site(4, si, st, folded=True, n_rows=4, n_cols=4)
+        run_site(synth.LLADA_SWEEP, si, st, folded=True, n_rows=4, n_cols=4)
 
 
 @pytest.mark.timeout(900)
@@ -172,8 +172,8 @@ def test_denoise_sweep_layouts(layout):
     layouts at 1024 tokens through the dense-P QKV and down linears."""
     M = 1024
     if layout in ("t0", "t64"):
-        st = synth.config_state(4, M=M, t=int(layout[1:]))
+        st = synth.config_state(synth.LLADA_SWEEP, M=M, t=int(layout[1:]))
     else:
         st = synth.state_edge(M, layout)
     for si in (0, 3):
-        run_site(4, si, st, n_rows=4, n_cols=4)
+        run_site(synth.LLADA_SWEEP, si, st, n_rows=4, n_cols=4)

@@ -318,8 +318,8 @@ def test_quant_act_tac_folded_fused(g, M, K):
 
 def test_config0_end_to_end():
     """The small configuration in full: 128 tokens, K = N = 512, dense P."""
-    st = synth.config_state(0)
-    t = synth.site_tensors(0, 0, st)
+    st = synth.config_state(synth.SINGLE_LINEAR)
+    t = synth.site_tensors(synth.SINGLE_LINEAR, 0, st)
     say("config 0 end to end")
     Xd, Pd = dev(t.X), dev(t.P)
     Wq, s_w = sq.sgat_prepare_weights(dev(t.W), Pd)
@@ -448,8 +448,8 @@ def test_w8a8_gemm_bit_exact(M, N, K):
 
 
 def test_w8a8_config0_end_to_end():
-    st = synth.config_state(0)
-    t = synth.site_tensors(0, 0, st)
+    st = synth.config_state(synth.SINGLE_LINEAR)
+    t = synth.site_tensors(synth.SINGLE_LINEAR, 0, st)
     Pd = dev(t.P)
     Wq, s_w = sq.sgat_prepare_weights_w8(dev(t.W), Pd)
     Aq, s_a = sq.sgat_quant_act_w8(dev(t.X), dev(st), Pd, t.dm, t.du)
