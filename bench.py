@@ -1,18 +1,23 @@
-"""Benchmark: STaR-Quant W4A4 SGAT linear layer set per denoising step on one MI355X.
+"""Benchmark: STaR-Quant W4A4 SGAT layer set per denoising step on one MI355X.
 
-Workload (default): the LLaDA-8B-shaped layer set, one sequence of 1024 tokens
-(512 unmasked prompt tokens, 512 generation tokens with 8 of 16 32-token blocks
-masked): QKV 4096->12288, O 4096->4096 with TAC (g = 16) ahead of it,
-gate+up 4096->24576, down 12288->4096, all W4A4 SGAT, fp16 in and out.
+Headline workload: the Dream-7B-shaped layer set (Qwen2.5-7B geometry), a batch of
+8 sequences x 2048 tokens = 16384 tokens, each sequence with a mask fraction drawn
+uniformly in [0.1, 0.9]: QKV 3584->4608, O 3584->3584 with TAC (g = 16) ahead of
+it, gate+up 3584->37888, down 18944->3584, all W4A4 SGAT with fp16 in and out.
 
 One step = the whole per-step hot path for every linear of the set:
-    [TAC] -> x P G_s (dense fp32 transform, Eq. 11) -> per-token int4 -> W4A4 GEMM
+    [TAC] -> x P G_s (dense fp32 basis applied online, Eq. 11) -> per-token int4
+    -> W4A4 GEMM (Eq. 13)
 with the weights prepared offline (Eq. 12, outside the timed region) and every
-input resident in HBM.  A second measurement runs the deployment form in which P
-is folded into the weights and the upstream activations, so the step is
-[TAC] -> gate -> int4 -> GEMM; it is reported next to the main figure.
+input resident in HBM.  Nested blocks: the same layer set with P folded into the
+weights and the upstream activations (the deployment form: [TAC] -> gate -> int4
+-> GEMM); the LLaDA-8B-shaped layer set at 1024 tokens (dense, folded, W8A8 and
+with the matrix-core transform); the single 128-token linear; TAC at g = 128 ahead
+of the O projection (dense and folded, with the identity-block no-op); the 64-step
+denoising sweep at 16, 1024 and 16384 tokens; the small-token steps; the GEMM
+token-count sweep; the offline TAC calibration; and the oracle timed on the host.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline] [--only-headline]
 
 Prints one JSON line.  Synthetic, seeded inputs (no datasets, no trained weights).
 """
@@ -21,6 +26,7 @@ from __future__ import annotations
 import argparse
 import json
 import os
+import platform
 import sys
 import time
 
@@ -34,9 +40,10 @@ PEAK_HBM_GBS = 8000.0
 PEAK_INT8_TOPS = 5000.0           # dense int8 MFMA, TOP/s
 PEAK_FP16_TFLOPS = 2500.0         # dense fp16 MFMA, TFLOP/s
 PEAK_FP6_TFLOPS = 10100.0         # dense FP6 / FP4 MFMA, TFLOP/s
+PEAK_FP32_TFLOPS = 157.3          # fp32 vector, published (counts packed fp32 issue)
 # fp32 FMA on the VALU without packed-fp32 instructions (the library is built
 # without them): 256 CU x 4 SIMD x 16 lanes x 2 flop x 2.4 GHz
-PEAK_FP32_VALU_TFLOPS = 78.6
+PEAK_FP32_NONPACKED_TFLOPS = 78.6
 
 
 def recorded_traffic(kernel: str, field: str = "traffic_bytes_per_launch"):
@@ -62,23 +69,25 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample", type=int, default=384, help="tokens in the oracle timing sample")
-    ap.add_argument("--only", choices=["dense", "folded", "both"], default="both")
+    ap.add_argument("--cpu-rows", type=int, default=64, help="token rows per linear in the all-cores oracle timing")
+    ap.add_argument("--cpu-rows-1core", type=int, default=16, help="token rows per linear in the 1-core timing")
+    ap.add_argument("--only-headline", action="store_true", help="the headline step only (no nested blocks)")
+    ap.add_argument("--no-llada", action="store_true", help="skip the LLaDA-shaped 1024-token blocks")
     ap.add_argument("--no-w8", action="store_true", help="skip the W8A8 (App. D) folded-basis measurement")
-    ap.add_argument("--no-large", action="store_true",
-                    help="skip the 16384-token Dream-shaped layer set (large-token GEMM figures)")
-    ap.add_argument("--no-small", action="store_true",
-                    help="skip the 16/32/64-token denoising-step layer sets (small-token HBM figures)")
+    ap.add_argument("--no-small", action="store_true", help="skip the 16/32/64-token steps")
     ap.add_argument("--no-calib", action="store_true", help="skip the TAC calibration timing")
     ap.add_argument("--no-fast", action="store_true", help="skip the dense step with the matrix-core transform")
     ap.add_argument("--no-sweep", action="store_true", help="skip the GEMM token-count sweep")
+    ap.add_argument("--no-denoise", action="store_true", help="skip the 64-step denoising sweep")
+    ap.add_argument("--no-fp6", action="store_true", help="skip the FP6 variant of the folded Dream step")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain 1 GiB device copy (reference for HBM byte counters)")
     return ap.parse_args()
 
 
 class Timer:
-    """HIP event pairs on the launching stream, summed per label."""
+    """HIP event pairs on the launching stream, per label: the sum, the mean and
+    the median duration of that label's launches."""
 
     def __init__(self, torch):
         self.torch = torch
@@ -92,12 +101,41 @@ class Timer:
         e.record()
         self.pairs.setdefault(label, []).append((s, e))
 
+    def times(self, label):
+        return [s.elapsed_time(e) for s, e in self.pairs.get(label, [])]
+
     def ms(self, label):
-        ps = self.pairs.get(label, [])
-        return sum(s.elapsed_time(e) for s, e in ps), len(ps)
+        t = self.times(label)
+        return sum(t), len(t)
+
+    def mean(self, label):
+        t = self.times(label)
+        return sum(t) / len(t) if t else float("nan")
+
+    def median(self, label):
+        t = sorted(self.times(label))
+        return t[len(t) // 2] if t else float("nan")
 
     def reset(self):
         self.pairs = {}
+
+
+def run_steps(torch, step, steps, warmup):
+    """W untimed warm-up steps, then exactly `steps` steps between two HIP events,
+    synchronised on both sides.  step(timer, i) enqueues one step.  Returns the
+    milliseconds per step and the timer of the timed steps."""
+    for i in range(warmup):
+        step(Timer(torch), i)
+    torch.cuda.synchronize()
+    timer = Timer(torch)
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    start.record()
+    for i in range(steps):
+        step(timer, i)
+    end.record()
+    torch.cuda.synchronize()
+    return start.elapsed_time(end) / steps, timer
 
 
 LLC_DEFEAT_BYTES = 800 << 20     # weight copies cycled per timing: over 3x the 256 MB last-level cache
@@ -111,9 +149,8 @@ def rotating_copies(Wq, s_w, floor=4):
     return [(Wq, s_w)] + [(Wq.clone(), s_w.clone()) for _ in range(n - 1)]
 
 
-def graph_ms(torch, fn, calls, replays=5):
-    """Median milliseconds per call of fn(i), i = 0 .. calls - 1, captured back to
-    back in one HIP graph, so that no host work sits between the launches."""
+def capture(torch, fn, calls):
+    """fn(0) .. fn(calls - 1) captured back to back in one HIP graph."""
     fn(0)
     torch.cuda.synchronize()
     g = torch.cuda.CUDAGraph()
@@ -125,6 +162,13 @@ def graph_ms(torch, fn, calls, replays=5):
                 fn(i)
     torch.cuda.current_stream().wait_stream(s)
     torch.cuda.synchronize()
+    return g
+
+
+def replay_ms(torch, g, calls, replays=5):
+    """Median over `replays` graph replays of the milliseconds per captured call."""
+    g.replay()                                  # warm
+    torch.cuda.synchronize()
     ts = []
     for _ in range(replays):
         e0 = torch.cuda.Event(enable_timing=True)
@@ -135,82 +179,162 @@ def graph_ms(torch, fn, calls, replays=5):
         torch.cuda.synchronize()
         ts.append(e0.elapsed_time(e1) / calls)
     ts.sort()
-    return ts[len(ts) // 2], g
+    return ts[len(ts) // 2]
 
 
-def large_token_block(torch, sq, synth, dev, steps, warmup):
-    """Dream-shaped layer set, 8 x 2048 tokens, folded P: per linear the gate +
-    int4 quantiser (TAC ahead of O) and the W4A4 GEMM.  Event pairs per call; the
-    kernels are long enough that the host keeps the queue full."""
-    cfg = synth.CONFIGS[synth.DREAM]
-    st_np = synth.config_state(synth.DREAM)
-    M = len(st_np)
-    state = torch.from_numpy(st_np).to(dev)
-    sites = []
+def graph_ms(torch, fn, calls, replays=5):
+    """Median milliseconds per call of fn(i), i = 0 .. calls - 1, captured back to
+    back in one HIP graph, so that no host work sits between the launches."""
+    g = capture(torch, fn, calls)
+    return replay_ms(torch, g, calls, replays), g
+
+
+def transform_flop(M, K):
+    """Algorithmic flop of the dense transform: the other state's band (K/32
+    columns) is never needed, so 2 M K (K - K/32)."""
+    return 2.0 * M * K * (K - K // 32)
+
+
+# ------------------------------------------------------------------ layer sets
+
+def load_sites(torch, sq, synth, dev, cid, state_np, *, with_P, keep_host_rows=None):
+    """Device tensors of every linear of workload `cid`: activations, weights,
+    optional dense basis, TAC parameters, and the output / workspace buffers.
+    keep_host_rows: token rows whose host copies (with P and the TAC parameters)
+    are kept for the oracle timing."""
+    cfg = synth.CONFIGS[cid]
+    M = len(state_np)
+    sites, hosts = [], []
     for si, site in enumerate(cfg.sites):
-        t = synth.site_tensors(synth.DREAM, si, st_np, with_P=False)
-        W = torch.from_numpy(t.W).to(dev)
-        Wq, s_w = sq.sgat_prepare_weights(W, None)
-        del W
-        d = dict(name=site.name, K=site.K, N=site.N, dm=t.dm, du=t.du, X=torch.from_numpy(t.X).to(dev),
-                 Wq=Wq, Wf=sq.weights_to_frag(Wq), s_w=s_w,
-                 Aq=torch.empty((M, site.K // 2), dtype=torch.uint8, device=dev),
-                 s_a=torch.empty((M,), dtype=torch.float32, device=dev),
-                 Y=torch.empty((M, site.N), dtype=torch.float16, device=dev))
+        t = synth.site_tensors(cid, si, state_np, with_P=with_P)
+        d = dict(name=site.name, K=site.K, N=site.N, dm=t.dm, du=t.du, tac=site.tac,
+                 X=torch.from_numpy(t.X).to(dev), W=torch.from_numpy(t.W).to(dev),
+                 P=torch.from_numpy(t.P).to(dev) if with_P else None)
         if site.tac:
             d.update(tac_M=torch.from_numpy(t.tac_M).to(dev), tac_d=torch.from_numpy(t.tac_d).to(dev), g=t.g)
-        d["qws"] = torch.empty(max(sq.quant_act_workspace_bytes(M, site.K, False, site.tac), 1), dtype=torch.uint8,
-                               device=dev)
+        if keep_host_rows is not None:
+            h = dict(name=site.name, K=site.K, N=site.N, dm=t.dm, du=t.du, X=t.X[keep_host_rows].copy(),
+                     st=state_np[keep_host_rows].copy(), P=t.P)
+            if site.tac:
+                h.update(tM=t.tac_M, td=t.tac_d, g=t.g)
+            hosts.append(h)
+        d["Aq"] = torch.empty((M, site.K // 2), dtype=torch.uint8, device=dev)
+        d["s_a"] = torch.empty((M,), dtype=torch.float32, device=dev)
+        d["Y"] = torch.empty((M, site.N), dtype=torch.float16, device=dev)
         d["gws"] = torch.empty(max(sq.gemm_workspace_bytes(M, site.N, site.K), 1), dtype=torch.uint8, device=dev)
         sites.append(d)
         del t
-    timer = Timer(torch)
+    return sites, hosts
 
-    def step(tm):
+
+def prepare(sq, sites, with_P):
+    """Offline weight side (Eq. 12) and the fragment order the GEMM streams."""
+    for d in sites:
+        Wq, d["s_w"] = sq.sgat_prepare_weights(d["W"], d["P"] if with_P else None)
+        d["Wf"] = sq.weights_to_frag(Wq)
+        d["Wq"] = Wq
+
+
+def dense_step_fn(sq, state, sites, xp, z):
+    """One dense-P step: per linear [TAC] -> transform and gate -> int4 -> GEMM,
+    each launch bracketed by HIP events under its own label."""
+    def step(tm, i):
         for d in sites:
+            src = d["X"]
+            if d["tac"]:
+                tm.wrap("tac/" + d["name"], lambda: sq.tac_apply(d["X"], d["tac_M"], d["tac_d"], d["g"],
+                                                                 out=z[:d["X"].numel()].view_as(d["X"])))
+                src = z[:d["X"].numel()].view_as(d["X"])
+            xs = xp[:d["X"].numel()].view(d["X"].shape)
+            tm.wrap("transform/" + d["name"], lambda: sq.sgat_transform(src, state, d["P"], d["dm"], d["du"], out=xs))
+            tm.wrap("quant/" + d["name"], lambda: sq.sgat_quantize(xs, Aq=d["Aq"], s=d["s_a"]))
+            tm.wrap("gemm/" + d["name"], lambda: sq.w4a4_gemm_frag(d["Aq"], d["s_a"], d["Wf"], d["s_w"], Y=d["Y"],
+                                                                   ws=d["gws"]))
+    return step
+
+
+def dense_report(M, sites, ms, timer):
+    """Per-kernel mean and median launch durations of a dense step, the layer
+    set's SGAT-linear TOPS, and the transform / GEMM rates."""
+    per = {}
+    tr_flop = tr_ms = gm_ops = gm_ms = 0.0
+    for d in sites:
+        n = d["name"]
+        f = transform_flop(M, d["K"])
+        ops = 2.0 * M * d["N"] * d["K"]
+        t_tr, t_gm = timer.mean("transform/" + n), timer.mean("gemm/" + n)
+        per[n] = {"K": d["K"], "N": d["N"],
+                  "transform_us": t_tr * 1e3, "transform_us_median": timer.median("transform/" + n) * 1e3,
+                  "transform_tflops": f / t_tr / 1e9,
+                  "quant_us": timer.mean("quant/" + n) * 1e3,
+                  "gemm_us": t_gm * 1e3, "gemm_us_median": timer.median("gemm/" + n) * 1e3,
+                  "gemm_tops": ops / t_gm / 1e9, "gemm_frac_int8_peak": ops / t_gm / 1e9 / PEAK_INT8_TOPS}
+        if d["tac"]:
+            per[n]["tac_us"] = timer.mean("tac/" + n) * 1e3
+        tr_flop += f
+        tr_ms += t_tr
+        gm_ops += ops
+        gm_ms += t_gm
+    return {"tokens": M, "ms_per_step": ms, "tokens_per_s": M / (ms / 1e3),
+            "sgat_linear_tops": gm_ops / (ms / 1e3) / 1e12,
+            "transform_ms": tr_ms, "transform_tflops": tr_flop / tr_ms / 1e9,
+            "gemm_ms": gm_ms, "gemm_tops": gm_ops / gm_ms / 1e9, "gemm_frac_int8_peak": gm_ops / gm_ms / 1e9 /
+            PEAK_INT8_TOPS, "per_site": per}
+
+
+def transform_roofline(M, d, timer, traffic_key):
+    n = d["name"]
+    ach = transform_flop(M, d["K"]) / timer.mean("transform/" + n) / 1e9
+    return {"bound": "alu", "achieved": ach, "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
+            "frac": ach / PEAK_FP32_TFLOPS,
+            "peak_nonpacked_fp32": PEAK_FP32_NONPACKED_TFLOPS, "frac_nonpacked_fp32": ach / PEAK_FP32_NONPACKED_TFLOPS,
+            "traffic": recorded_traffic(traffic_key),
+            "kernel": f"transform (dense fp32 x P, fixed order) at the {n} linear, M={M}, K={d['K']}",
+            "flop_per_launch": transform_flop(M, d["K"]), "launch_us_mean": timer.mean("transform/" + n) * 1e3}
+
+
+def workspaces(torch, sites, M, dev):
+    """One transform output buffer for the widest linear and one TAC output
+    buffer for the linears with TAC; the linears run one after the other on one
+    stream, so they share them."""
+    xp = torch.empty(M * max(d["K"] for d in sites), dtype=torch.float32, device=dev)
+    ktac = [d["K"] for d in sites if d["tac"]]
+    z = torch.empty(M * max(ktac), dtype=torch.float16, device=dev) if ktac else None
+    return xp, z
+
+
+def folded_block(torch, sq, sites, state, M, steps, warmup, copies=1):
+    """The deployment form (P folded upstream): per linear the gate + int4
+    quantiser (TAC fused ahead of O for g <= 16) and the W4A4 GEMM.  `copies`
+    rotating sets of prepared weights keep the last-level cache from serving them."""
+    for d in sites:
+        d["qws"] = torch.empty(max(sq.quant_act_workspace_bytes(M, d["K"], False, d["tac"]), 1), dtype=torch.uint8,
+                               device=d["X"].device)
+    wsets = [[(d["Wf"], d["s_w"]) for d in sites]] + [[(d["Wf"].clone(), d["s_w"].clone()) for d in sites]
+                                                      for _ in range(copies - 1)]
+
+    def step(tm, it):
+        for d, (Wf, s_w) in zip(sites, wsets[it % copies]):
             tm.wrap("q/" + d["name"], lambda: sq.sgat_quant_act(d["X"], state, None, d["dm"], d["du"], d.get("tac_M"),
                                                                  d.get("tac_d"), d.get("g", 0), Aq=d["Aq"],
                                                                  s_a=d["s_a"], ws=d["qws"]))
-            tm.wrap("g/" + d["name"], lambda: sq.w4a4_gemm_frag(d["Aq"], d["s_a"], d["Wf"], d["s_w"], Y=d["Y"],
-                                                                 ws=d["gws"]))
-    for _ in range(warmup):
-        step(Timer(torch))
-    torch.cuda.synchronize()
-    e0 = torch.cuda.Event(enable_timing=True)
-    e1 = torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(steps):
-        step(timer)
-    e1.record()
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / steps
-    per = {}
-    tot_ops = tot_ms = 0.0
+            tm.wrap("g/" + d["name"], lambda: sq.w4a4_gemm_frag(d["Aq"], d["s_a"], Wf, s_w, Y=d["Y"], ws=d["gws"]))
+    ms, timer = run_steps(torch, step, steps, warmup)
+    per, tot_ops, tot_ms = {}, 0.0, 0.0
     for d in sites:
-        gms = timer.ms("g/" + d["name"])[0] / steps
+        n = d["name"]
+        gms = timer.mean("g/" + n)
         ops = 2.0 * M * d["N"] * d["K"]
-        per[d["name"]] = {"M": M, "N": d["N"], "K": d["K"], "gemm_us": gms * 1e3, "tops": ops / gms / 1e9,
-                          "frac_int8_peak": ops / gms / 1e9 / PEAK_INT8_TOPS,
-                          "quant_act_us": timer.ms("q/" + d["name"])[0] / steps * 1e3}
+        per[n] = {"M": M, "N": d["N"], "K": d["K"], "gemm_us": gms * 1e3, "gemm_us_median": timer.median("g/" + n) * 1e3,
+                  "tops": ops / gms / 1e9, "frac_int8_peak": ops / gms / 1e9 / PEAK_INT8_TOPS,
+                  "quant_act_us": timer.mean("q/" + n) * 1e3}
         tot_ops += ops
         tot_ms += gms
-    dom = max(per, key=lambda n: per[n]["gemm_us"])
-    fp6 = fp6_variant(torch, sq, sites, state, M, steps, warmup)
-    for d in sites:      # context: the vendor library's int8 GEMM (torch._int_mm) at the same shape
-        per[d["name"]]["vendor_int8_gemm_us"] = vendor_int8_us(torch, M, d["N"], d["K"], d["X"].device)
-    out = {"workload": "Dream-7B-shaped SGAT layer set (QKV 3584->4608, O+TAC 3584->3584, gate+up 3584->37888, "
-                       "down 18944->3584), 8 x 2048 tokens, folded P",
-           "tokens": M, "ms_per_step": ms, "tokens_per_s": M / (ms / 1e3),
-           "gemm_tops": tot_ops / tot_ms / 1e9, "gemm_frac_int8_peak": tot_ops / tot_ms / 1e9 / PEAK_INT8_TOPS,
-           "per_site": per,
-           "roofline": {"bound": "mfma", "achieved": per[dom]["tops"], "peak": PEAK_INT8_TOPS, "unit": "TOP/s",
-                        "frac": per[dom]["frac_int8_peak"],
-                        "traffic": recorded_traffic("gemm_large") if dom == "gate_up" else None,
-                        "kernel": f"w4a4 gemm ({dom})"},
-           "fp6": fp6}
-    del sites
-    torch.cuda.empty_cache()
-    return out
+    del wsets
+    return {"tokens": M, "ms_per_step": ms, "tokens_per_s": M / (ms / 1e3),
+            "sgat_linear_tops": tot_ops / (ms / 1e3) / 1e12,
+            "gemm_tops": tot_ops / tot_ms / 1e9, "gemm_frac_int8_peak": tot_ops / tot_ms / 1e9 / PEAK_INT8_TOPS,
+            "per_site": per}
 
 
 def vendor_int8_us(torch, M, N, K, dev, reps=5):
@@ -237,18 +361,17 @@ def vendor_int8_us(torch, M, N, K, dev, reps=5):
 
 
 def fp6_variant(torch, sq, sites, state, M, steps, warmup):
-    """The same layer set with the codes carried as e3m2 on the FP6 matrix cores:
-    per linear the gate + int4 quantiser, the conversion of the activation codes
-    to the FP6 operand layout, and the GEMM on FP6 operands (weights converted
-    once, offline).  Its outputs are checked equal to the int4 path's."""
+    """The same folded layer set with the codes carried as e3m2 on the FP6 matrix
+    cores: per linear the gate + int4 quantiser, the conversion of the activation
+    codes to the FP6 operand layout, and the GEMM on FP6 operands (weights
+    converted once, offline).  Its outputs are checked equal to the int4 path's."""
     ref = {d["name"]: d["Y"].clone() for d in sites}
     for d in sites:
         d["W6"] = sq.codes_to_fp6(d["Wq"])
         d["A6"] = torch.empty((M, sq.fp6_row_bytes(d["K"])), dtype=torch.uint8, device=d["Aq"].device)
         d["Y6"] = torch.empty_like(d["Y"])
-    timer = Timer(torch)
 
-    def step(tm):
+    def step(tm, i):
         for d in sites:
             tm.wrap("q/" + d["name"], lambda: sq.sgat_quant_act(d["X"], state, None, d["dm"], d["du"], d.get("tac_M"),
                                                                  d.get("tac_d"), d.get("g", 0), Aq=d["Aq"],
@@ -256,25 +379,15 @@ def fp6_variant(torch, sq, sites, state, M, steps, warmup):
             tm.wrap("c/" + d["name"], lambda: sq.codes_to_fp6(d["Aq"], out=d["A6"]))
             tm.wrap("g/" + d["name"], lambda: sq.w4a4_gemm_fp6(d["A6"], d["s_a"], d["W6"], d["s_w"], d["K"],
                                                                 Y=d["Y6"]))
-    for _ in range(warmup):
-        step(Timer(torch))
-    torch.cuda.synchronize()
-    e0 = torch.cuda.Event(enable_timing=True)
-    e1 = torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(steps):
-        step(timer)
-    e1.record()
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / steps
+    ms, timer = run_steps(torch, step, steps, warmup)
     per, tot_ops, tot_ms = {}, 0.0, 0.0
     for d in sites:
-        gms = timer.ms("g/" + d["name"])[0] / steps
+        gms = timer.mean("g/" + d["name"])
         ops = 2.0 * M * d["N"] * d["K"]
         per[d["name"]] = {"gemm_us": gms * 1e3, "tops": ops / gms / 1e9,
                           "frac_fp6_peak": ops / gms / 1e9 / PEAK_FP6_TFLOPS,
                           "frac_int8_peak": ops / gms / 1e9 / PEAK_INT8_TOPS,
-                          "convert_us": timer.ms("c/" + d["name"])[0] / steps * 1e3}
+                          "convert_us": timer.mean("c/" + d["name"]) * 1e3}
         tot_ops += ops
         tot_ms += gms
     same = all(torch.equal(ref[d["name"]], d["Y6"]) for d in sites)
@@ -286,6 +399,325 @@ def fp6_variant(torch, sq, sites, state, M, steps, warmup):
             "roofline": {"bound": "mfma", "achieved": per[dom]["tops"], "peak": PEAK_FP6_TFLOPS, "unit": "TFLOP/s",
                          "frac": per[dom]["frac_fp6_peak"], "traffic": None,
                          "kernel": f"w4a4 gemm on FP6 operands ({dom})"}}
+
+
+# ------------------------------------------------------------------ headline
+
+def headline_block(torch, sq, synth, dev, args):
+    """Dream-shaped layer set, 8 x 2048 tokens, dense P, TAC g = 16 ahead of O."""
+    state_np = synth.config_state(synth.DREAM)
+    M = len(state_np)
+    rows = np.random.default_rng(synth.SEED).choice(M, size=max(args.cpu_rows, args.cpu_rows_1core), replace=False)
+    t0 = time.time()
+    sites, hosts = load_sites(torch, sq, synth, dev, synth.DREAM, state_np, with_P=True,
+                              keep_host_rows=None if args.no_cpu_baseline else rows)
+    print(f"# Dream-shaped inputs generated in {time.time() - t0:.1f}s", file=sys.stderr, flush=True)
+    state = torch.from_numpy(state_np).to(dev)
+    prepare(sq, sites, True)
+    xp, z = workspaces(torch, sites, M, dev)
+    torch.cuda.synchronize()
+    ms, timer = run_steps(torch, dense_step_fn(sq, state, sites, xp, z), args.steps, args.warmup)
+    rep = dense_report(M, sites, ms, timer)
+    down = next(d for d in sites if d["name"] == "down")
+    rep["roofline"] = transform_roofline(M, down, timer, "transform_dream_down")
+    rep["workload"] = ("Dream-7B-shaped SGAT layer set (QKV 3584->4608, O+TAC g=16 3584->3584, gate+up "
+                       "3584->37888, down 18944->3584), 8 x 2048 tokens, dense online P")
+    del xp, z
+    for d in sites:
+        d["P"] = None
+    torch.cuda.empty_cache()
+    return rep, sites, state, state_np, hosts, rows
+
+
+def cpu_baseline_block(hosts, M, rows_all, rows_1core):
+    """The oracle as it stands, timed on the host: every linear of the Dream-shaped
+    dense-P layer set (TAC, transform and gate, quantise, GEMM against all N
+    output channels) on a seeded subset of the 16384 token rows; rows are
+    independent, so tokens/s scale linearly to the whole batch.  All host cores
+    (threads over rows) and one core."""
+    from oracle import oracle as O
+    nproc = os.cpu_count() or 1
+    try:
+        nproc = len(os.sched_getaffinity(0))
+    except AttributeError:
+        pass
+    ncpu = min(16, nproc)            # the host share of one GPU
+    model = platform.processor() or ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    rng = np.random.default_rng(0)
+    wq = {h["name"]: (rng.integers(0, 256, (h["N"], h["K"] // 2), dtype=np.uint8), np.ones(h["N"], np.float32))
+          for h in hosts}
+
+    def run(n, threads):
+        t1 = time.time()
+        for h in hosts:
+            Aq, s_a = O.quant_act(h["X"][:n], h["st"][:n], h["P"], h["dm"], h["du"], h.get("tM"), h.get("td"),
+                                  h.get("g", 0), threads=threads)
+            O.gemm(Aq, s_a, *wq[h["name"]], threads=threads)
+        return time.time() - t1
+
+    el_all = run(rows_all, ncpu)
+    el_one = run(rows_1core, 1)
+    return {"value": rows_all / el_all, "unit": "tokens/s", "cores": ncpu, "kind": "oracle",
+            "sample": f"{rows_all} seeded token rows of the {M} (scaled linearly: rows are independent) through "
+                      f"every linear of the Dream-shaped dense-P layer set (TAC g=16 for O, transform and gate, "
+                      f"quantise, GEMM against all N); weight preparation excluded; {el_all:.1f} s on "
+                      f"{ncpu} threads",
+            "value_1core": rows_1core / el_one, "sample_1core": f"{rows_1core} of the same rows on 1 thread, "
+                                                                f"{el_one:.1f} s",
+            "cpu_model": model, "nproc": nproc}
+
+
+# ------------------------------------------------------------------ nested blocks
+
+def llada_blocks(torch, sq, synth, dev, args):
+    """LLaDA-shaped layer set, 1024 tokens: dense P (the fixed-order transform and
+    the matrix-core transform), folded P, and W8A8 folded."""
+    state_np = synth.config_state(synth.LLADA)
+    M = len(state_np)
+    sites, _ = load_sites(torch, sq, synth, dev, synth.LLADA, state_np, with_P=True)
+    state = torch.from_numpy(state_np).to(dev)
+    prepare(sq, sites, True)
+    xp, z = workspaces(torch, sites, M, dev)
+    out = {}
+    ms, timer = run_steps(torch, dense_step_fn(sq, state, sites, xp, z), max(5, args.steps // 2), 2)
+    rep = dense_report(M, sites, ms, timer)
+    rep["roofline"] = transform_roofline(M, next(d for d in sites if d["name"] == "down"), timer,
+                                         "transform_llada_down")
+    rep["workload"] = "LLaDA-8B-shaped SGAT layer set, 1024 tokens, dense online P (TAC g=16 ahead of O)"
+    out["dense_P"] = rep
+    if not args.no_fast:
+        for d in sites:
+            d["Ps"] = sq.sgat_split_basis(d["P"])
+        canon = [(d["Aq"].clone(), d["s_a"].clone()) for d in sites]
+
+        def step_fast(tm, i):
+            for d in sites:
+                src = d["X"]
+                if d["tac"]:
+                    zz = z[:d["X"].numel()].view_as(d["X"])
+                    tm.wrap("tac/" + d["name"], lambda: sq.tac_apply(d["X"], d["tac_M"], d["tac_d"], d["g"], out=zz))
+                    src = zz
+                xs = xp[:d["X"].numel()].view(d["X"].shape)
+                tm.wrap("transform/" + d["name"], lambda: sq.sgat_transform_fast(src, state, d["Ps"], d["dm"], d["du"],
+                                                                                 out=xs))
+                tm.wrap("quant/" + d["name"], lambda: sq.sgat_quantize(xs, Aq=d["Aq"], s=d["s_a"]))
+                tm.wrap("gemm/" + d["name"], lambda: sq.w4a4_gemm_frag(d["Aq"], d["s_a"], d["Wf"], d["s_w"],
+                                                                       Y=d["Y"], ws=d["gws"]))
+        ms, timer = run_steps(torch, step_fast, max(5, args.steps // 2), 2)
+        flips = sum(int(((a ^ d["Aq"]) & 0x0F).ne(0).sum() + ((a ^ d["Aq"]) & 0xF0).ne(0).sum())
+                    for (a, _), d in zip(canon, sites))
+        ncodes = sum(d["Aq"].numel() * 2 for d in sites)
+        f = dense_report(M, sites, ms, timer)
+        f_ach = f["transform_tflops"]
+        out["dense_P_fast_transform"] = {
+            "tokens_per_s": f["tokens_per_s"], "ms_per_step": ms, "transform_ms": f["transform_ms"],
+            "roofline": {"bound": "mfma", "achieved": f_ach, "peak": PEAK_FP16_TFLOPS, "unit": "TFLOP/s",
+                         "frac": f_ach / PEAK_FP16_TFLOPS,
+                         "traffic": recorded_traffic("transform_fast", "traffic_bytes_per_launch_step_avg"),
+                         "kernel": "transform on the fp16 MFMA (hi + lo split: executes 2x the algorithmic flops)"},
+            "codes_differing_from_fixed_order": flips, "codes": ncodes}
+        for d in sites:
+            del d["Ps"]
+        del canon
+    del xp, z
+    for d in sites:
+        d["P"] = None
+    torch.cuda.empty_cache()
+    # folded P: weights prepared without P (the activations stand for inputs already in the P basis)
+    prepare(sq, sites, False)
+    fold = folded_block(torch, sq, sites, state, M, args.steps, args.warmup, copies=8)
+    fold["workload"] = "LLaDA-8B-shaped SGAT layer set, 1024 tokens, folded P, 8 rotating weight sets"
+    fold["roofline"] = {"bound": "mfma", "achieved": fold["gemm_tops"], "peak": PEAK_INT8_TOPS, "unit": "TOP/s",
+                        "frac": fold["gemm_frac_int8_peak"], "traffic": None, "kernel": "w4a4 gemm (all four sites)"}
+    out["folded_P"] = fold
+    if not args.no_w8:
+        w8 = []
+        for d in sites:
+            Wq8, s_w8 = sq.sgat_prepare_weights_w8(d["W"], None)
+            w8.append(dict(Wq8=Wq8, s_w8=s_w8, Aq8=torch.empty((M, d["K"]), dtype=torch.int8, device=dev),
+                           gws8=torch.empty(max(sq.gemm_workspace_bytes(M, d["N"], d["K"], 8), 1), dtype=torch.uint8,
+                                            device=dev)))
+        copies = [[(e["Wq8"], e["s_w8"]) for e in w8]] + [[(e["Wq8"].clone(), e["s_w8"].clone()) for e in w8]
+                                                          for _ in range(3)]
+
+        def step_w8(tm, it):
+            for d, e, (Wq8, s_w8) in zip(sites, w8, copies[it % len(copies)]):
+                tm.wrap("q8/" + d["name"], lambda: sq.sgat_quant_act_w8(d["X"], state, None, d["dm"], d["du"],
+                                                                       d.get("tac_M"), d.get("tac_d"), d.get("g", 0),
+                                                                       Aq=e["Aq8"], s_a=d["s_a"], ws=d["qws"]))
+                tm.wrap("g8/" + d["name"], lambda: sq.w8a8_gemm(e["Aq8"], d["s_a"], Wq8, s_w8, Y=d["Y"], ws=e["gws8"]))
+        ms, timer = run_steps(torch, step_w8, args.steps, args.warmup)
+        ops = sum(2.0 * M * d["N"] * d["K"] for d in sites)
+        gms = sum(timer.mean("g8/" + d["name"]) for d in sites)
+        out["w8a8_folded_P"] = {"tokens_per_s": M / (ms / 1e3), "ms_per_step": ms, "gemm_tops": ops / gms / 1e9,
+                                "gemm_frac_int8_peak": ops / gms / 1e9 / PEAK_INT8_TOPS,
+                                "quant_act_ms": sum(timer.mean("q8/" + d["name"]) for d in sites)}
+        del w8, copies
+    del sites
+    torch.cuda.empty_cache()
+    return out
+
+
+def single_linear_block(torch, sq, synth, dev):
+    """The 128-token single linear (K = N = 512), dense P and folded, graph-replayed."""
+    state_np = synth.config_state(synth.SINGLE_LINEAR)
+    M = len(state_np)
+    sites, _ = load_sites(torch, sq, synth, dev, synth.SINGLE_LINEAR, state_np, with_P=True)
+    state = torch.from_numpy(state_np).to(dev)
+    d = sites[0]
+    Wq, s_w = sq.sgat_prepare_weights(d["W"], d["P"])
+    Wf = sq.weights_to_frag(Wq)
+    qws = torch.empty(sq.quant_act_workspace_bytes(M, d["K"], True, False), dtype=torch.uint8, device=dev)
+
+    def step(i):
+        sq.sgat_quant_act(d["X"], state, d["P"], d["dm"], d["du"], Aq=d["Aq"], s_a=d["s_a"], ws=qws)
+        sq.w4a4_gemm_frag(d["Aq"], d["s_a"], Wf, s_w, Y=d["Y"], ws=d["gws"])
+    ms, g = graph_ms(torch, step, 16, replays=7)
+    del g
+    ops = 2.0 * M * d["N"] * d["K"]
+    return {"workload": "single SGAT W4A4 linear, 128 tokens, K = N = 512, dense P, HIP-graph replay",
+            "tokens": M, "us_per_step": ms * 1e3, "tokens_per_s": M / (ms / 1e3),
+            "sgat_linear_tops": ops / (ms / 1e3) / 1e12}
+
+
+def tac_oproj_block(torch, sq, synth, dev, steps=3):
+    """TAC (32 blocks of 128) on 8 x 2048 attention outputs of width 4096, then the
+    gate + int4 quantiser and the 4096 -> 4096 W4A4 GEMM: dense P (TAC, transform,
+    quantise, GEMM) and folded P (TAC, gate + quantise, GEMM), and the
+    identity-block case checked to leave the codes of the plain path unchanged."""
+    st_np = synth.config_state(synth.TAC_OPROJ)
+    M = len(st_np)
+    state = torch.from_numpy(st_np).to(dev)
+    t = synth.site_tensors(synth.TAC_OPROJ, 0, st_np, with_P=True)
+    K, N, g = t.site.K, t.site.N, t.g
+    W = torch.from_numpy(t.W).to(dev)
+    P = torch.from_numpy(t.P).to(dev)
+    X = torch.from_numpy(t.X).to(dev)
+    tM, td = torch.from_numpy(t.tac_M).to(dev), torch.from_numpy(t.tac_d).to(dev)
+    Z = torch.empty_like(X)
+    xp = torch.empty((M, K), dtype=torch.float32, device=dev)
+    Aq = torch.empty((M, K // 2), dtype=torch.uint8, device=dev)
+    s_a = torch.empty((M,), dtype=torch.float32, device=dev)
+    Y = torch.empty((M, N), dtype=torch.float16, device=dev)
+    gws = torch.empty(max(sq.gemm_workspace_bytes(M, N, K), 1), dtype=torch.uint8, device=dev)
+    out = {"workload": f"TAC g = {g} + O projection {K}->{N}, 8 x 2048 tokens", "tokens": M}
+    for mode in ("dense_P", "folded_P"):
+        Wq, s_w = sq.sgat_prepare_weights(W, P if mode == "dense_P" else None)
+        Wf = sq.weights_to_frag(Wq)
+        del Wq
+
+        def step(tm, i):
+            tm.wrap("tac", lambda: sq.tac_apply(X, tM, td, g, out=Z))
+            if mode == "dense_P":
+                tm.wrap("transform", lambda: sq.sgat_transform(Z, state, P, t.dm, t.du, out=xp))
+                tm.wrap("q", lambda: sq.sgat_quantize(xp, Aq=Aq, s=s_a))
+            else:
+                tm.wrap("q", lambda: sq.sgat_quant_act(Z, state, None, t.dm, t.du, Aq=Aq, s_a=s_a))
+            tm.wrap("g", lambda: sq.w4a4_gemm_frag(Aq, s_a, Wf, s_w, Y=Y, ws=gws))
+        ms, timer = run_steps(torch, step, steps, 1)
+        tac_ms, g_ms = timer.mean("tac"), timer.mean("g")
+        tac_flop = 2.0 * M * K * g
+        rec = {"ms_per_step": ms, "tokens_per_s": M / (ms / 1e3), "tac_ms": tac_ms, "quant_ms": timer.mean("q"),
+               "gemm_ms": g_ms, "gemm_frac_int8_peak": 2.0 * M * N * K / g_ms / 1e9 / PEAK_INT8_TOPS,
+               "roofline": {"bound": "alu", "achieved": tac_flop / tac_ms / 1e9, "peak": PEAK_FP32_TFLOPS,
+                            "unit": "TFLOP/s", "frac": tac_flop / tac_ms / 1e9 / PEAK_FP32_TFLOPS,
+                            "frac_nonpacked_fp32": tac_flop / tac_ms / 1e9 / PEAK_FP32_NONPACKED_TFLOPS,
+                            "traffic": recorded_traffic("tac_g128") if g == 128 else None,
+                            "kernel": f"tac (g = {g})"}}
+        if mode == "dense_P":
+            tr_ms = timer.mean("transform")
+            rec["transform_ms"] = tr_ms
+            rec["transform_tflops"] = transform_flop(M, K) / tr_ms / 1e9
+        out[mode] = rec
+        del Wf
+    # identity blocks: TAC is a no-op, so the codes equal those of the plain (no TAC) path
+    tI, dI = synth.tac_params(K, g, None, identity=True)
+    tIM, tId = torch.from_numpy(tI).to(dev), torch.from_numpy(dI).to(dev)
+    sq.tac_apply(X, tIM, tId, g, out=Z)
+    Aq_i, s_i = sq.sgat_quant_act(Z, state, None, t.dm, t.du)
+    Aq_p, s_p = sq.sgat_quant_act(X, state, None, t.dm, t.du)
+    out["identity_blocks_no_op"] = bool(torch.equal(Aq_i, Aq_p) and torch.equal(s_i, s_p))
+    del X, Z, xp, P, W, Y
+    torch.cuda.empty_cache()
+    return out
+
+
+def denoise_sweep_block(torch, sq, synth, dev, token_counts=(16, 1024, 16384)):
+    """The 64-step denoising sweep on the LLaDA-shaped layer set (folded P): at
+    each token count, every step t = 0 .. 64 (the mask fraction of the 256-token
+    generation block falling linearly from 1 to 0 after a 512-token prompt,
+    token i taking position (512 + i) mod 768) and the edge layouts
+    (all masked, none masked, alternating), each step graph-replayed.  The TAC
+    parameters are fixed across steps and only the state changes, so the
+    per-step time should not depend on t: max / min over t is reported.  The
+    activations are drawn once per token count (for step 32); only the state
+    vector changes from step to step."""
+    cfg = synth.CONFIGS[synth.LLADA_SWEEP]
+    out = {}
+    meta = []
+    for si, site in enumerate(cfg.sites):
+        t = synth.site_tensors(synth.LLADA_SWEEP, si, synth.config_state(synth.LLADA_SWEEP, M=16, t=32),
+                               with_P=False)
+        W = torch.from_numpy(t.W).to(dev)
+        Wq, s_w = sq.sgat_prepare_weights(W, None)
+        meta.append((site, sq.weights_to_frag(Wq), s_w))
+        del W, Wq, t
+    for M in token_counts:
+        st32 = synth.config_state(synth.LLADA_SWEEP, M=M, t=32)
+        sites = []
+        for si, (site, Wf, s_w) in enumerate(meta):
+            t = synth.site_tensors(synth.LLADA_SWEEP, si, st32, with_W=False, with_P=False)
+            K, N = site.K, site.N
+            d = dict(name=site.name, K=K, N=N, dm=t.dm, du=t.du, X=torch.from_numpy(t.X).to(dev),
+                     Aq=torch.empty((M, K // 2), dtype=torch.uint8, device=dev),
+                     s_a=torch.empty((M,), dtype=torch.float32, device=dev),
+                     Y=torch.empty((M, N), dtype=torch.float16, device=dev),
+                     gws=torch.empty(max(sq.gemm_workspace_bytes(M, N, K), 1), dtype=torch.uint8, device=dev),
+                     qws=torch.empty(max(sq.quant_act_workspace_bytes(M, K, False, site.tac), 1), dtype=torch.uint8,
+                                     device=dev))
+            if site.tac:
+                d.update(tac_M=torch.from_numpy(t.tac_M).to(dev), tac_d=torch.from_numpy(t.tac_d).to(dev), g=t.g)
+            sites.append(d)
+            del t
+        copies = 8 if M <= 64 else 1        # small steps stream their weights: keep them out of the LLC
+        wsets = [[(Wf, s_w) for (_, Wf, s_w) in meta]] + [[(Wf.clone(), s_w.clone()) for (_, Wf, s_w) in meta]
+                                                          for _ in range(copies - 1)]
+        layouts = [(str(tt), synth.config_state(synth.LLADA_SWEEP, M=M, t=tt)) for tt in range(65)]
+        layouts += [(k, synth.state_edge(M, k)) for k in ("all_masked", "none_masked", "alternating")]
+        times = {}
+        for label, st_np in layouts:
+            state = torch.from_numpy(st_np).to(dev)
+
+            def step(i, state=state):
+                for d, (Wf, s_w) in zip(sites, wsets[i % copies]):
+                    sq.sgat_quant_act(d["X"], state, None, d["dm"], d["du"], d.get("tac_M"), d.get("tac_d"),
+                                      d.get("g", 0), Aq=d["Aq"], s_a=d["s_a"], ws=d["qws"])
+                    sq.w4a4_gemm_frag(d["Aq"], d["s_a"], Wf, s_w, Y=d["Y"], ws=d["gws"])
+            calls = copies if M <= 64 else (4 if M <= 1024 else 1)
+            ms, g = graph_ms(torch, step, calls, replays=5 if M <= 1024 else 3)
+            del g
+            times[label] = ms * 1e3
+        steps_us = [times[str(tt)] for tt in range(65)]
+        out[str(M)] = {"us_per_step_t0_to_t64": steps_us,
+                       "us_per_step_edges": {k: times[k] for k in ("all_masked", "none_masked", "alternating")},
+                       "max_over_min_t": max(steps_us) / min(steps_us),
+                       "median_us": float(np.median(steps_us)),
+                       "tokens_per_s_median": M / (float(np.median(steps_us)) / 1e6)}
+        del sites, wsets
+        torch.cuda.empty_cache()
+    del meta
+    torch.cuda.empty_cache()
+    return {"workload": "LLaDA-8B-shaped layer set (folded P), denoising steps t = 0..64 (mask fraction 1 -> 0) "
+                        "and the edge layouts, at 16, 1024 and 16384 tokens, each step graph-replayed",
+            "per_tokens": out}
 
 
 def small_token_block(torch, sq, synth, dev, token_counts=(16, 32, 64), copies=8):
@@ -383,28 +815,24 @@ def small_token_block(torch, sq, synth, dev, token_counts=(16, 32, 64), copies=8
     return res
 
 
-def sweep_block(torch, sq, synth, dev, token_counts=(16, 64, 256, 1024, 4096, 16384), copies=1):
-    """Denoising-step sweep over token counts (LLaDA shapes, step 32 of 64, folded P):
-    the W4A4 GEMM of every linear, graph-replayed with rotating weights, as
-    achieved TOP/s and algorithmic GB/s, from memory-bound to compute-bound."""
+def sweep_block(torch, sq, synth, dev, token_counts=(16, 64, 256, 1024, 4096, 16384)):
+    """GEMM token-count sweep (LLaDA shapes, step 32 of 64, folded P): the W4A4
+    GEMM of every linear, graph-replayed with rotating weights, as achieved TOP/s
+    and algorithmic GB/s, from memory-bound to compute-bound."""
     cfg = synth.CONFIGS[synth.LLADA_SWEEP]
     st_max = synth.config_state(synth.LLADA_SWEEP, M=max(token_counts), t=32)
-    wsets, meta = [[] for _ in range(copies)], []
+    meta = []
     for si, site in enumerate(cfg.sites):
         t = synth.site_tensors(synth.LLADA_SWEEP, si, st_max[:16], with_P=False)
         W = torch.from_numpy(t.W).to(dev)
         Wq, s_w = sq.sgat_prepare_weights(W, None)
-        Wf = sq.weights_to_frag(Wq)
-        del W, Wq
-        for c in range(copies):
-            wsets[c].append((Wf.clone(), s_w.clone()))
-        meta.append(site)
-        del t, Wf, s_w
-    rots = [rotating_copies(*wsets[0][si]) for si in range(len(meta))]
+        meta.append((site, sq.weights_to_frag(Wq), s_w))
+        del W, Wq, t
+    rots = [rotating_copies(Wf, s_w) for (_, Wf, s_w) in meta]
     out = {}
     for M in token_counts:
         rec = {}
-        for si, site in enumerate(meta):
+        for si, (site, _, _) in enumerate(meta):
             K, N = site.K, site.N
             g = torch.Generator(device="cpu").manual_seed(M * 10 + si)
             Aq = torch.randint(0, 256, (M, K // 2), dtype=torch.uint8, generator=g).to(dev)
@@ -422,59 +850,10 @@ def sweep_block(torch, sq, synth, dev, token_counts=(16, 64, 256, 1024, 4096, 16
                               "gbs": byts / ms / 1e6, "frac_hbm_peak": byts / ms / 1e6 / PEAK_HBM_GBS}
             del Aq, s_a, Y, gws
         out[str(M)] = rec
-    del wsets, rots
+    del rots, meta
     torch.cuda.empty_cache()
     return {"workload": "W4A4 GEMMs of the LLaDA-shaped layer set, token counts 16 ... 16384, graph-replayed, "
                         ">= 800 MB of rotating weights per GEMM", "per_tokens": out}
-
-
-def tac_oproj_block(torch, sq, synth, dev, steps=5):
-    """TAC (32 blocks of 128) on 8 x 2048 attention outputs of width 4096, then the
-    gate + int4 quantiser and the 4096 -> 4096 W4A4 GEMM (folded P).  TAC at
-    g = 128 runs as its own kernel (the fused form covers g <= 16)."""
-    st_np = synth.config_state(synth.TAC_OPROJ)
-    M = len(st_np)
-    state = torch.from_numpy(st_np).to(dev)
-    t = synth.site_tensors(synth.TAC_OPROJ, 0, st_np, with_P=False)
-    K, N, g = t.site.K, t.site.N, t.g
-    W = torch.from_numpy(t.W).to(dev)
-    Wq, s_w = sq.sgat_prepare_weights(W, None)
-    Wf = sq.weights_to_frag(Wq)
-    del W, Wq
-    X = torch.from_numpy(t.X).to(dev)
-    tM, td = torch.from_numpy(t.tac_M).to(dev), torch.from_numpy(t.tac_d).to(dev)
-    Z = torch.empty_like(X)
-    Aq = torch.empty((M, K // 2), dtype=torch.uint8, device=dev)
-    s_a = torch.empty((M,), dtype=torch.float32, device=dev)
-    Y = torch.empty((M, N), dtype=torch.float16, device=dev)
-    gws = torch.empty(max(sq.gemm_workspace_bytes(M, N, K), 1), dtype=torch.uint8, device=dev)
-    timer = Timer(torch)
-
-    def step(tm):
-        tm.wrap("tac", lambda: sq.tac_apply(X, tM, td, g, out=Z))
-        tm.wrap("q", lambda: sq.sgat_quant_act(Z, state, None, t.dm, t.du, Aq=Aq, s_a=s_a))
-        tm.wrap("g", lambda: sq.w4a4_gemm_frag(Aq, s_a, Wf, s_w, Y=Y, ws=gws))
-    step(Timer(torch))
-    torch.cuda.synchronize()
-    e0 = torch.cuda.Event(enable_timing=True)
-    e1 = torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(steps):
-        step(timer)
-    e1.record()
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / steps
-    tac_ms = timer.ms("tac")[0] / steps
-    g_ms = timer.ms("g")[0] / steps
-    tac_flop = 2.0 * M * K * g
-    return {"workload": f"TAC g = {g} + O projection {K}->{N}, 8 x 2048 tokens, folded P",
-            "tokens": M, "ms_per_step": ms, "tokens_per_s": M / (ms / 1e3),
-            "tac_ms": tac_ms, "quant_ms": timer.ms("q")[0] / steps, "gemm_ms": g_ms,
-            "gemm_frac_int8_peak": 2.0 * M * N * K / g_ms / 1e9 / PEAK_INT8_TOPS,
-            "roofline": {"bound": "alu", "achieved": tac_flop / tac_ms / 1e9, "peak": PEAK_FP32_VALU_TFLOPS,
-                         "unit": "TFLOP/s", "frac": tac_flop / tac_ms / 1e9 / PEAK_FP32_VALU_TFLOPS,
-                         "traffic": recorded_traffic("tac_g128") if g == 128 else None,
-                         "kernel": f"tac (g = {g})"}}
 
 
 def tac_calibration_block(torch, sq, synth, dev, N=8192, C=4096, reps=5):
@@ -509,7 +888,8 @@ def tac_calibration_block(torch, sq, synth, dev, N=8192, C=4096, reps=5):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this benchmark runs on exactly one GPU; --gpus must be 1"}), flush=True)
+        print(json.dumps({"error": "this benchmark runs on exactly one GPU (one GPU's share of the layer set); "
+                                   "--gpus must be 1"}), flush=True)
         sys.exit(2)
     import torch
     import paper_2606_04945_amd as sq
@@ -518,149 +898,47 @@ def main():
     sq.lib()                                    # raises if the HIP library is missing
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    cfg = synth.CONFIGS[synth.LLADA]
-    M = cfg.M
-    state_np = synth.config_state(synth.LLADA)
-    state = torch.from_numpy(state_np).to(dev)
-    t0 = time.time()
-    sites = []
-    for si, site in enumerate(cfg.sites):
-        t = synth.site_tensors(synth.LLADA, si, state_np)
-        d = dict(site=site, K=site.K, N=site.N, dm=t.dm, du=t.du,
-                 X=torch.from_numpy(t.X).to(dev), P=torch.from_numpy(t.P).to(dev),
-                 W=torch.from_numpy(t.W).to(dev))
-        if site.tac:
-            d.update(tac_M=torch.from_numpy(t.tac_M).to(dev), tac_d=torch.from_numpy(t.tac_d).to(dev), g=t.g)
-        sites.append(d)
-    print(f"# inputs generated in {time.time() - t0:.1f}s", file=sys.stderr, flush=True)
 
-    # offline weight preparation (Eq. 12), outside the timed region
-    for d in sites:
-        d["Wq"], d["s_w"] = sq.sgat_prepare_weights(d["W"], d["P"])
-        d["Wf"] = sq.weights_to_frag(d["Wq"])
-        K, N = d["K"], d["N"]
-        d["z"] = torch.empty((M, K), dtype=torch.float16, device=dev) if "tac_M" in d else None
-        d["xp"] = torch.empty((M, K), dtype=torch.float32, device=dev)
-        d["Aq"] = torch.empty((M, K // 2), dtype=torch.uint8, device=dev)
-        d["s_a"] = torch.empty((M,), dtype=torch.float32, device=dev)
-        d["Y"] = torch.empty((M, N), dtype=torch.float16, device=dev)
-        nb = sq.gemm_workspace_bytes(M, N, K)
-        d["gws"] = torch.empty(max(nb, 1), dtype=torch.uint8, device=dev)
-        nq = sq.quant_act_workspace_bytes(M, K, False, "tac_M" in d)
-        d["qws"] = torch.empty(max(nq, 1), dtype=torch.uint8, device=dev)
-    if not args.no_w8:
+    head, sites, state, state_np, hosts, rows = headline_block(torch, sq, synth, dev, args)
+    M = head["tokens"]
+    nested = {}
+    if not args.only_headline:
+        # the same Dream-shaped inputs with P folded (weights prepared without P)
+        prepare(sq, sites, False)
+        large = folded_block(torch, sq, sites, state, M, max(3, args.steps // 4), 1)
+        large["workload"] = ("Dream-7B-shaped SGAT layer set, 8 x 2048 tokens, folded P (TAC g=16 fused with the "
+                             "O quantiser)")
+        dom = max(large["per_site"], key=lambda n: large["per_site"][n]["gemm_us"])
+        large["roofline"] = {"bound": "mfma", "achieved": large["per_site"][dom]["tops"], "peak": PEAK_INT8_TOPS,
+                             "unit": "TOP/s", "frac": large["per_site"][dom]["frac_int8_peak"],
+                             "traffic": recorded_traffic("gemm_large") if dom == "gate_up" else None,
+                             "kernel": f"w4a4 gemm ({dom})"}
+        if not args.no_fp6:
+            large["fp6"] = fp6_variant(torch, sq, sites, state, M, max(3, args.steps // 4), 1)
         for d in sites:
-            d["Wq8"], d["s_w8"] = sq.sgat_prepare_weights_w8(d["W"], d["P"])
-            K, N = d["K"], d["N"]
-            d["Aq8"] = torch.empty((M, K), dtype=torch.int8, device=dev)
-            d["gws8"] = torch.empty(max(sq.gemm_workspace_bytes(M, N, K, 8), 1), dtype=torch.uint8, device=dev)
-    # rotating copies of the prepared weights for the folded-basis runs (8 x 108 MB
-    # of 4-bit, 4 x 216 MB of 8-bit codes), so that the 256 MB last-level cache
-    # cannot hold a layer set's weights from one step to the next
-    wcopies = [[(d["Wf"].clone(), d["s_w"].clone()) for d in sites] for _ in range(8)]
-    w8copies = ([[(d["Wq8"].clone(), d["s_w8"].clone()) for d in sites] for _ in range(4)]
-                if not args.no_w8 else [])
-    torch.cuda.synchronize()
-    timer = Timer(torch)
+            large["per_site"][d["name"]]["vendor_int8_gemm_us"] = vendor_int8_us(torch, M, d["N"], d["K"], dev)
+        nested["dream_folded_P"] = large
+    del sites
+    torch.cuda.empty_cache()
 
-    def step_dense(tm):
-        for d in sites:
-            src = d["X"]
-            if d["z"] is not None:
-                tm.wrap("tac", lambda: sq.tac_apply(d["X"], d["tac_M"], d["tac_d"], d["g"], out=d["z"]))
-                src = d["z"]
-            tm.wrap("transform/" + d["site"].name,
-                    lambda: sq.sgat_transform(src, state, d["P"], d["dm"], d["du"], out=d["xp"]))
-            tm.wrap("quant", lambda: sq.sgat_quantize(d["xp"], Aq=d["Aq"], s=d["s_a"]))
-            tm.wrap("gemm/" + d["site"].name,
-                    lambda: sq.w4a4_gemm_frag(d["Aq"], d["s_a"], d["Wf"], d["s_w"], Y=d["Y"], ws=d["gws"]))
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline_block(hosts, M, min(args.cpu_rows, len(rows)), min(args.cpu_rows_1core, len(rows)))
+    del hosts
 
-    def step_dense_fast(tm):
-        for d in sites:
-            src = d["X"]
-            if d["z"] is not None:
-                tm.wrap("tac", lambda: sq.tac_apply(d["X"], d["tac_M"], d["tac_d"], d["g"], out=d["z"]))
-                src = d["z"]
-            tm.wrap("ftransform/" + d["site"].name,
-                    lambda: sq.sgat_transform_fast(src, state, d["Ps"], d["dm"], d["du"], out=d["xp"]))
-            tm.wrap("quant", lambda: sq.sgat_quantize(d["xp"], Aq=d["Aq"], s=d["s_a"]))
-            tm.wrap("gemm/" + d["site"].name,
-                    lambda: sq.w4a4_gemm_frag(d["Aq"], d["s_a"], d["Wf"], d["s_w"], Y=d["Y"], ws=d["gws"]))
-
-    def step_folded(tm, it):
-        ws = wcopies[it % len(wcopies)]
-        for d, (Wf, s_w) in zip(sites, ws):
-            tm.wrap("quant_act/" + d["site"].name,
-                    lambda: sq.sgat_quant_act(d["X"], state, None, d["dm"], d["du"], d.get("tac_M"),
-                                              d.get("tac_d"), d.get("g", 0), Aq=d["Aq"], s_a=d["s_a"],
-                                              ws=d["qws"]))
-            tm.wrap("gemm/" + d["site"].name,
-                    lambda: sq.w4a4_gemm_frag(d["Aq"], d["s_a"], Wf, s_w, Y=d["Y"], ws=d["gws"]))
-
-    def step_w8(tm, it):
-        for d, (Wq8, s_w8) in zip(sites, w8copies[it % len(w8copies)]):
-            tm.wrap("quant_act8/" + d["site"].name,
-                    lambda: sq.sgat_quant_act_w8(d["X"], state, None, d["dm"], d["du"], d.get("tac_M"),
-                                                 d.get("tac_d"), d.get("g", 0), Aq=d["Aq8"], s_a=d["s_a"],
-                                                 ws=d["qws"]))
-            tm.wrap("gemm8/" + d["site"].name,
-                    lambda: sq.w8a8_gemm(d["Aq8"], d["s_a"], Wq8, s_w8, Y=d["Y"], ws=d["gws8"]))
-
-    def run(step, steps, warmup):
-        for i in range(warmup):
-            step(Timer(torch), i)
-        torch.cuda.synchronize()
-        timer.reset()
-        start = torch.cuda.Event(enable_timing=True)
-        end = torch.cuda.Event(enable_timing=True)
-        start.record()
-        for i in range(steps):
-            step(timer, i)
-        end.record()
-        torch.cuda.synchronize()
-        return start.elapsed_time(end) / steps
-
-    out = {}
-    flops_tr = {d["site"].name: 2.0 * M * d["K"] * (d["K"] - d["K"] // 32) for d in sites}
-    ops_gemm = {d["site"].name: 2.0 * M * d["N"] * d["K"] for d in sites}
-
-    if args.only in ("dense", "both"):
-        ms_dense = run(lambda tm, i: step_dense(tm), args.steps, args.warmup)
-        tr_ms = sum(timer.ms("transform/" + n)[0] for n in flops_tr)
-        tr_flop = sum(flops_tr.values()) * args.steps
-        gm_ms = sum(timer.ms("gemm/" + n)[0] for n in ops_gemm)
-        gm_ops = sum(ops_gemm.values()) * args.steps
-        out["dense"] = dict(ms=ms_dense, transform_ms=tr_ms / args.steps, transform_tflops=tr_flop / tr_ms / 1e9,
-                            gemm_ms=gm_ms / args.steps, gemm_tops=gm_ops / gm_ms / 1e9,
-                            tac_ms=timer.ms("tac")[0] / args.steps, quant_ms=timer.ms("quant")[0] / args.steps,
-                            per_site_transform_ms={n: timer.ms("transform/" + n)[0] / args.steps for n in flops_tr})
-    if args.only in ("dense", "both") and not args.no_fast:
-        for d in sites:
-            d["Ps"] = sq.sgat_split_basis(d["P"])
-        # codes of one step through each transform, compared
-        step_dense(Timer(torch))
-        torch.cuda.synchronize()
-        canon = [(d["Aq"].clone(), d["s_a"].clone()) for d in sites]
-        step_dense_fast(Timer(torch))
-        torch.cuda.synchronize()
-        flips = sum(int(((a ^ d["Aq"]) & 0x0F).ne(0).sum() + ((a ^ d["Aq"]) & 0xF0).ne(0).sum())
-                    for (a, _), d in zip(canon, sites))
-        ncodes = sum(d["Aq"].numel() * 2 for d in sites)
-        ms_f = run(lambda tm, i: step_dense_fast(tm), args.steps, args.warmup)
-        tr_ms = sum(timer.ms("ftransform/" + n)[0] for n in flops_tr)
-        tr_flop = sum(flops_tr.values()) * args.steps
-        out["dense_fast"] = dict(ms=ms_f, transform_ms=tr_ms / args.steps, transform_tflops=tr_flop / tr_ms / 1e9,
-                                 code_flips=flips, codes=ncodes)
-        del canon
-    if args.only in ("folded", "both"):
-        ms_fold = run(step_folded, args.steps, args.warmup)
-        gm_ms = sum(timer.ms("gemm/" + n)[0] for n in ops_gemm)
-        gm_ops = sum(ops_gemm.values()) * args.steps
-        qa_ms = sum(timer.ms("quant_act/" + d["site"].name)[0] for d in sites)
-        out["folded"] = dict(ms=ms_fold, gemm_ms=gm_ms / args.steps, gemm_tops=gm_ops / gm_ms / 1e9,
-                             quant_act_ms=qa_ms / args.steps,
-                             per_site_gemm_ms={n: timer.ms("gemm/" + n)[0] / args.steps for n in ops_gemm})
-
+    if not args.only_headline:
+        if not args.no_llada:
+            nested.update({"llada_" + k: v for k, v in llada_blocks(torch, sq, synth, dev, args).items()})
+        nested["single_linear"] = single_linear_block(torch, sq, synth, dev)
+        nested["tac_oproj"] = tac_oproj_block(torch, sq, synth, dev)
+        if not args.no_denoise:
+            nested["denoise_sweep"] = denoise_sweep_block(torch, sq, synth, dev)
+        if not args.no_small:
+            nested["small_token"] = small_token_block(torch, sq, synth, dev)
+        if not args.no_sweep:
+            nested["token_sweep_gemm"] = sweep_block(torch, sq, synth, dev)
+        if not args.no_calib:
+            nested["tac_calibration"] = tac_calibration_block(torch, sq, synth, dev)
     if args.calibrate_copy:
         # a plain device-to-device copy of known size: its FETCH_SIZE / WRITE_SIZE
         # readings scale the counters of the kernels above to bytes
@@ -671,112 +949,27 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
-    if not args.no_w8:
-        ms_w8 = run(step_w8, args.steps, args.warmup)
-        gm_ms = sum(timer.ms("gemm8/" + n)[0] for n in ops_gemm)
-        gm_ops = sum(ops_gemm.values()) * args.steps
-        out["w8"] = dict(ms=ms_w8, gemm_tops=gm_ops / gm_ms / 1e9,
-                         quant_act_ms=sum(timer.ms("quant_act8/" + n)[0] for n in ops_gemm) / args.steps)
-
-    if not args.no_large:
-        out["large"] = large_token_block(torch, sq, synth, dev, max(3, args.steps // 4), 1)
-    if not args.no_small:
-        out["small"] = small_token_block(torch, sq, synth, dev)
-    if not args.no_large:
-        out["tac_oproj"] = tac_oproj_block(torch, sq, synth, dev)
-    if not args.no_sweep:
-        out["sweep"] = sweep_block(torch, sq, synth, dev)
-    if not args.no_calib:
-        out["calib"] = tac_calibration_block(torch, sq, synth, dev)
-
-    # ---------------------------------------------------------------- CPU baseline
-    cpu = None
-    if not args.no_cpu_baseline:
-        from oracle import oracle as O
-        threads = min(16, os.cpu_count() or 1)
-        n = args.cpu_sample
-        rows = np.linspace(0, M - 1, n).astype(int)
-        rng = np.random.default_rng(0)
-        hosts = []
-        for d in sites:
-            h = dict(X=d["X"][rows].cpu().numpy(), P=d["P"].cpu().numpy(), st=state_np[rows],
-                     Wq=rng.integers(0, 256, (d["N"], d["K"] // 2), dtype=np.uint8),
-                     s_w=np.ones(d["N"], np.float32))
-            if "tac_M" in d:
-                h.update(tM=d["tac_M"].cpu().numpy(), td=d["tac_d"].cpu().numpy(), g=d["g"])
-            hosts.append((d, h))
-        t1 = time.time()
-        for d, h in hosts:
-            Aq, s_a = O.quant_act(h["X"], h["st"], h["P"], d["dm"], d["du"], h.get("tM"), h.get("td"),
-                                  h.get("g", 0), threads=threads)
-            O.gemm(Aq, s_a, h["Wq"], h["s_w"], threads=threads)
-        el = time.time() - t1
-        cpu = {"value": n / el, "unit": "tokens/s", "cores": threads, "kind": "oracle",
-               "sample": f"{n} of the {M} tokens through the whole dense-P layer set (TAC, transform, "
-                         f"quantise, GEMM against all N); weight preparation excluded; {el:.1f} s"}
-
-    dense = out.get("dense")
-    fold = out.get("folded")
-    main_ms = dense["ms"] if dense else fold["ms"]
     res = {
         "metric": "W4A4 SGAT-linear TOPS & % int8-MFMA peak; layer-set tokens/s per denoise step",
-        "value": M / (main_ms / 1e3),
+        "value": head["tokens_per_s"],
         "unit": "tokens/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
-        "ms_per_step": main_ms,
+        "ms_per_step": head["ms_per_step"],
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "int4xint4->int32 GEMM, fp32 transform, fp16 I/O",
         "data": "synthetic (seeded; random-init weights and orthogonal bases)",
-        "weights": "int4 codes in fragment order (sq_weights_to_frag, once, outside the timed region); W8A8 and "
-                   "FP6 variants in their own layouts",
-        "config": {"workload": "LLaDA-8B-shaped SGAT layer set (QKV, O+TAC g=16, gate+up, down), "
-                               "1024 tokens, dense online P" if dense else
-                               "LLaDA-8B-shaped SGAT layer set, 1024 tokens, folded P",
-                   "tokens": M, "hidden": 4096, "ffn": 12288, "tac_block": 16},
+        "weights": "int4 codes in fragment order (sq_weights_to_frag, once, outside the timed region)",
+        "config": {"workload": head["workload"], "tokens": M, "batch": 8, "seq_len": 2048, "hidden": 3584,
+                   "ffn": 18944, "tac_block": 16},
+        "roofline": head["roofline"],
+        "sgat_linear_tops": head["sgat_linear_tops"],
+        "gemm": {"tops": head["gemm_tops"], "frac_int8_peak": head["gemm_frac_int8_peak"]},
+        "breakdown_ms": {"transform": head["transform_ms"], "gemm": head["gemm_ms"],
+                         "quant": sum(v["quant_us"] for v in head["per_site"].values()) / 1e3,
+                         "tac": sum(v.get("tac_us", 0.0) for v in head["per_site"].values()) / 1e3},
+        "per_site": head["per_site"],
     }
-    if dense:
-        ach = dense["transform_tflops"]
-        res["roofline"] = {"bound": "alu", "achieved": ach, "peak": PEAK_FP32_VALU_TFLOPS, "unit": "TFLOP/s",
-                           "frac": ach / PEAK_FP32_VALU_TFLOPS,
-                           "traffic": recorded_traffic("transform", "traffic_bytes_per_launch_step_avg"),
-                           "kernel": "transform (dense fp32 x P, fixed order)"}
-        res["breakdown_ms"] = {k: dense[k] for k in ("transform_ms", "gemm_ms", "tac_ms", "quant_ms")}
-        res["gemm"] = {"tops": dense["gemm_tops"], "frac_int8_peak": dense["gemm_tops"] / PEAK_INT8_TOPS}
-        res["sgat_linear_tops"] = sum(ops_gemm.values()) / (dense["ms"] / 1e3) / 1e12
-    if fold:
-        res["folded_P"] = {
-            "value": M / (fold["ms"] / 1e3), "unit": "tokens/s", "ms_per_step": fold["ms"],
-            "sgat_linear_tops": sum(ops_gemm.values()) / (fold["ms"] / 1e3) / 1e12,
-            "roofline": {"bound": "mfma", "achieved": fold["gemm_tops"], "peak": PEAK_INT8_TOPS, "unit": "TOP/s",
-                         "frac": fold["gemm_tops"] / PEAK_INT8_TOPS, "kernel": "w4a4 gemm"},
-            "quant_act_ms": fold["quant_act_ms"], "per_site_gemm_ms": fold["per_site_gemm_ms"]}
-        if not dense:
-            res["roofline"] = dict(res["folded_P"]["roofline"], traffic=None)
-    if "w8" in out:
-        w8 = out["w8"]
-        res["w8a8_folded_P"] = {"value": M / (w8["ms"] / 1e3), "unit": "tokens/s", "ms_per_step": w8["ms"],
-                                "gemm_tops": w8["gemm_tops"], "gemm_frac_int8_peak": w8["gemm_tops"] / PEAK_INT8_TOPS,
-                                "quant_act_ms": w8["quant_act_ms"]}
-    if "dense_fast" in out:
-        f = out["dense_fast"]
-        res["dense_P_fast_transform"] = {
-            "value": M / (f["ms"] / 1e3), "unit": "tokens/s", "ms_per_step": f["ms"],
-            "transform_ms": f["transform_ms"],
-            "roofline": {"bound": "mfma", "achieved": f["transform_tflops"], "peak": PEAK_FP16_TFLOPS,
-                         "unit": "TFLOP/s", "frac": f["transform_tflops"] / PEAK_FP16_TFLOPS,
-                         "traffic": recorded_traffic("transform_fast", "traffic_bytes_per_launch_step_avg"),
-                         "kernel": "transform on the fp16 MFMA (hi + lo split: executes 2x the algorithmic flops)"},
-            "codes_differing_from_fixed_order": f["code_flips"], "codes": f["codes"]}
-    if "large" in out:
-        res["large_token"] = out["large"]
-    if "small" in out:
-        res["small_token"] = out["small"]
-    if "tac_oproj" in out:
-        res["tac_oproj"] = out["tac_oproj"]
-    if "sweep" in out:
-        res["token_sweep_gemm"] = out["sweep"]
-    if "calib" in out:
-        res["tac_calibration"] = out["calib"]
+    res.update(nested)
     if cpu:
         res["cpu_baseline"] = cpu
     print(json.dumps(res), flush=True)

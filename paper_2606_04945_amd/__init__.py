@@ -12,6 +12,7 @@ and streams.  Outputs and workspaces are allocated with torch when not given.
 """
 from __future__ import annotations
 
+import functools
 from typing import Optional, Tuple
 
 import torch
@@ -25,6 +26,22 @@ __all__ = ["sgat_prepare_weights", "sgat_transform", "sgat_quantize", "sgat_quan
            "tac_calibrate", "tac_calibrate_workspace_bytes", "sgat_split_basis", "sgat_transform_fast",
            "fp6_row_bytes", "codes_to_fp6", "w4a4_gemm_fp6",
            "frag_weight_bytes", "weights_to_frag", "w4a4_gemm_frag"]
+
+
+def _on_stream(fn):
+    """Runs a binding call with `stream` (when given) as torch's current stream,
+    so that every tensor the call allocates (outputs, workspaces) belongs to the
+    stream its kernels run on and the caching allocator cannot hand that memory
+    to other work while they use it.  A raw HIP stream handle is wrapped as an
+    external stream."""
+    @functools.wraps(fn)
+    def wrapper(*args, stream=None, **kw):
+        if stream is None:
+            return fn(*args, stream=None, **kw)
+        s = stream if isinstance(stream, torch.cuda.Stream) else torch.cuda.ExternalStream(int(stream))
+        with torch.cuda.stream(s):
+            return fn(*args, stream=s, **kw)
+    return wrapper
 
 
 def _ptr(t: Optional[torch.Tensor]):
@@ -87,6 +104,7 @@ def _codes_spec(bits: int, K: int):
     return (torch.int8, K) if bits == 8 else (torch.uint8, K // 2)
 
 
+@_on_stream
 def sgat_prepare_weights(W: torch.Tensor, P: Optional[torch.Tensor] = None, *, Wq=None, s_w=None, ws=None,
                          stream=None, bits: int = 4):
     """W~ = Q_w(P^T W^T) as rows of W P: returns (Wq, s_w [N] fp32); Wq is [N][K/2]
@@ -111,6 +129,7 @@ def sgat_prepare_weights_w8(W, P=None, **kw):
     return sgat_prepare_weights(W, P, bits=8, **kw)
 
 
+@_on_stream
 def sgat_transform(X: torch.Tensor, state: Optional[torch.Tensor], P: Optional[torch.Tensor],
                    d_m: Optional[int] = None, d_u: Optional[int] = None, *, out=None, stream=None):
     """x'_i = x_i P G_{s_i} (Eq. 11), fp32 [M][K]."""
@@ -128,6 +147,7 @@ def sgat_transform(X: torch.Tensor, state: Optional[torch.Tensor], P: Optional[t
     return out
 
 
+@_on_stream
 def sgat_quantize(Xp: torch.Tensor, *, Aq=None, s=None, stream=None, bits: int = 4):
     """Per-row symmetric quantisation of fp32 rows (Eq. 2, z = 0): returns (Aq, s [M] fp32)."""
     M, K = Xp.shape
@@ -148,6 +168,7 @@ def sgat_quantize_w8(Xp, **kw):
     return sgat_quantize(Xp, bits=8, **kw)
 
 
+@_on_stream
 def sgat_quant_act(X: torch.Tensor, state: Optional[torch.Tensor], P: Optional[torch.Tensor] = None,
                    d_m: Optional[int] = None, d_u: Optional[int] = None, tac_M: Optional[torch.Tensor] = None,
                    tac_d: Optional[torch.Tensor] = None, g: int = 0, *, Aq=None, s_a=None, ws=None, stream=None,
@@ -182,6 +203,7 @@ def sgat_quant_act_w8(X, state, P=None, d_m=None, d_u=None, tac_M=None, tac_d=No
     return sgat_quant_act(X, state, P, d_m, d_u, tac_M, tac_d, g, bits=8, **kw)
 
 
+@_on_stream
 def w4a4_gemm(Aq: torch.Tensor, s_a: torch.Tensor, Wq: torch.Tensor, s_w: torch.Tensor, *, Y=None, acc=None,
               want_Y: bool = True, want_acc: bool = False, ws=None, stream=None, bits: int = 4):
     """Y = fp16((acc * s_a) * s_w) with acc = Aq . Wq^T exact (Eq. 13).  Returns Y, or (Y, acc).
@@ -218,6 +240,7 @@ def fp6_row_bytes(K: int) -> int:
     return n
 
 
+@_on_stream
 def codes_to_fp6(codes: torch.Tensor, *, out=None, stream=None):
     """Packed int4 codes [R, K/2] -> the FP6 (e3m2) operand layout [R, fp6_row_bytes(K)]."""
     R, Kh = codes.shape
@@ -231,6 +254,7 @@ def codes_to_fp6(codes: torch.Tensor, *, out=None, stream=None):
     return out
 
 
+@_on_stream
 def w4a4_gemm_fp6(A6: torch.Tensor, s_a: torch.Tensor, W6: torch.Tensor, s_w: torch.Tensor, K: int, *, Y=None,
                   acc=None, want_Y: bool = True, want_acc: bool = False, stream=None):
     """The W4A4 GEMM (Eq. 13) on FP6 operands (codes_to_fp6 layout) and the FP6
@@ -261,6 +285,7 @@ def frag_weight_bytes(N: int, K: int) -> int:
     return n
 
 
+@_on_stream
 def weights_to_frag(Wq: torch.Tensor, *, out=None, stream=None):
     """Packed int4 weights [N, K/2] -> fragment order [ceil(K/128), ceil(N/16), 1024] (uint8)."""
     N, Kh = Wq.shape
@@ -275,6 +300,7 @@ def weights_to_frag(Wq: torch.Tensor, *, out=None, stream=None):
     return out
 
 
+@_on_stream
 def w4a4_gemm_frag(Aq: torch.Tensor, s_a: torch.Tensor, Wf: torch.Tensor, s_w: torch.Tensor, *, Y=None, acc=None,
                    want_Y: bool = True, want_acc: bool = False, ws=None, stream=None):
     """w4a4_gemm (Eq. 13) with the weights in fragment order (weights_to_frag);
@@ -297,6 +323,7 @@ def w4a4_gemm_frag(Aq: torch.Tensor, s_a: torch.Tensor, Wf: torch.Tensor, s_w: t
     return (Y, acc) if want_acc else Y
 
 
+@_on_stream
 def tac_apply(Z: torch.Tensor, tac_M: torch.Tensor, tac_d: torch.Tensor, g: int, *, out=None, stream=None):
     """Z_b M_b^T + 1 d_b^T per block of g channels (Eq. 17), fp16 out."""
     M, C = Z.shape
@@ -317,6 +344,7 @@ def tac_calibrate_workspace_bytes(N: int, C: int, g: int) -> int:
     return int(lib().sq_tac_calibrate_workspace_bytes(N, C, g))
 
 
+@_on_stream
 def tac_calibrate(Z_fp: torch.Tensor, Z_q: torch.Tensor, g: int, *, rho: float = TAC_RHO, eps: float = TAC_EPS,
                   eta: float = TAC_ETA, alpha: float = TAC_ALPHA, want_fp64: bool = False, tac_M=None, tac_d=None,
                   ws=None, stream=None):
@@ -341,6 +369,7 @@ def tac_calibrate(Z_fp: torch.Tensor, Z_q: torch.Tensor, g: int, *, rho: float =
     return (tac_M, tac_d, M64, d64) if want_fp64 else (tac_M, tac_d)
 
 
+@_on_stream
 def sgat_split_basis(P: torch.Tensor, *, out=None, stream=None):
     """fp16 hi / lo split of 2^14 P, transposed: Ps [K, 2K] for sgat_transform_fast."""
     K = P.shape[0]
@@ -352,6 +381,7 @@ def sgat_split_basis(P: torch.Tensor, *, out=None, stream=None):
     return out
 
 
+@_on_stream
 def sgat_transform_fast(X: torch.Tensor, state: Optional[torch.Tensor], Ps: torch.Tensor,
                         d_m: Optional[int] = None, d_u: Optional[int] = None, *, out=None, stream=None):
     """x' = x P G_s on the fp16 matrix cores (within a stated bound of the exact
