@@ -20,7 +20,9 @@
  * ---------------------------------------
  *  - Every tensor pointer is a DEVICE pointer owned by the caller; the library
  *    never allocates, frees or retains device memory, and keeps no state between
- *    calls other than the thread-local error message.
+ *    calls other than the thread-local error message (one exception:
+ *    w4a4_gemm_frag_noalloc, for callers that cannot allocate, uses a
+ *    fixed-size scratch array the library holds on each GPU).
  *  - Row-major, dense.  fp16 tensors are passed as uint16_t* holding IEEE
  *    binary16 bits.  Packed int4 tensors are uint8_t* with two codes per byte:
  *    byte t of a row holds code 2t in bits 0-3 and code 2t+1 in bits 4-7, each a
@@ -189,30 +191,6 @@ int w8a8_gemm(const int8_t* Aq, const float* s_a, const int8_t* Wq, const float*
               void* ws, size_t ws_bytes, void* stream);
 
 /*
- * tac_calibrate -- the closed-form estimate of the TAC parameters (Sec. 3.3,
- * closed-form estimation; App. C), from paired attention outputs collected at
- * the TAC insertion point with the quantisers off (Z_fp) and on (Z_q).  Per
- * block b of g channels, in fp64:
- *   mu_b = (1/N) sum_i z_i, Sigma_b = (1/N) sum_i z_i z_i^T - mu_b mu_b^T (both inputs);
- *   lambda_b = rho max(Tr(Sigma_q) / g, eps);
- *   M_b = Sigma_fp^(1/2) (Sigma_q + lambda_b I)^(-1/2), each power through a
- *         symmetric eigendecomposition with eigenvalues clamped below at 1e-12;
- *   M_b = U diag(s) V^T -> U diag((1 - eta) s + eta mean(s)) V^T   (smoothing);
- *   M_b -> (1 - alpha) M_b + alpha I                                 (shrinkage);
- *   d_b = mu_fp - M_b mu_q.
- * The appendix's defaults are rho = 3e-4, eps = 1e-8, eta = 0.15, alpha = 0.55.
- *   Z_fp, Z_q [N][C] fp16, N >= 1 tokens; C as K (C % 64 == 0); g as for TAC.
- *   tac_M out [C/g][g][g] fp16 (M_b[r][c]), tac_d out [C] fp16: each one
- *         round-to-nearest-even from the fp64 value; the layout tac_apply and
- *         sgat_quant_act read.
- *   M64 out [C/g][g][g] fp64 and d64 out [C] fp64: the unrounded values, or NULL.
- *   ws    device workspace of at least sq_tac_calibrate_workspace_bytes(N, C, g)
- *         (required).
- * Sums run in a fixed order, so results depend only on the inputs; they agree
- * with any other fp64 evaluation to rounding, not bit for bit.  Offline: run
- * once per layer after the activation transform is fixed.
- */
-/*
  * Fast activation transform on the fp16 matrix cores (the matrix-core form of
  * Eq. 11).  The basis is split once: v = 2^14 P, hi = fp16(v), lo = fp16(v - hi),
  * stored as Ps [K][2K] fp16 with Ps[j][k] = hi(P[k][j]) and Ps[j][K + k] =
@@ -282,6 +260,54 @@ int w4a4_gemm_frag(const uint8_t* Aq, const float* s_a, const uint8_t* Wf, const
                    int32_t M, int32_t N, int32_t K, uint16_t* Y, int32_t* acc,
                    void* ws, size_t ws_bytes, void* stream);
 
+/*
+ * w4a4_gemm_frag_noalloc -- for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): w4a4_gemm_frag without the workspace argument.  Same arguments
+ * otherwise, same rules, same results bit for bit.  The K-split partial sums
+ * that w4a4_gemm_frag keeps in the caller's workspace go to scratch memory the
+ * library holds instead: a device array of SQ_NOALLOC_SCRATCH_BYTES per GPU,
+ * held from the first call on that GPU until the process ends.  The call
+ * allocates nothing (no hipMalloc, no library allocator); the first call on a
+ * device looks up the array's address once.
+ *   - A shape whose partial sums would exceed SQ_NOALLOC_SCRATCH_BYTES is
+ *     rejected with SQ_ERR_WORKSPACE (sq_gemm_workspace_bytes(M, N, K) gives
+ *     the need; no shape this GEMM splits needs more than 16 MiB).
+ *   - `stream` must belong to the current device (SQ_ERR_SHAPE otherwise).
+ *   - Every call on one GPU shares that GPU's array: calls that overlap in
+ *     time on one GPU (on different streams, or from different threads
+ *     without ordering) race on it and may return wrong results.  Calls
+ *     ordered on one stream are safe.  Nothing in the array needs to start at
+ *     zero; it keeps the last call's partial sums.
+ */
+#define SQ_NOALLOC_SCRATCH_BYTES ((size_t)16 << 20)
+int w4a4_gemm_frag_noalloc(const uint8_t* Aq, const float* s_a, const uint8_t* Wf, const float* s_w,
+                           int32_t M, int32_t N, int32_t K, uint16_t* Y, int32_t* acc, void* stream);
+
+/*
+ * tac_calibrate -- the closed-form estimate of the TAC parameters (Sec. 3.3,
+ * closed-form estimation; App. C), from paired attention outputs collected at
+ * the TAC insertion point with the quantisers off (Z_fp) and on (Z_q).  Per
+ * block b of g channels, in fp64:
+ *   mu_b = (1/N) sum_i z_i, Sigma_b = (1/N) sum_i z_i z_i^T - mu_b mu_b^T (both inputs);
+ *   lambda_b = rho max(Tr(Sigma_q) / g, eps);
+ *   M_b = Sigma_fp^(1/2) (Sigma_q + lambda_b I)^(-1/2), each power through a
+ *         symmetric eigendecomposition with eigenvalues clamped below at 1e-12;
+ *   M_b = U diag(s) V^T -> U diag((1 - eta) s + eta mean(s)) V^T   (smoothing);
+ *   M_b -> (1 - alpha) M_b + alpha I                                 (shrinkage);
+ *   d_b = mu_fp - M_b mu_q.
+ * The appendix's defaults are rho = 3e-4, eps = 1e-8, eta = 0.15, alpha = 0.55.
+ *   Z_fp, Z_q [N][C] fp16, N >= 1 tokens; C as K (C % 64 == 0); g as for TAC.
+ *   tac_M out [C/g][g][g] fp16 (M_b[r][c]), tac_d out [C] fp16: each one
+ *         round-to-nearest-even from the fp64 value; the layout tac_apply and
+ *         sgat_quant_act read.
+ *   M64 out [C/g][g][g] fp64 and d64 out [C] fp64: the unrounded values, or NULL.
+ *   ws    device workspace of at least sq_tac_calibrate_workspace_bytes(N, C, g)
+ *         (required).
+ * Sums run in a fixed order, so results depend only on the inputs; they agree
+ * with any other fp64 evaluation to rounding, not bit for bit.  Offline: run
+ * once per layer after the activation transform is fixed.
+ */
 size_t sq_tac_calibrate_workspace_bytes(int32_t N, int32_t C, int32_t g);
 int tac_calibrate(const uint16_t* Z_fp, const uint16_t* Z_q, int32_t N, int32_t C, int32_t g,
                   double rho, double eps, double eta, double alpha,

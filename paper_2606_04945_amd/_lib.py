@@ -38,6 +38,7 @@ SIGNATURES = {
     "sq_frag_weight_bytes": (_sz, [_i32, _i32]),
     "sq_weights_to_frag": (ctypes.c_int, [_p, _i32, _i32, _p, _p]),
     "w4a4_gemm_frag": (ctypes.c_int, [_p, _p, _p, _p, _i32, _i32, _i32, _p, _p, _p, _sz, _p]),
+    "w4a4_gemm_frag_noalloc": (ctypes.c_int, [_p, _p, _p, _p, _i32, _i32, _i32, _p, _p, _p]),
     "sq_tac_calibrate_workspace_bytes": (_sz, [_i32, _i32, _i32]),
     "tac_calibrate": (ctypes.c_int, [_p, _p, _i32, _i32, _i32, ctypes.c_double, ctypes.c_double, ctypes.c_double,
                                      ctypes.c_double, _p, _p, _p, _p, _p, _sz, _p]),

@@ -4,6 +4,9 @@
 #include <stdarg.h>
 #include <stdio.h>
 
+#include <atomic>
+#include <mutex>
+
 #include "../../include/starquant.h"
 #include "sq_internal.hpp"
 
@@ -195,6 +198,61 @@ int gemm(const uint8_t* Aq, const float* s_a, const uint8_t* Wq, const float* s_
         sq::launch_gemm(Aq, s_a, Wq, s_w, M, N, K, Y, acc, ws, static_cast<hipStream_t>(stream), bits), "gemm");
 }
 
+// Shared argument checks of the fragment-ordered GEMM entry points; *done is
+// set when there is nothing to compute (M == 0 or N == 0).
+int check_gemm_frag(const uint8_t* Aq, const float* s_a, const uint8_t* Wf, const float* s_w, int32_t M, int32_t N,
+                    int32_t K, uint16_t* Y, int32_t* acc, const char* name, int* done) {
+    SQ_TRY(check_K(K));
+    SQ_REQUIRE(M >= 0 && N >= 0, SQ_ERR_SHAPE, "M=%d N=%d: need >= 0", M, N);
+    SQ_REQUIRE(M <= kMaxTiledRows, SQ_ERR_SHAPE, "%s: M=%d: at most %d rows per call", name, M, kMaxTiledRows);
+    SQ_REQUIRE(N % 8 == 0, SQ_ERR_SHAPE, "N=%d: need N %% 8 == 0", N);
+    SQ_REQUIRE((size_t)M * K / 2 < (1u << 31) && sq::frag_weight_bytes(N, K) < (1u << 31), SQ_ERR_SHAPE,
+               "%s: each operand must be under 2 GiB (M=%d N=%d K=%d)", name, M, N, K);
+    *done = M == 0 || N == 0;
+    if (*done) return SQ_OK;
+    SQ_REQUIRE(Aq && s_a && Wf && s_w && (Y || acc), SQ_ERR_NULL,
+               "%s: Aq, s_a, Wf, s_w and one of Y / acc are required", name);
+    SQ_REQUIRE(aligned16(Aq) && aligned16(s_a) && aligned16(Wf) && aligned16(s_w) && aligned16(Y) && aligned16(acc),
+               SQ_ERR_ALIGN, "%s: pointers must be 16-byte aligned", name);
+    return SQ_OK;
+}
+
+// Scratch of w4a4_gemm_frag_noalloc: a file-scope device array, which every
+// GPU the library runs on holds (its own copy) until the process ends.  It
+// takes the K-split partial sums, the only scratch the GEMM uses; those are
+// written in full before they are read, so nothing has to start at zero.
+// Host code never passes the array's name to a kernel: it stands for a host
+// symbol there.  The device address comes from hipGetSymbolAddress, once per
+// device, on the first call that needs it with that device current.
+constexpr size_t kNoallocScratchBytes = SQ_NOALLOC_SCRATCH_BYTES;
+__device__ __align__(256) uint8_t scratch[kNoallocScratchBytes];
+std::atomic<void*> g_scratch_ptr[sq::kMaxDevices];
+std::mutex g_scratch_mu;
+
+int scratch_for(void* stream, void** out) {
+    int dev = -1;
+    SQ_TRY(hip_status(hipGetDevice(&dev), "hipGetDevice"));
+    SQ_REQUIRE(dev >= 0 && dev < sq::kMaxDevices, SQ_ERR_HIP, "device %d out of range", dev);
+    if (stream) {   // the address belongs to the current device, so the stream must too
+        hipDevice_t sdev = -1;
+        SQ_TRY(hip_status(hipStreamGetDevice(static_cast<hipStream_t>(stream), &sdev), "hipStreamGetDevice"));
+        SQ_REQUIRE(sdev == dev, SQ_ERR_SHAPE, "the stream belongs to device %d, not the current device %d",
+                   (int)sdev, dev);
+    }
+    void* p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+    if (!p) {
+        std::lock_guard<std::mutex> lock(g_scratch_mu);
+        p = g_scratch_ptr[dev].load(std::memory_order_relaxed);
+        if (!p) {
+            SQ_TRY(hip_status(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)), "hipGetSymbolAddress(scratch)"));
+            SQ_REQUIRE(p, SQ_ERR_HIP, "hipGetSymbolAddress(scratch) gave a null address");
+            g_scratch_ptr[dev].store(p, std::memory_order_release);
+        }
+    }
+    *out = p;
+    return SQ_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -330,23 +388,31 @@ int sq_weights_to_frag(const uint8_t* Wq, int32_t N, int32_t K, uint8_t* Wf, voi
 
 int w4a4_gemm_frag(const uint8_t* Aq, const float* s_a, const uint8_t* Wf, const float* s_w, int32_t M, int32_t N,
                    int32_t K, uint16_t* Y, int32_t* acc, void* ws, size_t ws_bytes, void* stream) {
-    SQ_TRY(check_K(K));
-    SQ_REQUIRE(M >= 0 && N >= 0, SQ_ERR_SHAPE, "M=%d N=%d: need >= 0", M, N);
-    SQ_REQUIRE(M <= kMaxTiledRows, SQ_ERR_SHAPE, "w4a4_gemm_frag: M=%d: at most %d rows per call", M, kMaxTiledRows);
-    SQ_REQUIRE(N % 8 == 0, SQ_ERR_SHAPE, "N=%d: need N %% 8 == 0", N);
-    SQ_REQUIRE((size_t)M * K / 2 < (1u << 31) && sq::frag_weight_bytes(N, K) < (1u << 31), SQ_ERR_SHAPE,
-               "w4a4_gemm_frag: each operand must be under 2 GiB (M=%d N=%d K=%d)", M, N, K);
-    if (M == 0 || N == 0) return SQ_OK;
-    SQ_REQUIRE(Aq && s_a && Wf && s_w && (Y || acc), SQ_ERR_NULL,
-               "w4a4_gemm_frag: Aq, s_a, Wf, s_w and one of Y / acc are required");
-    SQ_REQUIRE(aligned16(Aq) && aligned16(s_a) && aligned16(Wf) && aligned16(s_w) && aligned16(Y) &&
-                   aligned16(acc) && aligned16(ws),
-               SQ_ERR_ALIGN, "w4a4_gemm_frag: pointers must be 16-byte aligned");
+    int done = 0;
+    SQ_TRY(check_gemm_frag(Aq, s_a, Wf, s_w, M, N, K, Y, acc, "w4a4_gemm_frag", &done));
+    if (done) return SQ_OK;
+    SQ_REQUIRE(aligned16(ws), SQ_ERR_ALIGN, "w4a4_gemm_frag: pointers must be 16-byte aligned");
     const size_t need = sq_gemm_workspace_bytes(M, N, K);
     SQ_REQUIRE(ws_bytes >= need && (need == 0 || ws), SQ_ERR_WORKSPACE, "w4a4_gemm_frag: workspace %zu B < %zu B",
                ws_bytes, need);
     return hip_status(
         sq::launch_gemm_frag(Aq, s_a, Wf, s_w, M, N, K, Y, acc, ws, static_cast<hipStream_t>(stream)), "gemm_frag");
+}
+
+int w4a4_gemm_frag_noalloc(const uint8_t* Aq, const float* s_a, const uint8_t* Wf, const float* s_w, int32_t M,
+                           int32_t N, int32_t K, uint16_t* Y, int32_t* acc, void* stream) {
+    int done = 0;
+    SQ_TRY(check_gemm_frag(Aq, s_a, Wf, s_w, M, N, K, Y, acc, "w4a4_gemm_frag_noalloc", &done));
+    if (done) return SQ_OK;
+    const size_t need = sq_gemm_workspace_bytes(M, N, K);
+    SQ_REQUIRE(need <= kNoallocScratchBytes, SQ_ERR_WORKSPACE,
+               "w4a4_gemm_frag_noalloc: this shape needs %zu B of scratch, above the %zu B the library holds "
+               "(M=%d N=%d K=%d)", need, kNoallocScratchBytes, M, N, K);
+    void* ws = nullptr;
+    if (need > 0) SQ_TRY(scratch_for(stream, &ws));
+    return hip_status(
+        sq::launch_gemm_frag(Aq, s_a, Wf, s_w, M, N, K, Y, acc, ws, static_cast<hipStream_t>(stream)),
+        "gemm_frag_noalloc");
 }
 
 size_t sq_tac_calibrate_workspace_bytes(int32_t N, int32_t C, int32_t g) {

@@ -208,3 +208,29 @@ def test_frag_entry_points_validate(lib):
     assert lib.sq_weights_to_frag(FAKE + 512, 16, 128, FAKE, None) == L.SQ_ERR_SHAPE
     assert lib.sq_weights_to_frag(None, 0, 128, None, None) == L.SQ_OK
     assert lib.sq_weights_to_frag(FAKE, 1 << 20, 4096, FAKE + (1 << 40), None) == L.SQ_ERR_SHAPE
+
+
+def test_noalloc_gemm_validates(lib):
+    args = (FAKE, FAKE, FAKE, FAKE)
+    f = lib.w4a4_gemm_frag_noalloc
+    assert f(*args, 4, 16, 100, FAKE, None, None) == L.SQ_ERR_SHAPE
+    assert f(*args, 4, 12, 128, FAKE, None, None) == L.SQ_ERR_SHAPE
+    assert f(*args, -1, 16, 128, FAKE, None, None) == L.SQ_ERR_SHAPE
+    assert f(*args, 4, 16, 128, None, None, None) == L.SQ_ERR_NULL
+    assert f(FAKE, FAKE, FAKE + 8, FAKE, 4, 16, 128, FAKE, None, None) == L.SQ_ERR_ALIGN
+    assert f(*args, 1 << 20, 16, 4096, FAKE, None, None) == L.SQ_ERR_SHAPE
+    assert f(None, None, None, None, 0, 16, 128, None, None, None) == L.SQ_OK
+    assert f(None, None, None, None, 4, 0, 128, None, None, None) == L.SQ_OK
+
+
+def test_noalloc_scratch_covers_every_split_shape(lib):
+    """The GEMM splits K only below 256 output tiles of 64 x 64, so the partial
+    sums never exceed the 16 MiB the no-allocation entry point holds: checked
+    over token counts, widths and depths on both sides of every threshold."""
+    cap = 16 << 20
+    worst = 0
+    for M in (17, 49, 64, 65, 100, 128, 200, 255, 256, 300, 512, 1000, 1024, 2048, 4096):
+        for N in (8, 64, 520, 1024, 2048, 4096, 4608, 8192, 12288, 16384, 24576, 37888, 65536):
+            for K in (64, 512, 4096, 8192, 12288, 18944, 65536, 131072):
+                worst = max(worst, lib.sq_gemm_workspace_bytes(M, N, K))
+    assert 0 < worst <= cap
