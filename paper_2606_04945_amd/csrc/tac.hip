@@ -184,116 +184,145 @@ hipError_t launch_tac(const uint16_t* Z, const uint16_t* Mb, const uint16_t* d, 
 }  // namespace sq
 
 // ---------------------------------------------------------------------------
-// TAC fused with the gate and the per-token int4 quantiser, for g <= 16 and an
+// TAC fused with the gate and the per-token quantiser, for g <= 16 and an
 // input already in the P basis (no dense transform): z -> fp16(M_b z_b + d_b)
-// -> G_s -> absmax -> codes, without materialising z'.  Thread t owns channels
-// [8t, 8t + 8) of every token row (K / 8 active threads), keeps those channels'
-// block-matrix rows (8 x g) and biases in registers, and walks the workgroup's
-// tokens one row at a time: 8 outputs of g fused multiply-adds each (same order
-// and rounding as tac_kernel), the gate, a block max, then the 8 codes packed
-// into 4 bytes.
+// -> G_s -> absmax -> codes, without materialising z'.
+//
+// A workgroup owns a run of token rows.  Its consumer waves cover the row's
+// channels, 8 per thread (K / 8 active threads), each thread keeping the block
+// rows (8 x g fp16) and biases of its channels in registers for the whole run.
+// One more wave, the producer, only moves data: it copies each row of the run
+// from HBM straight into a ring of D row slots in LDS (buffer loads with the
+// LDS destination), D - 1 rows ahead of the consumers.  So the consumers never
+// load from memory inside the loop (their only memory operations there are
+// the code stores), and the producer never stores, so its counter waits count
+// its own loads exactly.  One workgroup barrier per row does three jobs: the
+// row has landed in its slot, every wave has written its partial max of the
+// previous row, and the slot read two rows back is free again.  After it the
+// consumers finish the previous row (block max, codes, store) and compute the
+// current one (g fused multiply-adds per output in the order and rounding of
+// tac_kernel, the gate, the wave max), so a row's two halves sit on either side
+// of one barrier.
 namespace sq {
 namespace {
 
-constexpr int kFusedThreads = 512;
+constexpr int kTqMaxConsumerWaves = 8;       // K <= 4096
+constexpr int kTqRing = 6;                   // row slots in the LDS ring
+constexpr int kTqMaxRows = 64;               // rows per workgroup (their states live in LDS)
 typedef _Float16 v8h __attribute__((ext_vector_type(8)));
 
-__device__ __forceinline__ float block_max_db(float v, float (*red)[kFusedThreads / kWave], int parity) {
-    v = wave_max(v);
-    const int w = threadIdx.x / kWave, l = threadIdx.x % kWave;
-    if (l == 0) red[parity][w] = v;
-    __syncthreads();
-    float r = 0.0f;
-    const int nw = (int)(blockDim.x + kWave - 1) / kWave;
-    for (int i = 0; i < nw; ++i) r = fmaxf(r, red[parity][i]);
-    return r;
+// Producer: wait until at most `n` of this wave's ring loads are in flight
+// (n = consumer waves x rows still ahead; the immediate must be a constant).
+__device__ __forceinline__ void wait_ring(int n) {
+    switch (n) {
+#define SQ_W(N) case N: wait_vm<N>(); break;
+        SQ_W(0) SQ_W(1) SQ_W(2) SQ_W(3) SQ_W(4) SQ_W(5) SQ_W(6) SQ_W(7) SQ_W(8) SQ_W(9) SQ_W(10) SQ_W(11)
+        SQ_W(12) SQ_W(14) SQ_W(15) SQ_W(16) SQ_W(18) SQ_W(20) SQ_W(21) SQ_W(24) SQ_W(25) SQ_W(28) SQ_W(30)
+        SQ_W(32) SQ_W(35) SQ_W(40)
+#undef SQ_W
+        default: wait_vm<0>(); break;
+    }
+}
+
+// Max over the wave of non-negative values, through DPP lane moves (no LDS):
+// quads, then halves of 16-lane rows, rows, then rows 0-1 into row 1, 2-3 into
+// row 3 and row 1 into row 3; lane 63 ends with the maximum.  Non-negative
+// floats order as their bit patterns do as integers.
+__device__ __forceinline__ float wave_max_dpp(float v) {
+    int x = __float_as_int(v);
+    x = max(x, __builtin_amdgcn_update_dpp(x, x, 0xB1, 0xF, 0xF, false));    // quad_perm [1, 0, 3, 2]
+    x = max(x, __builtin_amdgcn_update_dpp(x, x, 0x4E, 0xF, 0xF, false));    // quad_perm [2, 3, 0, 1]
+    x = max(x, __builtin_amdgcn_update_dpp(x, x, 0x141, 0xF, 0xF, false));   // row_half_mirror
+    x = max(x, __builtin_amdgcn_update_dpp(x, x, 0x140, 0xF, 0xF, false));   // row_mirror
+    x = max(x, __builtin_amdgcn_update_dpp(x, x, 0x142, 0xA, 0xF, false));   // row_bcast:15
+    x = max(x, __builtin_amdgcn_update_dpp(x, x, 0x143, 0xC, 0xF, false));   // row_bcast:31
+    return __int_as_float(__builtin_amdgcn_readlane(x, 63));
+}
+
+// LDS writes of this wave are complete, then the workgroup barrier (a bare
+// s_barrier: __syncthreads would also wait for the producer's loads in flight)
+__device__ __forceinline__ void ring_barrier() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt((15) | (7 << 4) | (0 << 8) | (3 << 14));   // lgkmcnt(0), vmcnt untouched
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
 }
 
 template <int G, int BITS>
-__global__ __launch_bounds__(kFusedThreads) void tac_quant_kernel(const uint16_t* __restrict__ Z,
-                                                                  const uint16_t* __restrict__ Mb,
-                                                                  const uint16_t* __restrict__ d,
-                                                                  const uint8_t* __restrict__ state, int M, int K,
-                                                                  int dm, int du, int rows_per_wg,
-                                                                  uint8_t* __restrict__ Aq,
-                                                                  float* __restrict__ s_out) {
+__global__ __launch_bounds__(64 * (kTqMaxConsumerWaves + 1)) void tac_quant_kernel(
+    const uint16_t* __restrict__ Z, const uint16_t* __restrict__ Mb, const uint16_t* __restrict__ d,
+    const uint8_t* __restrict__ state, int M, int K, int dm, int du, int rows_per_wg, uint8_t* __restrict__ Aq,
+    float* __restrict__ s_out) {
     constexpr int ZW = G > 8 ? G : 8;                   // input channels a thread reads (whole blocks)
-    __shared__ float red[2][kFusedThreads / kWave];
-    // staging of the block-matrix rows (G >= 4): per wave, TPP slots of 16 G + 16 bytes
-    constexpr int kStage = G >= 4 ? (G == 16 ? 32 : 64) * (16 * G + 16) : 16;
-    __shared__ __attribute__((aligned(16))) uint8_t pstage[kFusedThreads / kWave * kStage];
-    const int t = threadIdx.x;
-    const bool active = 8 * t < K;
+    extern __shared__ __attribute__((aligned(16))) float tq_smem[];
+    uint8_t* smem = reinterpret_cast<uint8_t*>(tq_smem);
+    const int cw = (K / 8 + kWave - 1) / kWave;         // consumer waves
+    const int slot_bytes = cw * 1024;                   // one row: 16 bytes per consumer thread
+    uint8_t* ring = smem;
+    float* red = reinterpret_cast<float*>(smem + kTqRing * slot_bytes);        // [2][kTqMaxConsumerWaves]
+    uint8_t* st_lds = reinterpret_cast<uint8_t*>(red + 2 * kTqMaxConsumerWaves); // [rows_per_wg]
+
+    const int t = threadIdx.x, lane = t % kWave;
+    const int wave = __builtin_amdgcn_readfirstlane(t / kWave);
+    const bool producer = wave == cw;
+    const bool active = !producer && 8 * t < K;
     const int c0 = 8 * t;                               // first output channel of this thread
     const int z0 = (c0 / ZW) * ZW;                      // first input channel it reads
     const int row_begin = blockIdx.x * rows_per_wg;
-    const int row_end = min(M, row_begin + rows_per_wg);
-    // A row's inputs (its activations and state byte) are requested before the
-    // previous row's work, the first row's around the block parameters, so these
-    // fetches overlap instead of following one another.  Buffer loads: inactive
-    // threads and a call without states read zeros, with no branch.
+    const int nrows = min(M, row_begin + rows_per_wg) - row_begin;
     const bool gated = state != nullptr;
-    const __amdgpu_buffer_rsrc_t rS = make_rsrc(state, gated ? (uint32_t)M : 0u);
-    v4i zr[ZW / 8];
-    uint32_t sb = 0;
-    auto fetch_z = [&](int row) {
-        const __amdgpu_buffer_rsrc_t rz = make_rsrc(Z + (size_t)row * K, (uint32_t)K * 2);
-#pragma unroll
-        for (int v = 0; v < ZW / 8; ++v)
-            zr[v] = __builtin_amdgcn_raw_buffer_load_b128(rz, active ? (z0 + 8 * v) * 2 : (int)kOOB, 0, 0);
-    };
-    auto fetch_s = [&](int row) { sb = __builtin_amdgcn_raw_buffer_load_b8(rS, row, 0, 0); };
-    if (row_begin < row_end) fetch_z(row_begin);
+
+    if (t < nrows) st_lds[t] = gated ? state[row_begin + t] : 0;
+
     // tac_M viewed as [K][G]: this thread's rows c0 .. c0 + 7 are 8 G fp16
     // values, held as G vectors of 8 (element r G + c of the run = row r,
-    // column c) and widened to fp32 where they are used
+    // column c), widened by the mixed-precision multiply-adds
     v8h mh[G];
     float dv[8];
-    const int cm = active ? c0 : 0;                     // inactive threads read the first rows, unused
+    const int cm = active ? c0 : 0;                     // other threads read the first rows, unused
     if constexpr (G >= 4) {
         // A thread's rows are PB = 16 G contiguous bytes at PB t, so loaded
         // directly the lanes of one 16-byte load would touch up to 64 cache
-        // lines.  Instead each wave loads its 64 runs with whole-wave
-        // contiguous 16-byte loads, writes them to per-thread LDS slots padded
-        // by 16 bytes (so the 16-byte reads below are free of bank conflicts),
-        // and each thread reads its own slot back; for G = 16 in two passes of
-        // 32 threads, one after the other so that only one pass's loads hold
-        // registers.  A wave's LDS accesses are performed in order, so only
-        // the compiler has to be kept from reordering them (the fences).
+        // lines.  Instead each consumer wave loads the runs of TPP of its
+        // threads at a time with whole-wave contiguous 16-byte loads, writes
+        // them to per-thread slots padded by 16 bytes (in the ring, not yet in
+        // use), so the 16-byte reads back are free of bank conflicts, and those
+        // threads read their slots.  A wave's LDS accesses are performed in
+        // order, so only the compiler has to be kept from reordering them.
         constexpr int PB = 16 * G, NC = PB / 16, SLOT = PB + 16;
-        constexpr int TPP = G == 16 ? 32 : 64;          // threads per pass
+        constexpr int TPP = G == 16 ? 16 : (G == 8 ? 32 : 64);   // at most 5 KB per wave per pass
         constexpr int PASSES = kWave / TPP;
         constexpr int LOADS = TPP * NC / kWave;         // 16-byte loads per lane per pass
-        const int wave = t / kWave, lane = t % kWave;
-        uint8_t* stage = pstage + wave * (TPP * SLOT);
-        const __amdgpu_buffer_rsrc_t rM = make_rsrc(Mb, (uint32_t)K * G * 2);
-        const int slab = wave * kWave * NC;             // first chunk of this wave's runs
-        auto load_pass = [&](int p, v4i* ch) {
+        static_assert(TPP * SLOT <= 1024 * kTqRing, "parameter staging fits in a wave's share of the ring");
+        if (!producer) {
+            uint8_t* stage = ring + wave * (TPP * SLOT);
+            const __amdgpu_buffer_rsrc_t rM = make_rsrc(Mb, (uint32_t)K * G * 2);
+            const int slab = wave * kWave * NC;         // first chunk of this wave's runs
+            auto wave_sync = [] {
+                __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+                __builtin_amdgcn_wave_barrier();
+                __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+            };
 #pragma unroll
-            for (int i = 0; i < LOADS; ++i)
-                ch[i] = __builtin_amdgcn_raw_buffer_load_b128(rM, (slab + p * TPP * NC + i * kWave + lane) * 16, 0, 0);
-        };
-        auto wave_sync = [] {
-            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-            __builtin_amdgcn_wave_barrier();
-            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-        };
+            for (int p = 0; p < PASSES; ++p) {
+                v4i ch[LOADS];
 #pragma unroll
-        for (int p = 0; p < PASSES; ++p) {
-            v4i ch[LOADS];
-            load_pass(p, ch);
+                for (int i = 0; i < LOADS; ++i)
+                    ch[i] = __builtin_amdgcn_raw_buffer_load_b128(rM, (slab + p * TPP * NC + i * kWave + lane) * 16,
+                                                                  0, 0);
 #pragma unroll
-            for (int i = 0; i < LOADS; ++i) {
-                const int c = i * kWave + lane;         // chunk of this pass: thread c / NC, piece c % NC
-                *reinterpret_cast<v4i*>(stage + (c / NC) * SLOT + (c % NC) * 16) = ch[i];
+                for (int i = 0; i < LOADS; ++i) {
+                    const int c = i * kWave + lane;     // chunk of this pass: thread c / NC, piece c % NC
+                    *reinterpret_cast<v4i*>(stage + (c / NC) * SLOT + (c % NC) * 16) = ch[i];
+                }
+                wave_sync();
+                if (lane / TPP == p) {
+#pragma unroll
+                    for (int j = 0; j < NC; ++j)
+                        mh[j] = *reinterpret_cast<const v8h*>(stage + (lane - p * TPP) * SLOT + j * 16);
+                }
+                wave_sync();
             }
-            wave_sync();
-            if (lane / TPP == p) {
-#pragma unroll
-                for (int j = 0; j < NC; ++j)
-                    mh[j] = *reinterpret_cast<const v8h*>(stage + (lane - p * TPP) * SLOT + j * 16);
-            }
-            wave_sync();
         }
     } else {
         // runs of 16 or 32 bytes: the lanes of a load already cover whole lines
@@ -302,91 +331,143 @@ __global__ __launch_bounds__(kFusedThreads) void tac_quant_kernel(const uint16_t
     }
 #pragma unroll
     for (int r = 0; r < 8; ++r) dv[r] = h2f(d[cm + r]);
-    if (row_begin < row_end) fetch_s(row_begin);
-    for (int row = row_begin; row < row_end; ++row) {
-        // keeps the block rows packed as fp16 (the multiply-adds widen them):
-        // hoisting their conversion out of the loop would hold 8 G fp32
-        // registers and leave room for fewer waves
+    __syncthreads();                                    // parameters read; states in LDS; the ring is free
+
+    // producer: row r of the run into slot r % kTqRing, one 1 KB load per consumer wave
+    if (producer) {
+        auto issue = [&](int r) {
+            const u32x4 rz = sgpr_rsrc(Z + (size_t)(row_begin + r) * K, (uint32_t)K * 2);
+            uint8_t* dst = ring + (r % kTqRing) * slot_bytes;
+            for (int j = 0; j < cw; ++j) dma16(rz, lds_addr(dst + j * 1024), (uint32_t)(j * kWave + lane) * 16);
+        };
+        for (int r = 0; r < kTqRing - 1 && r < nrows; ++r) issue(r);
+        for (int i = 0; i <= nrows; ++i) {
+            if (i < nrows) wait_ring(min(kTqRing - 2, nrows - 1 - i) * cw);   // row i has landed
+            ring_barrier();
+            if (i + kTqRing - 1 < nrows) issue(i + kTqRing - 1);             // into the slot row i - 1 used
+        }
+        return;
+    }
+
+    // consumers: the same number of barriers, each row split around one of them.
+    // The gate keeps or drops this thread's 8 channels together unless a band
+    // edge falls inside them (then it is applied channel by channel).
+    const bool keep_m = kept(c0, K, dm, du, true), keep_u = kept(c0, K, dm, du, false);
+    bool edge = false;
 #pragma unroll
-        for (int j = 0; j < G; ++j) asm volatile("" : "+v"(mh[j]));
-        float o[8];
+    for (int r = 1; r < 8; ++r)
+        edge |= kept(c0 + r, K, dm, du, true) != keep_m || kept(c0 + r, K, dm, du, false) != keep_u;
+    float op[8];                                        // the row being carried across the barrier
+    constexpr float kQmax = BITS == 4 ? 7.0f : 127.0f;
+    auto compute = [&](int i) {                         // row i: TAC, gate, partial max
         float amax = 0.0f;
-        float z[ZW];
-#pragma unroll
-        for (int v = 0; v < ZW / 8; ++v) {
-            const uint16_t* h = reinterpret_cast<const uint16_t*>(&zr[v]);
-#pragma unroll
-            for (int i = 0; i < 8; ++i) z[8 * v + i] = h2f(h[i]);
-        }
-        const bool masked = sb != 0;
-        if (row + 1 < row_end) {
-            fetch_z(row + 1);
-            fetch_s(row + 1);
-        }
         if (active) {
+            const uint8_t* src = ring + (i % kTqRing) * slot_bytes + z0 * 2;
+            v8h zh[ZW / 8];
+#pragma unroll
+            for (int v = 0; v < ZW / 8; ++v) zh[v] = *reinterpret_cast<const v8h*>(src + 16 * v);
+            const bool masked = st_lds[i] != 0;
+#pragma unroll
+            for (int j = 0; j < G; ++j) asm volatile("" : "+v"(mh[j]));
 #pragma unroll
             for (int r = 0; r < 8; ++r) {
-                const int base = ((c0 - z0 + r) / G) * G;   // block start within z[]
+                // block start within zh: c0 is a multiple of 8, so for g = 16 the
+                // thread's 8 outputs lie in one block whose inputs are all of zh,
+                // and for g <= 8 the block of output r starts at (r / g) g
+                const int base = G == 16 ? 0 : (r / G) * G;
                 float acc = 0.0f;
 #pragma unroll
                 for (int c = 0; c < G; ++c) {
-                    const int e = r * G + c;
-                    acc = __builtin_fmaf((float)mh[e / 8][e % 8], z[base + c], acc);
+                    const int e = r * G + c, zi = base + c;
+                    acc = __builtin_fmaf((float)mh[e / 8][e % 8], (float)zh[zi / 8][zi % 8], acc);
                 }
-                const float v = h2f(f2h(acc + dv[r]));  // TAC output, materialised as fp16
-                o[r] = (!gated | kept_sel(c0 + r, K, dm, du, masked)) ? v : 0.0f;
-                amax = fmaxf(amax, fabsf(o[r]));
+                op[r] = h2f(f2h(acc + dv[r]));             // TAC output, materialised as fp16
             }
+            if (gated) {
+                if (__builtin_expect(edge, 0)) {
+#pragma unroll
+                    for (int r = 0; r < 8; ++r) op[r] = kept(c0 + r, K, dm, du, masked) ? op[r] : 0.0f;
+                } else {
+                    const bool keep = masked ? keep_m : keep_u;
+#pragma unroll
+                    for (int r = 0; r < 8; ++r) op[r] = keep ? op[r] : 0.0f;
+                }
+            }
+#pragma unroll
+            for (int r = 0; r < 8; ++r) amax = fmaxf(amax, fabsf(op[r]));
         }
-        const float s = block_max_db(amax, red, row & 1) / (BITS == 4 ? 7.0f : 127.0f);
+        amax = wave_max_dpp(amax);
+        if (lane == 0) red[(i & 1) * kTqMaxConsumerWaves + wave] = amax;
+    };
+    auto finish = [&](int i) {                          // row i: block max, codes, store
+        // partial maxima of absent waves are never written: only the first cw count
+        const float4* rp = reinterpret_cast<const float4*>(red + (i & 1) * kTqMaxConsumerWaves);
+        const float4 r0 = rp[0], r1 = rp[1];
+        const float rv[8] = {r0.x, r0.y, r0.z, r0.w, r1.x, r1.y, r1.z, r1.w};
+        float a = rv[0];
+#pragma unroll
+        for (int w = 1; w < kTqMaxConsumerWaves; ++w) a = w < cw ? fmaxf(a, rv[w]) : a;
+        const float s = a / kQmax;
         const float y = s != 0.0f ? 1.0f / s : 0.0f;
+        const int row = row_begin + i;
         if (t == 0) s_out[row] = s;
-        if (active) {
-            if (BITS == 4) {
-                uint32_t w = 0;
-                if (s != 0.0f) {
-                    int c[8];
-                    quant_codes8<7>(o, s, y, c);
+        if (!active) return;
+        if (BITS == 4) {
+            uint32_t w4 = 0;
+            if (s != 0.0f) {
+                int c[8];
+                quant_codes8<7>(op, s, y, c);
 #pragma unroll
-                    for (int q = 0; q < 8; ++q) w |= (uint32_t)(c[q] & 15) << (4 * q);
-                }
-                *reinterpret_cast<uint32_t*>(Aq + (size_t)row * (K / 2) + 4 * t) = w;
-            } else {
-                uint32_t lo = 0, hi = 0;
-                if (s != 0.0f) {
-                    int c[8];
-                    quant_codes8<127>(o, s, y, c);
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        lo |= (uint32_t)(c[q] & 255) << (8 * q);
-                        hi |= (uint32_t)(c[4 + q] & 255) << (8 * q);
-                    }
-                }
-                *reinterpret_cast<uint2*>(Aq + (size_t)row * K + 8 * t) = make_uint2(lo, hi);
+                for (int q = 0; q < 8; ++q) w4 |= (uint32_t)(c[q] & 15) << (4 * q);
             }
+            *reinterpret_cast<uint32_t*>(Aq + (size_t)row * (K / 2) + 4 * t) = w4;
+        } else {
+            uint32_t lo = 0, hi = 0;
+            if (s != 0.0f) {
+                int c[8];
+                quant_codes8<127>(op, s, y, c);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    lo |= (uint32_t)(c[q] & 255) << (8 * q);
+                    hi |= (uint32_t)(c[4 + q] & 255) << (8 * q);
+                }
+            }
+            *reinterpret_cast<uint2*>(Aq + (size_t)row * K + 8 * t) = make_uint2(lo, hi);
         }
+    };
+    ring_barrier();
+    compute(0);
+    for (int i = 1; i < nrows; ++i) {
+        ring_barrier();
+        finish(i - 1);
+        compute(i);
     }
+    ring_barrier();
+    finish(nrows - 1);
 }
 
 }  // namespace
 
-bool tac_quant_fusable(int K, int g) { return g <= 16 && K % 16 == 0 && K / 8 <= kFusedThreads; }
+bool tac_quant_fusable(int K, int g) { return g <= 16 && K % 16 == 0 && K / 8 <= 64 * kTqMaxConsumerWaves; }
 
 hipError_t launch_tac_quant(const uint16_t* Z, const uint16_t* Mb, const uint16_t* d, const uint8_t* state, int M,
                             int K, int g, int dm, int du, uint8_t* Aq, float* s, hipStream_t st, int bits) {
-    const int threads = ((K / 8 + kWave - 1) / kWave) * kWave;
-    // enough workgroups to fill the chip, each reusing its parameters over several rows
-    int rows = M / 512;
-    rows = rows < 1 ? 1 : (rows > 16 ? 16 : rows);
+    const int cw = (K / 8 + kWave - 1) / kWave;
+    const int threads = (cw + 1) * kWave;
+    // about two workgroups per CU, each streaming a run of up to 64 rows
+    int rows = (M + 511) / 512;
+    rows = rows < 1 ? 1 : (rows > kTqMaxRows ? kTqMaxRows : rows);
     const dim3 grid((M + rows - 1) / rows);
+    // at most 6 x 8 KB + 128 bytes (K <= 4096): inside the default 64 KB dynamic-LDS limit
+    const size_t lds = (size_t)kTqRing * cw * 1024 + 2 * kTqMaxConsumerWaves * sizeof(float) + kTqMaxRows;
     switch (g * (bits == 8 ? -1 : 1)) {
 #define SQ_TQ(G)                                                                                                  \
     case G:                                                                                                       \
-        hipLaunchKernelGGL((tac_quant_kernel<G, 4>), grid, dim3(threads), 0, st, Z, Mb, d, state, M, K, dm, du,  \
+        hipLaunchKernelGGL((tac_quant_kernel<G, 4>), grid, dim3(threads), lds, st, Z, Mb, d, state, M, K, dm, du, \
                            rows, Aq, s);                                                                          \
         break;                                                                                                    \
     case -G:                                                                                                      \
-        hipLaunchKernelGGL((tac_quant_kernel<G, 8>), grid, dim3(threads), 0, st, Z, Mb, d, state, M, K, dm, du,  \
+        hipLaunchKernelGGL((tac_quant_kernel<G, 8>), grid, dim3(threads), lds, st, Z, Mb, d, state, M, K, dm, du, \
                            rows, Aq, s);                                                                          \
         break;
         SQ_TQ(1)

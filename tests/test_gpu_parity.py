@@ -295,10 +295,13 @@ def test_quant_act_with_tac(withP, g):
 
 
 @pytest.mark.parametrize("g", [1, 2, 4, 8, 16])
-@pytest.mark.parametrize("M,K", [(1, 64), (37, 512), (300, 3584), (129, 4096), (20, 8192)])
+@pytest.mark.parametrize("M,K", [(1, 64), (37, 512), (300, 3584), (129, 4096), (20, 8192), (1025, 1024),
+                                 (2100, 3584), (5000, 4096), (33000, 512)])
 def test_quant_act_tac_folded_fused(g, M, K):
     """TAC fused with the gate and quantiser (folded basis, g <= 16, K <= 4096; wider
-    rows take the staged path): bit-exact with the oracle's TAC-then-quantise."""
+    rows take the staged path): bit-exact with the oracle's TAC-then-quantise.  The
+    larger M give each workgroup a run of 2 ... 64 rows (a ragged last run
+    included), which streams through the ring of row slots."""
     X, st = _x(M, K, 8)
     Mb, d = synth.tac_params(K, g, synth.rng_for(703, g, K))
     dm, du = synth.default_band(K)
