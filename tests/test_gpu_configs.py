@@ -2,9 +2,14 @@
 uses: every linear of the LLaDA- and Dream-shaped layer sets, the TAC + O-projection
 workload (g = 128, 16384 tokens), and the denoising-step sweep over token counts.
 
-The GPU runs each whole layer; the oracle recomputes sampled token rows and sampled
-output channels one by one (rows are independent), and those must match bit for
-bit.  Properties that hold at any size are checked on every row."""
+The GPU runs each whole layer, with fragment-ordered weights (the benchmark's
+launch) and row-major weights, which must agree on every output; the oracle
+recomputes 64 sampled token rows (first and last, first and last of each state,
+random) one by one (rows are independent) against every output channel where
+the basis is folded (the oracle's weights are then cheap) and 256 sampled
+channels (every 128-column tile edge among them) with the dense basis, and
+those must match bit for bit.  Properties that hold at any size are checked on
+every row."""
 import os
 
 import numpy as np
@@ -47,27 +52,51 @@ def check_codes_all_rows(Aq, s_a):
     assert (mx[s > 0] == 7).all() and (mx[s == 0] == 0).all()
 
 
-def run_site(cid, si, state, *, g=None, folded=False, n_rows=6, n_cols=8, tac_identity=False):
+def sample_cols(N, n, seed):
+    """First and last columns, both sides of every 128- and 256-column tile edge
+    up to n / 4 of them, and random columns: n in all (every column if N <= n)."""
+    if N <= n:
+        return np.arange(N)
+    edges = np.arange(128, N, 128)
+    edges = edges[np.linspace(0, len(edges) - 1, min(len(edges), n // 8)).astype(int)] if len(edges) else edges
+    pick = np.unique(np.r_[0, N - 1, edges - 1, edges])
+    rest = np.setdiff1d(np.arange(N), pick)
+    extra = np.random.default_rng(seed).choice(rest, size=max(0, n - len(pick)), replace=False)
+    return np.unique(np.r_[pick, extra])
+
+
+def run_site(cid, si, state, *, g=None, folded=False, n_rows=64, n_cols=None, tac_identity=False):
+    """One linear of workload `cid` on the GPU, whole, in the benchmark's launch
+    (fragment-ordered weights) and with row-major weights (equal bit for bit);
+    then the oracle recomputes n_rows sampled token rows against n_cols sampled
+    output channels (every channel when n_cols is None: the default for a folded
+    basis, whose oracle weights are cheap), bit for bit."""
     t = synth.site_tensors(cid, si, state, tac_identity=tac_identity, g=g, with_P=not folded)
     K, N, M = t.site.K, t.site.N, len(state)
-    say(f"config {cid} site {t.site.name} M={M} K={K} N={N} tac={t.g} folded={folded}")
+    if n_cols is None and not folded:
+        n_cols = 256
+    say(f"config {cid} site {t.site.name} M={M} K={K} N={N} tac={t.g} folded={folded} rows={n_rows} "
+        f"cols={'all' if n_cols is None else n_cols}")
     Xd, Wd = dev(t.X), dev(t.W)
     Pd = None if folded else dev(t.P)
     tM = dev(t.tac_M) if t.tac_M is not None else None
     td = dev(t.tac_d) if t.tac_d is not None else None
     Wq, s_w = sq.sgat_prepare_weights(Wd, Pd)
     Aq, s_a = sq.sgat_quant_act(Xd, dev(state), Pd, t.dm, t.du, tM, td, t.g)
-    Y, acc = sq.w4a4_gemm(Aq, s_a, Wq, s_w, want_acc=True)
+    Y, acc = sq.w4a4_gemm_frag(Aq, s_a, sq.weights_to_frag(Wq), s_w, want_acc=True)
+    Yr, accr = sq.w4a4_gemm(Aq, s_a, Wq, s_w, want_acc=True)
+    assert torch.equal(acc, accr) and torch.equal(Y, Yr), "fragment-ordered and row-major weights differ"
+    del Yr, accr
     torch.cuda.synchronize()
     rows = sample_rows(state, n_rows, 1000 + si)
-    cols = np.unique(np.r_[0, N - 1, np.random.default_rng(2000 + si).choice(N, n_cols, replace=False)])
+    cols = np.arange(N) if n_cols is None else sample_cols(N, n_cols, 2000 + si)
     P = None if folded else t.P
     rq, rs = O.quant_act(t.X[rows], state[rows], P, t.dm, t.du, t.tac_M, t.tac_d, t.g, threads=THREADS)
     if folded:
-        wq, ws = O.quant_act(t.W[cols], None, None, 0, 0)
+        wq, ws = O.quant_act(t.W[cols], None, None, 0, 0, threads=THREADS)
     else:
         wq, ws = O.prepare_weights(t.W[cols], P, threads=THREADS)
-    ry, racc = O.gemm(rq, rs, wq, ws)
+    ry, racc = O.gemm(rq, rs, wq, ws, threads=THREADS)
     assert_bits(host(s_a)[rows], rs, "s_a rows")
     assert_bits(host(Aq)[rows], rq, "Aq rows")
     assert_bits(host(s_w)[cols], ws, "s_w rows")
@@ -92,7 +121,7 @@ def test_llada_layer_set(si, folded):
 @pytest.mark.timeout(900)
 @pytest.mark.parametrize("si", range(4), ids=[s.name for s in synth.CONFIGS[synth.DREAM].sites])
 def test_dream_layer_set(si):
-    run_site(synth.DREAM, si, synth.config_state(synth.DREAM), n_rows=4, n_cols=6)
+    run_site(synth.DREAM, si, synth.config_state(synth.DREAM))
 
 
 @pytest.mark.timeout(600)
@@ -117,11 +146,11 @@ def test_llada_layer_set_w8a8(si):
     Aq, s_a = sq.sgat_quant_act_w8(dev(t.X), dev(st), None, t.dm, t.du, tM, td, t.g)
     Y, acc = sq.w8a8_gemm(Aq, s_a, Wq, s_w, want_acc=True)
     torch.cuda.synchronize()
-    rows = sample_rows(st, 6, 3000 + si)
-    cols = np.unique(np.r_[0, N - 1, np.random.default_rng(4000 + si).choice(N, 8, replace=False)])
+    rows = sample_rows(st, 64, 3000 + si)
+    cols = np.arange(N)
     rq, rs = O.quant_act_q8(t.X[rows], st[rows], None, t.dm, t.du, t.tac_M, t.tac_d, t.g, threads=THREADS)
-    wq, ws = O.prepare_weights_q8(t.W[cols], None)
-    ry, racc = O.gemm_q8(rq, rs, wq, ws)
+    wq, ws = O.prepare_weights_q8(t.W[cols], None, threads=THREADS)
+    ry, racc = O.gemm_q8(rq, rs, wq, ws, threads=THREADS)
     assert_bits(host(s_a)[rows], rs, "s_a rows")
     assert_bits(host(Aq)[rows], rq, "Aq rows")
     assert_bits(host(Wq)[cols], wq, "Wq rows")
@@ -162,7 +191,7 @@ def test_denoise_sweep_token_counts(M):
     (folded P, the per-step GEMM path), at step t = 32, sampled rows vs the oracle."""
     st = synth.config_state(synth.LLADA_SWEEP, M=M, t=32)
     for si in range(4):
-        run_site(synth.LLADA_SWEEP, si, st, folded=True, n_rows=4, n_cols=4)
+        run_site(synth.LLADA_SWEEP, si, st, folded=True)
 
 
 @pytest.mark.timeout(900)
@@ -176,4 +205,4 @@ def test_denoise_sweep_layouts(layout):
     else:
         st = synth.state_edge(M, layout)
     for si in (0, 3):
-        run_site(synth.LLADA_SWEEP, si, st, n_rows=4, n_cols=4)
+        run_site(synth.LLADA_SWEEP, si, st, n_rows=16, n_cols=64)
