@@ -847,8 +847,10 @@ hipError_t finish_split(const Plan& p, int32_t* part, const float* s_a, const fl
 // rotating weights):
 //  - M <= 48: the short-M kernels (weight streaming; activations shared in LDS
 //    for wide 4-bit layers, K split inside the workgroup otherwise);
-//  - at least 768 tiles of 256 x 128: 256 x 128 (eight waves of 64 x 64);
-//  - at least 512 tiles of 128 x 128: 128 x 128 (four waves of 64 x 64);
+//  - 4-bit codes with at least 448 tiles of 256 x 128 or of 128 x 128:
+//    256 x 128 (eight waves of 64 x 64) at 448 ... 512 tiles of it, else
+//    128 x 128 (four waves of 64 x 64) (see below); 8-bit codes: 256 x 128
+//    from 768 tiles, 128 x 128 from 512;
 //  - at least 512 tiles of 64 x 128: 64 x 128 (four waves of 64 x 32);
 //  - otherwise 64 x 64 (four waves of 32 x 32), with K split below 256 tiles
 //    (twice as deep for K >= 8192) and kept at 8 k steps or more per split.
@@ -882,6 +884,18 @@ Plan choose_plan(int M, int N, int K, int bits) {
             p.cfg = 3;
             p.waves = kw;
         }
+    } else if (bits == 4 && (tiles(256, 128) >= 448 || tiles(128, 128) >= 448)) {
+        // 4-bit codes, from interleaved graph-replayed timings of both plans on
+        // the layer-set shapes at 512 ... 16384 tokens: 256 x 128 wins only when
+        // its 448 ... 512 tiles fill one round of two workgroups per CU (4096
+        // tokens of the 3584- and 4096-wide layers, by 2-7 %); everywhere else
+        // 128 x 128 (three workgroups per CU) is as fast or faster, by up to
+        // 16 % where the 256 x 128 tiles leave a partly filled last round
+        // (16384 x 4608: 6 % ; 4096 x 4608: 16 %) and 10 % over 64 x 128 at
+        // 448 ... 511 tiles of 128 x 128
+        const bool big = tiles(256, 128) >= 448 && tiles(256, 128) <= 512;
+        p = make_plan(M, N, K, big ? 256 : 128, 128, 1, bits);
+        p.cfg = big ? 0 : 1;
     } else if (tiles(256, 128) >= 768) {
         p = make_plan(M, N, K, 256, 128, 1, bits);
         p.cfg = 0;

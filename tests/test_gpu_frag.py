@@ -57,7 +57,7 @@ SHAPES = [
     (16, 4096, 1024), (32, 4096, 1024),
     # tiled plans: 64 x 64 with K splits, 64 x 128, 128 x 128, 256 x 128
     (49, 4104, 4160), (64, 24576, 4096), (300, 1032, 576), (1024, 4096, 4096), (2100, 4104, 3584),
-    (4096, 8200, 4160), (513, 4104, 12288),
+    (4096, 8200, 4160), (513, 4104, 12288), (4096, 4096, 192), (4000, 4000, 4160),
 ]
 
 
