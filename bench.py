@@ -692,7 +692,8 @@ def denoise_sweep_block(torch, sq, synth, dev, token_counts=(16, 1024, 16384)):
                                                           for _ in range(copies - 1)]
         layouts = [(str(tt), synth.config_state(synth.LLADA_SWEEP, M=M, t=tt)) for tt in range(65)]
         layouts += [(k, synth.state_edge(M, k)) for k in ("all_masked", "none_masked", "alternating")]
-        times = {}
+        calls = copies if M <= 64 else (4 if M <= 1024 else 1)
+        graphs = {}
         for label, st_np in layouts:
             state = torch.from_numpy(st_np).to(dev)
 
@@ -701,10 +702,20 @@ def denoise_sweep_block(torch, sq, synth, dev, token_counts=(16, 1024, 16384)):
                     sq.sgat_quant_act(d["X"], state, None, d["dm"], d["du"], d.get("tac_M"), d.get("tac_d"),
                                       d.get("g", 0), Aq=d["Aq"], s_a=d["s_a"], ws=d["qws"])
                     sq.w4a4_gemm_frag(d["Aq"], d["s_a"], Wf, s_w, Y=d["Y"], ws=d["gws"])
-            calls = copies if M <= 64 else (4 if M <= 1024 else 1)
-            ms, g = graph_ms(torch, step, calls, replays=5 if M <= 1024 else 3)
-            del g
-            times[label] = ms * 1e3
+            graphs[label] = (capture(torch, step, calls), state)
+        # every step's graph replayed in turn, several passes (clocks warmed
+        # first), and each step's median over the passes: drifts of the clock
+        # over the sweep then fall on every step alike
+        for g, _ in graphs.values():
+            g.replay()
+        torch.cuda.synchronize()
+        passes = 5 if M <= 1024 else 3
+        per = {label: [] for label in graphs}
+        for _ in range(passes):
+            for label, (g, _) in graphs.items():
+                per[label].append(replay_ms(torch, g, calls, replays=1))
+        times = {label: sorted(v)[len(v) // 2] * 1e3 for label, v in per.items()}
+        del graphs
         steps_us = [times[str(tt)] for tt in range(65)]
         out[str(M)] = {"us_per_step_t0_to_t64": steps_us,
                        "us_per_step_edges": {k: times[k] for k in ("all_masked", "none_masked", "alternating")},

@@ -850,7 +850,7 @@ hipError_t finish_split(const Plan& p, int32_t* part, const float* s_a, const fl
 //  - 4-bit codes with at least 448 tiles of 256 x 128 or of 128 x 128:
 //    256 x 128 (eight waves of 64 x 64) at 448 ... 512 tiles of it, else
 //    128 x 128 (four waves of 64 x 64) (see below); 8-bit codes: 256 x 128
-//    from 768 tiles, 128 x 128 from 512;
+//    from 512 of its tiles, else 128 x 128 from 192 of its tiles;
 //  - at least 512 tiles of 64 x 128: 64 x 128 (four waves of 64 x 32);
 //  - otherwise 64 x 64 (four waves of 32 x 32), with K split below 256 tiles
 //    (twice as deep for K >= 8192) and kept at 8 k steps or more per split.
@@ -896,9 +896,17 @@ Plan choose_plan(int M, int N, int K, int bits) {
         const bool big = tiles(256, 128) >= 448 && tiles(256, 128) <= 512;
         p = make_plan(M, N, K, big ? 256 : 128, 128, 1, bits);
         p.cfg = big ? 0 : 1;
-    } else if (tiles(256, 128) >= 768) {
+    } else if (bits == 8 && tiles(256, 128) >= 512) {
+        // 8-bit codes (graph-replayed timings of the LLaDA-shaped layers at 256,
+        // 1024 and 4096 tokens): 256 x 128 from 512 of its tiles (4096 tokens:
+        // 0.37-0.40 of int8 peak against 0.31-0.33 for 128 x 128), 128 x 128
+        // from 192 of its tiles (1024 tokens: QKV, O and down 4-21 % faster
+        // than 64 x 128 or 256 x 128)
         p = make_plan(M, N, K, 256, 128, 1, bits);
         p.cfg = 0;
+    } else if (bits == 8 && tiles(128, 128) >= 192) {
+        p = make_plan(M, N, K, 128, 128, 1, bits);
+        p.cfg = 1;
     } else if (tiles(128, 128) >= 512) {
         p = make_plan(M, N, K, 128, 128, 1, bits);
         p.cfg = 1;
