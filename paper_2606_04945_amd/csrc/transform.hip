@@ -13,6 +13,18 @@
 // thread owns TM x 8 outputs (an accumulator and a chunk total for each), with
 // X (converted fp16 -> fp32) and P staged through double-buffered LDS 16 k at a
 // time and the next global tile prefetched into registers during compute.
+//
+// Rows grouped by state (the paper's split of the batch into masked and
+// unmasked tokens, Eq. 7): when some 128-column tile lies wholly inside one of
+// the two bands, row tiles are taken over the rows in the order "masked rows,
+// then unmasked rows" (each group ascending).  A row tile whose rows all share
+// one state then skips the column tiles of the band that state drops (they
+// are +0, Eq. 10) instead of computing and discarding them; only the one row
+// tile that straddles the two groups computes every column.  Each workgroup
+// finds its rows itself from the state vector (a count of masked rows per
+// thread, a workgroup scan, then the rows whose rank falls in its tile), so
+// the call needs no workspace.  The order of the rows changes nothing in any
+// row's result.
 #include "sq_internal.hpp"
 
 namespace sq {
@@ -23,15 +35,50 @@ constexpr int kBN = 128;
 constexpr int kBK = 16;
 constexpr int kTN = 8;
 
+// This workgroup's rows when rows are grouped by state: rowmap[i] is the row
+// of rank rt * BM + i in the order (masked rows, then unmasked rows), or -1
+// past the last row; returns the number of masked rows.
+template <int BM>
+__device__ int group_rows(const uint8_t* __restrict__ state, int M, int rt, int* rowmap, int* scan) {
+    const int tid = threadIdx.x;
+    const int per = (M + kThreads - 1) / kThreads;   // states per thread, in one contiguous run
+    const int b = min(M, tid * per), e = min(M, b + per);
+    int cnt = 0;
+    for (int i = b; i < e; ++i) cnt += state[i] != 0;
+    if (tid < BM) rowmap[tid] = -1;
+    scan[tid] = cnt;
+    __syncthreads();
+    // inclusive scan of the per-thread counts (Hillis-Steele over 256 entries)
+    for (int o = 1; o < kThreads; o <<= 1) {
+        const int v = tid >= o ? scan[tid - o] : 0;
+        __syncthreads();
+        scan[tid] += v;
+        __syncthreads();
+    }
+    const int nm = scan[kThreads - 1];
+    int m_rank = scan[tid] - cnt;                    // masked rows before this run
+    int u_rank = nm + (b - m_rank);                  // rank of its first unmasked row
+    const int lo = rt * BM;
+    for (int i = b; i < e; ++i) {
+        const bool masked = state[i] != 0;
+        const int rank = masked ? m_rank++ : u_rank++;
+        if (rank >= lo && rank < lo + BM) rowmap[rank - lo] = i;
+    }
+    __syncthreads();
+    return nm;
+}
+
 template <int TM>
 __global__ __launch_bounds__(kThreads) void transform_kernel(
     const uint16_t* __restrict__ X, const uint8_t* __restrict__ state, const float* __restrict__ P,
-    int M, int K, int dm, int du, float* __restrict__ Xp) {
+    int M, int K, int dm, int du, int grouped, float* __restrict__ Xp) {
     constexpr int BM = 16 * TM;
     constexpr int AP = BM + 4;                       // padded LDS row (k-major A tile)
     constexpr int BP = kBN + 4;
     __shared__ float As[2][kBK][AP];
     __shared__ float Bs[2][kBK][BP];
+    __shared__ int rowmap[BM];
+    __shared__ int scan[kThreads];
 
     const int tid = threadIdx.x;
     const int tx = tid % 16, ty = tid / 16;
@@ -42,6 +89,30 @@ __global__ __launch_bounds__(kThreads) void transform_kernel(
     const int R = (M + BM - 1) / BM;
     xcd_tile(blockIdx.x, R, (K + kBN - 1) / kBN, R < 16 ? R : 16, rt, ct);
     const int row0 = rt * BM, col0 = ct * kBN;
+    // rows of this tile: in order, or grouped by state (then a tile of one
+    // state whose columns all lie in the band that state drops writes +0)
+    if (grouped) {
+        const int nm = group_rows<BM>(state, M, rt, rowmap, scan);
+        const int rows_end = min(M, row0 + BM);
+        const bool all_m = rows_end <= nm, all_u = row0 >= nm;
+        const bool dropped = (all_m && col0 >= K - du) ||
+                             (all_u && col0 >= K - dm - du && col0 + kBN <= K - du);
+        if (dropped) {
+            const int cbase = col0 + tx * kTN;
+            if (cbase >= K) return;
+            for (int i = 0; i < TM; ++i) {
+                const int r = rowmap[ty * TM + i];
+                if (r < 0) continue;
+                float4* dst = reinterpret_cast<float4*>(Xp + (size_t)r * K + cbase);
+                dst[0] = make_float4(0.f, 0.f, 0.f, 0.f);
+                dst[1] = make_float4(0.f, 0.f, 0.f, 0.f);
+            }
+            return;
+        }
+    } else if (tid < BM) {
+        rowmap[tid] = row0 + tid < M ? row0 + tid : -1;
+    }
+    if (!grouped) __syncthreads();
 
     // global -> register prefetch slots
     // A: BM rows x 16 k fp16 = BM*2 16-byte vectors; thread t takes vectors t, t+256, ..
@@ -50,15 +121,20 @@ __global__ __launch_bounds__(kThreads) void transform_kernel(
     // P: 16 rows x 128 cols fp32 = 512 float4; thread t takes t and t+256
     float4 rb[2];
 
+    // the rows this thread loads, fixed for the whole k loop
+    int arow[AV];
+#pragma unroll
+    for (int v = 0; v < AV; ++v) {
+        const int e = tid + v * kThreads;
+        arow[v] = e < BM * 2 ? rowmap[e >> 1] : -1;
+    }
     auto load_tiles = [&](int k0) {
 #pragma unroll
         for (int v = 0; v < AV; ++v) {
             const int e = tid + v * kThreads;
             ra[v] = make_uint4(0, 0, 0, 0);
-            if (e < BM * 2) {
-                const int r = e >> 1, h = e & 1, row = row0 + r;
-                if (row < M) ra[v] = *reinterpret_cast<const uint4*>(X + (size_t)row * K + k0 + h * 8);
-            }
+            if (arow[v] >= 0)
+                ra[v] = *reinterpret_cast<const uint4*>(X + (size_t)arow[v] * K + k0 + (e & 1) * 8);
         }
 #pragma unroll
         for (int v = 0; v < 2; ++v) {
@@ -135,8 +211,8 @@ __global__ __launch_bounds__(kThreads) void transform_kernel(
     if (cbase >= K) return;
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
-        const int row = row0 + ty * TM + i;
-        if (row >= M) break;
+        const int row = rowmap[ty * TM + i];
+        if (row < 0) continue;
         float o[kTN];
         if (state) {
             const bool masked = state[row] != 0;
@@ -184,13 +260,18 @@ hipError_t launch_transform(const uint16_t* X, const uint8_t* state, const float
     }
     const int ncol = (K + kBN - 1) / kBN;
     if ((size_t)((M + 63) / 64) * ncol > 0x7fffffffu) return hipErrorInvalidConfiguration;
+    // group rows by state only where a column tile lies wholly in a band
+    const int u0 = K - du, m0 = K - dm - du;
+    const bool band_tile = (u0 + kBN - 1) / kBN * kBN < K ||            // a tile wholly in [u0, K)
+                           (m0 + kBN - 1) / kBN * kBN + kBN <= u0;      // a tile wholly in [m0, u0)
+    const int grouped = state != nullptr && band_tile ? 1 : 0;
     // enough workgroups to cover the 256 CUs at least twice, else the taller tile
     if ((size_t)ncol * ((M + 127) / 128) >= 512) {
         hipLaunchKernelGGL(transform_kernel<8>, dim3(((M + 127) / 128) * ncol), dim3(kThreads), 0, st, X, state, P,
-                           M, K, dm, du, Xp);
+                           M, K, dm, du, grouped, Xp);
     } else {
         hipLaunchKernelGGL(transform_kernel<4>, dim3(((M + 63) / 64) * ncol), dim3(kThreads), 0, st, X, state, P,
-                           M, K, dm, du, Xp);
+                           M, K, dm, du, grouped, Xp);
     }
     return hipGetLastError();
 }

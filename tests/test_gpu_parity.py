@@ -122,6 +122,28 @@ def test_transform_bit_exact(M, K):
     assert_bits(host(xp0), O.transform(X, None, P, 0, 0, threads=THREADS), "x' ungated")
 
 
+@pytest.mark.parametrize("M,K,dm,du", [(300, 1024, 256, 384), (1000, 4096, 128, 128), (70, 4096, 128, 128),
+                                        (513, 1024, 0, 384), (260, 1024, 256, 0)])
+@pytest.mark.parametrize("layout", ["random", "all_masked", "none_masked", "alternating", "blocks"])
+def test_transform_rows_grouped_by_state(M, K, dm, du, layout):
+    """Bands that hold whole 128-column tiles: rows are taken grouped by state and
+    row tiles of one state skip the tiles of the band they drop; the result is
+    the oracle's bit for bit, the dropped columns +0."""
+    rng = np.random.default_rng(M + K + dm)
+    st = {"random": (rng.random(M) < 0.4), "all_masked": np.ones(M, bool), "none_masked": np.zeros(M, bool),
+          "alternating": np.arange(M) % 2 == 1, "blocks": (np.arange(M) // 37) % 3 == 0}[layout].astype(np.uint8)
+    X, _ = _x(M, K, 9, state=st)
+    P = synth.orthogonal(K, synth.rng_for(604, K))
+    say(f"transform grouped M={M} K={K} dm={dm} du={du} {layout}")
+    xp = host(sq.sgat_transform(dev(X), dev(st), dev(P), dm, du))
+    ref = O.transform(X, st, P, dm, du, threads=THREADS)
+    assert_bits(xp, ref, "x'")
+    dropped_u = st.astype(bool)[:, None] & (np.arange(K) >= K - du)[None, :]
+    dropped_m = ~st.astype(bool)[:, None] & ((np.arange(K) >= K - dm - du) & (np.arange(K) < K - du))[None, :]
+    gone = xp[dropped_u | dropped_m]
+    assert (gone == 0).all() and not np.signbit(gone).any()
+
+
 def test_transform_identity_basis_equals_folded():
     X, st = _x(40, 512, 4)
     dm, du = synth.default_band(512)
