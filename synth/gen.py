@@ -11,8 +11,10 @@ stored dtype):
 * weights W, fp16 [N][K]: N(0, 0.02);
 * SGAT basis P, fp32 [K][K]: a Gaussian matrix orthogonalised by QR with the
   signs of diag(R) folded in (the initialisation of App. B).  For K > 512 the
-  basis is the Kronecker product of two such factors, which is dense and
-  orthogonal but costs seconds instead of minutes on the host;
+  basis is (A kron B) Pi (C kron D), with A, B, C, D such factors of sizes K/b
+  and b (b = 128, or 64) and Pi a random permutation: dense, orthogonal and
+  free of a Kronecker structure, built in seconds (a full K x K QR at K =
+  18944 takes many minutes on the host), in fp64 and stored as fp32;
 * TAC parameters: M_b = I + N(0, 0.01) per g x g block and d ~ N(0, 0.01),
   both fp16 (Eq. 17); the identity case is M_b = I, d = 0;
 * token states, uint8 [M]: 0 = unmasked, 1 = masked, with the layouts below;
@@ -143,13 +145,16 @@ def orthogonal(K: int, rng) -> np.ndarray:
     if K % b:
         raise ValueError("K must be a multiple of 64")
     a = K // b
-    A = _gaussian_orthogonal(a, rng)
-    B = _gaussian_orthogonal(b, rng)
-    out = np.empty((K, K), np.float32)
-    # kron(A, B)[ia*b + ib, ja*b + jb] = A[ia, ja] * B[ib, jb]
-    for ia in range(a):
-        out[ia * b:(ia + 1) * b, :] = (B[:, None, :] * A[ia][None, :, None]).reshape(b, K)
-    return out
+    A, B = _gaussian_orthogonal(a, rng), _gaussian_orthogonal(b, rng)
+    C, D = _gaussian_orthogonal(a, rng), _gaussian_orthogonal(b, rng)
+    perm = rng.permutation(K)
+    # Y = Pi (C kron D): row p is row perm[p] of the Kronecker product,
+    # kron(C, D)[ia b + ib, :] = kron(C[ia], D[ib]); viewed as [a][b][K]
+    Y = (C[perm // b][:, :, None] * D[perm % b][:, None, :]).reshape(a, b, K)
+    # (A kron B) Y: B on the second index, then A on the first
+    Y = np.matmul(B, Y)
+    out = np.tensordot(A, Y, axes=(1, 0)).reshape(K, K)
+    return out.astype(np.float32)
 
 
 def tac_params(C: int, g: int, rng, std: float = 0.01, identity: bool = False):
