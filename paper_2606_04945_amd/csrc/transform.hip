@@ -11,8 +11,15 @@
 //
 // Tiling: a 256-thread workgroup owns BM = 16*TM rows x 128 columns; each
 // thread owns TM x 8 outputs (an accumulator and a chunk total for each), with
-// X (converted fp16 -> fp32) and P staged through double-buffered LDS 16 k at a
-// time and the next global tile prefetched into registers during compute.
+// X (converted fp16 -> fp32) and P staged through double-buffered LDS 32 k at a
+// time and the next global tile prefetched into registers during compute.  The
+// fragments of step k + 1 are read from LDS while step k multiplies (two
+// register sets), and the prefetch loads are unconditional (rows past M and
+// columns past K read a valid address and are zeroed when staged), so that no
+// wait for them sits before the multiply: with a conditional load the compiler
+// split the fp16 pairs right after it and so waited for global memory at the
+// top of every step.  The high fp16 of each loaded pair is converted in place
+// (an SDWA word select) for the same reason.
 //
 // Rows grouped by state (the paper's split of the batch into masked and
 // unmasked tokens, Eq. 7): when some 128-column tile lies wholly inside one of
@@ -32,7 +39,7 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kBN = 128;
-constexpr int kBK = 16;
+constexpr int kBK = 32;
 constexpr int kTN = 8;
 
 // This workgroup's rows when rows are grouped by state: rowmap[i] is the row
@@ -68,8 +75,15 @@ __device__ int group_rows(const uint8_t* __restrict__ state, int M, int rt, int*
     return nm;
 }
 
+// fp16 pair -> two fp32 (exact), low half first; the asm keeps the conversion
+// where the value is staged instead of next to its load.
+__device__ __forceinline__ void h2f_pair(uint32_t w, float& lo, float& hi) {
+    asm volatile("v_cvt_f32_f16_e32 %0, %2\n\tv_cvt_f32_f16_sdwa %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_1"
+                 : "=&v"(lo), "=&v"(hi) : "v"(w));
+}
+
 template <int TM>
-__global__ __launch_bounds__(kThreads) void transform_kernel(
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void transform_kernel(
     const uint16_t* __restrict__ X, const uint8_t* __restrict__ state, const float* __restrict__ P,
     int M, int K, int dm, int du, int grouped, float* __restrict__ Xp) {
     constexpr int BM = 16 * TM;
@@ -115,51 +129,63 @@ __global__ __launch_bounds__(kThreads) void transform_kernel(
     if (!grouped) __syncthreads();
 
     // global -> register prefetch slots
-    // A: BM rows x 16 k fp16 = BM*2 16-byte vectors; thread t takes vectors t, t+256, ..
-    constexpr int AV = (BM * 2 + kThreads - 1) / kThreads;
+    // A: BM rows x 32 k fp16 = 4 16-byte vectors per row; thread t takes vectors t, t+256, ..
+    constexpr int VPR = kBK / 8;
+    constexpr int AV = (BM * VPR + kThreads - 1) / kThreads;
     uint4 ra[AV];
-    // P: 16 rows x 128 cols fp32 = 512 float4; thread t takes t and t+256
-    float4 rb[2];
+    // P: 32 rows x 128 cols fp32 = 1024 float4; thread t takes t, t+256, t+512, t+768
+    constexpr int NB = kBK * kBN / 4 / kThreads;
+    float4 rb[NB];
 
-    // the rows this thread loads, fixed for the whole k loop
+    // the rows and columns this thread loads, fixed for the whole k loop; a row
+    // past M or a column past K reads row 0 / column 0 and is zeroed when staged
     int arow[AV];
+    const uint16_t* aptr[AV];
 #pragma unroll
     for (int v = 0; v < AV; ++v) {
         const int e = tid + v * kThreads;
-        arow[v] = e < BM * 2 ? rowmap[e >> 1] : -1;
+        arow[v] = e < BM * VPR ? rowmap[e / VPR] : -1;
+        aptr[v] = X + (size_t)(arow[v] >= 0 ? arow[v] : 0) * K + (e % VPR) * 8;
+    }
+    bool bok[NB];
+    const float* bptr[NB];
+#pragma unroll
+    for (int v = 0; v < NB; ++v) {
+        const int e = tid + v * kThreads;
+        const int kr = e / 32, c4 = (e % 32) * 4;
+        bok[v] = col0 + c4 < K;
+        bptr[v] = P + (size_t)kr * K + (bok[v] ? col0 + c4 : 0);
     }
     auto load_tiles = [&](int k0) {
 #pragma unroll
-        for (int v = 0; v < AV; ++v) {
-            const int e = tid + v * kThreads;
-            ra[v] = make_uint4(0, 0, 0, 0);
-            if (arow[v] >= 0)
-                ra[v] = *reinterpret_cast<const uint4*>(X + (size_t)arow[v] * K + k0 + (e & 1) * 8);
-        }
+        for (int v = 0; v < AV; ++v)
+            if (BM * VPR >= (v + 1) * kThreads || tid + v * kThreads < BM * VPR)
+                ra[v] = *reinterpret_cast<const uint4*>(aptr[v] + k0);
 #pragma unroll
-        for (int v = 0; v < 2; ++v) {
-            const int e = tid + v * kThreads;
-            const int kr = e / 32, c4 = (e % 32) * 4;
-            rb[v] = make_float4(0.f, 0.f, 0.f, 0.f);
-            if (col0 + c4 < K) rb[v] = *reinterpret_cast<const float4*>(P + (size_t)(k0 + kr) * K + col0 + c4);
-        }
+        for (int v = 0; v < NB; ++v) rb[v] = *reinterpret_cast<const float4*>(bptr[v] + (size_t)k0 * K);
     };
     auto store_tiles = [&](int buf) {
 #pragma unroll
         for (int v = 0; v < AV; ++v) {
             const int e = tid + v * kThreads;
-            if (e < BM * 2) {
-                const int r = e >> 1, h = e & 1;
-                const uint16_t* hv = reinterpret_cast<const uint16_t*>(&ra[v]);
+            if (e < BM * VPR) {
+                const int r = e / VPR, h = e % VPR;
+                const uint4 w = arow[v] >= 0 ? ra[v] : make_uint4(0, 0, 0, 0);
+                const uint32_t wv[4] = {w.x, w.y, w.z, w.w};
 #pragma unroll
-                for (int q = 0; q < 8; ++q) As[buf][h * 8 + q][r] = h2f(hv[q]);
+                for (int q = 0; q < 4; ++q) {
+                    float lo, hi;
+                    h2f_pair(wv[q], lo, hi);
+                    As[buf][h * 8 + 2 * q][r] = lo;
+                    As[buf][h * 8 + 2 * q + 1][r] = hi;
+                }
             }
         }
 #pragma unroll
-        for (int v = 0; v < 2; ++v) {
+        for (int v = 0; v < NB; ++v) {
             const int e = tid + v * kThreads;
             const int kr = e / 32, c4 = (e % 32) * 4;
-            *reinterpret_cast<float4*>(&Bs[buf][kr][c4]) = rb[v];
+            *reinterpret_cast<float4*>(&Bs[buf][kr][c4]) = bok[v] ? rb[v] : make_float4(0.f, 0.f, 0.f, 0.f);
         }
     };
 
@@ -176,23 +202,27 @@ __global__ __launch_bounds__(kThreads) void transform_kernel(
     for (int kt = 0; kt < nk; ++kt) {
         const int buf = kt & 1;
         if (kt + 1 < nk) load_tiles((kt + 1) * kBK);
-#pragma unroll
-        for (int kk = 0; kk < kBK; ++kk) {
-            float a[TM], b[kTN];
+        float a[2][TM], b[2][kTN];
+        auto frag = [&](int kk, float* aa, float* bb) {
 #pragma unroll
             for (int i = 0; i < TM; i += 4) {
                 const float4 t = *reinterpret_cast<const float4*>(&As[buf][kk][ty * TM + i]);
-                a[i] = t.x, a[i + 1] = t.y, a[i + 2] = t.z, a[i + 3] = t.w;
+                aa[i] = t.x, aa[i + 1] = t.y, aa[i + 2] = t.z, aa[i + 3] = t.w;
             }
 #pragma unroll
             for (int j = 0; j < kTN; j += 4) {
                 const float4 t = *reinterpret_cast<const float4*>(&Bs[buf][kk][tx * kTN + j]);
-                b[j] = t.x, b[j + 1] = t.y, b[j + 2] = t.z, b[j + 3] = t.w;
+                bb[j] = t.x, bb[j + 1] = t.y, bb[j + 2] = t.z, bb[j + 3] = t.w;
             }
+        };
+        frag(0, a[0], b[0]);
+#pragma unroll
+        for (int kk = 0; kk < kBK; ++kk) {
+            if (kk + 1 < kBK) frag(kk + 1, a[(kk + 1) & 1], b[(kk + 1) & 1]);
 #pragma unroll
             for (int i = 0; i < TM; ++i)
 #pragma unroll
-                for (int j = 0; j < kTN; ++j) acc[i][j] = __builtin_fmaf(a[i], b[j], acc[i][j]);
+                for (int j = 0; j < kTN; ++j) acc[i][j] = __builtin_fmaf(a[kk & 1][i], b[kk & 1][j], acc[i][j]);
         }
         const int kend = (kt + 1) * kBK;
         if (kend % kChunk == 0 || kend == K) {       // chunk boundary: fold into the total
