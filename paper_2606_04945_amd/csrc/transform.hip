@@ -211,7 +211,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
             }
 #pragma unroll
             for (int j = 0; j < kTN; j += 4) {
-                const float4 t = *reinterpret_cast<const float4*>(&Bs[buf][kk][tx * kTN + j]);
+                const float4 t = *reinterpret_cast<const float4*>(&Bs[buf][kk][tx * 4 + (j / 4) * 64]);
                 bb[j] = t.x, bb[j + 1] = t.y, bb[j + 2] = t.z, bb[j + 3] = t.w;
             }
         };
@@ -237,24 +237,22 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
         }
     }
 
-    const int cbase = col0 + tx * kTN;
-    if (cbase >= K) return;
+    // this thread's columns: col0 + 4 tx + {0..3} and col0 + 64 + 4 tx + {0..3}
+    // (eight neighbouring lanes then read 128 contiguous bytes of a B row)
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
         const int row = rowmap[ty * TM + i];
         if (row < 0) continue;
-        float o[kTN];
-        if (state) {
-            const bool masked = state[row] != 0;
+        const bool masked = state ? state[row] != 0 : false;
 #pragma unroll
-            for (int j = 0; j < kTN; ++j) o[j] = kept(cbase + j, K, dm, du, masked) ? tot[i][j] : 0.0f;
-        } else {
+        for (int hf = 0; hf < 2; ++hf) {
+            const int cb = col0 + hf * 64 + tx * 4;
+            if (cb >= K) continue;
+            float o[4];
 #pragma unroll
-            for (int j = 0; j < kTN; ++j) o[j] = tot[i][j];
+            for (int j = 0; j < 4; ++j) o[j] = (!state || kept(cb + j, K, dm, du, masked)) ? tot[i][hf * 4 + j] : 0.0f;
+            *reinterpret_cast<float4*>(Xp + (size_t)row * K + cb) = make_float4(o[0], o[1], o[2], o[3]);
         }
-        float4* dst = reinterpret_cast<float4*>(Xp + (size_t)row * K + cbase);
-        dst[0] = make_float4(o[0], o[1], o[2], o[3]);
-        dst[1] = make_float4(o[4], o[5], o[6], o[7]);
     }
 }
 
