@@ -4,21 +4,16 @@
 // Fixed evaluation order (part of the result, because the codes quantised from
 // x' flip at rounding midpoints): output (i, j) accumulates k in chunks of 256,
 // each chunk an fp32 fused multiply-add chain in ascending k from +0, and the
-// chunk sums are added in ascending order to a +0 total.  That order is a
-// plain register-tiled SGEMM on the VALU whose k loop is never split across
-// threads; MFMA is not used because its internal summation order is not this
-// one.
+// chunk sums are added in ascending order to a +0 total.
 //
-// Tiling: a 256-thread workgroup owns BM = 16*TM rows x 128 columns; each
-// thread owns TM x 8 outputs (an accumulator and a chunk total for each), with
-// X (converted fp16 -> fp32) and P staged through double-buffered LDS 32 k at a
-// time and the next global tile prefetched into registers during compute.  The
-// fragments of step k + 1 are read from LDS while step k multiplies (two
-// register sets), and the prefetch loads are unconditional (rows past M and
-// columns past K read a valid address and are zeroed when staged), so that no
-// wait for them sits before the multiply: with a conditional load the compiler
-// split the fp16 pairs right after it and so waited for global memory at the
-// top of every step.  The high fp16 of each loaded pair is converted in place
+// Tiling: a 256-thread workgroup (four waves) owns a BM x BN tile of outputs
+// (128 x 128, 64 x 128, or 32 x 256 for a few rows), each output with a chunk
+// accumulator (in the matrix-core result registers) and a total.  X (converted
+// fp16 -> fp32 on the way) and P are staged through double-buffered LDS 32 k at
+// a time, the next global tile prefetched into registers during the multiply.
+// The prefetch loads are unconditional (rows past M and columns past K read a
+// valid address and are zeroed when staged), so that no wait for them sits
+// before the multiply; the high fp16 of each loaded pair is converted in place
 // (an SDWA word select) for the same reason.
 //
 // Rows grouped by state (the paper's split of the batch into masked and
@@ -38,9 +33,7 @@ namespace sq {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kBN = 128;
 constexpr int kBK = 32;
-constexpr int kTN = 8;
 
 // This workgroup's rows when rows are grouped by state: rowmap[i] is the row
 // of rank rt * BM + i in the order (masked rows, then unmasked rows), or -1
@@ -82,27 +75,45 @@ __device__ __forceinline__ void h2f_pair(uint32_t w, float& lo, float& hi) {
                  : "=&v"(lo), "=&v"(hi) : "v"(w));
 }
 
-template <int TM>
+typedef float f32x32 __attribute__((ext_vector_type(32)));
+
+// The matrix-core form of the same fixed order.  v_mfma_f32_32x32x1_2b_f32
+// multiplies one k at a time: each of its 2 x 32 x 32 outputs receives exactly
+// one product per instruction, d = fma(a, b, c) with a single rounding,
+// subnormals kept (checked bit for bit against fmaf chains, signed zeros and
+// subnormal results included).  A chain of these instructions over ascending k
+// from a zeroed accumulator is therefore the chunk chain itself, and the chunk
+// totals are added on the VALU exactly as before.  The instruction's two
+// blocks are the two 32-column halves of a wave's 64 columns (the A operand
+// repeats the same 32 rows in both lane halves); TMI instructions per k cover
+// 32 TMI rows.  A wave owns 32 TMI x 64 outputs, a workgroup WR x WC waves.
+//
+// Operand lane layout (block b = lane / 32): A lane 32 b + i holds row i, B
+// lane 32 b + j holds column j; result register v of block b = v / 16 holds
+// row 8 ((v % 16) / 4) + 4 (lane / 32) + v % 4, column lane % 32.
+template <int TMI, int WR, int WC>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void transform_kernel(
     const uint16_t* __restrict__ X, const uint8_t* __restrict__ state, const float* __restrict__ P,
     int M, int K, int dm, int du, int grouped, float* __restrict__ Xp) {
-    constexpr int BM = 16 * TM;
-    constexpr int AP = BM + 4;                       // padded LDS row (k-major A tile)
-    constexpr int BP = kBN + 4;
+    static_assert(WR * WC * kWave == kThreads, "four waves");
+    constexpr int BM = 32 * TMI * WR;
+    constexpr int BN = 64 * WC;
+    constexpr int AP = BM + 2;                       // padded LDS row (k-major A tile)
     __shared__ float As[2][kBK][AP];
-    __shared__ float Bs[2][kBK][BP];
+    __shared__ float Bs[2][kBK][BN];
     __shared__ int rowmap[BM];
     __shared__ int scan[kThreads];
 
     const int tid = threadIdx.x;
-    const int tx = tid % 16, ty = tid / 16;
+    const int lane = tid % kWave, wave = tid / kWave;
+    const int wr = wave / WC, wc = wave % WC;
     // up to 16 row tiles of a column tile of P run on one XCD at the same
-    // time, so that XCD's L2 fetches the column tile once per group (all of a
-    // 1024-token batch is one group) and the XCDs work on different columns
+    // time, so that XCD's L2 fetches the column tile once per group and the
+    // XCDs work on different columns
     int rt, ct;
     const int R = (M + BM - 1) / BM;
-    xcd_tile(blockIdx.x, R, (K + kBN - 1) / kBN, R < 16 ? R : 16, rt, ct);
-    const int row0 = rt * BM, col0 = ct * kBN;
+    xcd_tile(blockIdx.x, R, (K + BN - 1) / BN, R < 16 ? R : 16, rt, ct);
+    const int row0 = rt * BM, col0 = ct * BN;
     // rows of this tile: in order, or grouped by state (then a tile of one
     // state whose columns all lie in the band that state drops writes +0)
     if (grouped) {
@@ -110,31 +121,29 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
         const int rows_end = min(M, row0 + BM);
         const bool all_m = rows_end <= nm, all_u = row0 >= nm;
         const bool dropped = (all_m && col0 >= K - du) ||
-                             (all_u && col0 >= K - dm - du && col0 + kBN <= K - du);
+                             (all_u && col0 >= K - dm - du && col0 + BN <= K - du);
         if (dropped) {
-            const int cbase = col0 + tx * kTN;
-            if (cbase >= K) return;
-            for (int i = 0; i < TM; ++i) {
-                const int r = rowmap[ty * TM + i];
-                if (r < 0) continue;
-                float4* dst = reinterpret_cast<float4*>(Xp + (size_t)r * K + cbase);
-                dst[0] = make_float4(0.f, 0.f, 0.f, 0.f);
-                dst[1] = make_float4(0.f, 0.f, 0.f, 0.f);
+            const int ncol4 = min(BN, K - col0) / 4;
+            for (int e = tid; e < BM * ncol4; e += kThreads) {
+                const int r = rowmap[e / ncol4];
+                if (r >= 0)
+                    *reinterpret_cast<float4*>(Xp + (size_t)r * K + col0 + (e % ncol4) * 4) =
+                        make_float4(0.f, 0.f, 0.f, 0.f);
             }
             return;
         }
-    } else if (tid < BM) {
-        rowmap[tid] = row0 + tid < M ? row0 + tid : -1;
+    } else {
+        if (tid < BM) rowmap[tid] = row0 + tid < M ? row0 + tid : -1;
+        __syncthreads();
     }
-    if (!grouped) __syncthreads();
 
     // global -> register prefetch slots
     // A: BM rows x 32 k fp16 = 4 16-byte vectors per row; thread t takes vectors t, t+256, ..
     constexpr int VPR = kBK / 8;
     constexpr int AV = (BM * VPR + kThreads - 1) / kThreads;
     uint4 ra[AV];
-    // P: 32 rows x 128 cols fp32 = 1024 float4; thread t takes t, t+256, t+512, t+768
-    constexpr int NB = kBK * kBN / 4 / kThreads;
+    // P: 32 rows x BN cols fp32 = 8 BN float4; thread t takes t, t+256, ..
+    constexpr int NB = kBK * BN / 4 / kThreads;
     float4 rb[NB];
 
     // the rows and columns this thread loads, fixed for the whole k loop; a row
@@ -152,7 +161,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
 #pragma unroll
     for (int v = 0; v < NB; ++v) {
         const int e = tid + v * kThreads;
-        const int kr = e / 32, c4 = (e % 32) * 4;
+        const int kr = e / (BN / 4), c4 = (e % (BN / 4)) * 4;
         bok[v] = col0 + c4 < K;
         bptr[v] = P + (size_t)kr * K + (bok[v] ? col0 + c4 : 0);
     }
@@ -184,17 +193,19 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
 #pragma unroll
         for (int v = 0; v < NB; ++v) {
             const int e = tid + v * kThreads;
-            const int kr = e / 32, c4 = (e % 32) * 4;
+            const int kr = e / (BN / 4), c4 = (e % (BN / 4)) * 4;
             *reinterpret_cast<float4*>(&Bs[buf][kr][c4]) = bok[v] ? rb[v] : make_float4(0.f, 0.f, 0.f, 0.f);
         }
     };
 
-    float acc[TM][kTN], tot[TM][kTN];
+    f32x32 acc[TMI], tot[TMI];
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
+    for (int t = 0; t < TMI; ++t)
 #pragma unroll
-        for (int j = 0; j < kTN; ++j) acc[i][j] = 0.0f, tot[i][j] = 0.0f;
+        for (int v = 0; v < 32; ++v) acc[t][v] = 0.0f, tot[t][v] = 0.0f;
 
+    const int arow0 = wr * 32 * TMI + (lane & 31);   // A operand row of this lane (both lane halves)
+    const int bcol = wc * 64 + lane;                 // B operand column of this lane
     const int nk = K / kBK;
     load_tiles(0);
     store_tiles(0);
@@ -202,34 +213,19 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     for (int kt = 0; kt < nk; ++kt) {
         const int buf = kt & 1;
         if (kt + 1 < nk) load_tiles((kt + 1) * kBK);
-        float a[2][TM], b[2][kTN];
-        auto frag = [&](int kk, float* aa, float* bb) {
-#pragma unroll
-            for (int i = 0; i < TM; i += 4) {
-                const float4 t = *reinterpret_cast<const float4*>(&As[buf][kk][ty * TM + i]);
-                aa[i] = t.x, aa[i + 1] = t.y, aa[i + 2] = t.z, aa[i + 3] = t.w;
-            }
-#pragma unroll
-            for (int j = 0; j < kTN; j += 4) {
-                const float4 t = *reinterpret_cast<const float4*>(&Bs[buf][kk][tx * 4 + (j / 4) * 64]);
-                bb[j] = t.x, bb[j + 1] = t.y, bb[j + 2] = t.z, bb[j + 3] = t.w;
-            }
-        };
-        frag(0, a[0], b[0]);
 #pragma unroll
         for (int kk = 0; kk < kBK; ++kk) {
-            if (kk + 1 < kBK) frag(kk + 1, a[(kk + 1) & 1], b[(kk + 1) & 1]);
+            const float b = Bs[buf][kk][bcol];
 #pragma unroll
-            for (int i = 0; i < TM; ++i)
-#pragma unroll
-                for (int j = 0; j < kTN; ++j) acc[i][j] = __builtin_fmaf(a[kk & 1][i], b[kk & 1][j], acc[i][j]);
+            for (int t = 0; t < TMI; ++t)
+                acc[t] = __builtin_amdgcn_mfma_f32_32x32x1f32(As[buf][kk][arow0 + 32 * t], b, acc[t], 0, 0, 0);
         }
         const int kend = (kt + 1) * kBK;
         if (kend % kChunk == 0 || kend == K) {       // chunk boundary: fold into the total
 #pragma unroll
-            for (int i = 0; i < TM; ++i)
+            for (int t = 0; t < TMI; ++t)
 #pragma unroll
-                for (int j = 0; j < kTN; ++j) tot[i][j] = tot[i][j] + acc[i][j], acc[i][j] = 0.0f;
+                for (int v = 0; v < 32; ++v) tot[t][v] = tot[t][v] + acc[t][v], acc[t][v] = 0.0f;
         }
         if (kt + 1 < nk) {
             store_tiles(buf ^ 1);
@@ -237,23 +233,18 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
         }
     }
 
-    // this thread's columns: col0 + 4 tx + {0..3} and col0 + 64 + 4 tx + {0..3}
-    // (eight neighbouring lanes then read 128 contiguous bytes of a B row)
+    // result register v of row group t: tile row 32 (WR-row) + 8 ((v % 16) / 4) + 4 (lane / 32) + v % 4,
+    // tile column 64 wc + 32 (v / 16) + lane % 32; 32 lanes store 128 contiguous bytes of a row
 #pragma unroll
-    for (int i = 0; i < TM; ++i) {
-        const int row = rowmap[ty * TM + i];
-        if (row < 0) continue;
-        const bool masked = state ? state[row] != 0 : false;
+    for (int t = 0; t < TMI; ++t)
 #pragma unroll
-        for (int hf = 0; hf < 2; ++hf) {
-            const int cb = col0 + hf * 64 + tx * 4;
-            if (cb >= K) continue;
-            float o[4];
-#pragma unroll
-            for (int j = 0; j < 4; ++j) o[j] = (!state || kept(cb + j, K, dm, du, masked)) ? tot[i][hf * 4 + j] : 0.0f;
-            *reinterpret_cast<float4*>(Xp + (size_t)row * K + cb) = make_float4(o[0], o[1], o[2], o[3]);
+        for (int v = 0; v < 32; ++v) {
+            const int r = rowmap[wr * 32 * TMI + 32 * t + 8 * ((v % 16) / 4) + 4 * (lane / 32) + (v % 4)];
+            const int col = col0 + wc * 64 + 32 * (v / 16) + (lane % 32);
+            if (r < 0 || col >= K) continue;
+            const bool keep = !state || kept(col, K, dm, du, state[r] != 0);
+            Xp[(size_t)r * K + col] = keep ? tot[t][v] : 0.0f;
         }
-    }
 }
 
 // P == NULL: the input is already in the P basis; x' = x, then the gate.
@@ -286,21 +277,28 @@ hipError_t launch_transform(const uint16_t* X, const uint8_t* state, const float
         hipLaunchKernelGGL(gate_copy_kernel, dim3(blocks), dim3(kThreads), 0, st, X, state, M, K, dm, du, Xp);
         return hipGetLastError();
     }
-    const int ncol = (K + kBN - 1) / kBN;
-    if ((size_t)((M + 63) / 64) * ncol > 0x7fffffffu) return hipErrorInvalidConfiguration;
+    // 128 x 128 tiles where they give at least two workgroups per CU, else 64 x 128,
+    // and 32 x 256 for a few rows
+    const int tiles128 = ((M + 127) / 128) * ((K + 127) / 128);
+    const int BM = tiles128 >= 512 ? 128 : (M > 32 ? 64 : 32);
+    const int BN = BM == 32 ? 256 : 128;
+    const int ncol = (K + BN - 1) / BN;
+    if ((size_t)((M + BM - 1) / BM) * ncol > 0x7fffffffu) return hipErrorInvalidConfiguration;
     // group rows by state only where a column tile lies wholly in a band
     const int u0 = K - du, m0 = K - dm - du;
-    const bool band_tile = (u0 + kBN - 1) / kBN * kBN < K ||            // a tile wholly in [u0, K)
-                           (m0 + kBN - 1) / kBN * kBN + kBN <= u0;      // a tile wholly in [m0, u0)
+    const bool band_tile = (u0 + BN - 1) / BN * BN < K ||            // a tile wholly in [u0, K)
+                           (m0 + BN - 1) / BN * BN + BN <= u0;       // a tile wholly in [m0, u0)
     const int grouped = state != nullptr && band_tile ? 1 : 0;
-    // enough workgroups to cover the 256 CUs at least twice, else the taller tile
-    if ((size_t)ncol * ((M + 127) / 128) >= 512) {
-        hipLaunchKernelGGL(transform_kernel<8>, dim3(((M + 127) / 128) * ncol), dim3(kThreads), 0, st, X, state, P,
-                           M, K, dm, du, grouped, Xp);
-    } else {
-        hipLaunchKernelGGL(transform_kernel<4>, dim3(((M + 63) / 64) * ncol), dim3(kThreads), 0, st, X, state, P,
-                           M, K, dm, du, grouped, Xp);
-    }
+    const dim3 grid(((M + BM - 1) / BM) * ncol);
+    if (BM == 128)
+        hipLaunchKernelGGL((transform_kernel<2, 2, 2>), grid, dim3(kThreads), 0, st, X, state, P, M, K, dm, du,
+                           grouped, Xp);
+    else if (BM == 64)
+        hipLaunchKernelGGL((transform_kernel<1, 2, 2>), grid, dim3(kThreads), 0, st, X, state, P, M, K, dm, du,
+                           grouped, Xp);
+    else
+        hipLaunchKernelGGL((transform_kernel<1, 1, 4>), grid, dim3(kThreads), 0, st, X, state, P, M, K, dm, du,
+                           grouped, Xp);
     return hipGetLastError();
 }
 

@@ -109,7 +109,7 @@ def test_quant_act_folded_no_gate_and_custom_bands():
 
 # ------------------------------------------------------------------ dense transform
 
-@pytest.mark.parametrize("M,K", [(1, 64), (5, 192), (130, 512), (257, 1024), (33, 4096)])
+@pytest.mark.parametrize("M,K", [(1, 64), (5, 192), (130, 512), (257, 1024), (33, 4096), (2100, 4096), (2000, 4160)])
 def test_transform_bit_exact(M, K):
     X, st = _x(M, K, 3)
     P = synth.orthogonal(K, synth.rng_for(600, K))
@@ -123,7 +123,7 @@ def test_transform_bit_exact(M, K):
 
 
 @pytest.mark.parametrize("M,K,dm,du", [(300, 1024, 256, 384), (1000, 4096, 128, 128), (70, 4096, 128, 128),
-                                        (513, 1024, 0, 384), (260, 1024, 256, 0)])
+                                        (513, 1024, 0, 384), (260, 1024, 256, 0), (2100, 4096, 128, 128)])
 @pytest.mark.parametrize("layout", ["random", "all_masked", "none_masked", "alternating", "blocks"])
 def test_transform_rows_grouped_by_state(M, K, dm, du, layout):
     """Bands that hold whole 128-column tiles: rows are taken grouped by state and
