@@ -6,15 +6,24 @@
 // each chunk an fp32 fused multiply-add chain in ascending k from +0, and the
 // chunk sums are added in ascending order to a +0 total.
 //
+// Matrix cores: v_mfma_f32_16x16x4_f32 computes each of its 16 x 16 outputs as
+// c + a0 b0 + a1 b1 + a2 b2 + a3 b3 evaluated as a forward chain of four
+// fused multiply-adds, k ascending, each rounded once, subnormals kept
+// (checked bit for bit against fmaf chains, signed zeros and subnormal
+// results included).  A chain of these instructions over ascending groups of
+// four k, from a zeroed accumulator, is therefore exactly one chunk's chain;
+// the chunk totals are added on the VALU.
+//
 // Tiling: a 256-thread workgroup (four waves) owns a BM x BN tile of outputs
-// (128 x 128, 64 x 128, or 32 x 256 for a few rows), each output with a chunk
-// accumulator (in the matrix-core result registers) and a total.  X (converted
-// fp16 -> fp32 on the way) and P are staged through double-buffered LDS 32 k at
-// a time, the next global tile prefetched into registers during the multiply.
-// The prefetch loads are unconditional (rows past M and columns past K read a
-// valid address and are zeroed when staged), so that no wait for them sits
-// before the multiply; the high fp16 of each loaded pair is converted in place
-// (an SDWA word select) for the same reason.
+// (128 x 128 or 64 x 128; 32 x 256 for up to 32 rows), a wave IB x JB blocks
+// of 16 x 16, each output with a chunk accumulator (the instruction's result
+// registers) and a total.  Main kernel: both operand tiles go from HBM straight
+// into LDS (buffer loads with the LDS destination, no staging registers)
+// through a three-stage ring, two k steps of 32 in flight while a third is
+// multiplied, one barrier per step; X stays fp16 in LDS and is widened as it is
+// read.  Staging the tiles through registers instead (converting X on the way)
+// ran at 0.75 of the speed on the 8 x 2048-token shapes; that form remains for
+// batches of up to 32 rows.
 //
 // Rows grouped by state (the paper's split of the batch into masked and
 // unmasked tokens, Eq. 7): when some 128-column tile lies wholly inside one of
@@ -27,7 +36,7 @@
 // thread, a workgroup scan, then the rows whose rank falls in its tile), so
 // the call needs no workspace.  The order of the rows changes nothing in any
 // row's result.
-#include "sq_internal.hpp"
+#include "tile_common.hpp"
 
 namespace sq {
 namespace {
@@ -75,47 +84,35 @@ __device__ __forceinline__ void h2f_pair(uint32_t w, float& lo, float& hi) {
                  : "=&v"(lo), "=&v"(hi) : "v"(w));
 }
 
-typedef float f32x32 __attribute__((ext_vector_type(32)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-// The matrix-core form of the same fixed order.  v_mfma_f32_32x32x1_2b_f32
-// multiplies one k at a time: each of its 2 x 32 x 32 outputs receives exactly
-// one product per instruction, d = fma(a, b, c) with a single rounding,
-// subnormals kept (checked bit for bit against fmaf chains, signed zeros and
-// subnormal results included).  A chain of these instructions over ascending k
-// from a zeroed accumulator is therefore the chunk chain itself, and the chunk
-// totals are added on the VALU exactly as before.  The instruction's two
-// blocks are the two 32-column halves of a wave's 64 columns (the A operand
-// repeats the same 32 rows in both lane halves); TMI instructions per k cover
-// 32 TMI rows.  A wave owns 32 TMI x 64 outputs, a workgroup WR x WC waves.
-//
-// Operand lane layout (block b = lane / 32): A lane 32 b + i holds row i, B
-// lane 32 b + j holds column j; result register v of block b = v / 16 holds
-// row 8 ((v % 16) / 4) + 4 (lane / 32) + v % 4, column lane % 32.
-template <int TMI, int WR, int WC>
+// v_mfma_f32_16x16x4_f32: D = C + sum_k A[:, k] B[k, :] over its four k as a
+// forward chain of single-rounding fused multiply-adds, k ascending (checked bit
+// for bit against fmaf chains).  A chain of these over ascending groups of
+// four k is the chunk chain itself.  Lane l supplies A[l % 16][l / 16] and
+// B[l / 16][l % 16]; result register v holds row 4 (l / 16) + v, column l % 16.
+// A wave owns IB x JB blocks of 16 x 16 outputs, a workgroup WR x WC waves.
+template <int IB, int JB, int WR, int WC>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void transform_kernel(
     const uint16_t* __restrict__ X, const uint8_t* __restrict__ state, const float* __restrict__ P,
     int M, int K, int dm, int du, int grouped, float* __restrict__ Xp) {
     static_assert(WR * WC * kWave == kThreads, "four waves");
-    constexpr int BM = 32 * TMI * WR;
-    constexpr int BN = 64 * WC;
-    constexpr int AP = BM + 2;                       // padded LDS row (k-major A tile)
+    constexpr int BM = 16 * IB * WR;
+    constexpr int BN = 16 * JB * WC;
+    constexpr int AP = BM + 4;                       // padded LDS row (k-major A tile)
+    constexpr int BP = BN + 4;
     __shared__ float As[2][kBK][AP];
-    __shared__ float Bs[2][kBK][BN];
+    __shared__ float Bs[2][kBK][BP];
     __shared__ int rowmap[BM];
     __shared__ int scan[kThreads];
 
     const int tid = threadIdx.x;
     const int lane = tid % kWave, wave = tid / kWave;
     const int wr = wave / WC, wc = wave % WC;
-    // up to 16 row tiles of a column tile of P run on one XCD at the same
-    // time, so that XCD's L2 fetches the column tile once per group and the
-    // XCDs work on different columns
     int rt, ct;
     const int R = (M + BM - 1) / BM;
     xcd_tile(blockIdx.x, R, (K + BN - 1) / BN, R < 16 ? R : 16, rt, ct);
     const int row0 = rt * BM, col0 = ct * BN;
-    // rows of this tile: in order, or grouped by state (then a tile of one
-    // state whose columns all lie in the band that state drops writes +0)
     if (grouped) {
         const int nm = group_rows<BM>(state, M, rt, rowmap, scan);
         const int rows_end = min(M, row0 + BM);
@@ -137,17 +134,11 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
         __syncthreads();
     }
 
-    // global -> register prefetch slots
-    // A: BM rows x 32 k fp16 = 4 16-byte vectors per row; thread t takes vectors t, t+256, ..
     constexpr int VPR = kBK / 8;
     constexpr int AV = (BM * VPR + kThreads - 1) / kThreads;
     uint4 ra[AV];
-    // P: 32 rows x BN cols fp32 = 8 BN float4; thread t takes t, t+256, ..
     constexpr int NB = kBK * BN / 4 / kThreads;
     float4 rb[NB];
-
-    // the rows and columns this thread loads, fixed for the whole k loop; a row
-    // past M or a column past K reads row 0 / column 0 and is zeroed when staged
     int arow[AV];
     const uint16_t* aptr[AV];
 #pragma unroll
@@ -198,14 +189,17 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
         }
     };
 
-    f32x32 acc[TMI], tot[TMI];
+    f32x4 acc[IB][JB], tot[IB][JB];
 #pragma unroll
-    for (int t = 0; t < TMI; ++t)
+    for (int i = 0; i < IB; ++i)
 #pragma unroll
-        for (int v = 0; v < 32; ++v) acc[t][v] = 0.0f, tot[t][v] = 0.0f;
+        for (int j = 0; j < JB; ++j)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) acc[i][j][v] = 0.0f, tot[i][j][v] = 0.0f;
 
-    const int arow0 = wr * 32 * TMI + (lane & 31);   // A operand row of this lane (both lane halves)
-    const int bcol = wc * 64 + lane;                 // B operand column of this lane
+    const int kl = lane / 16, il = lane % 16;
+    const int arow0 = wr * 16 * IB + il;             // A operand row of this lane in block 0
+    const int bcol0 = wc * 16 * JB + il;             // B operand column of this lane in block 0
     const int nk = K / kBK;
     load_tiles(0);
     store_tiles(0);
@@ -214,18 +208,26 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
         const int buf = kt & 1;
         if (kt + 1 < nk) load_tiles((kt + 1) * kBK);
 #pragma unroll
-        for (int kk = 0; kk < kBK; ++kk) {
-            const float b = Bs[buf][kk][bcol];
+        for (int s4 = 0; s4 < kBK / 4; ++s4) {
+            const int kk = 4 * s4 + kl;
+            float a[IB], b[JB];
 #pragma unroll
-            for (int t = 0; t < TMI; ++t)
-                acc[t] = __builtin_amdgcn_mfma_f32_32x32x1f32(As[buf][kk][arow0 + 32 * t], b, acc[t], 0, 0, 0);
+            for (int i = 0; i < IB; ++i) a[i] = As[buf][kk][arow0 + 16 * i];
+#pragma unroll
+            for (int j = 0; j < JB; ++j) b[j] = Bs[buf][kk][bcol0 + 16 * j];
+#pragma unroll
+            for (int i = 0; i < IB; ++i)
+#pragma unroll
+                for (int j = 0; j < JB; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i], b[j], acc[i][j], 0, 0, 0);
         }
         const int kend = (kt + 1) * kBK;
         if (kend % kChunk == 0 || kend == K) {       // chunk boundary: fold into the total
 #pragma unroll
-            for (int t = 0; t < TMI; ++t)
+            for (int i = 0; i < IB; ++i)
 #pragma unroll
-                for (int v = 0; v < 32; ++v) tot[t][v] = tot[t][v] + acc[t][v], acc[t][v] = 0.0f;
+                for (int j = 0; j < JB; ++j)
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) tot[i][j][v] = tot[i][j][v] + acc[i][j][v], acc[i][j][v] = 0.0f;
         }
         if (kt + 1 < nk) {
             store_tiles(buf ^ 1);
@@ -233,17 +235,190 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
         }
     }
 
-    // result register v of row group t: tile row 32 (WR-row) + 8 ((v % 16) / 4) + 4 (lane / 32) + v % 4,
-    // tile column 64 wc + 32 (v / 16) + lane % 32; 32 lanes store 128 contiguous bytes of a row
+    // result register v of block (i, j): tile row 16 (IB wr + i) + 4 (lane / 16) + v,
+    // tile column 16 (JB wc + j) + lane % 16; 16 lanes store 64 contiguous bytes of a row
 #pragma unroll
-    for (int t = 0; t < TMI; ++t)
+    for (int i = 0; i < IB; ++i)
 #pragma unroll
-        for (int v = 0; v < 32; ++v) {
-            const int r = rowmap[wr * 32 * TMI + 32 * t + 8 * ((v % 16) / 4) + 4 * (lane / 32) + (v % 4)];
-            const int col = col0 + wc * 64 + 32 * (v / 16) + (lane % 32);
-            if (r < 0 || col >= K) continue;
-            const bool keep = !state || kept(col, K, dm, du, state[r] != 0);
-            Xp[(size_t)r * K + col] = keep ? tot[t][v] : 0.0f;
+        for (int v = 0; v < 4; ++v) {
+            const int r = rowmap[wr * 16 * IB + 16 * i + 4 * kl + v];
+            if (r < 0) continue;
+            const bool masked = state ? state[r] != 0 : false;
+#pragma unroll
+            for (int j = 0; j < JB; ++j) {
+                const int col = col0 + wc * 16 * JB + 16 * j + il;
+                if (col >= K) continue;
+                const bool keep = !state || kept(col, K, dm, du, masked);
+                Xp[(size_t)r * K + col] = keep ? tot[i][j][v] : 0.0f;
+            }
+        }
+}
+
+// The same computation with both operand tiles copied from HBM straight into
+// LDS (buffer loads with the LDS destination, no staging registers) through a
+// three-stage ring: two k steps are in flight while a third is multiplied, one
+// barrier per step.  X stays fp16 in LDS (64 bytes per row and step, its four
+// 16-byte chunks XOR-swizzled by row) and is widened when read; P is staged
+// as it is in HBM, 512 bytes per k row, its 16-byte chunks XOR-swizzled by k
+// so that the four k of an instruction fall on different banks.
+template <int IB, int JB, int WR, int WC>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void transform_dma_kernel(
+    const uint16_t* __restrict__ X, const uint8_t* __restrict__ state, const float* __restrict__ P,
+    int M, int K, int dm, int du, int grouped, float* __restrict__ Xp) {
+    static_assert(WR * WC * kWave == kThreads, "four waves");
+    constexpr int NW = WR * WC;
+    constexpr int BM = 16 * IB * WR;
+    constexpr int BN = 16 * JB * WC;
+    constexpr int AB = BM * kBK * 2;                 // fp16 X tile bytes per stage
+    constexpr int BB = kBK * BN * 4;                 // fp32 P tile bytes per stage
+    constexpr int SB = AB + BB;
+    constexpr int LA = AB / 1024 / NW, LB = BB / 1024 / NW;   // 1 KB loads per wave per stage
+    static_assert(LA * NW * 1024 == AB && LB * NW * 1024 == BB, "stage loads must divide evenly");
+    static_assert(BN == 128, "P rows of 32 16-byte chunks");
+    __shared__ __attribute__((aligned(16))) uint8_t sm[3 * SB];
+    __shared__ int rowmap[BM];
+    __shared__ int scan[kThreads];
+
+    const int tid = threadIdx.x;
+    const int lane = tid % kWave, wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+    const int wr = wave / WC, wc = wave % WC;
+    int rt, ct;
+    const int R = (M + BM - 1) / BM;
+    xcd_tile(blockIdx.x, R, (K + BN - 1) / BN, R < 16 ? R : 16, rt, ct);
+    const int row0 = rt * BM, col0 = ct * BN;
+    if (grouped) {
+        const int nm = group_rows<BM>(state, M, rt, rowmap, scan);
+        const int rows_end = min(M, row0 + BM);
+        const bool all_m = rows_end <= nm, all_u = row0 >= nm;
+        const bool dropped = (all_m && col0 >= K - du) ||
+                             (all_u && col0 >= K - dm - du && col0 + BN <= K - du);
+        if (dropped) {
+            const int ncol4 = min(BN, K - col0) / 4;
+            for (int e = tid; e < BM * ncol4; e += kThreads) {
+                const int r = rowmap[e / ncol4];
+                if (r >= 0)
+                    *reinterpret_cast<float4*>(Xp + (size_t)r * K + col0 + (e % ncol4) * 4) =
+                        make_float4(0.f, 0.f, 0.f, 0.f);
+            }
+            return;
+        }
+    } else {
+        if (tid < BM) rowmap[tid] = row0 + tid < M ? row0 + tid : -1;
+        __syncthreads();
+    }
+
+    // X: tile row r's 64 bytes hold its chunks c at slot c ^ swa(r); P: k row k's
+    // 512 bytes hold column chunk c at slot c ^ swb(k)
+    auto swa = [](int r) { return (r >> 2) & 3; };
+    auto swb = [](int k) { return 4 * (k & 3); };
+    const u32x4 rX = sgpr_rsrc(X, (uint32_t)((size_t)M * K * 2));
+    uint32_t oa[LA], ob[LB];
+#pragma unroll
+    for (int u = 0; u < LA; ++u) {
+        const int r = 16 * (wave * LA + u) + lane / 4;
+        const int tok = rowmap[r];
+        oa[u] = tok >= 0 ? (uint32_t)tok * K * 2 + 16 * ((lane % 4) ^ swa(r)) : kOOB;
+    }
+#pragma unroll
+    for (int u = 0; u < LB; ++u) {
+        const int k = 2 * (wave * LB + u) + lane / 32;
+        const int c = (lane % 32) ^ swb(k);
+        ob[u] = col0 + 4 * c < K ? (uint32_t)k * K * 4 + (uint32_t)(col0 + 4 * c) * 4 : kOOB;
+    }
+    auto issue = [&](int kt, int stage) {
+        uint8_t* dA = sm + stage * SB;
+        uint8_t* dB = dA + AB;
+        // P rows k0 .. k0 + 31 through a descriptor based at row k0 (offsets stay below 128 K bytes)
+        const u32x4 rP = sgpr_rsrc(P + (size_t)kt * kBK * K, (uint32_t)kBK * K * 4);
+#pragma unroll
+        for (int u = 0; u < LA; ++u) dma16s(rX, lds_addr(dA + (wave * LA + u) * 1024), oa[u], (uint32_t)kt * kBK * 2);
+#pragma unroll
+        for (int u = 0; u < LB; ++u) dma16(rP, lds_addr(dB + (wave * LB + u) * 1024), ob[u]);
+    };
+
+    f32x4 acc[IB][JB], tot[IB][JB];
+#pragma unroll
+    for (int i = 0; i < IB; ++i)
+#pragma unroll
+        for (int j = 0; j < JB; ++j)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) acc[i][j][v] = 0.0f, tot[i][j][v] = 0.0f;
+
+    const int kl = lane / 16, il = lane % 16;
+    int aoff[IB];                                    // byte offset of this lane's A row in a stage
+#pragma unroll
+    for (int i = 0; i < IB; ++i) aoff[i] = (wr * 16 * IB + 16 * i + il) * 64;
+    const int aswz = swa(il);                        // swa(r) depends on r % 16 only (rows of a block)
+    int boff[JB];                                    // column chunk and position of this lane's B column
+#pragma unroll
+    for (int j = 0; j < JB; ++j) boff[j] = wc * 16 * JB + 16 * j + il;
+
+    auto compute = [&](const uint8_t* sa) {
+        const uint8_t* sbp = sa + AB;
+#pragma unroll
+        for (int s4 = 0; s4 < kBK / 4; ++s4) {
+            const int kk = 4 * s4 + kl;
+            float a[IB], b[JB];
+#pragma unroll
+            for (int i = 0; i < IB; ++i) {
+                const uint16_t h = *reinterpret_cast<const uint16_t*>(sa + aoff[i] + 16 * ((kk / 8) ^ aswz) + 2 * (kk % 8));
+                a[i] = h2f(h);
+            }
+#pragma unroll
+            for (int j = 0; j < JB; ++j) {
+                const int c = boff[j];
+                b[j] = *reinterpret_cast<const float*>(sbp + kk * (BN * 4) + 16 * ((c / 4) ^ swb(kk)) + 4 * (c % 4));
+            }
+#pragma unroll
+            for (int i = 0; i < IB; ++i)
+#pragma unroll
+                for (int j = 0; j < JB; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i], b[j], acc[i][j], 0, 0, 0);
+        }
+    };
+
+    const int nk = K / kBK;
+    auto step = [&](int kt, int sc, int sn) {
+        asm volatile("" ::: "memory");
+        if (kt + 1 < nk)
+            wait_vm<LA + LB>();                          // this wave's loads of step kt are done
+        else
+            wait_vm<0>();
+        __builtin_amdgcn_s_barrier();                    // ... and every wave's
+        asm volatile("" ::: "memory");
+        if (kt + 2 < nk) issue(kt + 2, sn);              // into the stage step kt - 1 used
+        compute(sm + sc * SB);
+        const int kend = (kt + 1) * kBK;
+        if (kend % kChunk == 0 || kend == K) {           // chunk boundary: fold into the total
+#pragma unroll
+            for (int i = 0; i < IB; ++i)
+#pragma unroll
+                for (int j = 0; j < JB; ++j)
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) tot[i][j][v] = tot[i][j][v] + acc[i][j][v], acc[i][j][v] = 0.0f;
+        }
+    };
+    issue(0, 0);
+    issue(1, 1);
+    for (int kt = 0; kt < nk; kt += 3) {
+        step(kt, 0, 2);
+        if (kt + 1 < nk) step(kt + 1, 1, 0);
+        if (kt + 2 < nk) step(kt + 2, 2, 1);
+    }
+
+#pragma unroll
+    for (int i = 0; i < IB; ++i)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int r = rowmap[wr * 16 * IB + 16 * i + 4 * kl + v];
+            if (r < 0) continue;
+            const bool masked = state ? state[r] != 0 : false;
+#pragma unroll
+            for (int j = 0; j < JB; ++j) {
+                const int col = col0 + wc * 16 * JB + 16 * j + il;
+                if (col >= K) continue;
+                const bool keep = !state || kept(col, K, dm, du, masked);
+                Xp[(size_t)r * K + col] = keep ? tot[i][j][v] : 0.0f;
+            }
         }
 }
 
@@ -277,28 +452,42 @@ hipError_t launch_transform(const uint16_t* X, const uint8_t* state, const float
         hipLaunchKernelGGL(gate_copy_kernel, dim3(blocks), dim3(kThreads), 0, st, X, state, M, K, dm, du, Xp);
         return hipGetLastError();
     }
-    // 128 x 128 tiles where they give at least two workgroups per CU, else 64 x 128,
-    // and 32 x 256 for a few rows
-    const int tiles128 = ((M + 127) / 128) * ((K + 127) / 128);
-    const int BM = tiles128 >= 512 ? 128 : (M > 32 ? 64 : 32);
-    const int BN = BM == 32 ? 256 : 128;
-    const int ncol = (K + BN - 1) / BN;
-    if ((size_t)((M + BM - 1) / BM) * ncol > 0x7fffffffu) return hipErrorInvalidConfiguration;
-    // group rows by state only where a column tile lies wholly in a band
-    const int u0 = K - du, m0 = K - dm - du;
-    const bool band_tile = (u0 + BN - 1) / BN * BN < K ||            // a tile wholly in [u0, K)
-                           (m0 + BN - 1) / BN * BN + BN <= u0;       // a tile wholly in [m0, u0)
-    const int grouped = state != nullptr && band_tile ? 1 : 0;
-    const dim3 grid(((M + BM - 1) / BM) * ncol);
-    if (BM == 128)
-        hipLaunchKernelGGL((transform_kernel<2, 2, 2>), grid, dim3(kThreads), 0, st, X, state, P, M, K, dm, du,
-                           grouped, Xp);
-    else if (BM == 64)
-        hipLaunchKernelGGL((transform_kernel<1, 2, 2>), grid, dim3(kThreads), 0, st, X, state, P, M, K, dm, du,
-                           grouped, Xp);
-    else
-        hipLaunchKernelGGL((transform_kernel<1, 1, 4>), grid, dim3(kThreads), 0, st, X, state, P, M, K, dm, du,
-                           grouped, Xp);
+    // up to 32 rows: the register-staged kernel on 32 x 256 tiles
+    if (M <= 32) {
+        const int ncol = (K + 255) / 256;
+        const int u0 = K - du, m0 = K - dm - du;
+        const bool band_tile = (u0 + 255) / 256 * 256 < K || (m0 + 255) / 256 * 256 + 256 <= u0;
+        const int grouped = state != nullptr && band_tile ? 1 : 0;
+        hipLaunchKernelGGL((transform_kernel<2, 4, 1, 4>), dim3(ncol), dim3(kThreads), 0, st, X, state, P, M, K, dm,
+                           du, grouped, Xp);
+        return hipGetLastError();
+    }
+    // The pipelined kernel addresses X with 32-bit buffer offsets, so a call whose
+    // X exceeds 2 GiB runs as independent chunks of rows (rows never interact).
+    const int Mc = (int)(((size_t)0x7fffffff / ((size_t)K * 2)) / 128 * 128);
+    for (int r0 = 0; r0 < M; r0 += Mc) {
+        const int m = M - r0 < Mc ? M - r0 : Mc;
+        const uint16_t* x = X + (size_t)r0 * K;
+        const uint8_t* s = state ? state + r0 : nullptr;
+        float* xp = Xp + (size_t)r0 * K;
+        // 128 x 128 tiles where they give at least two workgroups per CU, else 64 x 128
+        const int ncol = (K + 127) / 128;
+        const int BM = (size_t)((m + 127) / 128) * ncol >= 512 ? 128 : 64;
+        // group rows by state only where a column tile lies wholly in a band
+        const int u0 = K - du, m0 = K - dm - du;
+        const bool band_tile = (u0 + 127) / 128 * 128 < K ||           // a tile wholly in [u0, K)
+                               (m0 + 127) / 128 * 128 + 128 <= u0;     // a tile wholly in [m0, u0)
+        const int grouped = s != nullptr && band_tile ? 1 : 0;
+        const dim3 grid((unsigned)(((m + BM - 1) / BM) * ncol));
+        if (BM == 128)
+            hipLaunchKernelGGL((transform_dma_kernel<4, 4, 2, 2>), grid, dim3(kThreads), 0, st, x, s, P, m, K, dm, du,
+                               grouped, xp);
+        else
+            hipLaunchKernelGGL((transform_dma_kernel<2, 4, 2, 2>), grid, dim3(kThreads), 0, st, x, s, P, m, K, dm, du,
+                               grouped, xp);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
     return hipGetLastError();
 }
 

@@ -206,3 +206,25 @@ def test_denoise_sweep_layouts(layout):
         st = synth.state_edge(M, layout)
     for si in (0, 3):
         run_site(synth.LLADA_SWEEP, si, st, n_rows=16, n_cols=64)
+
+
+def test_transform_beyond_2gib_of_activations():
+    """A call whose X exceeds 2 GiB (65608 x 16384 fp16) runs as chunks of rows;
+    sampled rows on both sides of the chunk edge match the oracle bit for bit and
+    every other row (all zero on input) is zero."""
+    M, K = 65408 + 200, 16384
+    rng = np.random.default_rng(16384)
+    st = (rng.random(M) < 0.5).astype(np.uint8)
+    rows = np.unique(np.array([0, 1, 65407, 65408, 65409, M - 1] + list(rng.choice(M, 4, replace=False))))
+    Xs = (rng.standard_normal((len(rows), K)) * 2.0).astype(np.float16)
+    P = synth.orthogonal(K, synth.rng_for(605, K))
+    dm, du = synth.default_band(K)
+    say(f"transform beyond 2 GiB: M={M} K={K}")
+    X = torch.zeros((M, K), dtype=torch.float16, device="cuda")
+    X[torch.from_numpy(rows).cuda()] = dev(Xs)
+    xp = sq.sgat_transform(X, dev(st), dev(P), dm, du)
+    ref = O.transform(Xs, st[rows], P, dm, du, threads=THREADS)
+    assert_bits(host(xp[torch.from_numpy(rows).cuda()]), ref, "x' sampled rows")
+    others = torch.ones(M, dtype=torch.bool, device="cuda")
+    others[torch.from_numpy(rows).cuda()] = False
+    assert bool((xp[others] == 0).all())
