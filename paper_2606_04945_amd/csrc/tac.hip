@@ -3,12 +3,14 @@
 // each sum an fp32 fused multiply-add chain in ascending c from +0, bias last.
 //
 // The map is a batch of small [tokens x g] x [g x g] products, one per block.
-// It runs on the VALU because the fixed FMA order is part of the result; the
-// kernel is a register-tiled batched SGEMM: a workgroup owns TT tokens x CW
-// channels (CW = max(g, 64) so a span holds whole blocks), stages the span's
-// block matrices and the token tile through LDS as fp32, and each thread keeps
-// 8 tokens x 8 channels of accumulators (8 x 4 when g < 8), so each pair of
-// LDS reads feeds 64 (32) fused multiply-adds.
+// For widths that are a multiple of 128 channels it runs on the matrix cores
+// (tac_mfma_kernel, below), whose fp32 instruction reproduces that chain bit
+// for bit.  Other widths take tac_kernel, a register-tiled batched SGEMM on the
+// VALU: a workgroup owns TT tokens x CW channels (CW = max(g, 64) so a span
+// holds whole blocks), stages the span's block matrices and the token tile
+// through LDS as fp32, and each thread keeps 8 tokens x 8 channels of
+// accumulators (8 x 4 when g < 8), so each pair of LDS reads feeds 64 (32)
+// fused multiply-adds.
 #include "tile_common.hpp"
 
 namespace sq {
@@ -158,6 +160,132 @@ __global__ __launch_bounds__(kThreads) void tac_kernel(const uint16_t* __restric
     }
 }
 
+// The matrix-core form, for C a multiple of 128.  v_mfma_f32_16x16x4_f32
+// evaluates its four products as a forward chain of single-rounding fused
+// multiply-adds, k ascending (subnormals kept), so a chain of these
+// instructions over ascending groups of four c is exactly the fixed chain
+// above.  Outputs are taken 16 channels at a time: for g >= 16 the chain of a
+// 16-channel group runs over the g inputs of its block; for g < 16 it runs over
+// the group's own 16 inputs against a block-diagonal 16 x 16 operand whose
+// off-block entries are zero.  A zero product leaves a running sum unchanged
+// (the chain starts at +0 and never reaches -0), so the result is the same chain
+// over the block's g inputs.  A workgroup (four waves) owns 128 tokens x 128
+// channels: the token tile and the 128 rows of the block matrices are staged
+// in LDS as fp16 (widened as they are read), each wave multiplies 32 tokens x
+// 128 channels, and the fp16 results leave through LDS in 16-byte stores.
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+constexpr int kTacTile = 128;
+
+template <int G>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void tac_mfma_kernel(
+    const uint16_t* __restrict__ Z, const uint16_t* __restrict__ Mb, const uint16_t* __restrict__ d, int M, int C,
+    uint16_t* __restrict__ out) {
+    constexpr int TR = kTacTile, CW = kTacTile;
+    constexpr int L = G < 16 ? 16 : G;               // chain length of a 16-channel output group
+    constexpr int ZP = CW + 8;                       // fp16 row of the token tile: 16-byte aligned, rows 4 banks apart
+    constexpr int MP = G >= 8 ? G + 8 : G;           // fp16 row of the block-matrix tile
+    __shared__ __attribute__((aligned(16))) uint16_t zs[TR * ZP];
+    __shared__ __attribute__((aligned(16))) uint16_t ms[CW * MP];
+
+    const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
+    const int span0 = blockIdx.x * CW, tok0 = blockIdx.y * TR;
+
+    // token tile: 16 16-byte vectors per row; rows past M read as zero
+#pragma unroll
+    for (int v = 0; v < TR * CW / 8 / kThreads; ++v) {
+        const int e = tid + v * kThreads, r = e / (CW / 8), q = e % (CW / 8);
+        uint4 w = make_uint4(0, 0, 0, 0);
+        if (tok0 + r < M) w = *reinterpret_cast<const uint4*>(Z + (size_t)(tok0 + r) * C + span0 + 8 * q);
+        *reinterpret_cast<uint4*>(zs + r * ZP + 8 * q) = w;
+    }
+    // block-matrix rows of the span's channels: tac_M viewed as [C][G], rows span0 .. span0 + 127
+    {
+        const uint16_t* src = Mb + (size_t)span0 * G;
+        for (int e = tid; e < CW * G / 8; e += kThreads) {
+            const uint4 w = *reinterpret_cast<const uint4*>(src + 8 * e);
+            if (G >= 8) {
+                const int r = 8 * e / G, c = 8 * e % G;
+                *reinterpret_cast<uint4*>(ms + r * MP + c) = w;
+            } else {
+                *reinterpret_cast<uint4*>(ms + 8 * e) = w;
+            }
+        }
+    }
+    __syncthreads();
+
+    const int il = lane % 16, kl = lane / 16;
+    f32x4 acc[2][CW / 16];
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+        for (int og = 0; og < CW / 16; ++og)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) acc[rb][og][v] = 0.0f;
+
+    const uint16_t* za = zs + (32 * wave + il) * ZP;          // this lane's token row (row block 0)
+    if constexpr (G < 32) {
+        // one 16-channel group per chain input range
+#pragma unroll
+        for (int og = 0; og < CW / 16; ++og) {
+            const int in0 = G < 16 ? 16 * og : (16 * og / G) * G;   // first input channel of the chain
+            const int mrow = 16 * og + il;                   // block-matrix row (output channel) of this lane
+#pragma unroll
+            for (int s4 = 0; s4 < L / 4; ++s4) {
+                const int c = 4 * s4 + kl;                   // position in the chain
+                const float b = G >= 16 ? h2f(ms[mrow * MP + c])
+                                        : (c / G == il / G ? h2f(ms[mrow * MP + c % G]) : 0.0f);
+#pragma unroll
+                for (int rb = 0; rb < 2; ++rb) {
+                    const float a = h2f(za[rb * 16 * ZP + in0 + c]);
+                    acc[rb][og] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc[rb][og], 0, 0, 0);
+                }
+            }
+        }
+    } else {
+        // the G / 16 groups of a block share their inputs: each token value read feeds all of them
+        constexpr int NG = G / 16;
+#pragma unroll
+        for (int blk = 0; blk < CW / G; ++blk) {
+#pragma unroll 4
+            for (int s4 = 0; s4 < G / 4; ++s4) {
+                const int c = 4 * s4 + kl;
+                float a[2];
+#pragma unroll
+                for (int rb = 0; rb < 2; ++rb) a[rb] = h2f(za[rb * 16 * ZP + blk * G + c]);
+#pragma unroll
+                for (int q = 0; q < NG; ++q) {
+                    const int og = blk * NG + q;
+                    const float b = h2f(ms[(16 * og + il) * MP + c]);
+#pragma unroll
+                    for (int rb = 0; rb < 2; ++rb)
+                        acc[rb][og] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[rb], b, acc[rb][og], 0, 0, 0);
+                }
+            }
+        }
+    }
+
+    // z' = fp16(sum + d), through LDS (the token tile is no longer read) to 16-byte stores
+    float dv[CW / 16];
+#pragma unroll
+    for (int og = 0; og < CW / 16; ++og) dv[og] = h2f(d[span0 + 16 * og + il]);
+    __syncthreads();
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+        for (int og = 0; og < CW / 16; ++og)
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+                zs[(32 * wave + 16 * rb + 4 * kl + v) * ZP + 16 * og + il] = f2h(acc[rb][og][v] + dv[og]);
+    __syncthreads();
+#pragma unroll
+    for (int v = 0; v < TR * CW / 8 / kThreads; ++v) {
+        const int e = tid + v * kThreads, r = e / (CW / 8), q = e % (CW / 8);
+        if (tok0 + r < M)
+            *reinterpret_cast<uint4*>(out + (size_t)(tok0 + r) * C + span0 + 8 * q) =
+                *reinterpret_cast<const uint4*>(zs + r * ZP + 8 * q);
+    }
+}
+
 template <int CW, int CPT>
 hipError_t launch_cw(const uint16_t* Z, const uint16_t* Mb, const uint16_t* d, int M, int C, int g,
                      uint16_t* out, hipStream_t st) {
@@ -176,6 +304,19 @@ hipError_t launch_cw(const uint16_t* Z, const uint16_t* Mb, const uint16_t* d, i
 
 hipError_t launch_tac(const uint16_t* Z, const uint16_t* Mb, const uint16_t* d, int M, int C, int g,
                       uint16_t* out, hipStream_t st) {
+    if (C % kTacTile == 0) {
+        const dim3 grid(C / kTacTile, (M + kTacTile - 1) / kTacTile);
+        switch (g) {
+#define SQ_TM(G)                                                                                              \
+    case G:                                                                                                   \
+        hipLaunchKernelGGL(tac_mfma_kernel<G>, grid, dim3(kThreads), 0, st, Z, Mb, d, M, C, out);             \
+        return hipGetLastError();
+            SQ_TM(1) SQ_TM(2) SQ_TM(4) SQ_TM(8) SQ_TM(16) SQ_TM(32) SQ_TM(64) SQ_TM(128)
+#undef SQ_TM
+            default:
+                return hipErrorInvalidValue;
+        }
+    }
     if (g < 8) return launch_cw<64, 4>(Z, Mb, d, M, C, g, out, st);
     if (g <= 64) return launch_cw<64, 8>(Z, Mb, d, M, C, g, out, st);
     return launch_cw<128, 8>(Z, Mb, d, M, C, g, out, st);

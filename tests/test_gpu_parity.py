@@ -284,10 +284,21 @@ def test_gemm_split_and_unsplit_agree():
 # ------------------------------------------------------------------ TAC
 
 @pytest.mark.parametrize("g", [1, 2, 4, 8, 16, 32, 64, 128])
-@pytest.mark.parametrize("M,C", [(1, 128), (100, 512), (257, 4096)])
+@pytest.mark.parametrize("M,C", [(1, 128), (100, 512), (257, 4096), (1000, 3584)])
 def test_tac_bit_exact(g, M, C):
     Z = (np.random.default_rng(g + M).standard_normal((M, C)) * 2).astype(np.float16)
     Mb, d = synth.tac_params(C, g, synth.rng_for(700, g, C))
+    say(f"tac g={g} M={M} C={C}")
+    out = host(sq.tac_apply(dev(Z), dev(Mb), dev(d), g))
+    assert_bits(out, O.tac(Z, Mb, d, g, threads=THREADS), "tac")
+
+
+@pytest.mark.parametrize("g", [1, 2, 4, 8, 16, 32, 64])
+@pytest.mark.parametrize("M,C", [(70, 192), (300, 320)])
+def test_tac_bit_exact_widths_off_the_tile(g, M, C):
+    """Widths that are not a multiple of 128 channels take the VALU kernel."""
+    Z = (np.random.default_rng(g + M + 1).standard_normal((M, C)) * 2).astype(np.float16)
+    Mb, d = synth.tac_params(C, g, synth.rng_for(704, g, C))
     say(f"tac g={g} M={M} C={C}")
     out = host(sq.tac_apply(dev(Z), dev(Mb), dev(d), g))
     assert_bits(out, O.tac(Z, Mb, d, g, threads=THREADS), "tac")
