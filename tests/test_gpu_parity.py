@@ -144,6 +144,25 @@ def test_transform_rows_grouped_by_state(M, K, dm, du, layout):
     assert (gone == 0).all() and not np.signbit(gone).any()
 
 
+def test_transform_subnormal_products_and_signed_zeros():
+    """A basis of subnormal and zero entries: products, chunk sums and totals are
+    fp32 subnormals or signed zeros, kept (not flushed) and summed exactly as the
+    oracle's IEEE chain does; zero columns give +0 for every row."""
+    M, K = 200, 512
+    X, st = _x(M, K, 12)
+    P = synth.orthogonal(K, synth.rng_for(606, K)) * np.float32(2.0 ** -136)   # entries around 2^-140
+    P[:, 5::7] = 0.0
+    P[:, 6::7] = -0.0
+    P = P.astype(np.float32)
+    assert (np.abs(P[P != 0]) < np.float32(2.0 ** -126)).all()
+    say(f"transform subnormal basis M={M} K={K}")
+    for M_ in (M, 20):   # the pipelined kernel and the one for up to 32 rows
+        xp = host(sq.sgat_transform(dev(X[:M_]), None, dev(P)))
+        ref = O.transform(X[:M_], None, P, 0, 0, threads=THREADS)
+        assert (ref != 0).any() and (np.abs(ref[ref != 0]) < np.float32(2.0 ** -126)).any()
+        assert_bits(xp, ref, f"x' (subnormal basis, {M_} rows)")
+
+
 def test_transform_identity_basis_equals_folded():
     X, st = _x(40, 512, 4)
     dm, du = synth.default_band(512)
