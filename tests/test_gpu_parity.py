@@ -476,6 +476,20 @@ def test_w8_quant_act(withP, g):
     assert_bits(host(Aq), rq, "Aq")
 
 
+@pytest.mark.parametrize("M,K", [(2100, 3584), (17, 4096)])
+def test_w8_quant_act_tac_fused(M, K):
+    """8-bit codes from the fused TAC pass (g = 16, folded basis) on several
+    16-token tiles and a ragged last one."""
+    X, st = _x(M, K, 10)
+    dm, du = synth.default_band(K)
+    Mb, d = synth.tac_params(K, 16, synth.rng_for(706, K))
+    say(f"w8 quant_act fused tac M={M} K={K}")
+    Aq, s = sq.sgat_quant_act_w8(dev(X), dev(st), None, dm, du, dev(Mb), dev(d), 16)
+    rq, rs = O.quant_act_q8(X, st, None, dm, du, Mb, d, 16, threads=THREADS)
+    assert_bits(host(s), rs, "s_a")
+    assert_bits(host(Aq), rq, "Aq")
+
+
 @pytest.mark.parametrize("withP", [True, False])
 def test_w8_prepare_weights(withP):
     N, K = 200, 1024
