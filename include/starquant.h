@@ -37,6 +37,12 @@
  *    16-byte aligned.  TAC block size g is a power of two, 1 <= g <= 128, g | C.
  *    w4a4_gemm, w8a8_gemm, tac_apply and sgat_quant_act with TAC take at most
  *    4194240 (65535 x 64) rows per call.
+ *  - Debugging: with the environment variable SQ_DEBUG_SYNC set (to anything
+ *    but "" or "0") when the library first checks it, every kernel launch is
+ *    followed by hipDeviceSynchronize and an error check, so an asynchronous
+ *    fault is returned as SQ_ERR_HIP by the call that launched the faulting
+ *    kernel, named in sq_last_error().  This serialises the device and must
+ *    not be used under stream capture.
  *  - Arithmetic is fixed so that results are a unique function of the inputs:
  *    fp32 IEEE throughout (correctly rounded divide, round-to-nearest-even, no
  *    flush of subnormals); the transform accumulates k in chunks of 256 with a

@@ -2,6 +2,7 @@
 // Every argument is checked before the first launch; on failure nothing is
 // enqueued and the reason is kept in a thread-local message.
 #include <stdarg.h>
+#include <stdlib.h>
 #include <stdio.h>
 
 #include <atomic>
@@ -22,7 +23,24 @@ int fail(int code, const char* fmt, ...) {
     return code;
 }
 
+// SQ_DEBUG_SYNC set to anything but "" or "0" (read once, at the first call):
+// every launch is followed by a device-wide synchronisation and an error
+// check, so an asynchronous fault is reported by the call whose kernel raised
+// it, named in the message.  For debugging only: it serialises the device and
+// cannot be used under stream capture.
+bool debug_sync() {
+    static const bool on = [] {
+        const char* v = getenv("SQ_DEBUG_SYNC");
+        return v != nullptr && v[0] != '\0' && !(v[0] == '0' && v[1] == '\0');
+    }();
+    return on;
+}
+
 int hip_status(hipError_t e, const char* what) {
+    if (e == hipSuccess && debug_sync()) {
+        e = hipDeviceSynchronize();
+        if (e == hipSuccess) e = hipGetLastError();
+    }
     if (e == hipSuccess) return SQ_OK;
     return fail(SQ_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
