@@ -14,10 +14,12 @@
 // four k, from a zeroed accumulator, is therefore exactly one chunk's chain;
 // the chunk totals are added on the VALU.
 //
-// Tiling: a 256-thread workgroup (four waves) owns a BM x BN tile of outputs
-// (128 x 128 or 64 x 128; 32 x 256 for up to 32 rows), a wave IB x JB blocks
-// of 16 x 16, each output with a chunk accumulator (the instruction's result
-// registers) and a total.  Main kernel: both operand tiles go from HBM straight
+// Tiling: a workgroup owns a BM x BN tile of outputs, a wave IB x JB blocks of
+// 16 x 16, each output with a chunk accumulator (the instruction's result
+// registers) and a total: 128 x 128 tiles of eight waves of 32 x 64 (four waves
+// per SIMD at two workgroups per CU; four waves of 64 x 64 were 3-9 % slower),
+// 64 x 128 tiles of four waves where 128-row tiles would leave CUs idle, and
+// 32 x 256 for up to 32 rows.  Main kernel: both operand tiles go from HBM straight
 // into LDS (buffer loads with the LDS destination, no staging registers)
 // through a three-stage ring, two k steps of 32 in flight while a third is
 // multiplied, one barrier per step; X stays fp16 in LDS and is widened as it is
@@ -47,24 +49,24 @@ constexpr int kBK = 32;
 // This workgroup's rows when rows are grouped by state: rowmap[i] is the row
 // of rank rt * BM + i in the order (masked rows, then unmasked rows), or -1
 // past the last row; returns the number of masked rows.
-template <int BM>
+template <int BM, int NT = kThreads>
 __device__ int group_rows(const uint8_t* __restrict__ state, int M, int rt, int* rowmap, int* scan) {
     const int tid = threadIdx.x;
-    const int per = (M + kThreads - 1) / kThreads;   // states per thread, in one contiguous run
+    const int per = (M + NT - 1) / NT;               // states per thread, in one contiguous run
     const int b = min(M, tid * per), e = min(M, b + per);
     int cnt = 0;
     for (int i = b; i < e; ++i) cnt += state[i] != 0;
     if (tid < BM) rowmap[tid] = -1;
     scan[tid] = cnt;
     __syncthreads();
-    // inclusive scan of the per-thread counts (Hillis-Steele over 256 entries)
-    for (int o = 1; o < kThreads; o <<= 1) {
+    // inclusive scan of the per-thread counts (Hillis-Steele over NT entries)
+    for (int o = 1; o < NT; o <<= 1) {
         const int v = tid >= o ? scan[tid - o] : 0;
         __syncthreads();
         scan[tid] += v;
         __syncthreads();
     }
-    const int nm = scan[kThreads - 1];
+    const int nm = scan[NT - 1];
     int m_rank = scan[tid] - cnt;                    // masked rows before this run
     int u_rank = nm + (b - m_rank);                  // rank of its first unmasked row
     const int lo = rt * BM;
@@ -261,11 +263,11 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
 // 16-byte chunks XOR-swizzled by row) and is widened when read; P is staged
 // as it is in HBM, 512 bytes per k row, its 16-byte chunks XOR-swizzled by k
 // so that the four k of an instruction fall on different banks.
-template <int IB, int JB, int WR, int WC>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void transform_dma_kernel(
+template <int IB, int JB, int WR, int WC, int NT = 64 * WR * WC>
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(NT / 128))) void transform_dma_kernel(
     const uint16_t* __restrict__ X, const uint8_t* __restrict__ state, const float* __restrict__ P,
     int M, int K, int dm, int du, int grouped, float* __restrict__ Xp) {
-    static_assert(WR * WC * kWave == kThreads, "four waves");
+    static_assert(WR * WC * kWave == NT, "wave count");
     constexpr int NW = WR * WC;
     constexpr int BM = 16 * IB * WR;
     constexpr int BN = 16 * JB * WC;
@@ -277,7 +279,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     static_assert(BN == 128, "P rows of 32 16-byte chunks");
     __shared__ __attribute__((aligned(16))) uint8_t sm[3 * SB];
     __shared__ int rowmap[BM];
-    __shared__ int scan[kThreads];
+    __shared__ int scan[NT];
 
     const int tid = threadIdx.x;
     const int lane = tid % kWave, wave = __builtin_amdgcn_readfirstlane(tid / kWave);
@@ -287,14 +289,14 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     xcd_tile(blockIdx.x, R, (K + BN - 1) / BN, R < 16 ? R : 16, rt, ct);
     const int row0 = rt * BM, col0 = ct * BN;
     if (grouped) {
-        const int nm = group_rows<BM>(state, M, rt, rowmap, scan);
+        const int nm = group_rows<BM, NT>(state, M, rt, rowmap, scan);
         const int rows_end = min(M, row0 + BM);
         const bool all_m = rows_end <= nm, all_u = row0 >= nm;
         const bool dropped = (all_m && col0 >= K - du) ||
                              (all_u && col0 >= K - dm - du && col0 + BN <= K - du);
         if (dropped) {
             const int ncol4 = min(BN, K - col0) / 4;
-            for (int e = tid; e < BM * ncol4; e += kThreads) {
+            for (int e = tid; e < BM * ncol4; e += NT) {
                 const int r = rowmap[e / ncol4];
                 if (r >= 0)
                     *reinterpret_cast<float4*>(Xp + (size_t)r * K + col0 + (e % ncol4) * 4) =
@@ -480,7 +482,7 @@ hipError_t launch_transform(const uint16_t* X, const uint8_t* state, const float
         const int grouped = s != nullptr && band_tile ? 1 : 0;
         const dim3 grid((unsigned)(((m + BM - 1) / BM) * ncol));
         if (BM == 128)
-            hipLaunchKernelGGL((transform_dma_kernel<4, 4, 2, 2>), grid, dim3(kThreads), 0, st, x, s, P, m, K, dm, du,
+            hipLaunchKernelGGL((transform_dma_kernel<2, 4, 4, 2>), grid, dim3(512), 0, st, x, s, P, m, K, dm, du,
                                grouped, xp);
         else
             hipLaunchKernelGGL((transform_dma_kernel<2, 4, 2, 2>), grid, dim3(kThreads), 0, st, x, s, P, m, K, dm, du,
