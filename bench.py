@@ -286,10 +286,10 @@ def dense_report(M, sites, ms, timer):
 def transform_roofline(M, d, timer, traffic_key):
     n = d["name"]
     ach = transform_flop(M, d["K"]) / timer.mean("transform/" + n) / 1e9
-    return {"bound": "alu", "achieved": ach, "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
+    return {"bound": "mfma", "achieved": ach, "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
             "frac": ach / PEAK_FP32_TFLOPS,
             "traffic": recorded_traffic(traffic_key),
-            "kernel": f"transform (dense fp32 x P, fixed order) at the {n} linear, M={M}, K={d['K']}",
+            "kernel": f"transform (dense fp32 x P, fixed order, fp32 matrix cores) at the {n} linear, M={M}, K={d['K']}",
             "flop_per_launch": transform_flop(M, d["K"]), "launch_us_mean": timer.mean("transform/" + n) * 1e3}
 
 
@@ -627,7 +627,7 @@ def tac_oproj_block(torch, sq, synth, dev, steps=3):
         tac_flop = 2.0 * M * K * g
         rec = {"ms_per_step": ms, "tokens_per_s": M / (ms / 1e3), "tac_ms": tac_ms, "quant_ms": timer.mean("q"),
                "gemm_ms": g_ms, "gemm_frac_int8_peak": 2.0 * M * N * K / g_ms / 1e9 / PEAK_INT8_TOPS,
-               "roofline": {"bound": "alu", "achieved": tac_flop / tac_ms / 1e9, "peak": PEAK_FP32_TFLOPS,
+               "roofline": {"bound": "mfma", "achieved": tac_flop / tac_ms / 1e9, "peak": PEAK_FP32_TFLOPS,
                             "unit": "TFLOP/s", "frac": tac_flop / tac_ms / 1e9 / PEAK_FP32_TFLOPS,
                             "traffic": recorded_traffic("tac_g128") if g == 128 else None,
                             "kernel": f"tac (g = {g})"}}

@@ -96,13 +96,13 @@ __device__ __forceinline__ void quant_codes8(const float* x, float s, float y, i
     for (int q = 0; q < 8; ++q) {
         const float q0 = x[q] * y;
         r[q] = __builtin_rintf(q0);
-        near |= !(0.5f - fabsf(q0 - r[q]) > kNear);
+        near |= !(fabsf(q0 - r[q]) < 0.5f - kNear);
     }
     if (__builtin_expect(near, 0)) {
 #pragma unroll
         for (int q = 0; q < 8; ++q) {
             const float q0 = x[q] * y;
-            if (!(0.5f - fabsf(q0 - r[q]) > kNear)) r[q] = __builtin_rintf(x[q] / s);
+            if (!(fabsf(q0 - r[q]) < 0.5f - kNear)) r[q] = __builtin_rintf(x[q] / s);
         }
     }
     // clamp with one median-of-three (identical to the two-sided clamp for

@@ -169,18 +169,22 @@ __global__ __launch_bounds__(kThreads) void tac_kernel(const uint16_t* __restric
 // the group's own 16 inputs against a block-diagonal 16 x 16 operand whose
 // off-block entries are zero.  A zero product leaves a running sum unchanged
 // (the chain starts at +0 and never reaches -0), so the result is the same chain
-// over the block's g inputs.  A workgroup (four waves) owns 128 tokens x 128
+// over the block's g inputs.  A workgroup (eight waves) owns 128 tokens x 128
 // channels: the token tile and the 128 rows of the block matrices are staged
-// in LDS as fp16 (widened as they are read), each wave multiplies 32 tokens x
-// 128 channels, and the fp16 results leave through LDS in 16-byte stores.
+// in LDS as fp16 (widened as they are read), each wave multiplies 16 tokens x
+// 128 channels, and the fp16 results leave through LDS in 16-byte stores
+// (eight waves of 16 tokens were 5-18 % faster than four waves of 32).
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 constexpr int kTacTile = 128;
 
+constexpr int kTacWaves = kTacTile / 16;          // one wave per 16 tokens of the tile
+constexpr int kTacThreads = 64 * kTacWaves;
+
 template <int G>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void tac_mfma_kernel(
+__global__ __launch_bounds__(kTacThreads) __attribute__((amdgpu_waves_per_eu(kTacWaves / 2))) void tac_mfma_kernel(
     const uint16_t* __restrict__ Z, const uint16_t* __restrict__ Mb, const uint16_t* __restrict__ d, int M, int C,
     uint16_t* __restrict__ out) {
-    constexpr int TR = kTacTile, CW = kTacTile;
+    constexpr int TR = kTacTile, CW = kTacTile, NT = kTacThreads;
     constexpr int L = G < 16 ? 16 : G;               // chain length of a 16-channel output group
     constexpr int ZP = CW + 8;                       // fp16 row of the token tile: 16-byte aligned, rows 4 banks apart
     constexpr int MP = G >= 8 ? G + 8 : G;           // fp16 row of the block-matrix tile
@@ -192,8 +196,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
 
     // token tile: 16 16-byte vectors per row; rows past M read as zero
 #pragma unroll
-    for (int v = 0; v < TR * CW / 8 / kThreads; ++v) {
-        const int e = tid + v * kThreads, r = e / (CW / 8), q = e % (CW / 8);
+    for (int v = 0; v < TR * CW / 8 / NT; ++v) {
+        const int e = tid + v * NT, r = e / (CW / 8), q = e % (CW / 8);
         uint4 w = make_uint4(0, 0, 0, 0);
         if (tok0 + r < M) w = *reinterpret_cast<const uint4*>(Z + (size_t)(tok0 + r) * C + span0 + 8 * q);
         *reinterpret_cast<uint4*>(zs + r * ZP + 8 * q) = w;
@@ -201,7 +205,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     // block-matrix rows of the span's channels: tac_M viewed as [C][G], rows span0 .. span0 + 127
     {
         const uint16_t* src = Mb + (size_t)span0 * G;
-        for (int e = tid; e < CW * G / 8; e += kThreads) {
+        for (int e = tid; e < CW * G / 8; e += NT) {
             const uint4 w = *reinterpret_cast<const uint4*>(src + 8 * e);
             if (G >= 8) {
                 const int r = 8 * e / G, c = 8 * e % G;
@@ -214,15 +218,13 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     __syncthreads();
 
     const int il = lane % 16, kl = lane / 16;
-    f32x4 acc[2][CW / 16];
+    f32x4 acc[CW / 16];
 #pragma unroll
-    for (int rb = 0; rb < 2; ++rb)
+    for (int og = 0; og < CW / 16; ++og)
 #pragma unroll
-        for (int og = 0; og < CW / 16; ++og)
-#pragma unroll
-            for (int v = 0; v < 4; ++v) acc[rb][og][v] = 0.0f;
+        for (int v = 0; v < 4; ++v) acc[og][v] = 0.0f;
 
-    const uint16_t* za = zs + (32 * wave + il) * ZP;          // this lane's token row (row block 0)
+    const uint16_t* za = zs + (16 * wave + il) * ZP;   // this lane's token row
     if constexpr (G < 32) {
         // one 16-channel group per chain input range
 #pragma unroll
@@ -234,11 +236,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
                 const int c = 4 * s4 + kl;                   // position in the chain
                 const float b = G >= 16 ? h2f(ms[mrow * MP + c])
                                         : (c / G == il / G ? h2f(ms[mrow * MP + c % G]) : 0.0f);
-#pragma unroll
-                for (int rb = 0; rb < 2; ++rb) {
-                    const float a = h2f(za[rb * 16 * ZP + in0 + c]);
-                    acc[rb][og] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc[rb][og], 0, 0, 0);
-                }
+                const float a = h2f(za[in0 + c]);
+                acc[og] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc[og], 0, 0, 0);
             }
         }
     } else {
@@ -249,16 +248,12 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
 #pragma unroll 4
             for (int s4 = 0; s4 < G / 4; ++s4) {
                 const int c = 4 * s4 + kl;
-                float a[2];
-#pragma unroll
-                for (int rb = 0; rb < 2; ++rb) a[rb] = h2f(za[rb * 16 * ZP + blk * G + c]);
+                const float a = h2f(za[blk * G + c]);
 #pragma unroll
                 for (int q = 0; q < NG; ++q) {
                     const int og = blk * NG + q;
                     const float b = h2f(ms[(16 * og + il) * MP + c]);
-#pragma unroll
-                    for (int rb = 0; rb < 2; ++rb)
-                        acc[rb][og] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[rb], b, acc[rb][og], 0, 0, 0);
+                    acc[og] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc[og], 0, 0, 0);
                 }
             }
         }
@@ -270,16 +265,13 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     for (int og = 0; og < CW / 16; ++og) dv[og] = h2f(d[span0 + 16 * og + il]);
     __syncthreads();
 #pragma unroll
-    for (int rb = 0; rb < 2; ++rb)
+    for (int og = 0; og < CW / 16; ++og)
 #pragma unroll
-        for (int og = 0; og < CW / 16; ++og)
-#pragma unroll
-            for (int v = 0; v < 4; ++v)
-                zs[(32 * wave + 16 * rb + 4 * kl + v) * ZP + 16 * og + il] = f2h(acc[rb][og][v] + dv[og]);
+        for (int v = 0; v < 4; ++v) zs[(16 * wave + 4 * kl + v) * ZP + 16 * og + il] = f2h(acc[og][v] + dv[og]);
     __syncthreads();
 #pragma unroll
-    for (int v = 0; v < TR * CW / 8 / kThreads; ++v) {
-        const int e = tid + v * kThreads, r = e / (CW / 8), q = e % (CW / 8);
+    for (int v = 0; v < TR * CW / 8 / NT; ++v) {
+        const int e = tid + v * NT, r = e / (CW / 8), q = e % (CW / 8);
         if (tok0 + r < M)
             *reinterpret_cast<uint4*>(out + (size_t)(tok0 + r) * C + span0 + 8 * q) =
                 *reinterpret_cast<const uint4*>(zs + r * ZP + 8 * q);
@@ -309,7 +301,7 @@ hipError_t launch_tac(const uint16_t* Z, const uint16_t* Mb, const uint16_t* d, 
         switch (g) {
 #define SQ_TM(G)                                                                                              \
     case G:                                                                                                   \
-        hipLaunchKernelGGL(tac_mfma_kernel<G>, grid, dim3(kThreads), 0, st, Z, Mb, d, M, C, out);             \
+        hipLaunchKernelGGL(tac_mfma_kernel<G>, grid, dim3(kTacThreads), 0, st, Z, Mb, d, M, C, out);     \
         return hipGetLastError();
             SQ_TM(1) SQ_TM(2) SQ_TM(4) SQ_TM(8) SQ_TM(16) SQ_TM(32) SQ_TM(64) SQ_TM(128)
 #undef SQ_TM
@@ -587,12 +579,318 @@ __global__ __launch_bounds__(64 * (kTqMaxConsumerWaves + 1)) void tac_quant_kern
     finish(nrows - 1);
 }
 
+
+// ---------------------------------------------------------------------------
+// The same fused pass on the matrix cores for g = 16, for rows of four to eight
+// parts of 16 NG channels (NG = 28 or 32: hidden sizes 3584 and 4096 take
+// eight waves).  A workgroup walks 16-token tiles; each of its waves owns
+// 16 NG consecutive channels of every row.  Per tile a wave:
+//   * takes its z values straight from HBM, 16 bytes per lane (8 channels of
+//     one token), half a tile of loads ahead in a register ring;
+//   * rearranges them with two rounds of cross-row lane swaps into the operand
+//     the fp32 MFMA wants (lane (t, k) needs channels k, k + 4, k + 8, k + 12 of
+//     a 16-channel group for token t);
+//   * runs z'^T = M_b z^T for each 16-channel block (g = 16) as a chain of four
+//     v_mfma_f32_16x16x4_f32 over ascending c (the TAC chain of tac_kernel bit
+//     for bit, as in tac_mfma_kernel), adds the bias, applies the gate, rounds
+//     to fp16 and parks the result in its own LDS tile (each lane holds four
+//     consecutive channels of one token per block: one 8-byte write);
+//   * tracks the token's absmax, combines it over the wave and posts it.
+// One workgroup barrier per tile publishes the partial maxima.  Then each wave
+// forms the 16 token scales, reads its tile back as runs of 8 channels of one
+// token, codes them (quant_codes8, the rule of every quantiser here) and
+// stores the codes.  The block-matrix operands (four values per lane and
+// group, packed fp16) stay in registers for the whole walk, which is why a
+// wave takes many channels and a CU runs one workgroup of up to eight waves.
+constexpr int kTqmTok = 16;
+constexpr int kTqmMaxWaves = 8;
+
+// Lanes 16 r + k (row r = 0..3 of the wave, k = 0..15) hold x_0 .. x_3; on
+// return lane 16 r + k holds in x_p what lane 16 p + k held in x_r.  Two
+// rounds of lane-half / lane-row swaps.
+__device__ __forceinline__ void transpose_rows4(uint32_t& x0, uint32_t& x1, uint32_t& x2, uint32_t& x3) {
+    auto s02 = __builtin_amdgcn_permlane32_swap(x0, x2, false, false);
+    auto s13 = __builtin_amdgcn_permlane32_swap(x1, x3, false, false);
+    x0 = s02[0], x2 = s02[1], x1 = s13[0], x3 = s13[1];
+    auto s01 = __builtin_amdgcn_permlane16_swap(x0, x1, false, false);
+    auto s23 = __builtin_amdgcn_permlane16_swap(x2, x3, false, false);
+    x0 = s01[0], x1 = s01[1], x2 = s23[0], x3 = s23[1];
+}
+
+__device__ __forceinline__ float lo_h(uint32_t x) { return h2f((uint16_t)(x & 0xFFFFu)); }
+__device__ __forceinline__ float hi_h(uint32_t x) { return h2f((uint16_t)(x >> 16)); }
+
+template <int NG>
+struct TqmShape {
+    static constexpr int kCWV = 16 * NG;                        // channels per wave
+    static constexpr int kRS = 2 * kCWV + 16;                   // fp16 row of a wave's output tile (banks spread)
+    static constexpr int kStage = kCWV * 32;                    // block-matrix rows of a wave, staged once
+    static constexpr int kRegion = kStage > kTqmTok * kRS ? kStage : kTqmTok * kRS;
+    static size_t lds_bytes(int K) {
+        return (size_t)K * 4 + 2 * kTqmTok * kTqmMaxWaves * 4 + (size_t)(K / kCWV) * kRegion;
+    }
+};
+
+template <int BITS, int NG>
+__global__ __launch_bounds__(64 * kTqmMaxWaves) void tac_quant_mfma_kernel(
+    const uint16_t* __restrict__ Z, const uint16_t* __restrict__ Mb, const uint16_t* __restrict__ d,
+    const uint8_t* __restrict__ state, int M, int K, int dm, int du, uint8_t* __restrict__ Aq,
+    float* __restrict__ s_out) {
+    using S = TqmShape<NG>;
+    constexpr int CWV = S::kCWV, NC = NG / 2, D = NC / 2;       // D: chunk loads in flight per lane
+    constexpr float kQmax = BITS == 4 ? 7.0f : 127.0f;
+    constexpr int VPL = CWV / 32;                               // 8-channel runs per lane in the coding pass
+    static_assert(NC % D == 0 && VPL % 2 == 0 && CWV % kWave == 0, "static ring slots; runs coded in pairs");
+    extern __shared__ __attribute__((aligned(16))) float tqm_smem[];
+    const int lane = threadIdx.x % kWave, wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int il = lane % 16, kl = lane / 16;
+    const int W = K / CWV, ch0 = wave * CWV;
+    float* bias = tqm_smem;                                     // [K] fp32
+    float* red = bias + K;                                      // [2][16 tokens][8 waves]
+    uint8_t* region = reinterpret_cast<uint8_t*>(red + 2 * kTqmTok * kTqmMaxWaves) + wave * S::kRegion;
+    auto wave_sync = [] {
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    };
+
+    // biases of this wave's channels, widened (only this wave reads them); all
+    // loads are issued before the first is used
+    {
+        uint16_t bh[CWV / kWave];
+#pragma unroll
+        for (int i = 0; i < CWV / kWave; ++i) bh[i] = d[ch0 + lane + i * kWave];
+#pragma unroll
+        for (int i = 0; i < CWV / kWave; ++i) bias[ch0 + lane + i * kWave] = h2f(bh[i]);
+    }
+
+    // Block-matrix operands.  Row r of the wave's range is staged as 8 dwords,
+    // dword 2 m + h = (M[r][8 h + m], M[r][8 h + m + 4]) with M[r] the 16 block-
+    // matrix entries of channel r, so lane (t, k) reads its four values
+    // M[16 b + t][k + 4 s], s = 0..3, as dwords 2 k and 2 k + 1 of row 16 b + t.
+    // Task = (row, half); every lane's loads are issued before the first is used.
+    constexpr int TPL = 2 * CWV / kWave;                        // tasks per lane
+    uint16_t v[TPL][8];
+#pragma unroll
+    for (int it = 0; it < TPL; ++it) {
+        const int task = lane + it * kWave, r = task / 2, h = task % 2, ch = ch0 + r;
+        const uint4 w = *reinterpret_cast<const uint4*>(Mb + (size_t)ch * 16 + 8 * h);
+        const uint32_t wd[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[it][i] = (uint16_t)(wd[i / 2] >> (16 * (i % 2)));
+    }
+#pragma unroll
+    for (int it = 0; it < TPL; ++it) {
+        const int task = lane + it * kWave, r = task / 2, h = task % 2;
+#pragma unroll
+        for (int m = 0; m < 4; ++m)
+            *reinterpret_cast<uint32_t*>(region + r * 32 + (2 * m + h) * 4) =
+                (uint32_t)v[it][m] | ((uint32_t)v[it][m + 4] << 16);
+    }
+    wave_sync();
+    uint32_t mp[NG][2];
+#pragma unroll
+    for (int b = 0; b < NG; ++b) {
+        const uint2 w = *reinterpret_cast<const uint2*>(region + (16 * b + il) * 32 + 8 * kl);
+        mp[b][0] = w.x;
+        mp[b][1] = w.y;
+    }
+    wave_sync();   // the region now holds this wave's output tile
+
+    const int ntiles = (M + kTqmTok - 1) / kTqmTok;
+    const __amdgpu_buffer_rsrc_t rz = make_rsrc(Z, (uint32_t)((size_t)M * K * 2));
+    // byte offset of this lane's first 16 bytes of tile n (chunk j adds 64 j); past M reads zero
+    auto tile_base = [&](int n) -> uint32_t {
+        return n < ntiles ? (uint32_t)(((size_t)(n * kTqmTok + il) * K + ch0 + 8 * kl) * 2) : kOOB;
+    };
+    const int m_lo = K - dm - du, u_lo = K - du;
+    const bool gated = state != nullptr && dm + du > 0;
+    // bit b: group b of this wave meets the bands [m_lo, K) (one scalar word,
+    // tested per group, instead of a precomputed condition per group)
+    const int bgate = !gated ? NG : (m_lo <= ch0 ? 0 : ((m_lo - ch0) / 16 < NG ? (m_lo - ch0) / 16 : NG));
+    const uint32_t gmask = __builtin_amdgcn_readfirstlane(bgate >= 32 ? 0u : ~0u << bgate);
+    // States, codes and scales go through range-checked buffer accesses (reads
+    // past the end give 0, writes past it are dropped), so the loop has no
+    // branch around a memory access and the compiler can count the loads in
+    // flight exactly (a guessed count would make it wait for all of them).
+    const __amdgpu_buffer_rsrc_t rS = make_rsrc(state ? (const void*)state : (const void*)Z, state ? (uint32_t)M : 0u);
+    auto state_of = [&](int n) -> int {                         // nonzero: masked
+        return __builtin_amdgcn_raw_buffer_load_b8(rS, n < ntiles ? (uint32_t)(n * kTqmTok + il) : kOOB, 0, 0);
+    };
+    const uint32_t row_bytes = (uint32_t)K * BITS / 8;
+    const __amdgpu_buffer_rsrc_t rA = make_rsrc(Aq, (uint32_t)M * row_bytes);
+    const __amdgpu_buffer_rsrc_t rSo = make_rsrc(s_out, (uint32_t)M * 4);
+    const int rr = lane / 4, pp = lane % 4;                     // coding pass: token rr, runs pp VPL .. pp VPL + VPL - 1
+
+    int n = blockIdx.x;
+    int st_cur = state_of(n);                                   // issued ahead of the ring, as in the loop
+    uint32_t zb = tile_base(n);
+    v4i zr[D];
+#pragma unroll
+    for (int q = 0; q < D; ++q) zr[q] = __builtin_amdgcn_raw_buffer_load_b128(rz, zb + 64 * q, 0, 0);
+    for (int par = 0; n < ntiles; n += gridDim.x, par ^= 1) {
+        const int t0 = n * kTqmTok;
+        const uint32_t zn = tile_base(n + gridDim.x);
+        const int st_next = state_of(n + gridDim.x);            // needed one tile later
+        // the other state's band is dropped: [u_lo, K) for masked tokens, [m_lo, u_lo) otherwise
+        const bool masked = gated && st_cur != 0;
+        int drop_rel = 4 * kl - (masked ? u_lo : m_lo);         // channel gc + q of this lane is gc + q + 4 k
+        const int drop_n = masked ? K - u_lo : u_lo - m_lo;
+        asm volatile("" : "+v"(drop_rel));                      // (kept whole, not folded into per-group constants)
+
+        float amax = 0.0f;
+#pragma unroll
+        for (int j = 0; j < NC; ++j) {
+            const v4i z = zr[j % D];
+            zr[j % D] = j + D < NC ? __builtin_amdgcn_raw_buffer_load_b128(rz, zb + 64 * (j + D), 0, 0)
+                                   : __builtin_amdgcn_raw_buffer_load_b128(rz, zn + 64 * (j + D - NC), 0, 0);
+            // (c, c + 4) pairs of this lane's 8 channels, then across the four rows:
+            // x_p ends as (channel 8 p + k, 8 p + k + 4) of the 32-channel chunk
+            uint32_t x0 = __builtin_amdgcn_perm((uint32_t)z.z, (uint32_t)z.x, 0x05040100u);
+            uint32_t x1 = __builtin_amdgcn_perm((uint32_t)z.z, (uint32_t)z.x, 0x07060302u);
+            uint32_t x2 = __builtin_amdgcn_perm((uint32_t)z.w, (uint32_t)z.y, 0x05040100u);
+            uint32_t x3 = __builtin_amdgcn_perm((uint32_t)z.w, (uint32_t)z.y, 0x07060302u);
+            transpose_rows4(x0, x1, x2, x3);
+            // the chunk's two groups (2 j, 2 j + 1): their MFMA chains interleaved, so
+            // one's latency covers the other's; then the two epilogues
+            const int b0 = 2 * j;
+            asm volatile("" : "+v"(mp[b0][0]), "+v"(mp[b0][1]), "+v"(mp[b0 + 1][0]), "+v"(mp[b0 + 1][1]));
+            f32x4 acc[2] = {{0.0f, 0.0f, 0.0f, 0.0f}, {0.0f, 0.0f, 0.0f, 0.0f}};
+            // (widening the block-matrix operands only here: converted ahead, or
+            // hoisted out of the tile loop, they would double their registers)
+            acc[0] = __builtin_amdgcn_mfma_f32_16x16x4f32(lo_h(mp[b0][0]), lo_h(x0), acc[0], 0, 0, 0);
+            acc[1] = __builtin_amdgcn_mfma_f32_16x16x4f32(lo_h(mp[b0 + 1][0]), lo_h(x2), acc[1], 0, 0, 0);
+            acc[0] = __builtin_amdgcn_mfma_f32_16x16x4f32(hi_h(mp[b0][0]), hi_h(x0), acc[0], 0, 0, 0);
+            acc[1] = __builtin_amdgcn_mfma_f32_16x16x4f32(hi_h(mp[b0 + 1][0]), hi_h(x2), acc[1], 0, 0, 0);
+            acc[0] = __builtin_amdgcn_mfma_f32_16x16x4f32(lo_h(mp[b0][1]), lo_h(x1), acc[0], 0, 0, 0);
+            acc[1] = __builtin_amdgcn_mfma_f32_16x16x4f32(lo_h(mp[b0 + 1][1]), lo_h(x3), acc[1], 0, 0, 0);
+            acc[0] = __builtin_amdgcn_mfma_f32_16x16x4f32(hi_h(mp[b0][1]), hi_h(x1), acc[0], 0, 0, 0);
+            acc[1] = __builtin_amdgcn_mfma_f32_16x16x4f32(hi_h(mp[b0 + 1][1]), hi_h(x3), acc[1], 0, 0, 0);
+#pragma unroll
+            for (int gg = 0; gg < 2; ++gg) {
+                const int b = b0 + gg;
+                // this lane: channels gc + 4 k + v of token t; the gate (exact zeros)
+                // and the maximum act on the fp32 sums, whose fp16 rounding is monotone
+                const int gc = ch0 + 16 * b;
+                const float4 bv = *reinterpret_cast<const float4*>(bias + gc + 4 * kl);
+                float v[4] = {acc[gg][0] + bv.x, acc[gg][1] + bv.y, acc[gg][2] + bv.z, acc[gg][3] + bv.w};
+                if (gmask & (1u << b)) {                        // the group meets a band
+#pragma unroll
+                    for (int q = 0; q < 4; ++q)
+                        v[q] = (unsigned)(drop_rel + (gc + q)) < (unsigned)drop_n ? 0.0f : v[q];
+                }
+                amax = fmaxf(amax, fmaxf(fmaxf(fabsf(v[0]), fabsf(v[1])), fmaxf(fabsf(v[2]), fabsf(v[3]))));
+                uint16_t h[4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) h[q] = f2h(v[q]);
+                *reinterpret_cast<uint2*>(region + il * S::kRS + 2 * (16 * b + 4 * kl)) =
+                    make_uint2((uint32_t)h[0] | ((uint32_t)h[1] << 16), (uint32_t)h[2] | ((uint32_t)h[3] << 16));
+            }
+            // chunk by chunk: a chain of four dependent MFMAs already keeps the matrix
+            // pipe busy, and running further ahead only raises register pressure
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        // the token's maximum over this wave (lanes t, t + 16, t + 32, t + 48), rounded
+        // to fp16 as the values are (rounding is monotone: the max of the rounded values)
+        amax = fmaxf(amax, __shfl_xor(amax, 16, kWave));
+        amax = fmaxf(amax, __shfl_xor(amax, 32, kWave));
+        amax = h2f(f2h(amax));
+        if (kl == 0) red[(par * kTqmTok + il) * kTqmMaxWaves + wave] = amax;
+        ring_barrier();   // every wave's maxima and this wave's output tile are in LDS
+
+        // coding pass: lane -> token rr, runs of 8 channels pp VPL .. pp VPL + VPL - 1 of the wave's range
+        const float4* rp = reinterpret_cast<const float4*>(red + (par * kTqmTok + rr) * kTqmMaxWaves);
+        const float4 r0 = rp[0], r1 = rp[1];
+        const float rv[8] = {r0.x, r0.y, r0.z, r0.w, r1.x, r1.y, r1.z, r1.w};
+        float a = rv[0];
+#pragma unroll
+        for (int w = 1; w < kTqmMaxWaves; ++w) a = w < W ? fmaxf(a, rv[w]) : a;
+        const float s = a / kQmax;
+        const float y = s != 0.0f ? 1.0f / s : 0.0f;   // s = 0: every value is 0 and codes 0
+        if (wave == 0)
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(s), rSo, pp == 0 ? (uint32_t)(t0 + rr) * 4 : kOOB, 0, 0);
+        const uint8_t* src = region + rr * S::kRS + 16 * pp * VPL;
+        const uint32_t dst = (uint32_t)(t0 + rr) * row_bytes + (uint32_t)(ch0 + 8 * pp * VPL) * BITS / 8;
+#pragma unroll
+        for (int i0 = 0; i0 < VPL; i0 += 2) {
+            uint32_t wv[BITS == 4 ? 2 : 4];
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                const v4i hv = *reinterpret_cast<const v4i*>(src + 16 * (i0 + i));
+                const float x[8] = {lo_h(hv.x), hi_h(hv.x), lo_h(hv.y), hi_h(hv.y),
+                                    lo_h(hv.z), hi_h(hv.z), lo_h(hv.w), hi_h(hv.w)};
+                int c[8];
+                quant_codes8<BITS == 4 ? 7 : 127>(x, s, y, c);
+                if (BITS == 4) {
+                    uint32_t w4 = 0;
+#pragma unroll
+                    for (int q = 0; q < 8; ++q) w4 |= (uint32_t)(c[q] & 15) << (4 * q);
+                    wv[i] = w4;
+                } else {
+                    uint32_t lo = 0, hi = 0;
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        lo |= (uint32_t)(c[q] & 255) << (8 * q);
+                        hi |= (uint32_t)(c[4 + q] & 255) << (8 * q);
+                    }
+                    wv[2 * i] = lo, wv[2 * i + 1] = hi;
+                }
+            }
+            if (BITS == 4) {
+                typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+                __builtin_amdgcn_raw_buffer_store_b64(u32x2{wv[0], wv[1]}, rA, dst + 4 * i0, 0, 0);
+            } else {
+                __builtin_amdgcn_raw_buffer_store_b128(u32x4{wv[0], wv[1], wv[2], wv[3]}, rA, dst + 8 * i0, 0, 0);
+            }
+        }
+        wave_sync();   // this wave's tile is rewritten by its next tile
+        zb = zn;
+        st_cur = st_next;
+    }
+}
+
+// The matrix-core form (measured against tac_quant_kernel, interleaved on one
+// box): g = 16 only (at g <= 8 the VALU kernel multiplies g, not 16, values per
+// output and is faster), rows of four to eight 448- or 512-channel parts,
+// operands under 2 GiB, and at least 4096 tokens (256 tiles: one per CU; at
+// 2048 tokens the row-streaming kernel is faster).
+constexpr int kTqmMaxGroups = 256;                  // one workgroup per CU
+constexpr int kTqmMinRows = 4096;
+int tac_quant_mfma_ng(int M, int K, int g) {
+    if (g != 16 || M < kTqmMinRows || (size_t)M * K * 2 > ((size_t)1 << 31)) return 0;
+    if (K % 512 == 0 && K / 512 >= 4 && K / 512 <= kTqmMaxWaves) return 32;
+    if (K % 448 == 0 && K / 448 >= 4 && K / 448 <= kTqmMaxWaves) return 28;
+    return 0;
+}
+
+template <int BITS, int NG>
+hipError_t launch_tqm(int M, const uint16_t* Z, const uint16_t* Mb, const uint16_t* d, const uint8_t* state, int K,
+                      int dm, int du, uint8_t* Aq, float* s, hipStream_t st) {
+    using S = TqmShape<NG>;
+    static std::atomic<int> lds_set[kMaxDevices];   // above the 64 KB default for dynamic LDS
+    const hipError_t attr = allow_dynamic_lds(reinterpret_cast<const void*>(&tac_quant_mfma_kernel<BITS, NG>),
+                                              (int)S::lds_bytes(S::kCWV * kTqmMaxWaves), lds_set);
+    if (attr != hipSuccess) return attr;
+    const int ntiles = (M + kTqmTok - 1) / kTqmTok;
+    const dim3 grid(ntiles < kTqmMaxGroups ? ntiles : kTqmMaxGroups), block(64 * (K / S::kCWV));
+    hipLaunchKernelGGL((tac_quant_mfma_kernel<BITS, NG>), grid, block, S::lds_bytes(K), st, Z, Mb, d, state, M, K, dm,
+                       du, Aq, s);
+    return hipGetLastError();
+}
+
 }  // namespace
 
 bool tac_quant_fusable(int K, int g) { return g <= 16 && K % 16 == 0 && K / 8 <= 64 * kTqMaxConsumerWaves; }
 
 hipError_t launch_tac_quant(const uint16_t* Z, const uint16_t* Mb, const uint16_t* d, const uint8_t* state, int M,
                             int K, int g, int dm, int du, uint8_t* Aq, float* s, hipStream_t st, int bits) {
+    if (const int ng = tac_quant_mfma_ng(M, K, g)) {
+        if (bits == 8)
+            return ng == 32 ? launch_tqm<8, 32>(M, Z, Mb, d, state, K, dm, du, Aq, s, st)
+                            : launch_tqm<8, 28>(M, Z, Mb, d, state, K, dm, du, Aq, s, st);
+        return ng == 32 ? launch_tqm<4, 32>(M, Z, Mb, d, state, K, dm, du, Aq, s, st)
+                        : launch_tqm<4, 28>(M, Z, Mb, d, state, K, dm, du, Aq, s, st);
+    }
     const int cw = (K / 8 + kWave - 1) / kWave;
     const int threads = (cw + 1) * kWave;
     // about two workgroups per CU, each streaming a run of up to 64 rows

@@ -349,7 +349,7 @@ def test_quant_act_with_tac(withP, g):
 
 @pytest.mark.parametrize("g", [1, 2, 4, 8, 16])
 @pytest.mark.parametrize("M,K", [(1, 64), (37, 512), (300, 3584), (129, 4096), (20, 8192), (1025, 1024),
-                                 (2100, 3584), (5000, 4096), (33000, 512)])
+                                 (2100, 3584), (4100, 3584), (5000, 4096), (33000, 512)])
 def test_quant_act_tac_folded_fused(g, M, K):
     """TAC fused with the gate and quantiser (folded basis, g <= 16, K <= 4096; wider
     rows take the staged path): bit-exact with the oracle's TAC-then-quantise.  The
@@ -368,6 +368,24 @@ def test_quant_act_tac_folded_fused(g, M, K):
     rq, rs = O.quant_act(X, None, None, 0, 0, Mb, d, g, threads=THREADS)
     assert_bits(host(s), rs, "s_a (no gate)")
     assert_bits(host(Aq), rq, "Aq (no gate)")
+
+
+@pytest.mark.parametrize("bits", [4, 8])
+@pytest.mark.parametrize("M,K,dm,du", [(4100, 3584, 112, 112), (4100, 3584, 40, 24), (4096, 4096, 1000, 600),
+                                       (8200, 4096, 0, 0), (4111, 2048, 8, 520)])
+def test_quant_act_tac_fused_matrix_cores_bands(bits, M, K, dm, du):
+    """The matrix-core form of the fused TAC pass (g = 16, >= 4096 tokens, rows
+    of four to eight 448- or 512-channel parts): band edges inside a 16-channel
+    block, bands spanning several waves, no band, a ragged last 16-token tile,
+    several tiles per workgroup (8200 tokens), 4- and 8-bit codes."""
+    X, st = _x(M, K, 12)
+    Mb, d = synth.tac_params(K, 16, synth.rng_for(707, K, dm))
+    say(f"quant_act + fused tac (matrix cores) M={M} K={K} bands={dm},{du} bits={bits}")
+    qa, oq = (sq.sgat_quant_act, O.quant_act) if bits == 4 else (sq.sgat_quant_act_w8, O.quant_act_q8)
+    Aq, s = qa(dev(X), dev(st), None, dm, du, dev(Mb), dev(d), 16)
+    rq, rs = oq(X, st, None, dm, du, Mb, d, 16, threads=THREADS)
+    assert_bits(host(s), rs, "s_a")
+    assert_bits(host(Aq), rq, "Aq")
 
 
 # ------------------------------------------------------------------ end to end
@@ -476,7 +494,7 @@ def test_w8_quant_act(withP, g):
     assert_bits(host(Aq), rq, "Aq")
 
 
-@pytest.mark.parametrize("M,K", [(2100, 3584), (17, 4096)])
+@pytest.mark.parametrize("M,K", [(2100, 3584), (17, 4096), (4100, 3584)])
 def test_w8_quant_act_tac_fused(M, K):
     """8-bit codes from the fused TAC pass (g = 16, folded basis) on several
     16-token tiles and a ragged last one."""
