@@ -15,9 +15,11 @@
 // codes are defined by, this one trades that for the matrix cores.
 //
 // The kernel is the GEMM's three-stage direct-to-LDS pipeline on fp16
-// operands: 128 x 128, 64 x 128 or 64 x 64 output tiles, four waves, one
-// v_mfma_f32_16x16x32_f16 per 16 x 16 tile and k step of 32, the gate applied
-// in the epilogue, fp32 out.
+// operands: 128 x 128, 64 x 128 or 64 x 64 output tiles, four waves.  A stage
+// holds one k step of 32 of x and the matching steps of both halves of Ps
+// (hi and lo), so x is fetched and read from LDS once for both: two
+// v_mfma_f32_16x16x32_f16 per 16 x 16 tile and step (hi then lo, into one
+// accumulator), the gate applied in the epilogue, fp32 out.
 #include "tile_common.hpp"
 
 namespace sq {
@@ -54,8 +56,8 @@ __global__ __launch_bounds__(64 * WM * WN) void transform_mfma_kernel(const uint
                                                                      int dm, int du, float* __restrict__ Xp) {
     constexpr int NW = WM * WN;
     constexpr int BM = 16 * WM * TM, BN = 16 * WN * TN;
-    constexpr int AB = BM * kKStep, BB = BN * kKStep;   // bytes of one stage
-    constexpr int SB = AB + BB;
+    constexpr int AB = BM * kKStep, BB = BN * kKStep;   // bytes of one stage: x, then Ps hi, then Ps lo
+    constexpr int SB = AB + 2 * BB;
     constexpr int LA = AB / 1024 / NW, LB = BB / 1024 / NW;
     static_assert(LA * NW * 1024 == AB && LB * NW * 1024 == BB, "stage loads must divide evenly");
     __shared__ __attribute__((aligned(16))) uint8_t sm[3 * SB];
@@ -68,8 +70,8 @@ __global__ __launch_bounds__(64 * WM * WN) void transform_mfma_kernel(const uint
     const int row0 = rt * BM, col0 = ct * BN;
     const uint32_t lda = (uint32_t)K * 2;                // X row bytes
     const uint32_t ldb = (uint32_t)K * 4;                // Ps row bytes (hi then lo)
-    const int nka = (int)(lda / kKStep);                 // k steps over one copy of x
-    const int nk = (int)(ldb / kKStep);                  // k steps in all (x twice)
+    const int nk = (int)(lda / kKStep);                  // k steps (each with both halves of Ps)
+    const uint32_t lo_off = lda;                         // byte offset of the lo half in a Ps row
     const u32x4 rA = sgpr_rsrc(X, (uint32_t)M * lda);
     const u32x4 rB = sgpr_rsrc(Ps, (uint32_t)K * ldb);
     auto swz = [](int r) { return (r >> 1) & 3; };
@@ -90,12 +92,14 @@ __global__ __launch_bounds__(64 * WM * WN) void transform_mfma_kernel(const uint
     auto issue = [&](int kt, int stage) {
         uint8_t* dA = sm + stage * SB;
         uint8_t* dB = dA + AB;
-        const uint32_t ka = (uint32_t)(kt < nka ? kt : kt - nka) * kKStep;   // x is read twice
-        const uint32_t kb = (uint32_t)kt * kKStep;
+        const uint32_t ko = (uint32_t)kt * kKStep;
 #pragma unroll
-        for (int u = 0; u < LA; ++u) dma16(rA, lds_addr(dA + (wave * LA + u) * 1024), oa[u] == kOOB ? kOOB : oa[u] + ka);
+        for (int u = 0; u < LA; ++u) dma16(rA, lds_addr(dA + (wave * LA + u) * 1024), oa[u] == kOOB ? kOOB : oa[u] + ko);
 #pragma unroll
-        for (int u = 0; u < LB; ++u) dma16(rB, lds_addr(dB + (wave * LB + u) * 1024), ob[u] == kOOB ? kOOB : ob[u] + kb);
+        for (int u = 0; u < LB; ++u) {
+            dma16(rB, lds_addr(dB + (wave * LB + u) * 1024), ob[u] == kOOB ? kOOB : ob[u] + ko);
+            dma16(rB, lds_addr(dB + BB + (wave * LB + u) * 1024), ob[u] == kOOB ? kOOB : ob[u] + lo_off + ko);
+        }
     };
 
     v4f acc[TM][TN];
@@ -110,23 +114,28 @@ __global__ __launch_bounds__(64 * WM * WN) void transform_mfma_kernel(const uint
     auto step = [&](int kt, int sc, int sn) {
         asm volatile("" ::: "memory");
         if (kt + 1 < nk)
-            wait_vm<LA + LB>();
+            wait_vm<LA + 2 * LB>();
         else
             wait_vm<0>();
         __builtin_amdgcn_s_barrier();
         asm volatile("" ::: "memory");
         const uint8_t* st = sm + sc * SB;
-        v8h fa[TM], fb[TN];
+        v8h fa[TM], fh[TN], fl[TN];
 #pragma unroll
         for (int i = 0; i < TM; ++i) fa[i] = *reinterpret_cast<const v8h*>(st + offA + i * 16 * kKStep);
 #pragma unroll
-        for (int j = 0; j < TN; ++j) fb[j] = *reinterpret_cast<const v8h*>(st + offB + j * 16 * kKStep);
+        for (int j = 0; j < TN; ++j) {
+            fh[j] = *reinterpret_cast<const v8h*>(st + offB + j * 16 * kKStep);
+            fl[j] = *reinterpret_cast<const v8h*>(st + offB + BB + j * 16 * kKStep);
+        }
         if (kt + 2 < nk) issue(kt + 2, sn);
 #pragma unroll
         for (int i = 0; i < TM; ++i)
 #pragma unroll
-            for (int j = 0; j < TN; ++j)   // basis columns as the row operand: see the epilogue
-                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fb[j], fa[i], acc[i][j], 0, 0, 0);
+            for (int j = 0; j < TN; ++j) {   // basis columns as the row operand: see the epilogue
+                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fh[j], fa[i], acc[i][j], 0, 0, 0);
+                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fl[j], fa[i], acc[i][j], 0, 0, 0);
+            }
     };
     issue(0, 0);
     if (1 < nk) issue(1, 1);
