@@ -582,8 +582,8 @@ __global__ __launch_bounds__(64 * (kTqMaxConsumerWaves + 1)) void tac_quant_kern
 
 // ---------------------------------------------------------------------------
 // The same fused pass on the matrix cores for g = 16, for rows of four to eight
-// parts of 16 NG channels (NG = 28 or 32: hidden sizes 3584 and 4096 take
-// eight waves).  A workgroup walks 16-token tiles; each of its waves owns
+// parts of 16 NG = 512 channels (hidden size 3584 takes seven waves, 4096
+// eight).  A workgroup walks 16-token tiles; each of its waves owns
 // 16 NG consecutive channels of every row.  Per tile a wave:
 //   * takes its z values straight from HBM, 16 bytes per lane (8 channels of
 //     one token), half a tile of loads ahead in a register ring;
@@ -851,16 +851,15 @@ __global__ __launch_bounds__(64 * kTqmMaxWaves) void tac_quant_mfma_kernel(
 
 // The matrix-core form (measured against tac_quant_kernel, interleaved on one
 // box): g = 16 only (at g <= 8 the VALU kernel multiplies g, not 16, values per
-// output and is faster), rows of four to eight 448- or 512-channel parts,
+// output and is faster), rows of four to eight 512-channel parts (hidden sizes
+// 2048 ... 4096, 3584 among them),
 // operands under 2 GiB, and at least 4096 tokens (256 tiles: one per CU; at
 // 2048 tokens the row-streaming kernel is faster).
 constexpr int kTqmMaxGroups = 256;                  // one workgroup per CU
 constexpr int kTqmMinRows = 4096;
-int tac_quant_mfma_ng(int M, int K, int g) {
-    if (g != 16 || M < kTqmMinRows || (size_t)M * K * 2 > ((size_t)1 << 31)) return 0;
-    if (K % 512 == 0 && K / 512 >= 4 && K / 512 <= kTqmMaxWaves) return 32;
-    if (K % 448 == 0 && K / 448 >= 4 && K / 448 <= kTqmMaxWaves) return 28;
-    return 0;
+bool tac_quant_mfma_usable(int M, int K, int g) {
+    return g == 16 && M >= kTqmMinRows && (size_t)M * K * 2 <= ((size_t)1 << 31) && K % 512 == 0 && K / 512 >= 4 &&
+           K / 512 <= kTqmMaxWaves;
 }
 
 template <int BITS, int NG>
@@ -884,13 +883,9 @@ bool tac_quant_fusable(int K, int g) { return g <= 16 && K % 16 == 0 && K / 8 <=
 
 hipError_t launch_tac_quant(const uint16_t* Z, const uint16_t* Mb, const uint16_t* d, const uint8_t* state, int M,
                             int K, int g, int dm, int du, uint8_t* Aq, float* s, hipStream_t st, int bits) {
-    if (const int ng = tac_quant_mfma_ng(M, K, g)) {
-        if (bits == 8)
-            return ng == 32 ? launch_tqm<8, 32>(M, Z, Mb, d, state, K, dm, du, Aq, s, st)
-                            : launch_tqm<8, 28>(M, Z, Mb, d, state, K, dm, du, Aq, s, st);
-        return ng == 32 ? launch_tqm<4, 32>(M, Z, Mb, d, state, K, dm, du, Aq, s, st)
-                        : launch_tqm<4, 28>(M, Z, Mb, d, state, K, dm, du, Aq, s, st);
-    }
+    if (tac_quant_mfma_usable(M, K, g))
+        return bits == 8 ? launch_tqm<8, 32>(M, Z, Mb, d, state, K, dm, du, Aq, s, st)
+                         : launch_tqm<4, 32>(M, Z, Mb, d, state, K, dm, du, Aq, s, st);
     const int cw = (K / 8 + kWave - 1) / kWave;
     const int threads = (cw + 1) * kWave;
     // about two workgroups per CU, each streaming a run of up to 64 rows

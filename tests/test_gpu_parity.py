@@ -375,7 +375,7 @@ def test_quant_act_tac_folded_fused(g, M, K):
                                        (8200, 4096, 0, 0), (4111, 2048, 8, 520)])
 def test_quant_act_tac_fused_matrix_cores_bands(bits, M, K, dm, du):
     """The matrix-core form of the fused TAC pass (g = 16, >= 4096 tokens, rows
-    of four to eight 448- or 512-channel parts): band edges inside a 16-channel
+    of four to eight 512-channel parts): band edges inside a 16-channel
     block, bands spanning several waves, no band, a ragged last 16-token tile,
     several tiles per workgroup (8200 tokens), 4- and 8-bit codes."""
     X, st = _x(M, K, 12)
