@@ -804,9 +804,19 @@ hipError_t launch_short_frag(const Plan& p, const uint8_t* Aq, const float* s_a,
         case 1: return launch_short_frag_tm<1>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, st);
         case 2: return launch_short_frag_tm<2>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, st);
         case 3: return launch_short_frag_tm<3>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, st);
+        case 4: return launch_short_frag_tm<4>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, st);
         default: return hipErrorInvalidConfiguration;
     }
 }
+
+// Fragment-ordered weights at 49 ... 64 tokens: the short-M kernel with four
+// row tiles where it beats the tiled plan (its K split and separate reduction),
+// measured at 64 tokens: layers up to 12288 wide with K <= 4096 (LLaDA QKV 15.9
+// -> 12.8 us, O 10.2 -> 8.5; Dream QKV 10.5 -> 10.0, O 9.8 -> 8.0).  Wider or
+// deeper layers stay tiled (gate+up 17.1 against 19.3 us, down 14.9 against
+// 17.6): there each wave's expansion of four activation fragments per weight
+// fragment costs more than the tiled plan loses.
+bool frag_four_tiles(int M, int N, int K) { return M > 48 && M <= 64 && N <= 12288 && K <= 4096; }
 
 template <int TM, int BITS>
 hipError_t skinny_kw_tm(int kw, const uint8_t* Aq, const float* s_a, const uint8_t* Wq, const float* s_w, int M, int N,
@@ -983,7 +993,8 @@ hipError_t launch_weights_to_frag(const uint8_t* Wq, int N, int K, uint8_t* Wf, 
 
 hipError_t launch_gemm_frag(const uint8_t* Aq, const float* s_a, const uint8_t* Wf, const float* s_w, int M, int N,
                             int K, uint16_t* Y, int32_t* acc, void* ws, hipStream_t st) {
-    if (M <= 16 * kShortMaxTiles) return launch_short_frag(choose_frag_short(M, N, K), Aq, s_a, Wf, s_w, M, N, K, Y, acc, st);
+    if (M <= 16 * kShortMaxTiles || frag_four_tiles(M, N, K))
+        return launch_short_frag(choose_frag_short(M, N, K), Aq, s_a, Wf, s_w, M, N, K, Y, acc, st);
     const Plan p = choose_plan(M, N, K, 4);   // the tiled plans of row-major weights
     int32_t* part = static_cast<int32_t*>(ws);
     hipError_t e;

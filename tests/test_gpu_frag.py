@@ -5,7 +5,7 @@
 * the GEMM on weights the oracle reordered (so independent of the GPU
   converter) gives the oracle's int32 accumulators and fp16 outputs bit for bit;
 * on GPU-converted weights, at every short-M plan (wide, mid-width and narrow
-  layers; activations staged in LDS or read from L2; one to three row tiles),
+  layers; activations staged in LDS or read from L2; one to four row tiles),
   every tiled plan (with and without K splits) and at the largest K with the
   extreme sum 2^23, acc and Y equal the oracle's and w4a4_gemm's."""
 import numpy as np
@@ -55,6 +55,8 @@ SHAPES = [
     (1, 37888, 3584), (32, 37888, 3584), (16, 8192, 2560), (40, 8192, 2560), (32, 12288, 4096),
     (16, 4608, 3584), (48, 4608, 3584), (32, 4096, 4096), (20, 16392, 12288), (32, 8200, 12288),
     (16, 4096, 1024), (32, 4096, 1024),
+    # four row tiles at 49 ... 64 tokens for layers up to 12288 wide with K <= 4096
+    (64, 12288, 4096), (57, 4608, 3584), (64, 4096, 4096), (50, 3584, 3584), (61, 12288, 2048), (64, 1032, 576),
     # tiled plans: 64 x 64 with K splits, 64 x 128, 128 x 128, 256 x 128
     (49, 4104, 4160), (64, 24576, 4096), (300, 1032, 576), (1024, 4096, 4096), (2100, 4104, 3584),
     (4096, 8200, 4160), (513, 4104, 12288), (4096, 4096, 192), (4000, 4000, 4160),
