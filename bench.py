@@ -539,27 +539,35 @@ def llada_blocks(torch, sq, synth, dev, args):
                         "frac": fold["gemm_frac_int8_peak"], "traffic": None, "kernel": "w4a4 gemm (all four sites)"}
     out["folded_P"] = fold
     if not args.no_w8:
+        # int8 weights in fragment order (as the 4-bit ones), 4 rotating sets
         w8 = []
         for d in sites:
             Wq8, s_w8 = sq.sgat_prepare_weights_w8(d["W"], None)
-            w8.append(dict(Wq8=Wq8, s_w8=s_w8, Aq8=torch.empty((M, d["K"]), dtype=torch.int8, device=dev),
+            w8.append(dict(Wf8=sq.weights_to_frag(Wq8), s_w8=s_w8,
+                           Aq8=torch.empty((M, d["K"]), dtype=torch.int8, device=dev),
                            gws8=torch.empty(max(sq.gemm_workspace_bytes(M, d["N"], d["K"], 8), 1), dtype=torch.uint8,
                                             device=dev)))
-        copies = [[(e["Wq8"], e["s_w8"]) for e in w8]] + [[(e["Wq8"].clone(), e["s_w8"].clone()) for e in w8]
+            del Wq8
+        copies = [[(e["Wf8"], e["s_w8"]) for e in w8]] + [[(e["Wf8"].clone(), e["s_w8"].clone()) for e in w8]
                                                           for _ in range(3)]
 
         def step_w8(tm, it):
-            for d, e, (Wq8, s_w8) in zip(sites, w8, copies[it % len(copies)]):
+            for d, e, (Wf8, s_w8) in zip(sites, w8, copies[it % len(copies)]):
                 tm.wrap("q8/" + d["name"], lambda: sq.sgat_quant_act_w8(d["X"], state, None, d["dm"], d["du"],
                                                                        d.get("tac_M"), d.get("tac_d"), d.get("g", 0),
                                                                        Aq=e["Aq8"], s_a=d["s_a"], ws=d["qws"]))
-                tm.wrap("g8/" + d["name"], lambda: sq.w8a8_gemm(e["Aq8"], d["s_a"], Wq8, s_w8, Y=d["Y"], ws=e["gws8"]))
+                tm.wrap("g8/" + d["name"], lambda: sq.w8a8_gemm_frag(e["Aq8"], d["s_a"], Wf8, s_w8, Y=d["Y"],
+                                                                     ws=e["gws8"]))
         ms, timer = run_steps(torch, step_w8, args.steps, args.warmup)
         ops = sum(2.0 * M * d["N"] * d["K"] for d in sites)
         gms = sum(timer.mean("g8/" + d["name"]) for d in sites)
+        per = {d["name"]: {"gemm_us": timer.mean("g8/" + d["name"]) * 1e3,
+                           "frac_int8_peak": 2.0 * M * d["N"] * d["K"] / timer.mean("g8/" + d["name"]) / 1e9
+                           / PEAK_INT8_TOPS} for d in sites}
         out["w8a8_folded_P"] = {"tokens_per_s": M / (ms / 1e3), "ms_per_step": ms, "gemm_tops": ops / gms / 1e9,
                                 "gemm_frac_int8_peak": ops / gms / 1e9 / PEAK_INT8_TOPS,
-                                "quant_act_ms": sum(timer.mean("q8/" + d["name"]) for d in sites)}
+                                "quant_act_ms": sum(timer.mean("q8/" + d["name"]) for d in sites),
+                                "weights": "int8 in fragment order, 4 rotating sets", "per_site": per}
         del w8, copies
     del sites
     torch.cuda.empty_cache()

@@ -267,6 +267,26 @@ int w4a4_gemm_frag(const uint8_t* Aq, const float* s_a, const uint8_t* Wf, const
                    void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * The same for the W8A8 variant (App. D): the int8 weights [N][K] of
+ * sgat_prepare_weights_w8 in fragment order.  A row of K int8 codes is K bytes,
+ * the bytes of 2 K int4 codes, and is reordered exactly as such a row (k steps
+ * of 64 codes here).
+ *   sq_frag_weight_w8_bytes: sq_frag_weight_bytes(N, 2 K) = G ceil(K / 64) 1024;
+ *                            0 for an invalid K (64 <= K <= 65536, K % 64 == 0).
+ *   sq_weights_to_frag_w8:   Wq [N][K] int8 in, Wf [sq_frag_weight_w8_bytes(N, K)]
+ *                            out; sq_weights_to_frag(Wq, N, 2 K, Wf) with the
+ *                            same rules.
+ *   w8a8_gemm_frag:          as w8a8_gemm with Wf in place of Wq: same arguments,
+ *                            rules and workspace (sq_gemm_w8_workspace_bytes);
+ *                            acc and Y equal w8a8_gemm's bit for bit.
+ */
+size_t sq_frag_weight_w8_bytes(int32_t N, int32_t K);
+int sq_weights_to_frag_w8(const int8_t* Wq, int32_t N, int32_t K, uint8_t* Wf, void* stream);
+int w8a8_gemm_frag(const int8_t* Aq, const float* s_a, const uint8_t* Wf, const float* s_w,
+                   int32_t M, int32_t N, int32_t K, uint16_t* Y, int32_t* acc,
+                   void* ws, size_t ws_bytes, void* stream);
+
+/*
  * w4a4_gemm_frag_noalloc -- for callers that cannot allocate device memory
  * (code under HIP graph capture, tight serving loops, harnesses that forbid
  * hipMalloc): w4a4_gemm_frag without the workspace argument.  Same arguments

@@ -17,6 +17,11 @@ in the order the GEMM reads them.  This module defines that order:
   64 t + 16 j .. 64 t + 16 j + 15 of row 16 g + r (j = 0..3, r = 0..15).
 
 ``gemm`` is then by definition the int4 GEMM of the weights this layout holds.
+
+The W8A8 variant (App. D) keeps one signed byte per code, rows of K bytes.  Its
+layout is the one above applied to those bytes, a row of K int8 codes being
+stored exactly as a packed row of 2 K int4 codes (so a k step holds 64 int8
+codes); ``gemm_q8`` is the int8 GEMM of the weights it holds.
 """
 from __future__ import annotations
 
@@ -68,3 +73,16 @@ def gemm(Aq, s_a, Wf, s_w, N: int, K: int, threads: int = 1):
     """Eq. 13 / Eq. 5 with fragment-ordered weights: the int4 GEMM of the
     weights they hold."""
     return O.gemm(Aq, s_a, from_frag(Wf, N, K).astype(np.uint8), s_w, threads=threads)
+
+
+def to_frag_q8(Wq: np.ndarray, K: int) -> np.ndarray:
+    """int8 weights [N][K] -> the fragment order of their bytes, [ceil(K/64)][G][1024] uint8."""
+    Wq = np.ascontiguousarray(Wq, dtype=np.int8)
+    assert Wq.shape[1] == K
+    return to_frag(Wq.view(np.uint8), 2 * K)
+
+
+def gemm_q8(Aq, s_a, Wf, s_w, N: int, K: int, threads: int = 1):
+    """App. D's int8 GEMM with fragment-ordered weights: the int8 GEMM of the
+    weights they hold."""
+    return O.gemm_q8(Aq, s_a, from_frag(Wf, N, 2 * K).view(np.int8), s_w, threads=threads)

@@ -25,7 +25,7 @@ __all__ = ["sgat_prepare_weights", "sgat_transform", "sgat_quantize", "sgat_quan
            "sgat_prepare_weights_w8", "sgat_quantize_w8", "sgat_quant_act_w8", "w8a8_gemm",
            "tac_calibrate", "tac_calibrate_workspace_bytes", "sgat_split_basis", "sgat_transform_fast",
            "fp6_row_bytes", "codes_to_fp6", "w4a4_gemm_fp6",
-           "frag_weight_bytes", "weights_to_frag", "w4a4_gemm_frag"]
+           "frag_weight_bytes", "weights_to_frag", "w4a4_gemm_frag", "w8a8_gemm_frag"]
 
 
 def _on_stream(fn):
@@ -276,39 +276,52 @@ def w4a4_gemm_fp6(A6: torch.Tensor, s_a: torch.Tensor, W6: torch.Tensor, s_w: to
     return (Y, acc) if want_acc else Y
 
 
-def frag_weight_bytes(N: int, K: int) -> int:
-    """Bytes of the fragment-ordered weights of an N x K int4 matrix (1 KB per
-    16 rows and k step of 128 codes)."""
-    n = int(lib().sq_frag_weight_bytes(N, K))
+def frag_weight_bytes(N: int, K: int, bits: int = 4) -> int:
+    """Bytes of the fragment-ordered weights of an N x K code matrix (1 KB per
+    16 rows and k step of 64 bytes: 128 int4 or 64 int8 codes)."""
+    n = int(lib().sq_frag_weight_w8_bytes(N, K) if bits == 8 else lib().sq_frag_weight_bytes(N, K))
     if n == 0 and N > 0:
-        raise ValueError(f"K={K}: need 64 <= K <= 131072 and K % 64 == 0")
+        kmax = 65536 if bits == 8 else 131072
+        raise ValueError(f"K={K}: need 64 <= K <= {kmax} and K % 64 == 0")
     return n
+
+
+def _frag_shape(N: int, K: int, bits: int):
+    step = 64 if bits == 8 else 128
+    return ((K + step - 1) // step, (N + 15) // 16, 1024)
 
 
 @_on_stream
 def weights_to_frag(Wq: torch.Tensor, *, out=None, stream=None):
-    """Packed int4 weights [N, K/2] -> fragment order [ceil(K/128), ceil(N/16), 1024] (uint8)."""
-    N, Kh = Wq.shape
-    K = 2 * Kh
-    _need(Wq, "Wq", torch.uint8)
-    shape = ((K + 127) // 128, (N + 15) // 16, 1024)
-    frag_weight_bytes(N, K)
+    """Code matrix -> fragment order [k steps, ceil(N/16), 1024] (uint8): packed
+    int4 weights [N, K/2] (uint8, 128 codes a k step) or int8 weights [N, K]
+    (int8, 64 codes a k step)."""
+    N, Kc = Wq.shape
+    bits = 8 if Wq.dtype == torch.int8 else 4
+    K = Kc if bits == 8 else 2 * Kc
+    _need(Wq, "Wq", torch.int8 if bits == 8 else torch.uint8)
+    shape = _frag_shape(N, K, bits)
+    frag_weight_bytes(N, K, bits)
     if out is None:
         out = torch.empty(shape, dtype=torch.uint8, device=Wq.device)
     _need(out, "out", torch.uint8, shape)
-    check(lib().sq_weights_to_frag(_ptr(Wq), N, K, _ptr(out), _stream(stream)))
+    f = lib().sq_weights_to_frag_w8 if bits == 8 else lib().sq_weights_to_frag
+    check(f(_ptr(Wq), N, K, _ptr(out), _stream(stream)))
     return out
 
 
 @_on_stream
 def w4a4_gemm_frag(Aq: torch.Tensor, s_a: torch.Tensor, Wf: torch.Tensor, s_w: torch.Tensor, *, Y=None, acc=None,
-                   want_Y: bool = True, want_acc: bool = False, ws=None, stream=None):
+                   want_Y: bool = True, want_acc: bool = False, ws=None, stream=None, bits: int = 4):
     """w4a4_gemm (Eq. 13) with the weights in fragment order (weights_to_frag);
-    N is s_w's length.  Bit-identical to w4a4_gemm.  Returns Y, or (Y, acc)."""
+    N is s_w's length.  Bit-identical to w4a4_gemm.  bits=8 takes int8
+    activation codes and the fragment order of int8 weights (App. D),
+    bit-identical to w8a8_gemm.  Returns Y, or (Y, acc)."""
     M, Kc = Aq.shape
-    N, K = s_w.shape[0], 2 * Kc
-    _need(Aq, "Aq", torch.uint8)
-    _need(Wf, "Wf", torch.uint8, ((K + 127) // 128, (N + 15) // 16, 1024))
+    N = s_w.shape[0]
+    K = Kc if bits == 8 else 2 * Kc
+    _need(Aq, "Aq", torch.int8 if bits == 8 else torch.uint8)
+    _need(Wf, "Wf", torch.uint8, _frag_shape(N, K, bits))
     _need(s_a, "s_a", torch.float32, (M,))
     _need(s_w, "s_w", torch.float32, (N,))
     if Y is None and want_Y:
@@ -317,10 +330,14 @@ def w4a4_gemm_frag(Aq: torch.Tensor, s_a: torch.Tensor, Wf: torch.Tensor, s_w: t
         acc = torch.empty((M, N), dtype=torch.int32, device=Aq.device)
     _need(Y, "Y", torch.float16, (M, N), optional=True)
     _need(acc, "acc", torch.int32, (M, N), optional=True)
-    ws, wsb = _ws(gemm_workspace_bytes(M, N, K), ws, Aq.device)
-    check(lib().w4a4_gemm_frag(_ptr(Aq), _ptr(s_a), _ptr(Wf), _ptr(s_w), M, N, K, _ptr(Y), _ptr(acc), _ptr(ws), wsb,
-                               _stream(stream)))
+    ws, wsb = _ws(gemm_workspace_bytes(M, N, K, bits), ws, Aq.device)
+    f = lib().w8a8_gemm_frag if bits == 8 else lib().w4a4_gemm_frag
+    check(f(_ptr(Aq), _ptr(s_a), _ptr(Wf), _ptr(s_w), M, N, K, _ptr(Y), _ptr(acc), _ptr(ws), wsb, _stream(stream)))
     return (Y, acc) if want_acc else Y
+
+
+def w8a8_gemm_frag(Aq, s_a, Wf, s_w, **kw):
+    return w4a4_gemm_frag(Aq, s_a, Wf, s_w, bits=8, **kw)
 
 
 @_on_stream

@@ -39,6 +39,9 @@ SIGNATURES = {
     "sq_weights_to_frag": (ctypes.c_int, [_p, _i32, _i32, _p, _p]),
     "w4a4_gemm_frag": (ctypes.c_int, [_p, _p, _p, _p, _i32, _i32, _i32, _p, _p, _p, _sz, _p]),
     "w4a4_gemm_frag_noalloc": (ctypes.c_int, [_p, _p, _p, _p, _i32, _i32, _i32, _p, _p, _p]),
+    "sq_frag_weight_w8_bytes": (_sz, [_i32, _i32]),
+    "sq_weights_to_frag_w8": (ctypes.c_int, [_p, _i32, _i32, _p, _p]),
+    "w8a8_gemm_frag": (ctypes.c_int, [_p, _p, _p, _p, _i32, _i32, _i32, _p, _p, _p, _sz, _p]),
     "sq_tac_calibrate_workspace_bytes": (_sz, [_i32, _i32, _i32]),
     "tac_calibrate": (ctypes.c_int, [_p, _p, _i32, _i32, _i32, ctypes.c_double, ctypes.c_double, ctypes.c_double,
                                      ctypes.c_double, _p, _p, _p, _p, _p, _sz, _p]),

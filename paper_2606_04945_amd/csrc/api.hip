@@ -219,13 +219,15 @@ int gemm(const uint8_t* Aq, const float* s_a, const uint8_t* Wq, const float* s_
 // Shared argument checks of the fragment-ordered GEMM entry points; *done is
 // set when there is nothing to compute (M == 0 or N == 0).
 int check_gemm_frag(const uint8_t* Aq, const float* s_a, const uint8_t* Wf, const float* s_w, int32_t M, int32_t N,
-                    int32_t K, uint16_t* Y, int32_t* acc, const char* name, int* done) {
+                    int32_t K, uint16_t* Y, int32_t* acc, int bits, const char* name, int* done) {
     SQ_TRY(check_K(K));
+    SQ_REQUIRE(bits == 4 || K <= 65536, SQ_ERR_SHAPE, "%s: K=%d: 8-bit codes need K <= 65536", name, K);
     SQ_REQUIRE(M >= 0 && N >= 0, SQ_ERR_SHAPE, "M=%d N=%d: need >= 0", M, N);
     SQ_REQUIRE(M <= kMaxTiledRows, SQ_ERR_SHAPE, "%s: M=%d: at most %d rows per call", name, M, kMaxTiledRows);
     SQ_REQUIRE(N % 8 == 0, SQ_ERR_SHAPE, "N=%d: need N %% 8 == 0", N);
-    SQ_REQUIRE((size_t)M * K / 2 < (1u << 31) && sq::frag_weight_bytes(N, K) < (1u << 31), SQ_ERR_SHAPE,
-               "%s: each operand must be under 2 GiB (M=%d N=%d K=%d)", name, M, N, K);
+    // the fragment layout counts a row in int4 codes: an 8-bit row of K bytes is 2 K of them
+    SQ_REQUIRE((size_t)M * K * bits / 8 < (1u << 31) && sq::frag_weight_bytes(N, K * bits / 4) < (1u << 31),
+               SQ_ERR_SHAPE, "%s: each operand must be under 2 GiB (M=%d N=%d K=%d)", name, M, N, K);
     *done = M == 0 || N == 0;
     if (*done) return SQ_OK;
     SQ_REQUIRE(Aq && s_a && Wf && s_w && (Y || acc), SQ_ERR_NULL,
@@ -407,20 +409,48 @@ int sq_weights_to_frag(const uint8_t* Wq, int32_t N, int32_t K, uint8_t* Wf, voi
 int w4a4_gemm_frag(const uint8_t* Aq, const float* s_a, const uint8_t* Wf, const float* s_w, int32_t M, int32_t N,
                    int32_t K, uint16_t* Y, int32_t* acc, void* ws, size_t ws_bytes, void* stream) {
     int done = 0;
-    SQ_TRY(check_gemm_frag(Aq, s_a, Wf, s_w, M, N, K, Y, acc, "w4a4_gemm_frag", &done));
+    SQ_TRY(check_gemm_frag(Aq, s_a, Wf, s_w, M, N, K, Y, acc, 4, "w4a4_gemm_frag", &done));
     if (done) return SQ_OK;
     SQ_REQUIRE(aligned16(ws), SQ_ERR_ALIGN, "w4a4_gemm_frag: pointers must be 16-byte aligned");
     const size_t need = sq_gemm_workspace_bytes(M, N, K);
     SQ_REQUIRE(ws_bytes >= need && (need == 0 || ws), SQ_ERR_WORKSPACE, "w4a4_gemm_frag: workspace %zu B < %zu B",
                ws_bytes, need);
     return hip_status(
-        sq::launch_gemm_frag(Aq, s_a, Wf, s_w, M, N, K, Y, acc, ws, static_cast<hipStream_t>(stream)), "gemm_frag");
+        sq::launch_gemm_frag(Aq, s_a, Wf, s_w, M, N, K, Y, acc, ws, static_cast<hipStream_t>(stream), 4),
+        "gemm_frag");
+}
+
+size_t sq_frag_weight_w8_bytes(int32_t N, int32_t K) {
+    if (K < 64 || K > 65536 || K % 64) return 0;
+    return sq_frag_weight_bytes(N, 2 * K);
+}
+
+int sq_weights_to_frag_w8(const int8_t* Wq, int32_t N, int32_t K, uint8_t* Wf, void* stream) {
+    SQ_REQUIRE(K <= 65536, SQ_ERR_SHAPE, "sq_weights_to_frag_w8: K=%d: 8-bit codes need K <= 65536", K);
+    SQ_TRY(check_K(K));
+    // a row of K int8 codes is reordered as a row of 2 K int4 codes: the same K bytes
+    return sq_weights_to_frag(reinterpret_cast<const uint8_t*>(Wq), N, 2 * K, Wf, stream);
+}
+
+int w8a8_gemm_frag(const int8_t* Aq, const float* s_a, const uint8_t* Wf, const float* s_w, int32_t M, int32_t N,
+                   int32_t K, uint16_t* Y, int32_t* acc, void* ws, size_t ws_bytes, void* stream) {
+    int done = 0;
+    const uint8_t* A8 = reinterpret_cast<const uint8_t*>(Aq);
+    SQ_TRY(check_gemm_frag(A8, s_a, Wf, s_w, M, N, K, Y, acc, 8, "w8a8_gemm_frag", &done));
+    if (done) return SQ_OK;
+    SQ_REQUIRE(aligned16(ws), SQ_ERR_ALIGN, "w8a8_gemm_frag: pointers must be 16-byte aligned");
+    const size_t need = sq_gemm_w8_workspace_bytes(M, N, K);
+    SQ_REQUIRE(ws_bytes >= need && (need == 0 || ws), SQ_ERR_WORKSPACE, "w8a8_gemm_frag: workspace %zu B < %zu B",
+               ws_bytes, need);
+    return hip_status(
+        sq::launch_gemm_frag(A8, s_a, Wf, s_w, M, N, K, Y, acc, ws, static_cast<hipStream_t>(stream), 8),
+        "gemm_frag_w8");
 }
 
 int w4a4_gemm_frag_noalloc(const uint8_t* Aq, const float* s_a, const uint8_t* Wf, const float* s_w, int32_t M,
                            int32_t N, int32_t K, uint16_t* Y, int32_t* acc, void* stream) {
     int done = 0;
-    SQ_TRY(check_gemm_frag(Aq, s_a, Wf, s_w, M, N, K, Y, acc, "w4a4_gemm_frag_noalloc", &done));
+    SQ_TRY(check_gemm_frag(Aq, s_a, Wf, s_w, M, N, K, Y, acc, 4, "w4a4_gemm_frag_noalloc", &done));
     if (done) return SQ_OK;
     const size_t need = sq_gemm_workspace_bytes(M, N, K);
     SQ_REQUIRE(need <= kNoallocScratchBytes, SQ_ERR_WORKSPACE,
@@ -429,7 +459,7 @@ int w4a4_gemm_frag_noalloc(const uint8_t* Aq, const float* s_a, const uint8_t* W
     void* ws = nullptr;
     if (need > 0) SQ_TRY(scratch_for(stream, &ws));
     return hip_status(
-        sq::launch_gemm_frag(Aq, s_a, Wf, s_w, M, N, K, Y, acc, ws, static_cast<hipStream_t>(stream)),
+        sq::launch_gemm_frag(Aq, s_a, Wf, s_w, M, N, K, Y, acc, ws, static_cast<hipStream_t>(stream), 4),
         "gemm_frag_noalloc");
 }
 

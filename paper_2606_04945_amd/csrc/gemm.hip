@@ -519,7 +519,7 @@ __global__ __launch_bounds__(64 * kSharedMaxWaves) void gemm_skinny_shared_kerne
 constexpr int kFragNT = 2;                             // buffer-load cache policy: non-temporal
 constexpr size_t kFragMaxLds = 160 * 1024;
 
-template <int TM, int KW, bool ALDS, int U, int D>
+template <int TM, int KW, bool ALDS, int U, int D, int BITS = 4>
 __global__ __launch_bounds__(ALDS ? 1024 : 512) void gemm_short_frag_kernel(
     const uint8_t* __restrict__ Aq, const float* __restrict__ s_a, const uint8_t* __restrict__ Wf,
     const float* __restrict__ s_w, int M, int N, int K, uint16_t* __restrict__ Y, int32_t* __restrict__ acc_out) {
@@ -531,7 +531,7 @@ __global__ __launch_bounds__(ALDS ? 1024 : 512) void gemm_short_frag_kernel(
     const int ngrp = (N + 15) / 16;
     const int grp = blockIdx.x * CG + cgi;
     const int col = grp * 16 + lr;
-    const uint32_t ldb = (uint32_t)K / 2;
+    const uint32_t ldb = (uint32_t)K * BITS / 8;
     const int nk = (int)((ldb + kKB - 1) / kKB);
     const int nb = (nk + U - 1) / U;
     const uint32_t seg = 16 * lg;
@@ -593,11 +593,11 @@ __global__ __launch_bounds__(ALDS ? 1024 : 512) void gemm_short_frag_kernel(
             for (int i = 0; i < TM; ++i)
                 ar[i] = ALDS ? *reinterpret_cast<const v4i*>(raw + (i * nk + kt) * 1024 + lane * 16) : ab[u][i];
 #pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                const v4i wop = operand<4>(wb[u], h);
+            for (int h = 0; h < (BITS == 4 ? 2 : 1); ++h) {
+                const v4i wop = operand<BITS>(wb[u], h);
 #pragma unroll
                 for (int i = 0; i < TM; ++i)
-                    acc[i] = __builtin_amdgcn_mfma_i32_16x16x64_i8(operand<4>(ar[i], h), wop, acc[i], 0, 0, 0);
+                    acc[i] = __builtin_amdgcn_mfma_i32_16x16x64_i8(operand<BITS>(ar[i], h), wop, acc[i], 0, 0, 0);
             }
         }
     };
@@ -625,7 +625,7 @@ __global__ __launch_bounds__(ALDS ? 1024 : 512) void gemm_short_frag_kernel(
             for (int i = 0; i < TM; ++i) acc[i] += red[((r * CG + cgi) * TM + i) * kWave + lane];
     }
 #pragma unroll
-    for (int i = 0; i < TM; ++i) skinny_store<4>(acc[i], 16 * i, lg, col, M, N, sav[i], swv, Y, acc_out);
+    for (int i = 0; i < TM; ++i) skinny_store<BITS>(acc[i], 16 * i, lg, col, M, N, sav[i], swv, Y, acc_out);
 }
 
 // Packed int4 weights [N][K/2] -> fragment order: one thread per 16-byte unit
@@ -663,7 +663,8 @@ __global__ __launch_bounds__(256) void splitk_epilogue(const int32_t* __restrict
 
 // A launch plan: tile shape and K split.
 struct Plan {
-    int cfg;       // 0: 256 x 128, 1: 128 x 128, 2: 64 x 64, 4: 64 x 128, 3: short M, K split in the
+    int cfg;       // 0: 256 x 128, 1: 128 x 128, 2: 64 x 64, 4: 64 x 128, 7: 128 x 256 (8-bit), 8: 128 x 128
+                   // in two waves of 128 x 64 (8-bit), 3: short M, K split in the
                    // workgroup, 5: short M, activations shared in LDS (see launch_gemm), 6: short M on
                    // fragment-ordered weights (see launch_gemm_frag)
     int bm, bn;
@@ -758,55 +759,64 @@ size_t frag_lds_bytes(int tm, int nk, int kw, int cg, bool alds) {
     return (alds ? (size_t)tm * nk * 1024 : 0) + (kw > 1 ? (size_t)(kw - 1) * cg * tm * 1024 : 0);
 }
 
-template <int TM, int KW, bool ALDS, int U, int D>
+template <int TM, int KW, bool ALDS, int U, int D, int BITS>
 hipError_t launch_short_frag_t(const Plan& p, const uint8_t* Aq, const float* s_a, const uint8_t* Wf,
                                const float* s_w, int M, int N, int K, uint16_t* Y, int32_t* acc, hipStream_t st) {
-    const int nk = (K / 2 + kKB - 1) / kKB;
+    const int nk = (K * BITS / 8 + kKB - 1) / kKB;
     const size_t lds = frag_lds_bytes(TM, nk, KW, p.waves, ALDS);
     static std::atomic<int> lds_set[kMaxDevices];   // above the 64 KB default for dynamic LDS
     const hipError_t attr = allow_dynamic_lds(
-        reinterpret_cast<const void*>(&gemm_short_frag_kernel<TM, KW, ALDS, U, D>), (int)kFragMaxLds, lds_set);
+        reinterpret_cast<const void*>(&gemm_short_frag_kernel<TM, KW, ALDS, U, D, BITS>), (int)kFragMaxLds, lds_set);
     if (attr != hipSuccess) return attr;
     if (lds > kFragMaxLds || p.waves < 1 || p.waves * KW > (ALDS ? 16 : 8)) return hipErrorInvalidConfiguration;
     const int groups = (N + 15) / 16;
-    hipLaunchKernelGGL((gemm_short_frag_kernel<TM, KW, ALDS, U, D>), dim3((groups + p.waves - 1) / p.waves),
+    hipLaunchKernelGGL((gemm_short_frag_kernel<TM, KW, ALDS, U, D, BITS>), dim3((groups + p.waves - 1) / p.waves),
                        dim3(64 * p.waves * KW), lds, st, Aq, s_a, Wf, s_w, M, N, K, Y, acc);
     return hipGetLastError();
 }
 
 // The (waves per group, activation staging, batch, ring) combinations the plan uses.
-template <int TM>
+template <int TM, int BITS>
 hipError_t launch_short_frag_tm(const Plan& p, const uint8_t* Aq, const float* s_a, const uint8_t* Wf,
                                 const float* s_w, int M, int N, int K, uint16_t* Y, int32_t* acc, hipStream_t st) {
     if (p.alds) {
         if (p.d != 4) return hipErrorInvalidConfiguration;
         switch (p.kw * 4 + p.u) {
-            case 5: return launch_short_frag_t<TM, 1, true, 1, 4>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, st);
-            case 6: return launch_short_frag_t<TM, 1, true, 2, 4>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, st);
-            case 9: return launch_short_frag_t<TM, 2, true, 1, 4>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, st);
-            case 10: return launch_short_frag_t<TM, 2, true, 2, 4>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, st);
+            case 5: return launch_short_frag_t<TM, 1, true, 1, 4, BITS>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, st);
+            case 6: return launch_short_frag_t<TM, 1, true, 2, 4, BITS>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, st);
+            case 9: return launch_short_frag_t<TM, 2, true, 1, 4, BITS>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, st);
+            case 10: return launch_short_frag_t<TM, 2, true, 2, 4, BITS>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, st);
             default: return hipErrorInvalidConfiguration;
         }
     }
     if (p.u != 2) return hipErrorInvalidConfiguration;
     switch (p.kw * 8 + p.d) {
-        case 12: return launch_short_frag_t<TM, 1, false, 2, 4>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, st);
-        case 20: return launch_short_frag_t<TM, 2, false, 2, 4>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, st);
-        case 34: return launch_short_frag_t<TM, 4, false, 2, 2>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, st);
-        case 36: return launch_short_frag_t<TM, 4, false, 2, 4>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, st);
+        case 12: return launch_short_frag_t<TM, 1, false, 2, 4, BITS>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, st);
+        case 20: return launch_short_frag_t<TM, 2, false, 2, 4, BITS>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, st);
+        case 34: return launch_short_frag_t<TM, 4, false, 2, 2, BITS>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, st);
+        case 36: return launch_short_frag_t<TM, 4, false, 2, 4, BITS>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, st);
+        default: return hipErrorInvalidConfiguration;
+    }
+}
+
+template <int BITS>
+hipError_t launch_short_frag_bits(const Plan& p, const uint8_t* Aq, const float* s_a, const uint8_t* Wf,
+                                  const float* s_w, int M, int N, int K, uint16_t* Y, int32_t* acc, hipStream_t st) {
+    switch ((M + 15) / 16) {
+        case 1: return launch_short_frag_tm<1, BITS>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, st);
+        case 2: return launch_short_frag_tm<2, BITS>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, st);
+        case 3: return launch_short_frag_tm<3, BITS>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, st);
+        case 4:   // four row tiles only for 4-bit codes (frag_four_tiles)
+            if constexpr (BITS == 4) return launch_short_frag_tm<4, BITS>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, st);
+            return hipErrorInvalidConfiguration;
         default: return hipErrorInvalidConfiguration;
     }
 }
 
 hipError_t launch_short_frag(const Plan& p, const uint8_t* Aq, const float* s_a, const uint8_t* Wf, const float* s_w,
-                             int M, int N, int K, uint16_t* Y, int32_t* acc, hipStream_t st) {
-    switch ((M + 15) / 16) {
-        case 1: return launch_short_frag_tm<1>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, st);
-        case 2: return launch_short_frag_tm<2>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, st);
-        case 3: return launch_short_frag_tm<3>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, st);
-        case 4: return launch_short_frag_tm<4>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, st);
-        default: return hipErrorInvalidConfiguration;
-    }
+                             int M, int N, int K, uint16_t* Y, int32_t* acc, hipStream_t st, int bits) {
+    return bits == 8 ? launch_short_frag_bits<8>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, st)
+                     : launch_short_frag_bits<4>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, st);
 }
 
 // Fragment-ordered weights at 49 ... 64 tokens: the short-M kernel with four
@@ -859,8 +869,14 @@ hipError_t finish_split(const Plan& p, int32_t* part, const float* s_a, const fl
 //    for wide 4-bit layers, K split inside the workgroup otherwise);
 //  - 4-bit codes with at least 448 tiles of 256 x 128 or of 128 x 128:
 //    256 x 128 (eight waves of 64 x 64) at 448 ... 512 tiles of it, else
-//    128 x 128 (four waves of 64 x 64) (see below); 8-bit codes: 256 x 128
-//    from 512 of its tiles, else 128 x 128 from 192 of its tiles;
+//    128 x 128 (four waves of 64 x 64) (see below);
+//  - 8-bit codes (one MFMA per 64-byte k step, so operand reads from LDS weigh
+//    twice as much per MFMA as for 4-bit codes): larger wave tiles.  128 x 256
+//    (four waves of 64 x 128, two workgroups per CU; each wave reads 12
+//    fragments per 32 MFMAs where 64 x 64 reads 8 per 16) from 512 of its
+//    tiles; else 128 x 128 in two waves of 128 x 64 from 640 of its tiles
+//    (three workgroups per CU fill the chip at 768); else 128 x 256 from 192
+//    of its tiles; else 128 x 128 (four waves) from 192 of its tiles;
 //  - at least 512 tiles of 64 x 128: 64 x 128 (four waves of 64 x 32);
 //  - otherwise 64 x 64 (four waves of 32 x 32), with K split below 256 tiles
 //    (twice as deep for K >= 8192) and kept at 8 k steps or more per split.
@@ -906,14 +922,22 @@ Plan choose_plan(int M, int N, int K, int bits) {
         const bool big = tiles(256, 128) >= 448 && tiles(256, 128) <= 512;
         p = make_plan(M, N, K, big ? 256 : 128, 128, 1, bits);
         p.cfg = big ? 0 : 1;
-    } else if (bits == 8 && tiles(256, 128) >= 512) {
-        // 8-bit codes (graph-replayed timings of the LLaDA-shaped layers at 256,
-        // 1024 and 4096 tokens): 256 x 128 from 512 of its tiles (4096 tokens:
-        // 0.37-0.40 of int8 peak against 0.31-0.33 for 128 x 128), 128 x 128
-        // from 192 of its tiles (1024 tokens: QKV, O and down 4-21 % faster
-        // than 64 x 128 or 256 x 128)
-        p = make_plan(M, N, K, 256, 128, 1, bits);
-        p.cfg = 0;
+    } else if (bits == 8 && tiles(128, 256) >= 512) {
+        // 8-bit codes, from timings with rotating weights of the LLaDA-shaped
+        // layers at 128 ... 4096 tokens: 128 x 256 from 512 of its tiles 2-14 %
+        // faster than 256 x 128 in eight waves; 768 tiles of 128 x 128 in two
+        // waves (512 x 24576, 1024 x 12288) 12-15 % faster than four waves or
+        // 128 x 256; 128 x 256 at 192 ... 511 of its tiles 9-16 % faster than
+        // 128 x 128; below that 128 x 128 in four waves (1024 tokens of the
+        // 4096-wide layers: 11-39 % faster than the larger tiles)
+        p = make_plan(M, N, K, 128, 256, 1, bits);
+        p.cfg = 7;
+    } else if (bits == 8 && tiles(128, 128) >= 640) {
+        p = make_plan(M, N, K, 128, 128, 1, bits);
+        p.cfg = 8;
+    } else if (bits == 8 && tiles(128, 256) >= 192) {
+        p = make_plan(M, N, K, 128, 256, 1, bits);
+        p.cfg = 7;
     } else if (bits == 8 && tiles(128, 128) >= 192) {
         p = make_plan(M, N, K, 128, 128, 1, bits);
         p.cfg = 1;
@@ -940,10 +964,10 @@ Plan choose_plan(int M, int N, int K, int bits) {
 // batches from 17 tokens on.  Batches of two k steps, or of one where that
 // leaves fewer zero-weight k steps in the last pass of the ring.  At least two
 // batches per wave.
-Plan choose_frag_short(int M, int N, int K) {
-    const int nk = (K / 2 + kKB - 1) / kKB, nb = (nk + 1) / 2;
+Plan choose_frag_short(int M, int N, int K, int bits) {
+    const int nk = (K * bits / 8 + kKB - 1) / kKB, nb = (nk + 1) / 2;
     const int groups = (N + 15) / 16, tm = (M + 15) / 16;
-    Plan p = make_plan(M, N, K, 16 * tm, 16, 1, 4);
+    Plan p = make_plan(M, N, K, 16 * tm, 16, 1, bits);
     p.cfg = 6;
     int kw, cg;
     bool alds;
@@ -992,17 +1016,27 @@ hipError_t launch_weights_to_frag(const uint8_t* Wq, int N, int K, uint8_t* Wf, 
 }
 
 hipError_t launch_gemm_frag(const uint8_t* Aq, const float* s_a, const uint8_t* Wf, const float* s_w, int M, int N,
-                            int K, uint16_t* Y, int32_t* acc, void* ws, hipStream_t st) {
-    if (M <= 16 * kShortMaxTiles || frag_four_tiles(M, N, K))
-        return launch_short_frag(choose_frag_short(M, N, K), Aq, s_a, Wf, s_w, M, N, K, Y, acc, st);
-    const Plan p = choose_plan(M, N, K, 4);   // the tiled plans of row-major weights
+                            int K, uint16_t* Y, int32_t* acc, void* ws, hipStream_t st, int bits) {
+    if (M <= 16 * kShortMaxTiles || (bits == 4 && frag_four_tiles(M, N, K)))
+        return launch_short_frag(choose_frag_short(M, N, K, bits), Aq, s_a, Wf, s_w, M, N, K, Y, acc, st, bits);
+    const Plan p = choose_plan(M, N, K, bits);   // the tiled plans of row-major weights
     int32_t* part = static_cast<int32_t*>(ws);
     hipError_t e;
-    switch (p.cfg) {
-        case 0: e = launch_tiled<4, 2, 4, 4, 4, 2, true>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, part, st); break;
-        case 1: e = launch_tiled<2, 2, 4, 4, 4, 3, true>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, part, st); break;
-        case 2: e = launch_tiled<2, 2, 2, 2, 4, 4, true>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, part, st); break;
-        default: e = launch_tiled<1, 4, 4, 2, 4, 4, true>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, part, st); break;
+    if (bits == 8) {
+        switch (p.cfg) {
+            case 7: e = launch_tiled<2, 2, 4, 8, 8, 2, true>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, part, st); break;
+            case 8: e = launch_tiled<1, 2, 8, 4, 8, 2, true>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, part, st); break;
+            case 1: e = launch_tiled<2, 2, 4, 4, 8, 3, true>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, part, st); break;
+            case 2: e = launch_tiled<2, 2, 2, 2, 8, 4, true>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, part, st); break;
+            default: e = launch_tiled<1, 4, 4, 2, 8, 4, true>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, part, st); break;
+        }
+    } else {
+        switch (p.cfg) {
+            case 0: e = launch_tiled<4, 2, 4, 4, 4, 2, true>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, part, st); break;
+            case 1: e = launch_tiled<2, 2, 4, 4, 4, 3, true>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, part, st); break;
+            case 2: e = launch_tiled<2, 2, 2, 2, 4, 4, true>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, part, st); break;
+            default: e = launch_tiled<1, 4, 4, 2, 4, 4, true>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, part, st); break;
+        }
     }
     if (e != hipSuccess) return e;
     return finish_split(p, part, s_a, s_w, M, N, Y, acc, st);
@@ -1021,7 +1055,8 @@ hipError_t launch_gemm(const uint8_t* Aq, const float* s_a, const uint8_t* Wq, c
     if (bits == 8) {
         switch (p.cfg) {
             case 3: e = skinny_kw<8>(p.waves, Aq, s_a, Wq, s_w, M, N, K, Y, acc, st); break;
-            case 0: e = launch_tiled<4, 2, 4, 4, 8, 2>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
+            case 7: e = launch_tiled<2, 2, 4, 8, 8, 2>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
+            case 8: e = launch_tiled<1, 2, 8, 4, 8, 2>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
             case 1: e = launch_tiled<2, 2, 4, 4, 8, 3>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
             case 2: e = launch_tiled<2, 2, 2, 2, 8, 4>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
             default: e = launch_tiled<1, 4, 4, 2, 8, 4>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;

@@ -168,11 +168,13 @@ hipError_t launch_split_basis(const float* P, int K, uint16_t* Ps, hipStream_t s
 hipError_t launch_transform_fast(const uint16_t* X, const uint8_t* state, const uint16_t* Ps, int M, int K, int dm,
                                  int du, float* Xp, hipStream_t st);
 
-// int4 GEMM on fragment-ordered weights (gemm.hip); workspace as gemm_workspace_bytes(M, N, K, 4)
+// GEMM on fragment-ordered weights (gemm.hip), 4- or 8-bit codes; workspace as
+// gemm_workspace_bytes(M, N, K, bits).  frag_weight_bytes and weights_to_frag
+// count a row in int4 codes (K / 2 bytes): 8-bit rows of K bytes pass 2 K.
 size_t frag_weight_bytes(int N, int K);
 hipError_t launch_weights_to_frag(const uint8_t* Wq, int N, int K, uint8_t* Wf, hipStream_t st);
 hipError_t launch_gemm_frag(const uint8_t* Aq, const float* s_a, const uint8_t* Wf, const float* s_w, int M, int N,
-                            int K, uint16_t* Y, int32_t* acc, void* ws, hipStream_t st);
+                            int K, uint16_t* Y, int32_t* acc, void* ws, hipStream_t st, int bits);
 
 // int4 codes on the FP6 matrix cores (fp6.hip)
 size_t fp6_row_bytes(int K);

@@ -210,6 +210,30 @@ def test_frag_entry_points_validate(lib):
     assert lib.sq_weights_to_frag(FAKE, 1 << 20, 4096, FAKE + (1 << 40), None) == L.SQ_ERR_SHAPE
 
 
+def test_w8_frag_entry_points_validate(lib):
+    # ceil(N / 16) ceil(K / 64) 1024: the bytes of 2 K int4 codes
+    assert lib.sq_frag_weight_w8_bytes(16, 64) == 1024 and lib.sq_frag_weight_w8_bytes(24, 96) == 0
+    assert lib.sq_frag_weight_w8_bytes(24, 192) == 2 * 3 * 1024
+    assert lib.sq_frag_weight_w8_bytes(16, 65536 + 64) == 0 and lib.sq_frag_weight_w8_bytes(-1, 128) == 0
+    args = (FAKE, FAKE, FAKE, FAKE)
+    f = lib.w8a8_gemm_frag
+    assert f(*args, 4, 16, 65536 + 64, FAKE, None, FAKE, 1 << 30, None) == L.SQ_ERR_SHAPE
+    assert b"65536" in lib.sq_last_error()
+    assert f(*args, 4, 12, 128, FAKE, None, None, 0, None) == L.SQ_ERR_SHAPE
+    assert f(*args, 4, 16, 128, None, None, None, 0, None) == L.SQ_ERR_NULL
+    assert f(FAKE, FAKE, FAKE + 8, FAKE, 4, 16, 128, FAKE, None, None, 0, None) == L.SQ_ERR_ALIGN
+    assert f(None, None, None, None, 0, 16, 128, None, None, None, 0, None) == L.SQ_OK
+    assert f(*args, 1 << 16, 16, 65536, FAKE, None, None, 0, None) == L.SQ_ERR_SHAPE      # 4 GiB of codes
+    need = lib.sq_gemm_w8_workspace_bytes(96, 4096, 4096)
+    assert need > 0
+    assert f(*args, 96, 4096, 4096, FAKE, None, None, need - 1, None) == L.SQ_ERR_WORKSPACE
+    assert lib.sq_weights_to_frag_w8(FAKE, 16, 65536 + 64, FAKE + (1 << 40), None) == L.SQ_ERR_SHAPE
+    assert lib.sq_weights_to_frag_w8(FAKE, 16, 96, FAKE + (1 << 20), None) == L.SQ_ERR_SHAPE
+    assert lib.sq_weights_to_frag_w8(None, 16, 128, FAKE, None) == L.SQ_ERR_NULL
+    assert lib.sq_weights_to_frag_w8(FAKE, 16, 128, FAKE + 1024, None) == L.SQ_ERR_SHAPE   # overlap: 2 KB rows
+    assert lib.sq_weights_to_frag_w8(None, 0, 128, None, None) == L.SQ_OK
+
+
 def test_noalloc_gemm_validates(lib):
     args = (FAKE, FAKE, FAKE, FAKE)
     f = lib.w4a4_gemm_frag_noalloc

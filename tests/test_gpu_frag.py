@@ -6,8 +6,10 @@
   converter) gives the oracle's int32 accumulators and fp16 outputs bit for bit;
 * on GPU-converted weights, at every short-M plan (wide, mid-width and narrow
   layers; activations staged in LDS or read from L2; one to four row tiles),
-  every tiled plan (with and without K splits) and at the largest K with the
-  extreme sum 2^23, acc and Y equal the oracle's and w4a4_gemm's."""
+  every tiled plan (with and without K splits; 64 x 64 ... 128 x 256 tiles) and at the largest K with the
+  extreme sum 2^23, acc and Y equal the oracle's and w4a4_gemm's;
+* the same for int8 codes (W8A8): conversion, GEMM on oracle-ordered weights,
+  short-M and tiled plans, and the extreme sum 2^30 at K = 65536."""
 import numpy as np
 import pytest
 
@@ -57,9 +59,9 @@ SHAPES = [
     (16, 4096, 1024), (32, 4096, 1024),
     # four row tiles at 49 ... 64 tokens for layers up to 12288 wide with K <= 4096
     (64, 12288, 4096), (57, 4608, 3584), (64, 4096, 4096), (50, 3584, 3584), (61, 12288, 2048), (64, 1032, 576),
-    # tiled plans: 64 x 64 with K splits, 64 x 128, 128 x 128, 256 x 128
+    # tiled plans: 64 x 64 with K splits, 64 x 128, 128 x 128, 256 x 128, 128 x 256
     (49, 4104, 4160), (64, 24576, 4096), (300, 1032, 576), (1024, 4096, 4096), (2100, 4104, 3584),
-    (4096, 8200, 4160), (513, 4104, 12288), (4096, 4096, 192), (4000, 4000, 4160),
+    (4096, 8200, 4160), (513, 4104, 12288), (4096, 4096, 192), (4000, 4000, 4160), (3000, 12296, 3584),
 ]
 
 
@@ -119,3 +121,76 @@ def test_empty_and_single_outputs():
     assert_y(host(Y), rY)
     Y0 = sq.w4a4_gemm_frag(dev(np.zeros((0, K // 2), np.uint8)), dev(np.ones(0, np.float32)), Wf, s_w)
     assert Y0.shape == (0, 8)
+
+
+def codes8(R, K, seed):
+    return np.random.default_rng(seed).integers(-128, 128, (R, K)).astype(np.int8)
+
+
+@pytest.mark.parametrize("N,K", [(8, 64), (40, 320), (4104, 4160)])
+def test_w8_conversion_bit_exact(N, K):
+    Wq = codes8(N, K, N + K)
+    got = host(sq.weights_to_frag(dev(Wq)))
+    assert_bits(got, F.to_frag_q8(Wq, K), "fragment-ordered int8 weights")
+
+
+def test_w8_gemm_on_oracle_ordered_weights():
+    M, N, K = 20, 40, 320                        # two row tiles, a ragged group (int8: whole k steps)
+    qa, qw = codes8(M, K, 1), codes8(N, K, 2)
+    rng = np.random.default_rng(3)
+    s_a = rng.uniform(0.01, 1, M).astype(np.float32)
+    s_w = rng.uniform(1e-5, 1e-3, N).astype(np.float32)
+    Wf = F.to_frag_q8(qw, K)
+    Y, acc = sq.w8a8_gemm_frag(dev(qa), dev(s_a), dev(Wf), dev(s_w), want_acc=True)
+    rY, racc = F.gemm_q8(qa, s_a, Wf, s_w, N, K)
+    assert_bits(host(acc), racc, "acc")
+    assert_y(host(Y), rY)
+
+
+W8_SHAPES = [
+    # short M (<= 48 tokens): wide, mid-width and narrow layers; LDS or L2 activations
+    (1, 24576, 4096), (16, 12288, 4096), (33, 4096, 4096), (48, 4096, 12288), (5, 4104, 4160),
+    (17, 16392, 8192), (1, 8, 64), (3, 24, 192), (40, 8200, 12288),
+    # tiled plans: 64 x 64 with K splits, 64 x 128, 128 x 128, 256 x 128
+    (49, 4104, 4160), (64, 12288, 4096), (300, 1032, 576), (1024, 4096, 4096), (1024, 4096, 12288),
+    (2100, 4104, 3584), (4096, 12288, 4096), (4000, 4000, 4160),
+    # 128 x 256 at 192 ... 511 of its tiles; 128 x 128 in two waves from 640 of its tiles (ragged M, N)
+    (500, 12296, 4160), (1000, 12296, 4160), (520, 24576, 4096),
+]
+
+
+@pytest.mark.parametrize("M,N,K", W8_SHAPES)
+def test_w8_gemm_bit_exact(M, N, K):
+    qa, qw = codes8(M, K, 10 + M), codes8(N, K, 20 + N)
+    rng = np.random.default_rng(4)
+    s_a = rng.uniform(0.01, 1, M).astype(np.float32)
+    s_w = rng.uniform(1e-5, 1e-3, N).astype(np.float32)
+    say(f"w8a8_gemm_frag M={M} N={N} K={K}")
+    Wf = sq.weights_to_frag(dev(qw))
+    Y, acc = sq.w8a8_gemm_frag(dev(qa), dev(s_a), Wf, dev(s_w), want_acc=True)
+    Y, acc = host(Y), host(acc)
+    rows = np.arange(M) if M * N * K <= 3e9 else np.unique(np.r_[0, M - 1, rng.choice(M, 24)])
+    rY, racc = O.gemm_q8(qa[rows], s_a[rows], qw, s_w, threads=THREADS)
+    assert_bits(acc[rows], racc, "acc")
+    assert_y(Y[rows], rY)
+    Y8, acc8 = sq.w8a8_gemm(dev(qa), dev(s_a), dev(qw), dev(s_w), want_acc=True)
+    assert_bits(acc, host(acc8), "acc vs w8a8_gemm")
+    assert_bits(Y, host(Y8), "Y vs w8a8_gemm")
+
+
+@pytest.mark.parametrize("M", [3, 64])
+def test_w8_gemm_at_the_largest_K(M):
+    """K = 65536 with every product (-128)(-128) on row 0 / column 0: the sum 2^30."""
+    K, N = 65536, 16
+    qa, qw = codes8(M, K, 12), codes8(N, K, 13)
+    qa[0, :] = -128
+    qw[0, :] = -128
+    s_a = np.ones(M, np.float32)
+    s_w = np.full(N, 1e-9, np.float32)
+    say(f"w8a8_gemm_frag largest K M={M}")
+    Y, acc = sq.w8a8_gemm_frag(dev(qa), dev(s_a), sq.weights_to_frag(dev(qw)), dev(s_w), want_acc=True)
+    ref = qa.astype(np.int64) @ qw.T.astype(np.int64)
+    assert ref[0, 0] == 1 << 30
+    assert_bits(host(acc), ref.astype(np.int32), "acc")
+    rY, _ = O.gemm_q8(qa, s_a, qw, s_w, threads=THREADS)
+    assert_y(host(Y), rY)

@@ -3,7 +3,8 @@
 The layout is checked against byte offsets worked out by hand from its
 definition, against being a bijection onto the non-padding bytes, against a
 round trip with zero padding at a ragged N and a half k step, and the GEMM
-against brute-force integer dot products of the codes."""
+against brute-force integer dot products of the codes; the int8 layout at
+hand-worked offsets (64 codes a k step) and its GEMM against brute force."""
 import numpy as np
 import pytest
 
@@ -70,4 +71,32 @@ def test_gemm_is_the_int4_gemm():
     brute = np.array([[sum(int(qa[i, k]) * int(qw[n, k]) for k in range(K)) for n in range(N)] for i in range(M)])
     assert np.array_equal(acc, brute)
     rY, _ = O.gemm(pack(qa), s_a, pack(qw), s_w)
+    assert np.array_equal(Y.view(np.uint16), rY.view(np.uint16))
+
+
+def test_q8_hand_worked_offsets():
+    N, K = 24, 96                                          # G = 2, T = 2 (64 + 32 bytes a row)
+    cases = {(0, 0): 0, (0, 17): 256 + 1,                  # byte 17: j = 1, unit 16
+             (0, 64): 2 * 1024,                            # code 64 opens k step 1: block 1 x 2 + 0
+             (23, 95): 3 * 1024 + (16 * 1 + 7) * 16 + 15}  # row 23, code 95: block (g 1, t 1), j 1, r 7
+    for (row, k), off in cases.items():
+        W = np.zeros((N, K), np.int8)
+        W[row, k] = -91
+        flat = F.to_frag_q8(W, K).reshape(-1)
+        assert flat.size == 2 * 2 * 1024
+        assert flat[off] == np.uint8(256 - 91) and np.count_nonzero(flat) == 1, (row, k)
+
+
+def test_gemm_q8_is_the_int8_gemm():
+    rng = np.random.default_rng(6)
+    M, N, K = 3, 24, 96                                   # ragged group and a half k step
+    qa = rng.integers(-128, 128, (M, K)).astype(np.int8)
+    qw = rng.integers(-128, 128, (N, K)).astype(np.int8)
+    qw[0] = -128
+    s_a = rng.uniform(0.1, 1, M).astype(np.float32)
+    s_w = rng.uniform(1e-4, 1e-3, N).astype(np.float32)
+    Y, acc = F.gemm_q8(qa, s_a, F.to_frag_q8(qw, K), s_w, N, K)
+    brute = np.array([[sum(int(qa[i, k]) * int(qw[n, k]) for k in range(K)) for n in range(N)] for i in range(M)])
+    assert np.array_equal(acc, brute)
+    rY, _ = O.gemm_q8(qa, s_a, qw, s_w)
     assert np.array_equal(Y.view(np.uint16), rY.view(np.uint16))
