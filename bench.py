@@ -121,6 +121,13 @@ class Timer:
         self.pairs = {}
 
 
+class NullTimer:
+    """A timer that records nothing (for captured or whole-step timings)."""
+
+    def wrap(self, label, fn):
+        fn()
+
+
 def run_steps(torch, step, steps, warmup):
     """W untimed warm-up steps, then exactly `steps` steps between two HIP events,
     synchronised on both sides.  step(timer, i) enqueues one step.  Returns the
@@ -320,6 +327,10 @@ def folded_block(torch, sq, sites, state, M, steps, warmup, copies=1):
                                                                  s_a=d["s_a"], ws=d["qws"]))
             tm.wrap("g/" + d["name"], lambda: sq.w4a4_gemm_frag(d["Aq"], d["s_a"], Wf, s_w, Y=d["Y"], ws=d["gws"]))
     ms, timer = run_steps(torch, step, steps, warmup)
+    # the same steps, one per weight set, captured back to back in one HIP graph
+    # (no host work or timing events between the launches)
+    graph_ms_step, g = graph_ms(torch, lambda i: step(NullTimer(), i), copies, replays=max(3, min(steps, 10)))
+    del g
     per, tot_ops, tot_ms = {}, 0.0, 0.0
     for d in sites:
         n = d["name"]
@@ -332,6 +343,7 @@ def folded_block(torch, sq, sites, state, M, steps, warmup, copies=1):
         tot_ms += gms
     del wsets
     return {"tokens": M, "ms_per_step": ms, "tokens_per_s": M / (ms / 1e3),
+            "graph_ms_per_step": graph_ms_step, "graph_tokens_per_s": M / (graph_ms_step / 1e3),
             "sgat_linear_tops": tot_ops / (ms / 1e3) / 1e12,
             "gemm_tops": tot_ops / tot_ms / 1e9, "gemm_frac_int8_peak": tot_ops / tot_ms / 1e9 / PEAK_INT8_TOPS,
             "per_site": per}
@@ -559,12 +571,17 @@ def llada_blocks(torch, sq, synth, dev, args):
                 tm.wrap("g8/" + d["name"], lambda: sq.w8a8_gemm_frag(e["Aq8"], d["s_a"], Wf8, s_w8, Y=d["Y"],
                                                                      ws=e["gws8"]))
         ms, timer = run_steps(torch, step_w8, args.steps, args.warmup)
+        graph_ms_step, g = graph_ms(torch, lambda i: step_w8(NullTimer(), i), len(copies),
+                                    replays=max(3, min(args.steps, 10)))
+        del g
         ops = sum(2.0 * M * d["N"] * d["K"] for d in sites)
         gms = sum(timer.mean("g8/" + d["name"]) for d in sites)
         per = {d["name"]: {"gemm_us": timer.mean("g8/" + d["name"]) * 1e3,
                            "frac_int8_peak": 2.0 * M * d["N"] * d["K"] / timer.mean("g8/" + d["name"]) / 1e9
                            / PEAK_INT8_TOPS} for d in sites}
-        out["w8a8_folded_P"] = {"tokens_per_s": M / (ms / 1e3), "ms_per_step": ms, "gemm_tops": ops / gms / 1e9,
+        out["w8a8_folded_P"] = {"tokens_per_s": M / (ms / 1e3), "ms_per_step": ms,
+                                "graph_ms_per_step": graph_ms_step, "graph_tokens_per_s": M / (graph_ms_step / 1e3),
+                                "gemm_tops": ops / gms / 1e9,
                                 "gemm_frac_int8_peak": ops / gms / 1e9 / PEAK_INT8_TOPS,
                                 "quant_act_ms": sum(timer.mean("q8/" + d["name"]) for d in sites),
                                 "weights": "int8 in fragment order, 4 rotating sets", "per_site": per}
