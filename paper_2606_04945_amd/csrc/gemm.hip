@@ -71,21 +71,29 @@ __device__ __forceinline__ int acc_value(int raw) {   // 4-bit operands carry a 
     return BITS == 8 ? raw : (raw == INT32_MIN ? (1 << 23) : raw >> 8);
 }
 
-template <int WM, int WN, int TM, int TN, bool SPLIT, int BITS, int OCC, bool WF = false>
-__global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(OCC))) void gemm_tile_kernel(
+// KG > 1: KG sets of WM x WN waves share the tile and split its k steps
+// (set g multiplies steps g, g + KG, ...; a stage holds KG consecutive steps,
+// one per set), so a workgroup that owns a whole tile has KG times the waves;
+// the sets' partial sums meet in LDS (exact integer adds) before the epilogue.
+template <int WM, int WN, int TM, int TN, bool SPLIT, int BITS, int OCC, bool WF = false, int KG = 1>
+__global__ __launch_bounds__(64 * WM * WN * KG) __attribute__((amdgpu_waves_per_eu(OCC))) void gemm_tile_kernel(
     const uint8_t* __restrict__ Aq, const float* __restrict__ s_a, const uint8_t* __restrict__ Wq,
     const float* __restrict__ s_w, int M, int N, int K, int ksteps_per_split, uint16_t* __restrict__ Y,
     int32_t* __restrict__ acc_out, int32_t* __restrict__ part) {
-    constexpr int NW = WM * WN;
+    static_assert(KG == 1 || !SPLIT, "k groups replace the split across workgroups");
+    constexpr int NW = WM * WN;                          // waves of one k group
     constexpr int BM = 16 * WM * TM, BN = 16 * WN * TN;
-    constexpr int AB = BM * kKB, BB = BN * kKB;          // bytes of one stage
-    constexpr int SB = AB + BB;
+    constexpr int AB = BM * kKB, BB = BN * kKB;          // bytes of one k step
+    constexpr int SG = AB + BB;
+    constexpr int SB = KG * SG;                          // bytes of one stage
     constexpr int LA = AB / 1024 / NW, LB = BB / 1024 / NW;   // 1 KB loads per wave per stage
     static_assert(LA * NW * 1024 == AB && LB * NW * 1024 == BB, "stage loads must divide evenly");
+    static_assert((KG - 1) * NW * TM * TN * kWave * 16 <= 3 * SB, "k-group partial sums fit in the stages");
     __shared__ __attribute__((aligned(16))) uint8_t sm[3 * SB];
 
     const int tid = threadIdx.x;
-    const int lane = tid % kWave, wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+    const int lane = tid % kWave, wave_all = __builtin_amdgcn_readfirstlane(tid / kWave);
+    const int kg = wave_all / NW, wave = wave_all % NW;  // k group, wave within it
     const int wm = wave / WN, wn = wave % WN;
     const uint32_t ldb = (uint32_t)K * BITS / 8;
     const int nk_total = (int)((ldb + kKB - 1) / kKB);
@@ -100,8 +108,9 @@ __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(OC
     int rt, ct;
     xcd_tile(blockIdx.x, (M + BM - 1) / BM, (N + BN - 1) / BN, 8, rt, ct);
     const int row0 = rt * BM, col0 = ct * BN;
+    // stage indices: stage kt holds k steps KG kt .. KG kt + KG - 1
     const int kt0 = SPLIT ? blockIdx.z * ksteps_per_split : 0;
-    const int kt1 = SPLIT ? min(nk_total, kt0 + ksteps_per_split) : nk_total;
+    const int kt1 = SPLIT ? min(nk_total, kt0 + ksteps_per_split) : (nk_total + KG - 1) / KG;
 
     // this lane's source segment for each of its loads: tile row r = 16 j + lane / 4
     // holds, at chunk slot lane % 4, segment (lane % 4) ^ swz(r)
@@ -124,8 +133,10 @@ __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(OC
             ow[u] = col0 + r < N ? (uint32_t)(col0 + r) * ldb + sw_[u] : kOOB;
         }
     }
-    auto issue = [&](int kt, int stage) {
-        uint8_t* dA = sm + stage * SB;
+    auto issue = [&](int st_kt, int stage) {
+        // this k group's step of the stage; a step past the end reads as zeros
+        const int kt = KG * st_kt + kg;
+        uint8_t* dA = sm + stage * SB + kg * SG;
         uint8_t* dB = dA + AB;
         const uint32_t ko = (uint32_t)kt * kKB;
         const bool tail = kt >= nk_full;
@@ -249,7 +260,7 @@ __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(OC
         // is the overlap this pipeline exists for.
         __builtin_amdgcn_s_barrier();
         asm volatile("" ::: "memory");
-        frags(sm + sc * SB);
+        frags(sm + sc * SB + kg * SG);
         if (kt + 2 < kt1) issue(kt + 2, sn);             // into the stage step kt - 1 used
         mma();
     };
@@ -259,6 +270,25 @@ __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(OC
         step(kt, 0, 2);
         if (kt + 1 < kt1) step(kt + 1, 1, 0);
         if (kt + 2 < kt1) step(kt + 2, 2, 1);
+    }
+    if constexpr (KG > 1) {
+        // every wave is past its last fragment read: the stages take the partial sums
+        __syncthreads();
+        v4i* red = reinterpret_cast<v4i*>(sm);           // [KG - 1][NW][TM][TN][lane]
+        if (kg > 0) {
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j) red[((((kg - 1) * NW + wave) * TM + i) * TN + j) * kWave + lane] = acc[i][j];
+        }
+        __syncthreads();
+        if (kg > 0) return;
+#pragma unroll
+        for (int g = 0; g < KG - 1; ++g)
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j) acc[i][j] += red[(((g * NW + wave) * TM + i) * TN + j) * kWave + lane];
     }
     if (K < 131072)
         epilogue(std::true_type{});
@@ -664,7 +694,8 @@ __global__ __launch_bounds__(256) void splitk_epilogue(const int32_t* __restrict
 // A launch plan: tile shape and K split.
 struct Plan {
     int cfg;       // 0: 256 x 128, 1: 128 x 128, 2: 64 x 64, 4: 64 x 128, 7: 128 x 256 (8-bit), 8: 128 x 128
-                   // in two waves of 128 x 64 (8-bit), 3: short M, K split in the
+                   // in two waves of 128 x 64 (8-bit), 9: 128 x 128 in two k groups of four waves,
+                   // 3: short M, K split in the
                    // workgroup, 5: short M, activations shared in LDS (see launch_gemm), 6: short M on
                    // fragment-ordered weights (see launch_gemm_frag)
     int bm, bn;
@@ -737,19 +768,21 @@ hipError_t launch_skinny_shared(int waves, const uint8_t* Aq, const float* s_a, 
     }
 }
 
-template <int WM, int WN, int TM, int TN, int BITS = 4, int OCC = 1, bool WF = false>
+template <int WM, int WN, int TM, int TN, int BITS = 4, int OCC = 1, bool WF = false, int KG = 1>
 hipError_t launch_tiled(const Plan& p, const uint8_t* Aq, const float* s_a, const uint8_t* Wq, const float* s_w,
                        int M, int N, int K, uint16_t* Y, int32_t* acc, int32_t* part, hipStream_t st) {
     const size_t tiles = (size_t)((N + p.bn - 1) / p.bn) * (size_t)((M + p.bm - 1) / p.bm);
     if (tiles > 0x7fffffffu) return hipErrorInvalidConfiguration;
     dim3 grid((unsigned)tiles, 1, p.splits);
-    dim3 block(64 * WM * WN);
+    dim3 block(64 * WM * WN * KG);
     if (p.splits == 1) {
-        hipLaunchKernelGGL((gemm_tile_kernel<WM, WN, TM, TN, false, BITS, OCC, WF>), grid, block, 0, st, Aq, s_a, Wq,
-                           s_w, M, N, K, p.per, Y, acc, (int32_t*)nullptr);
-    } else {
+        hipLaunchKernelGGL((gemm_tile_kernel<WM, WN, TM, TN, false, BITS, OCC, WF, KG>), grid, block, 0, st, Aq, s_a,
+                           Wq, s_w, M, N, K, p.per, Y, acc, (int32_t*)nullptr);
+    } else if constexpr (KG == 1) {
         hipLaunchKernelGGL((gemm_tile_kernel<WM, WN, TM, TN, true, BITS, OCC, WF>), grid, block, 0, st, Aq, s_a, Wq,
                            s_w, M, N, K, p.per, (uint16_t*)nullptr, (int32_t*)nullptr, part);
+    } else {
+        return hipErrorInvalidConfiguration;
     }
     return hipGetLastError();
 }
@@ -877,6 +910,8 @@ hipError_t finish_split(const Plan& p, int32_t* part, const float* s_a, const fl
 //    tiles; else 128 x 128 in two waves of 128 x 64 from 640 of its tiles
 //    (three workgroups per CU fill the chip at 768); else 128 x 256 from 192
 //    of its tiles; else 128 x 128 (four waves) from 192 of its tiles;
+//  - 129 ... 256 tiles of 128 x 128 and at least 128 k steps (64 for 8-bit
+//    codes): 128 x 128 with two k groups of four waves (see below);
 //  - at least 512 tiles of 64 x 128: 64 x 128 (four waves of 64 x 32);
 //  - otherwise 64 x 64 (four waves of 32 x 32), with K split below 256 tiles
 //    (twice as deep for K >= 8192) and kept at 8 k steps or more per split.
@@ -910,6 +945,15 @@ Plan choose_plan(int M, int N, int K, int bits) {
             p.cfg = 3;
             p.waves = kw;
         }
+    } else if (tiles(128, 128) > 128 && tiles(128, 128) <= 256 && nk >= (bits == 8 ? 64 : 128)) {
+        // at most one 128 x 128 tile per CU and a deep K: two k groups of four
+        // waves per tile (interleaved timings with rotating weights against the
+        // plans below: 8-bit 1024 x 4096 x 4096 13 % faster, 1024 x 4096 x 12288
+        // 15 %, 256 x 12288 x 4096 9 %, 1024 x 3584 x 18944 18 %; 4-bit
+        // 1024 x 3584 x 18944 17 %, but 4 % slower at 1024 x 4096 x 12288 (96
+        // k steps) and 6 % at 768 x 4096 x 12288, hence 128 k steps for 4-bit)
+        p = make_plan(M, N, K, 128, 128, 1, bits);
+        p.cfg = 9;
     } else if (bits == 4 && (tiles(256, 128) >= 448 || tiles(128, 128) >= 448)) {
         // 4-bit codes, from interleaved graph-replayed timings of both plans on
         // the layer-set shapes at 512 ... 16384 tokens: 256 x 128 wins only when
@@ -1025,6 +1069,7 @@ hipError_t launch_gemm_frag(const uint8_t* Aq, const float* s_a, const uint8_t* 
     if (bits == 8) {
         switch (p.cfg) {
             case 7: e = launch_tiled<2, 2, 4, 8, 8, 2, true>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, part, st); break;
+            case 9: e = launch_tiled<2, 2, 4, 4, 8, 2, true, 2>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, part, st); break;
             case 8: e = launch_tiled<1, 2, 8, 4, 8, 2, true>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, part, st); break;
             case 1: e = launch_tiled<2, 2, 4, 4, 8, 3, true>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, part, st); break;
             case 2: e = launch_tiled<2, 2, 2, 2, 8, 4, true>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, part, st); break;
@@ -1033,6 +1078,7 @@ hipError_t launch_gemm_frag(const uint8_t* Aq, const float* s_a, const uint8_t* 
     } else {
         switch (p.cfg) {
             case 0: e = launch_tiled<4, 2, 4, 4, 4, 2, true>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, part, st); break;
+            case 9: e = launch_tiled<2, 2, 4, 4, 4, 2, true, 2>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, part, st); break;
             case 1: e = launch_tiled<2, 2, 4, 4, 4, 3, true>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, part, st); break;
             case 2: e = launch_tiled<2, 2, 2, 2, 4, 4, true>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, part, st); break;
             default: e = launch_tiled<1, 4, 4, 2, 4, 4, true>(p, Aq, s_a, Wf, s_w, M, N, K, Y, acc, part, st); break;
@@ -1056,6 +1102,7 @@ hipError_t launch_gemm(const uint8_t* Aq, const float* s_a, const uint8_t* Wq, c
         switch (p.cfg) {
             case 3: e = skinny_kw<8>(p.waves, Aq, s_a, Wq, s_w, M, N, K, Y, acc, st); break;
             case 7: e = launch_tiled<2, 2, 4, 8, 8, 2>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
+            case 9: e = launch_tiled<2, 2, 4, 4, 8, 2, false, 2>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
             case 8: e = launch_tiled<1, 2, 8, 4, 8, 2>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
             case 1: e = launch_tiled<2, 2, 4, 4, 8, 3>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
             case 2: e = launch_tiled<2, 2, 2, 2, 8, 4>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
@@ -1066,6 +1113,7 @@ hipError_t launch_gemm(const uint8_t* Aq, const float* s_a, const uint8_t* Wq, c
             case 3: e = skinny_kw<4>(p.waves, Aq, s_a, Wq, s_w, M, N, K, Y, acc, st); break;
             case 5: e = launch_skinny_shared(p.waves, Aq, s_a, Wq, s_w, M, N, K, Y, acc, st); break;
             case 0: e = launch_tiled<4, 2, 4, 4, 4, 2>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
+            case 9: e = launch_tiled<2, 2, 4, 4, 4, 2, false, 2>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
             case 1: e = launch_tiled<2, 2, 4, 4, 4, 3>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
             case 2: e = launch_tiled<2, 2, 2, 2, 4, 4>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;
             default: e = launch_tiled<1, 4, 4, 2, 4, 4>(p, Aq, s_a, Wq, s_w, M, N, K, Y, acc, part, st); break;

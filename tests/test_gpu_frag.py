@@ -6,7 +6,8 @@
   converter) gives the oracle's int32 accumulators and fp16 outputs bit for bit;
 * on GPU-converted weights, at every short-M plan (wide, mid-width and narrow
   layers; activations staged in LDS or read from L2; one to four row tiles),
-  every tiled plan (with and without K splits; 64 x 64 ... 128 x 256 tiles) and at the largest K with the
+  every tiled plan (with and without K splits; 64 x 64 ... 128 x 256 tiles; k
+  groups within a workgroup) and at the largest K with the
   extreme sum 2^23, acc and Y equal the oracle's and w4a4_gemm's;
 * the same for int8 codes (W8A8): conversion, GEMM on oracle-ordered weights,
   short-M and tiled plans, and the extreme sum 2^30 at K = 65536."""
@@ -62,6 +63,8 @@ SHAPES = [
     # tiled plans: 64 x 64 with K splits, 64 x 128, 128 x 128, 256 x 128, 128 x 256
     (49, 4104, 4160), (64, 24576, 4096), (300, 1032, 576), (1024, 4096, 4096), (2100, 4104, 3584),
     (4096, 8200, 4160), (513, 4104, 12288), (4096, 4096, 192), (4000, 4000, 4160), (3000, 12296, 3584),
+    # 128 x 128 in two k groups: ragged M and N, an odd number of k steps with half a last step
+    (1000, 3584, 19008), (1024, 3584, 18944), (1024, 4096, 12288),
 ]
 
 
@@ -156,6 +159,8 @@ W8_SHAPES = [
     (2100, 4104, 3584), (4096, 12288, 4096), (4000, 4000, 4160),
     # 128 x 256 at 192 ... 511 of its tiles; 128 x 128 in two waves from 640 of its tiles (ragged M, N)
     (500, 12296, 4160), (1000, 12296, 4160), (520, 24576, 4096),
+    # 128 x 128 in two k groups (an odd number of k steps; ragged M and N)
+    (1000, 4000, 12352), (1024, 4096, 4096), (256, 12288, 4096),
 ]
 
 

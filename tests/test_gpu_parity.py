@@ -216,7 +216,9 @@ GEMM_SHAPES = [(1, 8, 64), (16, 4096, 4096), (5, 4104, 4096), (9, 136, 192), (16
                (64, 24576, 4096), (48, 12304, 4032), (20, 16384, 8192), (64, 16392, 8192), (40, 4104, 12288),
                (77, 200, 192), (128, 256, 512), (300, 136, 4096), (300, 16384, 64), (1024, 1024, 1024),
                (1000, 8200, 64), (2100, 12296, 64), (513, 4104, 3584), (64, 512, 18944),
-               (4096, 4096, 192), (4000, 4000, 4160), (1000, 12296, 4160)]
+               (4096, 4096, 192), (4000, 4000, 4160), (1000, 12296, 4160),
+               # two k groups per tile: ragged M and N, an odd number of k steps (half a last step at 4 bits)
+               (1000, 4000, 12352), (1024, 3584, 18944), (1000, 3584, 19008)]
 
 
 @pytest.mark.parametrize("M,N,K", GEMM_SHAPES)
