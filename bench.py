@@ -548,7 +548,9 @@ def llada_blocks(torch, sq, synth, dev, args):
     fold = folded_block(torch, sq, sites, state, M, args.steps, args.warmup, copies=8)
     fold["workload"] = "LLaDA-8B-shaped SGAT layer set, 1024 tokens, folded P, 8 rotating weight sets"
     fold["roofline"] = {"bound": "mfma", "achieved": fold["gemm_tops"], "peak": PEAK_INT8_TOPS, "unit": "TOP/s",
-                        "frac": fold["gemm_frac_int8_peak"], "traffic": None, "kernel": "w4a4 gemm (all four sites)"}
+                        "frac": fold["gemm_frac_int8_peak"],
+                        "traffic": recorded_traffic("gemm_llada_folded_step", "traffic_bytes_per_step"),
+                        "kernel": "w4a4 gemm (all four sites; traffic per step)"}
     out["folded_P"] = fold
     if not args.no_w8:
         # int8 weights in fragment order (as the 4-bit ones), 4 rotating sets
