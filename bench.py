@@ -409,7 +409,8 @@ def fp6_variant(torch, sq, sites, state, M, steps, warmup):
     return {"ms_per_step": ms, "tokens_per_s": M / (ms / 1e3), "gemm_tops": tot_ops / tot_ms / 1e9,
             "per_site": per, "outputs_equal_int4_path": same,
             "roofline": {"bound": "mfma", "achieved": per[dom]["tops"], "peak": PEAK_FP6_TFLOPS, "unit": "TFLOP/s",
-                         "frac": per[dom]["frac_fp6_peak"], "traffic": None,
+                         "frac": per[dom]["frac_fp6_peak"],
+                         "traffic": recorded_traffic("gemm_fp6_gate_up") if dom == "gate_up" else None,
                          "kernel": f"w4a4 gemm on FP6 operands ({dom})"}}
 
 
