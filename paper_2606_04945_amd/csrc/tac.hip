@@ -720,7 +720,7 @@ __global__ __launch_bounds__(64 * kTqmMaxWaves) void tac_quant_mfma_kernel(
     const uint32_t row_bytes = (uint32_t)K * BITS / 8;
     const __amdgpu_buffer_rsrc_t rA = make_rsrc(Aq, (uint32_t)M * row_bytes);
     const __amdgpu_buffer_rsrc_t rSo = make_rsrc(s_out, (uint32_t)M * 4);
-    const int rr = lane / 4, pp = lane % 4;                     // coding pass: token rr, runs pp VPL .. pp VPL + VPL - 1
+    const int rr = lane / 4, pp = lane % 4;                     // coding pass: token rr, runs 8 j + 2 pp, 8 j + 2 pp + 1
 
     int n = blockIdx.x;
     int st_cur = state_of(n);                                   // issued ahead of the ring, as in the loop
@@ -798,7 +798,9 @@ __global__ __launch_bounds__(64 * kTqmMaxWaves) void tac_quant_mfma_kernel(
         if (kl == 0) red[(par * kTqmTok + il) * kTqmMaxWaves + wave] = amax;
         ring_barrier();   // every wave's maxima and this wave's output tile are in LDS
 
-        // coding pass: lane -> token rr, runs of 8 channels pp VPL .. pp VPL + VPL - 1 of the wave's range
+        // coding pass: lane -> token rr and, in each group of 8 runs of 8 channels of
+        // the wave's range, runs 2 pp and 2 pp + 1 (the four lanes of a token read 64
+        // consecutive LDS bytes per read, not runs 256 bytes apart in one bank)
         const float4* rp = reinterpret_cast<const float4*>(red + (par * kTqmTok + rr) * kTqmMaxWaves);
         const float4 r0 = rp[0], r1 = rp[1];
         const float rv[8] = {r0.x, r0.y, r0.z, r0.w, r1.x, r1.y, r1.z, r1.w};
@@ -809,14 +811,14 @@ __global__ __launch_bounds__(64 * kTqmMaxWaves) void tac_quant_mfma_kernel(
         const float y = s != 0.0f ? 1.0f / s : 0.0f;   // s = 0: every value is 0 and codes 0
         if (wave == 0)
             __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(s), rSo, pp == 0 ? (uint32_t)(t0 + rr) * 4 : kOOB, 0, 0);
-        const uint8_t* src = region + rr * S::kRS + 16 * pp * VPL;
-        const uint32_t dst = (uint32_t)(t0 + rr) * row_bytes + (uint32_t)(ch0 + 8 * pp * VPL) * BITS / 8;
+        const uint8_t* src = region + rr * S::kRS + 32 * pp;
+        const uint32_t dst = (uint32_t)(t0 + rr) * row_bytes + (uint32_t)(ch0 + 16 * pp) * BITS / 8;
 #pragma unroll
         for (int i0 = 0; i0 < VPL; i0 += 2) {
             uint32_t wv[BITS == 4 ? 2 : 4];
 #pragma unroll
             for (int i = 0; i < 2; ++i) {
-                const v4i hv = *reinterpret_cast<const v4i*>(src + 16 * (i0 + i));
+                const v4i hv = *reinterpret_cast<const v4i*>(src + 16 * (4 * i0 + i));
                 const float x[8] = {lo_h(hv.x), hi_h(hv.x), lo_h(hv.y), hi_h(hv.y),
                                     lo_h(hv.z), hi_h(hv.z), lo_h(hv.w), hi_h(hv.w)};
                 int c[8];
@@ -838,9 +840,9 @@ __global__ __launch_bounds__(64 * kTqmMaxWaves) void tac_quant_mfma_kernel(
             }
             if (BITS == 4) {
                 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-                __builtin_amdgcn_raw_buffer_store_b64(u32x2{wv[0], wv[1]}, rA, dst + 4 * i0, 0, 0);
+                __builtin_amdgcn_raw_buffer_store_b64(u32x2{wv[0], wv[1]}, rA, dst + 16 * i0, 0, 0);
             } else {
-                __builtin_amdgcn_raw_buffer_store_b128(u32x4{wv[0], wv[1], wv[2], wv[3]}, rA, dst + 8 * i0, 0, 0);
+                __builtin_amdgcn_raw_buffer_store_b128(u32x4{wv[0], wv[1], wv[2], wv[3]}, rA, dst + 32 * i0, 0, 0);
             }
         }
         wave_sync();   // this wave's tile is rewritten by its next tile
