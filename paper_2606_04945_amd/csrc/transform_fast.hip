@@ -15,7 +15,7 @@
 // codes are defined by, this one trades that for the matrix cores.
 //
 // The kernel is the GEMM's three-stage direct-to-LDS pipeline on fp16
-// operands: 128 x 128, 64 x 128 or 64 x 64 output tiles, four waves.  A stage
+// operands: 128 x 128 or 64 x 64 output tiles, four waves.  A stage
 // holds one k step of 32 of x and the matching steps of both halves of Ps
 // (hi and lo), so x is fetched and read from LDS once for both: two
 // v_mfma_f32_16x16x32_f16 per 16 x 16 tile and step (hi then lo, into one
@@ -174,15 +174,14 @@ hipError_t launch_split_basis(const float* P, int K, uint16_t* Ps, hipStream_t s
 hipError_t launch_transform_fast(const uint16_t* X, const uint8_t* state, const uint16_t* Ps, int M, int K, int dm,
                                  int du, float* Xp, hipStream_t st) {
     const size_t t128 = (size_t)((M + 127) / 128) * (size_t)((K + 127) / 128);
-    const size_t t64x128 = (size_t)((M + 63) / 64) * (size_t)((K + 127) / 128);
     const size_t t64 = (size_t)((M + 63) / 64) * (size_t)((K + 63) / 64);
     if (t64 > 0x7fffffffu) return hipErrorInvalidConfiguration;
-    if (t128 >= 512) {
+    // 128 x 128 tiles from one per CU on (1024 x 4096, 256 tiles: 73.6 us
+    // against 99.8 us for 512 tiles of 64 x 128 and 111.6 us for 1024 of 64 x 64;
+    // 1024 x 12288: 580 us against 862 and 1003)
+    if (t128 >= 256) {
         hipLaunchKernelGGL((transform_mfma_kernel<2, 2, 4, 4>), dim3((unsigned)t128), dim3(256), 0, st, X, state, Ps,
                            M, K, dm, du, Xp);
-    } else if (t64x128 >= 512) {
-        hipLaunchKernelGGL((transform_mfma_kernel<1, 4, 4, 2>), dim3((unsigned)t64x128), dim3(256), 0, st, X, state,
-                           Ps, M, K, dm, du, Xp);
     } else {
         hipLaunchKernelGGL((transform_mfma_kernel<2, 2, 2, 2>), dim3((unsigned)t64), dim3(256), 0, st, X, state, Ps,
                            M, K, dm, du, Xp);

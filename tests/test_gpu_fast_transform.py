@@ -32,7 +32,7 @@ def test_split_basis_bit_exact(K):
     assert_bits(Ps, F.split_basis(P), "Ps")
 
 
-SHAPES = [(1, 64), (77, 192), (300, 512), (130, 1024), (1024, 4096), (33, 12288)]
+SHAPES = [(1, 64), (77, 192), (300, 512), (130, 1024), (1024, 4096), (33, 12288), (520, 4096), (385, 8192)]
 
 
 @pytest.mark.parametrize("M,K", SHAPES)
